@@ -1,0 +1,282 @@
+"""Benchmark: Horovod-style fused ring-allreduce of N simulated ranks on one MI355X.
+
+One step = one allreduce (AVERAGE) of every rank's gradient tensors: the Tensor
+Fusion plan's copy-in, the ring's N-1 reduce-scatter and N-1 all-gather steps,
+and the copy-out, for every fusion buffer, with inputs already in GPU memory.
+The metric is algorithm bandwidth: one rank's fp32 gradient bytes / step time.
+
+    python bench.py [--steps K] [--warmup W] [--workload resnet50] [--no-per-config]
+
+Prints one JSON line.  Besides the headline workload it reports, per workload,
+the step time and the per-kernel time split measured with HIP events; the roofline
+object is for the kernel with the largest share of the step (HBM-bound: achieved
+algorithmic bytes / time against the 8 TB/s peak).  `cpu_baseline` times the CPU
+oracle on a bounded sample of the same workload on this host.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, 8 TB/s
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--workload", default="resnet50")
+    p.add_argument("--no-per-config", action="store_true", help="time only the headline workload")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-seconds", type=float, default=12.0, help="target oracle time for the CPU baseline")
+    return p.parse_args()
+
+
+def kernel_bytes(ar, kind, bi, step):
+    """Algorithmic HBM bytes one launch must move (reads + writes)."""
+    b = ar.buckets[bi]
+    n = ar.nranks
+    es_t = 4 if ar.dtype == 0 else 2  # tensor element size
+    es_b = 4 if ar.buf_dtype == 0 else 2  # buffer element size
+    data = sum(ar.numel[t] for t in b.tensors)
+    if kind == "pack":
+        return n * (es_t * data + es_b * b.count)
+    if kind == "unpack":
+        return n * (es_b + es_t) * data
+    compressed = b.direct and ar.compress
+    if kind == "rs":
+        if compressed:
+            return (10 if step == 0 else 8) * b.count
+        return 3 * es_b * b.count if not b.direct else 3 * es_t * b.count
+    if kind == "ag":
+        if compressed:
+            first, last = step == 0, step == n - 2
+            per = 2 + 4 + (4 if first else 0) + (0 if last else 2)
+            return per * b.count
+        return 2 * es_b * b.count if not b.direct else 2 * es_t * b.count
+    return 0
+
+
+def kernel_name(ar, kind, bi):
+    b = ar.buckets[bi]
+    if kind in ("rs", "ag"):
+        if b.direct and ar.compress:
+            return f"{kind}_step_c16"
+        return f"{kind}_step_{'f16' if (ar.buf_dtype == 1 and not b.direct) else 'f32'}"
+    return kind
+
+
+def measure(name, steps, warmup):
+    import torch
+
+    import paper_1802_05799_amd as hv
+    from workloads import configs
+    from workloads import gpu as wgpu
+
+    w = configs.get(name)
+    per_rank, storage, starts = wgpu.make_rank_tensors(w)
+    ar = hv.FusedAllreduce(per_rank, op=w.op, compress=w.compress)
+    stream = torch.cuda.current_stream()
+    sid = stream.cuda_stream
+    for _ in range(warmup):
+        ar(sid)
+    torch.cuda.synchronize()
+
+    # timed region: exactly `steps` whole allreduces, one event pair around them
+    t0 = time.perf_counter()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(steps):
+        ar(sid)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = e0.elapsed_time(e1) / steps
+
+    # the same steps once more with an event pair around every kernel launch
+    launches = ar.launches(sid)
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in launches]
+    per_kernel = {}
+    for _ in range(steps):
+        for (kind, bi, s, fn), (a, b) in zip(launches, evs):
+            a.record(stream)
+            fn()
+            b.record(stream)
+        torch.cuda.synchronize()
+        for (kind, bi, s, fn), (a, b) in zip(launches, evs):
+            k = kernel_name(ar, kind, bi)
+            d = per_kernel.setdefault(k, {"launches": 0, "ms": 0.0, "bytes": 0})
+            d["launches"] += 1
+            d["ms"] += a.elapsed_time(b)
+            d["bytes"] += kernel_bytes(ar, kind, bi, s)
+    traced_ms = sum(d["ms"] for d in per_kernel.values()) / steps
+    for d in per_kernel.values():
+        d["avg_us"] = 1000.0 * d["ms"] / d["launches"]
+        d["GBps"] = d["bytes"] / (d["ms"] * 1e-3) / 1e9 if d["ms"] > 0 else None
+        d["hbm_frac"] = d["GBps"] / HBM_PEAK_GBS if d["GBps"] else None
+        d["share"] = d["ms"] / (traced_ms * steps)
+        d["ms_per_step"] = d["ms"] / steps
+        del d["ms"]
+    res = {
+        "workload": name,
+        "nranks": w.nranks,
+        "ms_per_step": ms,
+        "algbw_GBps": w.rank_bytes / (ms * 1e-3) / 1e9,
+        "busbw_GBps": w.rank_bytes / (ms * 1e-3) / 1e9 * 2 * (w.nranks - 1) / w.nranks,
+        "wall_ms_per_step": 1000.0 * wall / steps,
+        "kernels": per_kernel,
+        "buckets": [(b.count, len(b.tensors), b.direct) for b in ar.buckets],
+    }
+    del ar, per_rank, storage
+    torch.cuda.empty_cache()
+    return res
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for f in sorted(os.listdir(os.path.join(ROOT, "paper_1802_05799_amd", "csrc"))):
+        with open(os.path.join(ROOT, "paper_1802_05799_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_for(kernel, workload):
+    """Counter-measured HBM bytes per launch, if recorded for the current kernel sources."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("source_hash") != kernel_source_hash():
+        return None
+    return rec.get("per_launch_bytes", {}).get(f"{workload}/{kernel}")
+
+
+def cpu_baseline(name, target_s):
+    """The oracle (plan, copy-in, ring, copy-out) on a bounded sample of the workload:
+    all N ranks, the last tensors of the ready list (the network's first layers, many
+    small tensors) up to 1.5M elements per rank, repeated until about target_s seconds."""
+    import numpy as np
+
+    from oracle import allreduce as oall
+    from workloads import configs, rng
+
+    w = configs.get(name)
+    numel, prefix = w.numel(), w.prefix()
+    pick, total = [], 0
+    for t in range(len(numel) - 1, -1, -1):
+        if total >= 1_500_000:
+            break
+        pick.append(t)
+        total += numel[t]
+    pick.reverse()
+    inputs = [[rng.values(w.dist, w.key(r), np.arange(prefix[t], prefix[t] + numel[t]), w.sigma) for t in pick]
+              for r in range(w.nranks)]
+    reps, t_oracle = 0, 0.0
+    while t_oracle < target_s:
+        t0 = time.perf_counter()
+        oall.allreduce(inputs, w.op, compress=w.compress)
+        t_oracle += time.perf_counter() - t0
+        reps += 1
+    rank_bytes = 4 * total
+    return {
+        "value": rank_bytes * reps / t_oracle / 1e9,
+        "unit": "GB/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": f"{name}: {len(pick)} tensors ({total} elements per rank, the first layers), "
+        f"{w.nranks} ranks, {reps} runs in {t_oracle:.1f} s, numpy single thread",
+        "host_cpus": os.cpu_count(),
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print(
+            "bench.py runs on one GPU: the N simulated ranks live side by side in that GPU's memory, "
+            "so there is no multi-GPU mode (run with --gpus 1).",
+            file=sys.stderr,
+        )
+        sys.exit(2)
+    import torch
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+
+    head = measure(args.workload, args.steps, args.warmup)
+    print(f"# {args.workload}: {head['ms_per_step']:.3f} ms/step, {head['algbw_GBps']:.1f} GB/s", file=sys.stderr,
+          flush=True)
+    per_config = {}
+    if not args.no_per_config:
+        from workloads import configs
+
+        for name in configs.WORKLOADS:
+            if name == args.workload:
+                r = head
+            else:
+                r = measure(name, max(3, args.steps // 2), 2)
+                print(f"# {name}: {r['ms_per_step']:.3f} ms/step, {r['algbw_GBps']:.1f} GB/s", file=sys.stderr,
+                      flush=True)
+            per_config[name] = {
+                "nranks": r["nranks"],
+                "ms_per_step": round(r["ms_per_step"], 4),
+                "algbw_GBps": round(r["algbw_GBps"], 2),
+                "busbw_GBps": round(r["busbw_GBps"], 2),
+                "kernels": {k: {"avg_us": round(v["avg_us"], 2), "GBps": v["GBps"] and round(v["GBps"], 1),
+                                "hbm_frac": v["hbm_frac"] and round(v["hbm_frac"], 4),
+                                "share": round(v["share"], 4)} for k, v in r["kernels"].items()},
+            }
+
+    dom_name, dom = max(head["kernels"].items(), key=lambda kv: kv[1]["share"])
+    roofline = {
+        "bound": "hbm",
+        "kernel": dom_name,
+        "achieved": round(dom["GBps"], 1),
+        "peak": HBM_PEAK_GBS,
+        "unit": "GB/s",
+        "frac": round(dom["GBps"] / HBM_PEAK_GBS, 4),
+        "traffic": traffic_for(dom_name, args.workload),
+        "avg_launch_us": round(dom["avg_us"], 2),
+        "launches_per_step": dom["launches"] // args.steps,
+        "algorithmic_bytes_per_step": dom["bytes"] // args.steps,
+    }
+    out = {
+        "metric": "allreduce algorithm bandwidth GB/s and % of MI355X HBM peak, per config",
+        "value": round(head["algbw_GBps"], 3),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(head["ms_per_step"], 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16" if head["workload"] == "vgg16fp16" else "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": args.workload,
+            "simulated_ranks": head["nranks"],
+            "op": "average",
+            "fusion_threshold_bytes": 64 << 20,
+            "buckets": head["buckets"],
+        },
+        "busbw_GBps": round(head["busbw_GBps"], 2),
+        "roofline": roofline,
+        "per_config": per_config,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(args.workload, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

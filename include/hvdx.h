@@ -1,0 +1,201 @@
+/*
+ * hvdx -- the data-parallel hot path of Horovod (Sergeev & Del Balso, "Horovod:
+ * fast and easy distributed deep learning in TensorFlow", 2018) for AMD MI355X.
+ *
+ * The library averages N workers' gradient tensors with Tensor Fusion (paper
+ * section 7) and the ring-allreduce (paper section 3).  The N ranks' buffers live
+ * side by side in one GPU's memory and every rank's per-step work runs there; a
+ * ring step is one kernel that performs all N ranks' transfers of that step.
+ *
+ * Conventions for every entry point
+ *   - "device" pointers address GPU memory, "host" pointers CPU memory.  Arrays
+ *     of device pointers are host arrays unless the comment says "device array".
+ *   - The caller owns all memory.  The library allocates and frees nothing.
+ *   - `stream` is a hipStream_t (NULL = the default stream).  Launches are
+ *     asynchronous and ordered on that stream; calls return before the GPU work
+ *     is done.  Faults inside kernels surface at the caller's next stream sync.
+ *   - Arguments are checked before anything is launched.  A negative return
+ *     value is an error code (HVDX_ERR_*); nothing has been enqueued then.
+ *     hvdx_last_error() gives a message for the calling thread's last error.
+ *   - Entry points keep no state between calls; concurrent calls on different
+ *     streams are safe when they touch disjoint memory.
+ */
+#ifndef HVDX_H
+#define HVDX_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define HVDX_VERSION 1
+
+/* element types */
+#define HVDX_FLOAT32 0
+#define HVDX_FLOAT16 1
+
+/* reduction: SUM, or AVERAGE = SUM divided by nranks (paper section 3, the
+ * data-parallel recipe's "average gradients" step; section 5, the optimizer
+ * wrapper that averages gradients) */
+#define HVDX_SUM 0
+#define HVDX_AVERAGE 1
+
+/* compression of the values that travel around the ring */
+#define HVDX_COMPRESS_NONE 0
+#define HVDX_COMPRESS_FP16 1
+
+/* status codes */
+#define HVDX_OK 0
+#define HVDX_ERR_INVALID (-1)     /* null pointer, bad size, bad enum value */
+#define HVDX_ERR_ALIAS (-2)       /* rank buffers or workspace overlap */
+#define HVDX_ERR_WORKSPACE (-3)   /* workspace missing or too small */
+#define HVDX_ERR_HIP (-4)         /* a HIP call failed; see hvdx_last_error() */
+#define HVDX_ERR_UNSUPPORTED (-5) /* valid request this build does not handle */
+
+#define HVDX_MAX_RANKS 128                          /* simulated ranks per call */
+#define HVDX_DEFAULT_FUSION_THRESHOLD (64LL << 20)  /* bytes (paper section 7: 64 MB) */
+#define HVDX_DEFAULT_FUSION_ALIGN 16                /* bytes */
+
+/* ring phases for hvdx_ring_step */
+#define HVDX_PHASE_REDUCE_SCATTER 0
+#define HVDX_PHASE_ALLGATHER 1
+
+/*
+ * hvdx_fuse_plan -- group tensors into fusion buffers (paper section 7, steps 1,
+ * 2 and 6: take the first ready tensors that fit in the buffer, repeat until all
+ * are reduced).  Host only; touches no GPU state.
+ *
+ *   numel[ntensors]        host, elements of each tensor in ready order (>= 0)
+ *   buf_dtype              HVDX_FLOAT32 or HVDX_FLOAT16: element type of the
+ *                          buffer; sizes are counted in its bytes
+ *   threshold_bytes        buffer capacity (>= 0); HVDX_DEFAULT_FUSION_THRESHOLD
+ *   align_bytes            each tensor starts at a multiple of this many bytes;
+ *                          a power of two, at least the element size
+ *   bucket_of[ntensors]    out, host: buffer index of each tensor
+ *   offset[ntensors]       out, host: element offset of each tensor in its buffer
+ *   bucket_count[ntensors] out, host: element count of each buffer (only the
+ *                          first *nbuckets entries are written)
+ *   bucket_direct[ntensors] out, host: 1 if the buffer is a single tensor larger
+ *                          than threshold_bytes, reduced in place without a copy
+ *   nbuckets               out, host: number of buffers
+ *
+ * Buffers take a contiguous run of the list; a tensor fits while the aligned
+ * end of the run stays <= threshold_bytes (equality fits).  Gaps before aligned
+ * offsets are padding.  A buffer's count is the end of its last tensor.
+ * Errors: HVDX_ERR_INVALID for a null pointer, ntensors < 0, a negative numel,
+ * an unknown dtype, or a bad threshold/alignment.
+ */
+int hvdx_fuse_plan(const int64_t* numel, int ntensors, int buf_dtype, int64_t threshold_bytes,
+                   int64_t align_bytes, int32_t* bucket_of, int64_t* offset, int64_t* bucket_count,
+                   int32_t* bucket_direct, int32_t* nbuckets);
+
+/*
+ * hvdx_fuse_pack -- copy every rank's tensors into its fusion buffer (paper
+ * section 7, step 3), one launch for all ranks and tensors.  Padding positions are
+ * written with zero.  With src_dtype FLOAT32 and buf_dtype FLOAT16 each value is
+ * rounded to nearest even (gradual underflow, overflow to infinity); FLOAT16 to
+ * FLOAT32 is exact.
+ *
+ *   srcs[nranks*ntensors]  DEVICE array of device pointers, rank-major
+ *                          (entry r*ntensors + t is rank r's tensor t), each
+ *                          numel[t] elements of src_dtype
+ *   numel[ntensors]        DEVICE array of int64, elements per tensor
+ *   offset[ntensors]       DEVICE array of int64, element offsets in the buffer,
+ *                          ascending, with offset[t] + numel[t] <= offset[t+1]
+ *                          and <= buf_count (as produced by hvdx_fuse_plan)
+ *   bufs[nranks]           host array of device pointers, each buf_count
+ *                          elements of buf_dtype; must not overlap
+ *   nranks                 1 .. HVDX_MAX_RANKS
+ *
+ * Every buffer element [0, buf_count) is written exactly once; tensor t of rank
+ * r is read only at [0, numel[t]).  Descriptor contents are the caller's
+ * responsibility (they are device data and are not checked).
+ * Errors: HVDX_ERR_INVALID (null pointers, sizes, dtypes), HVDX_ERR_ALIAS
+ * (overlapping buffers), HVDX_ERR_HIP (launch failure).
+ */
+int hvdx_fuse_pack(const void* const* srcs, const int64_t* numel, const int64_t* offset, int ntensors,
+                   int src_dtype, void* const* bufs, int64_t buf_count, int buf_dtype, int nranks,
+                   void* stream);
+
+/*
+ * hvdx_fuse_unpack -- copy every rank's reduced buffer out to its tensors (paper
+ * section 7, step 5), one launch for all ranks and tensors.  Padding is not
+ * copied.  Conversions as in hvdx_fuse_pack.
+ *
+ *   bufs[nranks]           host array of device pointers (buf_count of buf_dtype)
+ *   dsts[nranks*ntensors]  DEVICE array of device pointers, rank-major, each
+ *                          numel[t] elements of dst_dtype; written only at
+ *                          [0, numel[t])
+ *   numel, offset          DEVICE arrays as for hvdx_fuse_pack
+ * Errors: as hvdx_fuse_pack.
+ */
+int hvdx_fuse_unpack(const void* const* bufs, int64_t buf_count, int buf_dtype, void* const* dsts,
+                     const int64_t* numel, const int64_t* offset, int ntensors, int dst_dtype, int nranks,
+                     void* stream);
+
+/*
+ * hvdx_ring_allreduce -- the ring-allreduce of paper section 3: N-1 steps in which
+ * every rank adds the chunk received from its left neighbour into its own buffer,
+ * then N-1 steps in which the received chunk replaces its own.  In place on all
+ * nranks buffers; afterwards every buffer holds the same result.
+ *
+ *   bufs[nranks]     host array of device pointers, each count elements of
+ *                    dtype, pairwise non-overlapping
+ *   count            elements per rank buffer (>= 0; 0 is a no-op)
+ *   dtype            HVDX_FLOAT32 or HVDX_FLOAT16
+ *   op               HVDX_SUM or HVDX_AVERAGE
+ *   compress         HVDX_COMPRESS_NONE, or HVDX_COMPRESS_FP16 (dtype FLOAT32
+ *                    only): values are rounded to binary16 when first sent,
+ *                    added and averaged in binary16, and widened back into the
+ *                    binary32 buffers by the replacing steps
+ *   workspace        device memory of at least hvdx_ring_workspace_bytes(...)
+ *                    bytes, 256-byte aligned, disjoint from bufs; only used with
+ *                    compression (may be NULL otherwise); contents afterwards
+ *                    are unspecified
+ *
+ * Schedule: chunk c (of N near-equal contiguous chunks, the first count mod N
+ * one element longer) moves from rank (c+s) mod N to (c+s+1) mod N in adding
+ * step s and from rank (c-1+s) mod N to (c+s) mod N in replacing step s, so the
+ * sum of chunk c is formed in ring order starting at rank c.  Each addition is
+ * rounded to nearest even in dtype (binary16 when compressed); AVERAGE divides
+ * the complete sum by nranks once, correctly rounded, at the last adding step.
+ * Errors: HVDX_ERR_INVALID, HVDX_ERR_ALIAS, HVDX_ERR_WORKSPACE, HVDX_ERR_HIP.
+ */
+int hvdx_ring_allreduce(void* const* bufs, int nranks, int64_t count, int dtype, int op, int compress,
+                        void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * hvdx_ring_step -- one step of hvdx_ring_allreduce (all N transfers of adding or
+ * replacing step `step`, 0 <= step < nranks-1), for tracing and for checking
+ * intermediate states.  Running phase REDUCE_SCATTER steps 0..N-2 then
+ * ALLGATHER steps 0..N-2 in order, with the same arguments and workspace, is
+ * hvdx_ring_allreduce for nranks >= 2.  Arguments as hvdx_ring_allreduce.
+ */
+int hvdx_ring_step(void* const* bufs, int nranks, int64_t count, int dtype, int op, int compress, int phase,
+                   int step, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Workspace bytes hvdx_ring_allreduce needs: 0 unless compressing binary32 data,
+ * then nranks * (count rounded up to 128) * 2.  Host only. */
+size_t hvdx_ring_workspace_bytes(int nranks, int64_t count, int dtype, int compress);
+
+/* Chunk c of the ring partition of `count` elements over `nranks` ranks:
+ * start = c*q + min(c, r), len = q + (c < r) with q, r = count / nranks,
+ * count % nranks.  Host only.  HVDX_ERR_INVALID for bad arguments. */
+int hvdx_ring_chunk(int64_t count, int nranks, int c, int64_t* start, int64_t* len);
+
+/* Text for a status code (static storage). */
+const char* hvdx_strerror(int status);
+
+/* Detail of the calling thread's last failed call ("" if none). */
+const char* hvdx_last_error(void);
+
+/* HVDX_VERSION of the built library. */
+int hvdx_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HVDX_H */

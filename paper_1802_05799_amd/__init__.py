@@ -1,0 +1,49 @@
+"""hvdx: Horovod's data-parallel hot path (Tensor Fusion + ring-allreduce) on MI355X.
+
+Python binding of libhvdx.so.  torch is imported first so that the library binds
+to the HIP runtime torch already loaded (one runtime per process).
+
+    from paper_1802_05799_amd import FusedAllreduce
+    ar = FusedAllreduce(per_rank_grads, op="average")   # plan + buffers, once
+    ar()                                                  # reduce in place
+"""
+import torch  # noqa: F401  (must precede the library load)
+
+from ._lib import (  # noqa: F401
+    AVERAGE,
+    COMPRESS_FP16,
+    COMPRESS_NONE,
+    DEFAULT_FUSION_ALIGN,
+    DEFAULT_FUSION_THRESHOLD,
+    ERR_ALIAS,
+    ERR_HIP,
+    ERR_INVALID,
+    ERR_UNSUPPORTED,
+    ERR_WORKSPACE,
+    FLOAT16,
+    FLOAT32,
+    LIB_PATH,
+    MAX_RANKS,
+    OK,
+    PHASE_ALLGATHER,
+    PHASE_REDUCE_SCATTER,
+    SUM,
+    HvdxError,
+    hvdx_fuse_pack,
+    hvdx_fuse_plan,
+    hvdx_fuse_unpack,
+    hvdx_last_error,
+    hvdx_ring_allreduce,
+    hvdx_ring_chunk,
+    hvdx_ring_step,
+    hvdx_ring_workspace_bytes,
+    hvdx_strerror,
+    hvdx_version,
+)
+from .cycle import FusedAllreduce  # noqa: F401
+
+
+def allreduce_(per_rank, op: str = "average", compress: bool = False,
+               threshold_bytes: int = DEFAULT_FUSION_THRESHOLD, align_bytes: int = DEFAULT_FUSION_ALIGN) -> None:
+    """One in-place allreduce of every rank's tensor list (builds a one-off plan)."""
+    FusedAllreduce(per_rank, op, compress, threshold_bytes, align_bytes)()

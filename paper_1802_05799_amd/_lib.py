@@ -1,0 +1,139 @@
+"""ctypes binding of libhvdx.so: one Python function per C entry point, same names.
+
+Only argument marshalling happens here; every step of the path runs in the HIP
+kernels behind the C-ABI.  A missing library raises at import: there is no
+fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libhvdx.so")
+
+FLOAT32, FLOAT16 = 0, 1
+SUM, AVERAGE = 0, 1
+COMPRESS_NONE, COMPRESS_FP16 = 0, 1
+PHASE_REDUCE_SCATTER, PHASE_ALLGATHER = 0, 1
+OK, ERR_INVALID, ERR_ALIAS, ERR_WORKSPACE, ERR_HIP, ERR_UNSUPPORTED = 0, -1, -2, -3, -4, -5
+MAX_RANKS = 128
+DEFAULT_FUSION_THRESHOLD = 64 << 20
+DEFAULT_FUSION_ALIGN = 16
+
+_p = ctypes.c_void_p
+_i = ctypes.c_int
+_i64 = ctypes.c_int64
+_sz = ctypes.c_size_t
+_pp = ctypes.POINTER(ctypes.c_void_p)
+_pi64 = ctypes.POINTER(ctypes.c_int64)
+_pi32 = ctypes.POINTER(ctypes.c_int32)
+
+_SIGNATURES = {
+    "hvdx_fuse_plan": (_i, [_pi64, _i, _i, _i64, _i64, _pi32, _pi64, _pi64, _pi32, _pi32]),
+    "hvdx_fuse_pack": (_i, [_p, _p, _p, _i, _i, _pp, _i64, _i, _i, _p]),
+    "hvdx_fuse_unpack": (_i, [_pp, _i64, _i, _p, _p, _p, _i, _i, _i, _p]),
+    "hvdx_ring_allreduce": (_i, [_pp, _i, _i64, _i, _i, _i, _p, _sz, _p]),
+    "hvdx_ring_step": (_i, [_pp, _i, _i64, _i, _i, _i, _i, _i, _p, _sz, _p]),
+    "hvdx_ring_workspace_bytes": (_sz, [_i, _i64, _i, _i]),
+    "hvdx_ring_chunk": (_i, [_i64, _i, _i, _pi64, _pi64]),
+    "hvdx_strerror": (ctypes.c_char_p, [_i]),
+    "hvdx_last_error": (ctypes.c_char_p, []),
+    "hvdx_version": (_i, []),
+}
+
+
+class HvdxError(RuntimeError):
+    def __init__(self, status: int, detail: str):
+        super().__init__(f"hvdx status {status}: {detail}")
+        self.status = status
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_1802_05799_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    for name, (res, args) in _SIGNATURES.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    return lib
+
+
+lib = _load()
+
+
+def _check(status: int) -> None:
+    if status != OK:
+        detail = lib.hvdx_last_error().decode() or lib.hvdx_strerror(status).decode()
+        raise HvdxError(status, detail)
+
+
+def _ptr_array(ptrs):
+    arr = (ctypes.c_void_p * max(1, len(ptrs)))(*[int(p) for p in ptrs])
+    return ctypes.cast(arr, _pp), arr
+
+
+def hvdx_version() -> int:
+    return lib.hvdx_version()
+
+
+def hvdx_strerror(status: int) -> str:
+    return lib.hvdx_strerror(status).decode()
+
+
+def hvdx_last_error() -> str:
+    return lib.hvdx_last_error().decode()
+
+
+def hvdx_ring_chunk(count: int, nranks: int, c: int):
+    start, length = ctypes.c_int64(), ctypes.c_int64()
+    _check(lib.hvdx_ring_chunk(count, nranks, c, ctypes.byref(start), ctypes.byref(length)))
+    return start.value, length.value
+
+
+def hvdx_ring_workspace_bytes(nranks: int, count: int, dtype: int, compress: int) -> int:
+    return lib.hvdx_ring_workspace_bytes(nranks, count, dtype, compress)
+
+
+def hvdx_fuse_plan(numel, buf_dtype: int, threshold_bytes: int = DEFAULT_FUSION_THRESHOLD,
+                   align_bytes: int = DEFAULT_FUSION_ALIGN):
+    """Return (bucket_of, offset, bucket_count, bucket_direct) as Python lists."""
+    n = len(numel)
+    a_numel = (ctypes.c_int64 * max(1, n))(*numel)
+    bucket_of = (ctypes.c_int32 * max(1, n))()
+    offset = (ctypes.c_int64 * max(1, n))()
+    count = (ctypes.c_int64 * max(1, n))()
+    direct = (ctypes.c_int32 * max(1, n))()
+    nb = ctypes.c_int32()
+    _check(lib.hvdx_fuse_plan(a_numel, n, buf_dtype, threshold_bytes, align_bytes, bucket_of, offset, count,
+                              direct, ctypes.byref(nb)))
+    k = nb.value
+    return list(bucket_of[:n]), list(offset[:n]), list(count[:k]), list(direct[:k])
+
+
+def hvdx_fuse_pack(srcs_dev: int, numel_dev: int, offset_dev: int, ntensors: int, src_dtype: int, bufs,
+                   buf_count: int, buf_dtype: int, nranks: int, stream: int = 0) -> None:
+    pb, _keep = _ptr_array(bufs)
+    _check(lib.hvdx_fuse_pack(srcs_dev, numel_dev, offset_dev, ntensors, src_dtype, pb, buf_count, buf_dtype,
+                              nranks, stream))
+
+
+def hvdx_fuse_unpack(bufs, buf_count: int, buf_dtype: int, dsts_dev: int, numel_dev: int, offset_dev: int,
+                     ntensors: int, dst_dtype: int, nranks: int, stream: int = 0) -> None:
+    pb, _keep = _ptr_array(bufs)
+    _check(lib.hvdx_fuse_unpack(pb, buf_count, buf_dtype, dsts_dev, numel_dev, offset_dev, ntensors, dst_dtype,
+                                nranks, stream))
+
+
+def hvdx_ring_allreduce(bufs, nranks: int, count: int, dtype: int, op: int, compress: int = COMPRESS_NONE,
+                        workspace: int = 0, workspace_bytes: int = 0, stream: int = 0) -> None:
+    pb, _keep = _ptr_array(bufs)
+    _check(lib.hvdx_ring_allreduce(pb, nranks, count, dtype, op, compress, workspace, workspace_bytes, stream))
+
+
+def hvdx_ring_step(bufs, nranks: int, count: int, dtype: int, op: int, compress: int, phase: int, step: int,
+                   workspace: int = 0, workspace_bytes: int = 0, stream: int = 0) -> None:
+    pb, _keep = _ptr_array(bufs)
+    _check(lib.hvdx_ring_step(pb, nranks, count, dtype, op, compress, phase, step, workspace, workspace_bytes,
+                              stream))

@@ -1,0 +1,313 @@
+// C-ABI of libhvdx: argument checks, the Tensor Fusion plan (host), and the ring
+// step sequence.  Every check runs before the first HIP call, so invalid requests
+// return an error without touching the GPU.
+
+#include <stdarg.h>
+#include <stdio.h>
+
+#include <algorithm>
+#include <utility>
+#include <vector>
+
+#include "internal.hpp"
+
+namespace {
+
+thread_local char g_last_error[512] = "";
+
+int fail(int code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_last_error, sizeof g_last_error, fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(HVDX_ERR_HIP, "%s: %s (%s)", what, hipGetErrorName(e), hipGetErrorString(e));
+}
+
+int elem_size(int dtype) {
+  switch (dtype) {
+    case HVDX_FLOAT32: return 4;
+    case HVDX_FLOAT16: return 2;
+    default: return 0;
+  }
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+// Pairwise disjointness of [base, base + bytes) over all ranges (sorted sweep).
+bool overlapping(std::vector<std::pair<uintptr_t, uintptr_t>> ranges) {
+  std::sort(ranges.begin(), ranges.end());
+  for (size_t i = 1; i < ranges.size(); ++i)
+    if (ranges[i].first < ranges[i - 1].second) return true;
+  return false;
+}
+
+int check_rank_buffers(void* const* bufs, int nranks, int64_t count, int esize, const char* what) {
+  if (!bufs) return fail(HVDX_ERR_INVALID, "%s: rank pointer array is NULL", what);
+  if (nranks < 1 || nranks > HVDX_MAX_RANKS)
+    return fail(HVDX_ERR_INVALID, "%s: nranks=%d outside 1..%d", what, nranks, HVDX_MAX_RANKS);
+  if (count < 0) return fail(HVDX_ERR_INVALID, "%s: negative element count %lld", what, (long long)count);
+  for (int r = 0; r < nranks; ++r) {
+    if (!bufs[r] && count > 0) return fail(HVDX_ERR_INVALID, "%s: buffer of rank %d is NULL", what, r);
+    if (reinterpret_cast<uintptr_t>(bufs[r]) % esize)
+      return fail(HVDX_ERR_INVALID, "%s: buffer of rank %d is not aligned to its element size", what, r);
+  }
+  if (count > 0) {
+    std::vector<std::pair<uintptr_t, uintptr_t>> rg;
+    for (int r = 0; r < nranks; ++r) {
+      const uintptr_t b = reinterpret_cast<uintptr_t>(bufs[r]);
+      rg.emplace_back(b, b + (uintptr_t)count * esize);
+    }
+    if (overlapping(rg)) return fail(HVDX_ERR_ALIAS, "%s: rank buffers overlap", what);
+  }
+  return HVDX_OK;
+}
+
+hvdx::RankPtrs rank_ptrs(void* const* bufs, int nranks) {
+  hvdx::RankPtrs p{};
+  for (int r = 0; r < nranks; ++r) p.p[r] = bufs[r];
+  return p;
+}
+
+int64_t wire_stride(int64_t count) { return (count + 127) / 128 * 128; }
+
+// Arguments shared by hvdx_ring_allreduce and hvdx_ring_step.
+int check_ring(void* const* bufs, int nranks, int64_t count, int dtype, int op, int compress, void* workspace,
+               size_t workspace_bytes, const char* what) {
+  const int es = elem_size(dtype);
+  if (!es) return fail(HVDX_ERR_INVALID, "%s: unknown dtype %d", what, dtype);
+  if (op != HVDX_SUM && op != HVDX_AVERAGE) return fail(HVDX_ERR_INVALID, "%s: unknown op %d", what, op);
+  if (compress != HVDX_COMPRESS_NONE && compress != HVDX_COMPRESS_FP16)
+    return fail(HVDX_ERR_INVALID, "%s: unknown compression %d", what, compress);
+  if (compress == HVDX_COMPRESS_FP16 && dtype != HVDX_FLOAT32)
+    return fail(HVDX_ERR_INVALID, "%s: fp16 compression needs float32 buffers", what);
+  int rc = check_rank_buffers(bufs, nranks, count, es, what);
+  if (rc) return rc;
+  if (compress == HVDX_COMPRESS_FP16 && nranks > 1 && count > 0) {
+    const size_t need = hvdx_ring_workspace_bytes(nranks, count, dtype, compress);
+    if (!workspace || workspace_bytes < need)
+      return fail(HVDX_ERR_WORKSPACE, "%s: workspace of %zu bytes given, %zu needed", what,
+                  workspace ? workspace_bytes : (size_t)0, need);
+    if (reinterpret_cast<uintptr_t>(workspace) & 255)
+      return fail(HVDX_ERR_WORKSPACE, "%s: workspace is not 256-byte aligned", what);
+    std::vector<std::pair<uintptr_t, uintptr_t>> rg;
+    const uintptr_t w = reinterpret_cast<uintptr_t>(workspace);
+    rg.emplace_back(w, w + need);
+    for (int r = 0; r < nranks; ++r) {
+      const uintptr_t b = reinterpret_cast<uintptr_t>(bufs[r]);
+      rg.emplace_back(b, b + (uintptr_t)count * es);
+    }
+    if (overlapping(rg)) return fail(HVDX_ERR_ALIAS, "%s: workspace overlaps a rank buffer", what);
+  }
+  return HVDX_OK;
+}
+
+hvdx::RingArgs ring_args(int nranks, int64_t count, int step) {
+  hvdx::RingArgs a{};
+  a.n = nranks;
+  a.step = step;
+  a.q = count / nranks;
+  a.rem = count % nranks;
+  a.nf = (float)nranks;
+  a.inv = 1.0f / (float)nranks;
+  a.wire_stride = wire_stride(count);
+  return a;
+}
+
+int div_mode(int op, int nranks) {
+  if (op != HVDX_AVERAGE || nranks == 1) return hvdx::DIV_NONE;
+  return (nranks & (nranks - 1)) == 0 ? hvdx::DIV_POW2 : hvdx::DIV_TRUE;
+}
+
+bool vectors_ok(void* const* bufs, int nranks, const void* workspace) {
+  for (int r = 0; r < nranks; ++r)
+    if (!aligned16(bufs[r])) return false;
+  return aligned16(workspace);
+}
+
+// One step, arguments already checked, nranks >= 2, count > 0.
+int run_step(void* const* bufs, int nranks, int64_t count, int dtype, int op, int compress, int phase, int step,
+             void* workspace, hipStream_t st) {
+  const hvdx::RingArgs a = ring_args(nranks, count, step);
+  const hvdx::RankPtrs p = rank_ptrs(bufs, nranks);
+  const bool vok = vectors_ok(bufs, nranks, workspace);
+  const int dm = step == nranks - 2 ? div_mode(op, nranks) : hvdx::DIV_NONE;
+  hipError_t e;
+  if (compress == HVDX_COMPRESS_FP16) {
+    e = phase == HVDX_PHASE_REDUCE_SCATTER ? hvdx::launch_rs_step_c16(p, workspace, a, dm, vok, st)
+                                           : hvdx::launch_ag_step_c16(p, workspace, a, vok, st);
+  } else {
+    e = phase == HVDX_PHASE_REDUCE_SCATTER ? hvdx::launch_rs_step(p, a, dtype, dm, vok, st)
+                                           : hvdx::launch_ag_step(p, a, dtype, vok, st);
+  }
+  if (e != hipSuccess)
+    return hip_fail(e, phase == HVDX_PHASE_REDUCE_SCATTER ? "reduce-scatter step launch" : "allgather step launch");
+  return HVDX_OK;
+}
+
+int check_fusion(const void* const* tensors, const int64_t* numel, const int64_t* offset, int ntensors,
+                 int tensor_dtype, const void* const* bufs, int64_t buf_count, int buf_dtype, int nranks,
+                 const char* what) {
+  if (ntensors < 0) return fail(HVDX_ERR_INVALID, "%s: negative tensor count", what);
+  if (ntensors > 0 && (!tensors || !numel || !offset))
+    return fail(HVDX_ERR_INVALID, "%s: a descriptor array is NULL", what);
+  const int es = elem_size(buf_dtype);
+  if (!es || !elem_size(tensor_dtype)) return fail(HVDX_ERR_INVALID, "%s: unknown dtype", what);
+  if (tensor_dtype == HVDX_FLOAT16 && buf_dtype == HVDX_FLOAT32)
+    return fail(HVDX_ERR_UNSUPPORTED, "%s: float16 tensors with a float32 buffer", what);
+  int rc = check_rank_buffers(const_cast<void* const*>(bufs), nranks, buf_count, es, what);
+  if (rc) return rc;
+  for (int r = 0; r < nranks; ++r)
+    if (buf_count > 0 && !aligned16(bufs[r]))
+      return fail(HVDX_ERR_INVALID, "%s: fusion buffer of rank %d is not 16-byte aligned", what, r);
+  return HVDX_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int hvdx_version(void) { return HVDX_VERSION; }
+
+const char* hvdx_last_error(void) { return g_last_error; }
+
+const char* hvdx_strerror(int status) {
+  switch (status) {
+    case HVDX_OK: return "success";
+    case HVDX_ERR_INVALID: return "invalid argument";
+    case HVDX_ERR_ALIAS: return "overlapping buffers";
+    case HVDX_ERR_WORKSPACE: return "workspace missing or too small";
+    case HVDX_ERR_HIP: return "HIP runtime error";
+    case HVDX_ERR_UNSUPPORTED: return "unsupported combination";
+    default: return "unknown status";
+  }
+}
+
+int hvdx_ring_chunk(int64_t count, int nranks, int c, int64_t* start, int64_t* len) {
+  if (count < 0 || nranks < 1 || c < 0 || c >= nranks || !start || !len)
+    return fail(HVDX_ERR_INVALID, "hvdx_ring_chunk: bad arguments");
+  const int64_t q = count / nranks, r = count % nranks;
+  *start = (int64_t)c * q + std::min<int64_t>(c, r);
+  *len = q + (c < r ? 1 : 0);
+  return HVDX_OK;
+}
+
+size_t hvdx_ring_workspace_bytes(int nranks, int64_t count, int dtype, int compress) {
+  if (compress != HVDX_COMPRESS_FP16 || dtype != HVDX_FLOAT32 || nranks < 2 || count <= 0) return 0;
+  return (size_t)nranks * (size_t)wire_stride(count) * 2;
+}
+
+int hvdx_fuse_plan(const int64_t* numel, int ntensors, int buf_dtype, int64_t threshold_bytes, int64_t align_bytes,
+                   int32_t* bucket_of, int64_t* offset, int64_t* bucket_count, int32_t* bucket_direct,
+                   int32_t* nbuckets) {
+  const char* what = "hvdx_fuse_plan";
+  if (ntensors < 0) return fail(HVDX_ERR_INVALID, "%s: negative tensor count", what);
+  if (!nbuckets || (ntensors > 0 && (!numel || !bucket_of || !offset || !bucket_count || !bucket_direct)))
+    return fail(HVDX_ERR_INVALID, "%s: NULL array", what);
+  const int64_t es = elem_size(buf_dtype);
+  if (!es) return fail(HVDX_ERR_INVALID, "%s: unknown dtype %d", what, buf_dtype);
+  if (threshold_bytes < 0) return fail(HVDX_ERR_INVALID, "%s: negative threshold", what);
+  if (align_bytes < es || (align_bytes & (align_bytes - 1)))
+    return fail(HVDX_ERR_INVALID, "%s: alignment %lld is not a power of two >= the element size", what,
+                (long long)align_bytes);
+  for (int t = 0; t < ntensors; ++t)
+    if (numel[t] < 0 || numel[t] > (INT64_MAX / 4) / es)
+      return fail(HVDX_ERR_INVALID, "%s: bad element count for tensor %d", what, t);
+
+  // Walk the ready list once.  `open` is the buffer being filled, `used` its length in
+  // elements; a tensor joins it when its aligned start plus its bytes stay within the
+  // threshold, else the buffer is closed and the tensor starts a new one.  A tensor
+  // larger than the threshold closes the open buffer and forms a direct one.
+  int nb = 0;
+  int open = -1;
+  int64_t used = 0;
+  for (int t = 0; t < ntensors; ++t) {
+    const int64_t bytes = numel[t] * es;
+    if (bytes > threshold_bytes) {
+      open = -1;
+      bucket_of[t] = nb;
+      offset[t] = 0;
+      bucket_count[nb] = numel[t];
+      bucket_direct[nb] = 1;
+      ++nb;
+      continue;
+    }
+    int64_t start_bytes = 0;
+    if (open >= 0) {
+      start_bytes = (used * es + align_bytes - 1) / align_bytes * align_bytes;
+      if (start_bytes + bytes > threshold_bytes) open = -1;
+    }
+    if (open < 0) {
+      open = nb++;
+      bucket_direct[open] = 0;
+      start_bytes = 0;
+    }
+    bucket_of[t] = open;
+    offset[t] = start_bytes / es;
+    used = offset[t] + numel[t];
+    bucket_count[open] = used;
+  }
+  *nbuckets = nb;
+  return HVDX_OK;
+}
+
+int hvdx_fuse_pack(const void* const* srcs, const int64_t* numel, const int64_t* offset, int ntensors, int src_dtype,
+                   void* const* bufs, int64_t buf_count, int buf_dtype, int nranks, void* stream) {
+  int rc = check_fusion(srcs, numel, offset, ntensors, src_dtype, bufs, buf_count, buf_dtype, nranks,
+                        "hvdx_fuse_pack");
+  if (rc) return rc;
+  if (buf_count == 0) return HVDX_OK;
+  const hipError_t e = hvdx::launch_pack(srcs, numel, offset, ntensors, src_dtype, rank_ptrs(bufs, nranks),
+                                         buf_count, buf_dtype, nranks, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? HVDX_OK : hip_fail(e, "pack launch");
+}
+
+int hvdx_fuse_unpack(const void* const* bufs, int64_t buf_count, int buf_dtype, void* const* dsts,
+                     const int64_t* numel, const int64_t* offset, int ntensors, int dst_dtype, int nranks,
+                     void* stream) {
+  int rc = check_fusion(dsts, numel, offset, ntensors, dst_dtype, bufs, buf_count, buf_dtype, nranks,
+                        "hvdx_fuse_unpack");
+  if (rc) return rc;
+  if (buf_count == 0) return HVDX_OK;
+  const hipError_t e =
+      hvdx::launch_unpack(rank_ptrs(const_cast<void* const*>(bufs), nranks), buf_count, buf_dtype, dsts, numel,
+                          offset, ntensors, dst_dtype, nranks, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? HVDX_OK : hip_fail(e, "unpack launch");
+}
+
+int hvdx_ring_step(void* const* bufs, int nranks, int64_t count, int dtype, int op, int compress, int phase,
+                   int step, void* workspace, size_t workspace_bytes, void* stream) {
+  int rc = check_ring(bufs, nranks, count, dtype, op, compress, workspace, workspace_bytes, "hvdx_ring_step");
+  if (rc) return rc;
+  if (phase != HVDX_PHASE_REDUCE_SCATTER && phase != HVDX_PHASE_ALLGATHER)
+    return fail(HVDX_ERR_INVALID, "hvdx_ring_step: unknown phase %d", phase);
+  if (step < 0 || step > nranks - 2)
+    return fail(HVDX_ERR_INVALID, "hvdx_ring_step: step %d outside 0..%d", step, nranks - 2);
+  if (count == 0) return HVDX_OK;
+  return run_step(bufs, nranks, count, dtype, op, compress, phase, step, workspace,
+                  static_cast<hipStream_t>(stream));
+}
+
+int hvdx_ring_allreduce(void* const* bufs, int nranks, int64_t count, int dtype, int op, int compress,
+                        void* workspace, size_t workspace_bytes, void* stream) {
+  int rc = check_ring(bufs, nranks, count, dtype, op, compress, workspace, workspace_bytes, "hvdx_ring_allreduce");
+  if (rc) return rc;
+  if (count == 0) return HVDX_OK;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (nranks == 1) {  // no messages; AVERAGE divides by 1; compression still rounds
+    if (compress != HVDX_COMPRESS_FP16) return HVDX_OK;
+    const hipError_t e = hvdx::launch_roundtrip_c16(bufs[0], count, st);
+    return e == hipSuccess ? HVDX_OK : hip_fail(e, "fp16 round-trip launch");
+  }
+  for (int phase = HVDX_PHASE_REDUCE_SCATTER; phase <= HVDX_PHASE_ALLGATHER; ++phase)
+    for (int s = 0; s < nranks - 1; ++s) {
+      rc = run_step(bufs, nranks, count, dtype, op, compress, phase, s, workspace, st);
+      if (rc) return rc;
+    }
+  return HVDX_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,50 @@
+// Internal declarations shared by the library's translation units (not installed).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "hvdx.h"
+
+namespace hvdx {
+
+// Every rank's base pointer travels in the kernel arguments (1 KiB).
+struct RankPtrs {
+  void* p[HVDX_MAX_RANKS];
+};
+
+// Ring partition and step, identical for every block of one launch.
+struct RingArgs {
+  int n;          // ranks
+  int step;       // 0 .. n-2
+  int64_t q;      // count / n
+  int64_t rem;    // count % n
+  float nf;       // (float) n
+  float inv;      // 1 / n, used only when n is a power of two
+  int64_t wire_stride;  // elements per rank in the fp16 wire workspace
+};
+
+// How the last adding step finishes an AVERAGE.
+enum DivMode { DIV_NONE = 0, DIV_POW2 = 1, DIV_TRUE = 2 };
+
+constexpr int kBlock = 256;
+
+// Launchers (ring_kernels.hip).  Arguments are already validated; return a hipError_t.
+hipError_t launch_rs_step(const RankPtrs& bufs, const RingArgs& a, int dtype, int divmode, bool vector_ok,
+                          hipStream_t stream);
+hipError_t launch_ag_step(const RankPtrs& bufs, const RingArgs& a, int dtype, bool vector_ok, hipStream_t stream);
+hipError_t launch_rs_step_c16(const RankPtrs& x, void* wire, const RingArgs& a, int divmode, bool vector_ok,
+                              hipStream_t stream);
+hipError_t launch_ag_step_c16(const RankPtrs& x, void* wire, const RingArgs& a, bool vector_ok, hipStream_t stream);
+hipError_t launch_roundtrip_c16(void* x, int64_t count, hipStream_t stream);
+
+// Launchers (fusion_kernels.hip).
+hipError_t launch_pack(const void* const* srcs, const int64_t* numel, const int64_t* offset, int ntensors,
+                       int src_dtype, const RankPtrs& bufs, int64_t count, int buf_dtype, int nranks,
+                       hipStream_t stream);
+hipError_t launch_unpack(const RankPtrs& bufs, int64_t count, int buf_dtype, void* const* dsts,
+                         const int64_t* numel, const int64_t* offset, int ntensors, int dst_dtype, int nranks,
+                         hipStream_t stream);
+
+}  // namespace hvdx

@@ -1,0 +1,147 @@
+"""The Tensor Fusion cycle over N simulated ranks (paper section 7, steps 1-6).
+
+`FusedAllreduce` is built once for a fixed set of gradient tensors (one list per
+simulated rank, all in GPU memory) and then reduces them in place each time it is
+called: for every fusion buffer of the plan, copy in (pack), ring-allreduce, copy
+out (unpack); a tensor larger than the buffer runs the ring in place on the rank
+tensors themselves.  Torch provides the device memory and the stream; every step
+is a libhvdx kernel.
+
+The fusion buffers are allocated once, at the size of the largest fused bucket
+(at most the threshold, 64 MiB by default), and reused for every bucket, as the
+paper's step 2 describes.  The descriptor arrays the kernels read (tensor pointers,
+sizes, offsets) are uploaded once at construction, so the tensors must stay
+allocated and in place for the object's lifetime.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+
+import torch
+
+from . import _lib as L
+
+_TORCH_DTYPE = {L.FLOAT32: torch.float32, L.FLOAT16: torch.float16}
+_HVDX_DTYPE = {torch.float32: L.FLOAT32, torch.float16: L.FLOAT16}
+_OPS = {"sum": L.SUM, "average": L.AVERAGE}
+
+
+@dataclass
+class Bucket:
+    tensors: list  # indices into the ready list
+    offsets: list  # element offsets in the buffer
+    count: int  # buffer elements
+    direct: bool  # reduced in place without a copy
+    numel_dev: torch.Tensor | None = None
+    offset_dev: torch.Tensor | None = None
+    ptrs_dev: torch.Tensor | None = None
+
+
+class FusedAllreduce:
+    """In-place allreduce of N ranks' gradient lists (SUM or AVERAGE)."""
+
+    def __init__(self, per_rank, op: str = "average", compress: bool = False,
+                 threshold_bytes: int = L.DEFAULT_FUSION_THRESHOLD, align_bytes: int = L.DEFAULT_FUSION_ALIGN):
+        if not per_rank or len(per_rank) > L.MAX_RANKS:
+            raise ValueError(f"need 1..{L.MAX_RANKS} ranks")
+        if op not in _OPS:
+            raise ValueError(f"op must be one of {sorted(_OPS)}")
+        self.nranks = n = len(per_rank)
+        self.tensors = [list(ts) for ts in per_rank]
+        t0 = self.tensors[0]
+        ntensors = len(t0)
+        for ts in self.tensors:
+            if len(ts) != ntensors:
+                raise ValueError("every rank needs the same number of tensors")
+            for x, ref in zip(ts, t0):
+                if x.shape != ref.shape or x.dtype != ref.dtype or x.device != ref.device:
+                    raise ValueError("tensors must match across ranks in shape, dtype and device")
+                if not x.is_contiguous() or x.device.type != "cuda":
+                    raise ValueError("tensors must be contiguous GPU tensors")
+        self.device = t0[0].device if ntensors else torch.device("cuda", torch.cuda.current_device())
+        self.dtype = _HVDX_DTYPE[t0[0].dtype] if ntensors else L.FLOAT32
+        if compress and self.dtype != L.FLOAT32:
+            raise ValueError("fp16 compression applies to float32 gradients")
+        self.op = _OPS[op]
+        self.compress = L.COMPRESS_FP16 if compress else L.COMPRESS_NONE
+        self.buf_dtype = L.FLOAT16 if compress else self.dtype
+        self.numel = [x.numel() for x in t0]
+
+        bucket_of, offset, counts, direct = L.hvdx_fuse_plan(self.numel, self.buf_dtype, threshold_bytes,
+                                                             align_bytes)
+        self.buckets = [Bucket([], [], c, bool(d)) for c, d in zip(counts, direct)]
+        for t, (b, off) in enumerate(zip(bucket_of, offset)):
+            self.buckets[b].tensors.append(t)
+            self.buckets[b].offsets.append(off)
+
+        dev = self.device
+        cap = max([b.count for b in self.buckets if not b.direct], default=0)
+        # one fusion buffer per rank, allocated once and reused for every bucket
+        self.bufs = [torch.empty(max(cap, 1), dtype=_TORCH_DTYPE[self.buf_dtype], device=dev) for _ in range(n)]
+        ws = max([L.hvdx_ring_workspace_bytes(n, b.count, self.dtype, self.compress)
+                  for b in self.buckets if b.direct], default=0)
+        self.workspace = torch.empty(max(ws, 1), dtype=torch.uint8, device=dev)
+        self.workspace_bytes = ws
+        for b in self.buckets:
+            if b.direct:
+                continue
+            b.numel_dev = torch.tensor([self.numel[t] for t in b.tensors], dtype=torch.int64, device=dev)
+            b.offset_dev = torch.tensor(b.offsets, dtype=torch.int64, device=dev)
+            b.ptrs_dev = torch.tensor([self.tensors[r][t].data_ptr() for r in range(n) for t in b.tensors],
+                                      dtype=torch.int64, device=dev)
+        self._buf_ptrs = [x.data_ptr() for x in self.bufs]
+
+    # ---- the steps, exposed separately for tracing ------------------------------------
+    def pack(self, b: Bucket, stream: int) -> None:
+        L.hvdx_fuse_pack(b.ptrs_dev.data_ptr(), b.numel_dev.data_ptr(), b.offset_dev.data_ptr(), len(b.tensors),
+                         self.dtype, self._buf_ptrs, b.count, self.buf_dtype, self.nranks, stream)
+
+    def unpack(self, b: Bucket, stream: int) -> None:
+        L.hvdx_fuse_unpack(self._buf_ptrs, b.count, self.buf_dtype, b.ptrs_dev.data_ptr(), b.numel_dev.data_ptr(),
+                           b.offset_dev.data_ptr(), len(b.tensors), self.dtype, self.nranks, stream)
+
+    def ring_args(self, b: Bucket):
+        """(rank pointers, count, dtype, compress, workspace, workspace bytes) for a bucket's ring."""
+        if b.direct:
+            t = b.tensors[0]
+            ptrs = [self.tensors[r][t].data_ptr() for r in range(self.nranks)]
+            return ptrs, b.count, self.dtype, self.compress, self.workspace.data_ptr(), self.workspace_bytes
+        return self._buf_ptrs, b.count, self.buf_dtype, L.COMPRESS_NONE, 0, 0
+
+    def ring(self, b: Bucket, stream: int) -> None:
+        ptrs, count, dtype, compress, ws, wsb = self.ring_args(b)
+        L.hvdx_ring_allreduce(ptrs, self.nranks, count, dtype, self.op, compress, ws, wsb, stream)
+
+    def ring_step(self, b: Bucket, phase: int, step: int, stream: int) -> None:
+        ptrs, count, dtype, compress, ws, wsb = self.ring_args(b)
+        L.hvdx_ring_step(ptrs, self.nranks, count, dtype, self.op, compress, phase, step, ws, wsb, stream)
+
+    def launches(self, stream: int):
+        """The allreduce as its separate kernel launches, in order:
+        (kind, bucket index, step, zero-argument callable).  kind is "pack", "rs",
+        "ag", "unpack", or "ring" (a whole one-rank ring).  Running them all in order
+        is one call of this object."""
+        out = []
+        for bi, b in enumerate(self.buckets):
+            if not b.direct:
+                out.append(("pack", bi, -1, lambda b=b: self.pack(b, stream)))
+            if self.nranks == 1:
+                out.append(("ring", bi, -1, lambda b=b: self.ring(b, stream)))
+            else:
+                for ph, kind in ((L.PHASE_REDUCE_SCATTER, "rs"), (L.PHASE_ALLGATHER, "ag")):
+                    for s in range(self.nranks - 1):
+                        out.append((kind, bi, s, lambda b=b, ph=ph, s=s: self.ring_step(b, ph, s, stream)))
+            if not b.direct:
+                out.append(("unpack", bi, -1, lambda b=b: self.unpack(b, stream)))
+        return out
+
+    def __call__(self, stream: int | None = None) -> None:
+        if stream is None:
+            stream = torch.cuda.current_stream(self.device).cuda_stream
+        for b in self.buckets:
+            if b.direct:
+                self.ring(b, stream)
+            else:
+                self.pack(b, stream)
+                self.ring(b, stream)
+                self.unpack(b, stream)

@@ -1,0 +1,159 @@
+"""The C-ABI without a GPU: exported symbols, host-only entry points against the
+oracle, and argument checks (which return before any HIP call)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_1802_05799_amd as hv
+from oracle import fusion, ring
+from workloads import configs
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+FAKE = 0x7F0000000000  # a plausible device address; never dereferenced by these calls
+
+
+def declared_symbols():
+    with open(os.path.join(ROOT, "include", "hvdx.h")) as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(hvdx_\w+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported():
+    syms = declared_symbols()
+    assert len(syms) >= 10
+    lib = ctypes.CDLL(hv.LIB_PATH)
+    for s in syms:
+        assert hasattr(lib, s), s
+
+
+def test_version_and_strerror():
+    assert hv.hvdx_version() == 1
+    for code in (hv.OK, hv.ERR_INVALID, hv.ERR_ALIAS, hv.ERR_WORKSPACE, hv.ERR_HIP, hv.ERR_UNSUPPORTED):
+        assert hv.hvdx_strerror(code) and hv.hvdx_strerror(code) != "unknown status"
+    assert hv.hvdx_strerror(12345) == "unknown status"
+
+
+def plan_as_buckets(numel, buf_dtype, threshold, align):
+    bucket_of, offset, counts, direct = hv.hvdx_fuse_plan(numel, buf_dtype, threshold, align)
+    out = [([], [], c, bool(d)) for c, d in zip(counts, direct)]
+    for t, (b, o) in enumerate(zip(bucket_of, offset)):
+        out[b][0].append(t)
+        out[b][1].append(o)
+    return out
+
+
+def oracle_buckets(numel, esize, threshold, align):
+    return [(b.tensors, b.offsets, b.count, b.direct) for b in fusion.fuse_plan(numel, esize, threshold, align)]
+
+
+@pytest.mark.parametrize("name", list(configs.WORKLOADS))
+def test_plan_matches_oracle_on_workloads(name):
+    w = configs.get(name)
+    dt, es = (hv.FLOAT16, 2) if w.compress else (hv.FLOAT32, 4)
+    assert plan_as_buckets(w.numel(), dt, 64 << 20, 16) == oracle_buckets(w.numel(), es, 64 << 20, 16)
+
+
+def test_plan_matches_oracle_on_random_lists():
+    rng = np.random.default_rng(31)
+    for _ in range(500):
+        numel = [int(v) for v in rng.integers(0, 60, size=rng.integers(0, 40))]
+        dt, es = [(hv.FLOAT32, 4), (hv.FLOAT16, 2)][int(rng.integers(0, 2))]
+        align = int(rng.choice([es, 8, 16, 32, 256]))
+        threshold = int(rng.integers(0, 300))
+        assert plan_as_buckets(numel, dt, threshold, align) == oracle_buckets(numel, es, threshold, align)
+
+
+def test_ring_chunk_matches_oracle():
+    for n in (1, 2, 3, 7, 64, 128):
+        for count in (0, 1, n - 1, n, 20391, 102760448, 2**40 + 3):
+            starts, lengths = ring.chunk_bounds(count, n)
+            for c in range(n):
+                assert hv.hvdx_ring_chunk(count, n, c) == (starts[c], lengths[c])
+
+
+def test_workspace_bytes():
+    assert hv.hvdx_ring_workspace_bytes(64, 102760448, hv.FLOAT32, hv.COMPRESS_FP16) == 64 * 102760448 * 2
+    assert hv.hvdx_ring_workspace_bytes(4, 130, hv.FLOAT32, hv.COMPRESS_FP16) == 4 * 256 * 2
+    assert hv.hvdx_ring_workspace_bytes(4, 130, hv.FLOAT32, hv.COMPRESS_NONE) == 0
+    assert hv.hvdx_ring_workspace_bytes(1, 130, hv.FLOAT32, hv.COMPRESS_FP16) == 0
+    assert hv.hvdx_ring_workspace_bytes(4, 0, hv.FLOAT32, hv.COMPRESS_FP16) == 0
+
+
+def status_of(fn, *args):
+    """Status of a call that must be refused by the argument checks (or be a no-op):
+    these calls use fake device addresses and must never reach a kernel launch."""
+    try:
+        fn(*args)
+    except hv.HvdxError as e:
+        return e.status
+    return hv.OK
+
+
+def bufs(n, count, esize=4, stride=None):
+    stride = stride if stride is not None else ((count * esize + 255) // 256) * 256 + 256
+    return [FAKE + r * stride for r in range(n)]
+
+
+def test_ring_argument_errors():
+    ar = hv.hvdx_ring_allreduce
+    assert status_of(ar, bufs(2, 8), 0, 8, hv.FLOAT32, hv.SUM) == hv.ERR_INVALID  # nranks 0
+    assert status_of(ar, bufs(129, 8), 129, 8, hv.FLOAT32, hv.SUM) == hv.ERR_INVALID  # too many ranks
+    assert status_of(ar, bufs(2, 8), 2, -1, hv.FLOAT32, hv.SUM) == hv.ERR_INVALID  # negative count
+    assert status_of(ar, bufs(2, 8), 2, 8, 7, hv.SUM) == hv.ERR_INVALID  # dtype
+    assert status_of(ar, bufs(2, 8), 2, 8, hv.FLOAT32, 9) == hv.ERR_INVALID  # op
+    assert status_of(ar, bufs(2, 8), 2, 8, hv.FLOAT32, hv.SUM, 5) == hv.ERR_INVALID  # compression
+    assert status_of(ar, bufs(2, 8), 2, 8, hv.FLOAT16, hv.SUM, hv.COMPRESS_FP16) == hv.ERR_INVALID
+    assert status_of(ar, [FAKE, 0], 2, 8, hv.FLOAT32, hv.SUM) == hv.ERR_INVALID  # null buffer
+    assert status_of(ar, [FAKE, FAKE + 2], 2, 8, hv.FLOAT32, hv.SUM) == hv.ERR_INVALID  # misaligned
+    assert status_of(ar, [FAKE, FAKE + 16], 2, 8, hv.FLOAT32, hv.SUM) == hv.ERR_ALIAS  # overlap
+    assert status_of(ar, [FAKE + 64, FAKE, FAKE + 32], 3, 9, hv.FLOAT32, hv.SUM) == hv.ERR_ALIAS
+    # compression needs a large enough, aligned, disjoint workspace
+    b = bufs(4, 1000)
+    need = hv.hvdx_ring_workspace_bytes(4, 1000, hv.FLOAT32, hv.COMPRESS_FP16)
+    ws = FAKE + (1 << 30)
+    assert status_of(ar, b, 4, 1000, hv.FLOAT32, hv.AVERAGE, hv.COMPRESS_FP16, 0, 0) == hv.ERR_WORKSPACE
+    assert status_of(ar, b, 4, 1000, hv.FLOAT32, hv.AVERAGE, hv.COMPRESS_FP16, ws, need - 1) == hv.ERR_WORKSPACE
+    assert status_of(ar, b, 4, 1000, hv.FLOAT32, hv.AVERAGE, hv.COMPRESS_FP16, ws + 16, need) == hv.ERR_WORKSPACE
+    assert status_of(ar, b, 4, 1000, hv.FLOAT32, hv.AVERAGE, hv.COMPRESS_FP16, b[1], need) == hv.ERR_ALIAS
+    # count 0 is a no-op and touches nothing
+    assert status_of(ar, bufs(4, 0), 4, 0, hv.FLOAT32, hv.AVERAGE) == hv.OK
+    st = hv.hvdx_ring_step
+    assert status_of(st, bufs(3, 8), 3, 8, hv.FLOAT32, hv.SUM, 0, 2, 0) == hv.ERR_INVALID  # phase
+    assert status_of(st, bufs(3, 8), 3, 8, hv.FLOAT32, hv.SUM, 0, 0, 2) == hv.ERR_INVALID  # step > N-2
+    assert status_of(st, bufs(3, 8), 3, 8, hv.FLOAT32, hv.SUM, 0, 0, -1) == hv.ERR_INVALID
+    assert status_of(st, bufs(1, 8), 1, 8, hv.FLOAT32, hv.SUM, 0, 0, 0) == hv.ERR_INVALID  # no steps at N=1
+    assert "overlap" in hv.hvdx_last_error() or hv.hvdx_last_error()
+
+
+def test_fusion_argument_errors():
+    pk, up = hv.hvdx_fuse_pack, hv.hvdx_fuse_unpack
+    b = bufs(2, 64)
+    assert status_of(pk, 0, FAKE, FAKE, 3, hv.FLOAT32, b, 64, hv.FLOAT32, 2) == hv.ERR_INVALID
+    assert status_of(pk, FAKE, FAKE, FAKE, -1, hv.FLOAT32, b, 64, hv.FLOAT32, 2) == hv.ERR_INVALID
+    assert status_of(pk, FAKE, FAKE, FAKE, 3, hv.FLOAT16, b, 64, hv.FLOAT32, 2) == hv.ERR_UNSUPPORTED
+    assert status_of(pk, FAKE, FAKE, FAKE, 3, 5, b, 64, hv.FLOAT32, 2) == hv.ERR_INVALID
+    assert status_of(pk, FAKE, FAKE, FAKE, 3, hv.FLOAT32, [FAKE, FAKE + 64], 64, hv.FLOAT32, 2) == hv.ERR_ALIAS
+    assert status_of(pk, FAKE, FAKE, FAKE, 3, hv.FLOAT32, [FAKE + 4, FAKE + 4096], 64, hv.FLOAT32, 2) == hv.ERR_INVALID
+    assert status_of(up, b, 64, hv.FLOAT32, 0, FAKE, FAKE, 3, hv.FLOAT32, 2) == hv.ERR_INVALID
+    assert status_of(up, b, -5, hv.FLOAT32, FAKE, FAKE, FAKE, 3, hv.FLOAT32, 2) == hv.ERR_INVALID
+    assert status_of(up, b, 64, hv.FLOAT32, FAKE, FAKE, FAKE, 3, hv.FLOAT32, 0) == hv.ERR_INVALID
+    # an empty buffer is a no-op
+    assert status_of(pk, FAKE, FAKE, FAKE, 3, hv.FLOAT32, b, 0, hv.FLOAT32, 2) == hv.OK
+
+
+def test_plan_argument_errors():
+    with pytest.raises(hv.HvdxError):
+        hv.hvdx_fuse_plan([1, -2], hv.FLOAT32)
+    with pytest.raises(hv.HvdxError):
+        hv.hvdx_fuse_plan([1], hv.FLOAT32, 64, 12)
+    with pytest.raises(hv.HvdxError):
+        hv.hvdx_fuse_plan([1], hv.FLOAT32, 64, 2)
+    with pytest.raises(hv.HvdxError):
+        hv.hvdx_fuse_plan([1], 3)
+    with pytest.raises(hv.HvdxError):
+        hv.hvdx_fuse_plan([1], hv.FLOAT32, -1)
+    assert hv.hvdx_fuse_plan([], hv.FLOAT32) == ([], [], [], [])

@@ -1,0 +1,130 @@
+"""GPU copy-in / copy-out kernels and the whole Tensor Fusion cycle against the oracle."""
+import numpy as np
+import pytest
+import torch
+
+import paper_1802_05799_amd as hv
+from _gpu import NP_TO_HV, NP_TO_TORCH, assert_bits_equal, say
+from oracle import allreduce, fusion
+
+pytestmark = pytest.mark.gpu
+
+
+def make_tensors(rng, n, numel, dtype, misalign=False):
+    """Per-rank numpy tensors and their GPU copies (optionally at odd element offsets)."""
+    host = [[(rng.standard_normal(k) * 0.01).astype(dtype) for k in numel] for _ in range(n)]
+    dev, keep = [], []
+    for r in range(n):
+        row = []
+        for t, x in enumerate(host[r]):
+            off = (t * 3 + r) % 5 if misalign else 0
+            base = torch.zeros(x.size + off + 8, dtype=NP_TO_TORCH[x.dtype], device="cuda")
+            v = base[off : off + x.size]
+            v.copy_(torch.from_numpy(x))
+            row.append(v)
+            keep.append(base)
+        dev.append(row)
+    return host, dev, keep
+
+
+def descriptors(dev, bucket, numel):
+    n = len(dev)
+    ptrs = torch.tensor([dev[r][t].data_ptr() for r in range(n) for t in bucket.tensors], dtype=torch.int64,
+                        device="cuda")
+    nm = torch.tensor([numel[t] for t in bucket.tensors], dtype=torch.int64, device="cuda")
+    off = torch.tensor(bucket.offsets, dtype=torch.int64, device="cuda")
+    return ptrs, nm, off
+
+
+PACK_CASES = [
+    # (numel list, nranks, buffer esize, align bytes)
+    ([7, 64, 100, 1000, 4608, 4096, 513, 10000], 4, 4, 16),
+    ([0, 1, 0, 3, 5, 0, 0, 2, 17], 3, 4, 16),
+    ([1] * 3000 + [5000], 2, 4, 16),  # 1024 tensors in one tile
+    ([1] * 3000 + [5000], 2, 4, 4),  # more tensors in one tile than LDS holds
+    ([0] * 2000 + [5, 0, 0, 7] + [0] * 500 + [100], 3, 4, 16),  # runs of empty tensors
+    ([33, 31, 1, 2, 3, 4, 5, 6, 7, 8, 9, 100000], 5, 4, 4),  # no padding between tensors
+    ([33, 31, 1, 2, 3, 4, 5, 6, 7, 8, 9, 100000], 5, 4, 64),
+    ([257] * 40 + [70000, 3, 9000], 7, 2, 16),  # binary16 buffer
+    ([257] * 40 + [70000, 3, 9000], 7, 2, 2),
+]
+
+
+@pytest.mark.parametrize("misalign", [False, True], ids=["aligned", "misaligned"])
+@pytest.mark.parametrize("case", range(len(PACK_CASES)))
+def test_pack_unpack_match_oracle(case, misalign):
+    numel, n, esize, align = PACK_CASES[case]
+    rng = np.random.default_rng(200 + case)
+    buf_np = np.float32 if esize == 4 else np.float16
+    host, dev, keep = make_tensors(rng, n, numel, np.float32, misalign)
+    plan = fusion.fuse_plan(numel, esize, threshold=1 << 30, align=align)
+    (b,) = plan
+    say(f"pack case={case} misalign={misalign} count={b.count} tensors={len(numel)} n={n}")
+    ptrs, nm, off = descriptors(dev, b, numel)
+    bufs = [torch.full((b.count + 64,), 7.0, dtype=NP_TO_TORCH[np.dtype(buf_np)], device="cuda") for _ in range(n)]
+    st = torch.cuda.current_stream().cuda_stream
+    hv.hvdx_fuse_pack(ptrs.data_ptr(), nm.data_ptr(), off.data_ptr(), len(b.tensors), hv.FLOAT32,
+                      [x.data_ptr() for x in bufs], b.count, NP_TO_HV[np.dtype(buf_np)], n, st)
+    torch.cuda.synchronize()
+    for r in range(n):
+        want = fusion.pack(host[r], b, buf_np)
+        got = bufs[r].cpu().numpy()
+        assert_bits_equal(got[: b.count], want, f"pack rank {r}")
+        assert np.all(got[b.count :] == 7.0), "pack wrote past the buffer"
+    # scribble the tensors, then copy the buffers back out
+    for r in range(n):
+        for x in dev[r]:
+            x.fill_(-3.0)
+    hv.hvdx_fuse_unpack([x.data_ptr() for x in bufs], b.count, NP_TO_HV[np.dtype(buf_np)], ptrs.data_ptr(),
+                        nm.data_ptr(), off.data_ptr(), len(b.tensors), hv.FLOAT32, n, st)
+    torch.cuda.synchronize()
+    for r in range(n):
+        want = fusion.unpack(fusion.pack(host[r], b, buf_np), b, numel, np.float32)
+        for t in b.tensors:
+            assert_bits_equal(dev[r][t].cpu().numpy(), want[t], f"unpack rank {r} tensor {t}")
+
+
+def test_unpack_does_not_write_outside_tensors():
+    rng = np.random.default_rng(210)
+    numel = [5, 3, 9, 1]
+    n = 2
+    plan = fusion.fuse_plan(numel, 4, threshold=1 << 20)
+    (b,) = plan
+    guard = [torch.full((64,), 11.0, device="cuda") for _ in range(n * len(numel))]
+    dev = [[guard[r * len(numel) + t][8 : 8 + numel[t]] for t in range(len(numel))] for r in range(n)]
+    ptrs, nm, off = descriptors(dev, b, numel)
+    bufs = [torch.from_numpy((rng.standard_normal(b.count)).astype(np.float32)).cuda() for _ in range(n)]
+    hv.hvdx_fuse_unpack([x.data_ptr() for x in bufs], b.count, hv.FLOAT32, ptrs.data_ptr(), nm.data_ptr(),
+                        off.data_ptr(), len(numel), hv.FLOAT32, n, torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    for r in range(n):
+        for t in range(len(numel)):
+            g = guard[r * len(numel) + t].cpu().numpy()
+            assert np.all(g[:8] == 11.0) and np.all(g[8 + numel[t] :] == 11.0)
+            assert_bits_equal(g[8 : 8 + numel[t]], bufs[r].cpu().numpy()[b.offsets[t] : b.offsets[t] + numel[t]])
+
+
+CYCLE_CASES = [
+    # (numel, nranks, threshold bytes, compress, op)
+    ([7, 64, 100, 1000, 4608, 4096, 513, 10000], 4, 64 << 20, False, "average"),
+    ([7, 64, 100, 1000, 4608, 4096, 513, 10000], 4, 4096, False, "sum"),  # several buckets + direct tensors
+    ([7, 64, 100, 1000, 4608, 4096, 513, 10000], 3, 4096, True, "average"),
+    ([3000, 1, 2, 50000, 64, 64, 64, 128 * 1024, 9], 6, 40000, True, "average"),
+    ([3000, 1, 2, 50000, 64, 64, 64, 128 * 1024, 9], 5, 40000, False, "average"),
+    ([1], 1, 64, True, "average"),
+]
+
+
+@pytest.mark.parametrize("case", range(len(CYCLE_CASES)))
+def test_fused_allreduce_matches_oracle(case):
+    numel, n, threshold, compress, op = CYCLE_CASES[case]
+    rng = np.random.default_rng(300 + case)
+    host, dev, keep = make_tensors(rng, n, numel, np.float32)
+    say(f"cycle case={case} n={n} threshold={threshold} compress={compress}")
+    ar = hv.FusedAllreduce(dev, op=op, compress=compress, threshold_bytes=threshold)
+    ar()
+    torch.cuda.synchronize()
+    want = allreduce.allreduce(host, op, compress=compress, threshold=threshold)
+    for r in range(n):
+        for t in range(len(numel)):
+            assert_bits_equal(dev[r][t].cpu().numpy(), want[r][t], f"rank {r} tensor {t}")

@@ -1,0 +1,153 @@
+"""GPU ring kernels against the oracle, element by element and bit for bit."""
+import numpy as np
+import pytest
+import torch
+
+import _pins
+import paper_1802_05799_amd as hv
+from _gpu import OPS, assert_bits_equal, from_gpu_rows, gpu_ring, say, to_gpu_rows
+from oracle import fusion, ring
+
+pytestmark = pytest.mark.gpu
+
+
+def inputs(rng, n, count, dtype, scale=0.01):
+    x = rng.standard_normal((n, count)) * scale * rng.choice([0.01, 1.0, 100.0], size=(n, count))
+    return x.astype(dtype)
+
+
+def oracle_ring(x, op, compress=False):
+    if compress:
+        b = fusion.cast(x, np.float16)
+        ring.ring_allreduce(b, op)
+        return fusion.cast(b, np.float32)
+    return ring.ring_allreduce(x.copy(), op)
+
+
+CASES = []
+for _n in (1, 2, 3, 4, 5, 7, 8, 13, 16, 32, 64, 128):
+    for _count in sorted({0, 1, _n - 1, _n, 4 * _n + 3, 1000, 8 * 256 * 4 * 4 + 13, 100003}):
+        if _count >= 0:
+            CASES.append((_n, _count))
+
+
+@pytest.mark.parametrize("dtype", [np.float32, np.float16], ids=["f32", "f16"])
+def test_ring_matches_oracle(dtype):
+    rng = np.random.default_rng(100)
+    for n, count in CASES:
+        for op in ("sum", "average"):
+            say(f"ring dtype={np.dtype(dtype).name} n={n} count={count} op={op}")
+            x = inputs(rng, n, count, dtype)
+            assert_bits_equal(gpu_ring(x, op), oracle_ring(x, op), f"n={n} count={count} op={op}")
+
+
+def test_compressed_ring_matches_oracle():
+    rng = np.random.default_rng(101)
+    for n, count in CASES:
+        for op in ("sum", "average"):
+            say(f"compressed ring n={n} count={count} op={op}")
+            x = inputs(rng, n, count, np.float32)
+            assert_bits_equal(gpu_ring(x, op, compress=True), oracle_ring(x, op, True), f"n={n} count={count}")
+
+
+def test_unaligned_buffers_take_the_scalar_path():
+    rng = np.random.default_rng(102)
+    for off in (1, 2, 3):
+        for n, count in ((3, 1001), (8, 40000)):
+            for dtype in (np.float32, np.float16):
+                say(f"unaligned off={off} n={n} count={count} {np.dtype(dtype).name}")
+                x = inputs(rng, n, count, dtype)
+                assert_bits_equal(gpu_ring(x, "average", offset_elems=off), oracle_ring(x, "average"))
+            x = inputs(rng, n, count, np.float32)
+            assert_bits_equal(gpu_ring(x, "average", True, offset_elems=off), oracle_ring(x, "average", True))
+
+
+def test_special_values():
+    """Ties, subnormals (binary16 gradual underflow), signed zeros, infinities."""
+    n, count = 4, 4096
+    rng = np.random.default_rng(103)
+    x32 = (rng.standard_normal((n, count)) * 1e-5).astype(np.float32)  # many binary16 subnormals
+    x32[:, :8] = np.array([0.0, -0.0, 1.0, 2.0 ** -24, 65504.0, 65520.0, np.inf, -np.inf], np.float32)
+    x32[1, 8:16] = 2.0 ** 24
+    x32[:, 16:24] = 1.0
+    for op in ("sum", "average"):
+        say(f"special values op={op}")
+        assert_bits_equal(gpu_ring(x32, op), oracle_ring(x32, op), "f32")
+        x16 = fusion.cast(x32, np.float16)
+        assert_bits_equal(gpu_ring(x16, op), oracle_ring(x16, op), "f16")
+        assert_bits_equal(gpu_ring(x32, op, True), oracle_ring(x32, op, True), "compressed")
+
+
+def test_each_step_matches_oracle_states():
+    """hvdx_ring_step, one step at a time: every intermediate state equals the oracle's."""
+    rng = np.random.default_rng(104)
+    for n, count, dtype in ((3, 7, np.float32), (5, 1234, np.float32), (6, 4099, np.float16), (16, 70001, np.float32)):
+        for op in ("sum", "average"):
+            say(f"steps n={n} count={count} op={op}")
+            x = inputs(rng, n, count, dtype)
+            states = []
+            ring.ring_allreduce(x.copy(), op, observe=lambda ph, s, b: states.append((ph, s, b.copy())))
+            rows, keep = to_gpu_rows(x)
+            ptrs = [r.data_ptr() for r in rows]
+            dt = hv.FLOAT32 if dtype == np.float32 else hv.FLOAT16
+            for ph, s, want in states:
+                phase = hv.PHASE_REDUCE_SCATTER if ph == "rs" else hv.PHASE_ALLGATHER
+                hv.hvdx_ring_step(ptrs, n, count, dt, OPS[op], hv.COMPRESS_NONE, phase, s)
+                assert_bits_equal(from_gpu_rows(rows), want, f"{ph}{s}")
+
+
+def test_hand_worked_example_on_gpu():
+    states, _ = _pins.read_ring_golden()
+    rows, keep = to_gpu_rows(states["initial"])
+    ptrs = [r.data_ptr() for r in rows]
+    for key, phase, s in (("rs0", 0, 0), ("rs1", 0, 1), ("ag0", 1, 0), ("ag1", 1, 1)):
+        hv.hvdx_ring_step(ptrs, 3, 7, hv.FLOAT32, hv.SUM, hv.COMPRESS_NONE, phase, s)
+        assert_bits_equal(from_gpu_rows(rows), states[key], key)
+    assert_bits_equal(gpu_ring(states["initial"], "average"), states["avg_final"], "average")
+
+
+def test_compressed_steps_wire_and_outputs():
+    """Compressed steps: after the adding half the owner's wire copy holds the binary16
+    result of the oracle's fp16 ring; at the end every binary32 buffer holds it widened."""
+    rng = np.random.default_rng(105)
+    n, count = 5, 3001
+    x = inputs(rng, n, count, np.float32)
+    rows, keep = to_gpu_rows(x)
+    ptrs = [r.data_ptr() for r in rows]
+    wsb = hv.hvdx_ring_workspace_bytes(n, count, hv.FLOAT32, hv.COMPRESS_FP16)
+    ws = torch.zeros(wsb, dtype=torch.uint8, device="cuda")
+    states = []
+    ring.ring_allreduce(fusion.cast(x, np.float16), "average", observe=lambda ph, s, b: states.append(b.copy()))
+    for s in range(n - 1):
+        hv.hvdx_ring_step(ptrs, n, count, hv.FLOAT32, hv.AVERAGE, hv.COMPRESS_FP16, hv.PHASE_REDUCE_SCATTER, s,
+                          ws.data_ptr(), wsb)
+    torch.cuda.synchronize()
+    stride = (count + 127) // 128 * 128
+    wire = ws.view(torch.float16)[: n * stride].view(n, stride)[:, :count].cpu().numpy()
+    after_rs = states[n - 2]
+    starts, lengths = ring.chunk_bounds(count, n)
+    for c in range(n):
+        owner = (c - 1) % n
+        sl = slice(starts[c], starts[c] + lengths[c])
+        assert_bits_equal(wire[owner, sl], after_rs[owner, sl], f"owner of chunk {c}")
+    for s in range(n - 1):
+        hv.hvdx_ring_step(ptrs, n, count, hv.FLOAT32, hv.AVERAGE, hv.COMPRESS_FP16, hv.PHASE_ALLGATHER, s,
+                          ws.data_ptr(), wsb)
+    assert_bits_equal(from_gpu_rows(rows), fusion.cast(states[-1], np.float32), "final")
+
+
+def test_streams_and_repeat_calls():
+    """Work on a side stream, twice in a row on the same buffers."""
+    rng = np.random.default_rng(106)
+    n, count = 8, 1 << 20
+    x = inputs(rng, n, count, np.float32)
+    rows, keep = to_gpu_rows(x)
+    ptrs = [r.data_ptr() for r in rows]
+    s = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s):
+        hv.hvdx_ring_allreduce(ptrs, n, count, hv.FLOAT32, hv.SUM, 0, 0, 0, s.cuda_stream)
+        hv.hvdx_ring_allreduce(ptrs, n, count, hv.FLOAT32, hv.SUM, 0, 0, 0, s.cuda_stream)
+    s.synchronize()
+    want = ring.ring_allreduce(ring.ring_allreduce(x.copy(), "sum"), "sum")
+    assert_bits_equal(from_gpu_rows(rows), want, "twice")
