@@ -36,6 +36,8 @@ def parse():
     p.add_argument("--no-per-config", action="store_true", help="time only the headline workload")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="target oracle time for the CPU baseline")
+    p.add_argument("--calibration-copy-mib", type=int, default=0,
+                   help="first run 3 plain device copies of this many MiB (a known-traffic kernel for counters)")
     return p.parse_args()
 
 
@@ -100,22 +102,42 @@ def measure(name, steps, warmup):
     wall = time.perf_counter() - t0
     ms = e0.elapsed_time(e1) / steps
 
-    # the same steps once more with an event pair around every kernel launch
+    # the same steps once more, with an event pair around each run of consecutive
+    # launches of one kernel (e.g. the N-1 reduce-scatter steps of a bucket), so the
+    # events add little to what they measure
     launches = ar.launches(sid)
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in launches]
-    per_kernel = {}
-    for _ in range(steps):
-        for (kind, bi, s, fn), (a, b) in zip(launches, evs):
+    groups = []
+    for kind, bi, s, fn in launches:
+        key = (kernel_name(ar, kind, bi), bi, kind)
+        if groups and groups[-1][0] == key:
+            groups[-1][1].append((kind, bi, s, fn))
+        else:
+            groups.append((key, [(kind, bi, s, fn)]))
+    # every step's events are created up front and read after one final sync, so the
+    # host never stalls the GPU between an event pair; one untimed traced step first
+    evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in groups]
+           for _ in range(steps + 1)]
+    for step_evs in evs:  # torch creates the HIP events on first record: do that outside the timing
+        for a, b in step_evs:
             a.record(stream)
-            fn()
             b.record(stream)
-        torch.cuda.synchronize()
-        for (kind, bi, s, fn), (a, b) in zip(launches, evs):
-            k = kernel_name(ar, kind, bi)
-            d = per_kernel.setdefault(k, {"launches": 0, "ms": 0.0, "bytes": 0})
-            d["launches"] += 1
+    torch.cuda.synchronize()
+    if hasattr(torch.cuda, "_sleep"):  # a bounded spin lets the host enqueue ahead of the GPU
+        torch.cuda._sleep(50_000_000)
+    for step_evs in evs:
+        for (key, items), (a, b) in zip(groups, step_evs):
+            a.record(stream)
+            for _kind, _bi, _s, fn in items:
+                fn()
+            b.record(stream)
+    torch.cuda.synchronize()
+    per_kernel = {}
+    for step_evs in evs[1:]:
+        for (key, items), (a, b) in zip(groups, step_evs):
+            d = per_kernel.setdefault(key[0], {"launches": 0, "ms": 0.0, "bytes": 0})
+            d["launches"] += len(items)
             d["ms"] += a.elapsed_time(b)
-            d["bytes"] += kernel_bytes(ar, kind, bi, s)
+            d["bytes"] += sum(kernel_bytes(ar, kind, bi, s) for kind, bi, s, _fn in items)
     traced_ms = sum(d["ms"] for d in per_kernel.values()) / steps
     for d in per_kernel.values():
         d["avg_us"] = 1000.0 * d["ms"] / d["launches"]
@@ -211,6 +233,16 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(2)
+
+    if args.calibration_copy_mib:
+        n = args.calibration_copy_mib << 18  # float32 elements
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+        torch.cuda.empty_cache()
 
     head = measure(args.workload, args.steps, args.warmup)
     print(f"# {args.workload}: {head['ms_per_step']:.3f} ms/step, {head['algbw_GBps']:.1f} GB/s", file=sys.stderr,

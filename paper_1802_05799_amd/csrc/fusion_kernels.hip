@@ -20,8 +20,26 @@ namespace {
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 
-constexpr int kTileVecs = kBlock * 4;  // 16-byte buffer vectors per block tile
-constexpr int kLdsTensors = 1024 + 8;  // tensors a tile can stage in LDS
+// Shape of a copy kernel: POS 16-byte buffer vectors per lane (a tile is kBlock*POS
+// vectors), RB ranks whose loads are in flight together, RPB ranks per block (0 =
+// all), and non-temporal loads/stores.  Measured on MI355X with the workloads'
+// buckets (both stream their data once, so every access is non-temporal).
+template <int POS_, int RB_, int RPB_, bool NTL_, bool NTS_>
+struct CopyCfg {
+  static constexpr int POS = POS_, RB = RB_, RPB = RPB_;
+  static constexpr bool NTL = NTL_, NTS = NTS_;
+  static constexpr int kTileVecs = kBlock * POS_;
+  static constexpr int kLdsTensors = kBlock * POS_ + 8;  // a tile's tensors staged in LDS
+};
+#ifndef HVDX_PACK_CFG
+#define HVDX_PACK_CFG CopyCfg<2, 4, 4, true, true>
+#endif
+#ifndef HVDX_UNPACK_CFG
+#define HVDX_UNPACK_CFG CopyCfg<4, 2, 2, true, true>
+#endif
+using PackCfg = HVDX_PACK_CFG;
+using UnpackCfg = HVDX_UNPACK_CFG;
+constexpr int kLdsPtrs = 2048;  // (rank, tensor) pointers a tile can stage in LDS
 
 template <typename TB>
 struct BufVec {
@@ -33,13 +51,37 @@ struct BufVec {
 template <typename TT, typename TB>
 struct Mover;
 
+__device__ __forceinline__ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+// 16-byte loads and stores of the copy kernels, with optional non-temporal hints
+template <bool NT, typename V>
+__device__ __forceinline__ V ld16(const V* p) {
+  if constexpr (NT) return __builtin_nontemporal_load(p);
+  return *p;
+}
+template <bool NT, typename V>
+__device__ __forceinline__ void st16(V* p, V v) {
+  if constexpr (NT) __builtin_nontemporal_store(v, p);
+  else *p = v;
+}
+
 template <>
 struct Mover<float, float> {
-  __device__ static void to_buf(const float* src, float* dst) {
-    *reinterpret_cast<f32x4*>(dst) = *reinterpret_cast<const f32x4*>(src);
+  using buf_vec = f32x4;
+  // 4 tensor elements -> one buffer vector (tensor side may be unaligned)
+  template <bool NT>
+  __device__ static f32x4 load(const float* src) {
+    if (aligned16(src)) return ld16<NT>(reinterpret_cast<const f32x4*>(src));
+    return f32x4{src[0], src[1], src[2], src[3]};
   }
-  __device__ static void from_buf(const float* src, float* dst) {
-    *reinterpret_cast<f32x4*>(dst) = *reinterpret_cast<const f32x4*>(src);
+  template <bool NT>
+  __device__ static void store(float* dst, f32x4 v) {
+    if (aligned16(dst)) {
+      st16<NT>(reinterpret_cast<f32x4*>(dst), v);
+      return;
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) dst[k] = v[k];
   }
   __device__ static float cvt_in(float v) { return v; }
   __device__ static float cvt_out(float v) { return v; }
@@ -47,11 +89,23 @@ struct Mover<float, float> {
 
 template <>
 struct Mover<_Float16, _Float16> {
-  __device__ static void to_buf(const _Float16* src, _Float16* dst) {
-    *reinterpret_cast<f16x8*>(dst) = *reinterpret_cast<const f16x8*>(src);
+  using buf_vec = f16x8;
+  template <bool NT>
+  __device__ static f16x8 load(const _Float16* src) {
+    if (aligned16(src)) return ld16<NT>(reinterpret_cast<const f16x8*>(src));
+    f16x8 h;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) h[k] = src[k];
+    return h;
   }
-  __device__ static void from_buf(const _Float16* src, _Float16* dst) {
-    *reinterpret_cast<f16x8*>(dst) = *reinterpret_cast<const f16x8*>(src);
+  template <bool NT>
+  __device__ static void store(_Float16* dst, f16x8 v) {
+    if (aligned16(dst)) {
+      st16<NT>(reinterpret_cast<f16x8*>(dst), v);
+      return;
+    }
+#pragma unroll
+    for (int k = 0; k < 8; ++k) dst[k] = v[k];
   }
   __device__ static _Float16 cvt_in(_Float16 v) { return v; }
   __device__ static _Float16 cvt_out(_Float16 v) { return v; }
@@ -59,27 +113,43 @@ struct Mover<_Float16, _Float16> {
 
 template <>
 struct Mover<float, _Float16> {  // tensor binary32, buffer binary16
-  __device__ static void to_buf(const float* src, _Float16* dst) {
-    const f32x4 lo = reinterpret_cast<const f32x4*>(src)[0];
-    const f32x4 hi = reinterpret_cast<const f32x4*>(src)[1];
+  using buf_vec = f16x8;
+  template <bool NT>
+  __device__ static f16x8 load(const float* src) {
+    f32x4 lo, hi;
+    if (aligned16(src)) {
+      lo = ld16<NT>(reinterpret_cast<const f32x4*>(src));
+      hi = ld16<NT>(reinterpret_cast<const f32x4*>(src) + 1);
+    } else {
+      lo = f32x4{src[0], src[1], src[2], src[3]};
+      hi = f32x4{src[4], src[5], src[6], src[7]};
+    }
     f16x8 h;
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       h[k] = (_Float16)lo[k];
       h[k + 4] = (_Float16)hi[k];
     }
-    *reinterpret_cast<f16x8*>(dst) = h;
+    return h;
   }
-  __device__ static void from_buf(const _Float16* src, float* dst) {
-    const f16x8 h = *reinterpret_cast<const f16x8*>(src);
+  template <bool NT>
+  __device__ static void store(float* dst, f16x8 h) {
     f32x4 lo, hi;
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       lo[k] = (float)h[k];
       hi[k] = (float)h[k + 4];
     }
-    reinterpret_cast<f32x4*>(dst)[0] = lo;
-    reinterpret_cast<f32x4*>(dst)[1] = hi;
+    if (aligned16(dst)) {
+      st16<NT>(reinterpret_cast<f32x4*>(dst), lo);
+      st16<NT>(reinterpret_cast<f32x4*>(dst) + 1, hi);
+      return;
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      dst[k] = lo[k];
+      dst[k + 4] = hi[k];
+    }
   }
   __device__ static _Float16 cvt_in(float v) { return (_Float16)v; }
   __device__ static float cvt_out(_Float16 v) { return (float)v; }
@@ -106,20 +176,45 @@ struct TileTable {
   bool in_lds;      // their offsets/ends are staged in LDS
 };
 
-// Thread 0 locates the tile's tensors; everyone stages their offsets and ends.
+// Last tensor t in [lo, hi) with offset[t] <= p, or lo - 1 if none, found by one
+// 64-lane wavefront: each round the lanes probe 64 evenly spaced offsets and a ballot
+// narrows the range 64-fold (two rounds cover 4096 tensors).  Every lane of the
+// calling wavefront must take part; all get the answer.
+__device__ int64_t find_tensor_wave(const int64_t* offset, int64_t lo, int64_t hi, int64_t p) {
+  const int lane = threadIdx.x & 63;
+  while (lo < hi) {
+    const int64_t n = hi - lo;
+    const int64_t idx = lo + ((lane + 1) * n + 63) / 64 - 1;  // non-decreasing in lane, last = hi - 1
+    const unsigned long long mask = __ballot(offset[idx] <= p);
+    const int cnt = __popcll(mask);  // offsets are ascending: the true lanes come first
+    if (cnt == 64) {
+      lo = hi;
+    } else {
+      const int64_t stop = lo + ((int64_t)(cnt + 1) * n + 63) / 64 - 1;  // probe of lane cnt: > p
+      if (cnt > 0) lo = lo + ((int64_t)cnt * n + 63) / 64;              // one past the probe of lane cnt-1
+      hi = stop;
+    }
+  }
+  return lo - 1;
+}
+
+// The first wavefront locates the tile's tensors; everyone stages their offsets and ends.
+template <int LDS_TENSORS>
 __device__ TileTable stage_tile(const int64_t* offset, const int64_t* numel, int ntensors, int64_t p0, int64_t p1,
                                 int64_t* s_off, int64_t* s_end, int64_t* s_meta) {
-  if (threadIdx.x == 0) {
-    const int64_t t0 = find_tensor_global(offset, 0, ntensors, p0);
-    const int64_t t1 = find_tensor_global(offset, t0 < 0 ? 0 : t0, ntensors, p1 - 1);
-    s_meta[0] = t0;
-    s_meta[1] = t1 - t0 + 1;
+  if (threadIdx.x < 64) {
+    const int64_t t0 = find_tensor_wave(offset, 0, ntensors, p0);
+    const int64_t t1 = find_tensor_wave(offset, t0 < 0 ? 0 : t0, ntensors, p1 - 1);
+    if (threadIdx.x == 0) {
+      s_meta[0] = t0;
+      s_meta[1] = t1 - t0 + 1;
+    }
   }
   __syncthreads();
   TileTable tt;
   tt.t0 = s_meta[0];
   tt.nt = (int)s_meta[1];
-  tt.in_lds = tt.nt <= kLdsTensors;
+  tt.in_lds = tt.nt <= LDS_TENSORS;
   if (tt.in_lds) {
     for (int j = threadIdx.x; j < tt.nt; j += kBlock) {
       const int64_t t = tt.t0 + j;
@@ -165,150 +260,234 @@ __device__ __forceinline__ int64_t tensor_end(const TileTable& tt, const int64_t
   return t >= 0 ? offset[t] + numel[t] : INT64_MIN;
 }
 
-template <typename TT, typename TB>
+// What one lane does with one 16-byte buffer vector, the same for every rank.
+enum PosClass { POS_NONE = 0, POS_VEC = 1, POS_ZERO = 2, POS_EDGE = 3 };
+
+struct Pos {
+  int64_t p;    // buffer position of the vector's first element
+  int64_t t;    // tensor owning it (POS_VEC)
+  int64_t li;   // index of that element inside the tensor (POS_VEC)
+  int cls;
+};
+
+// Classify buffer vector [p, p+V): inside one tensor, all padding, or an edge that
+// needs the element-by-element path (tensor tails, unaligned tensor offsets).
+template <int V>
+__device__ __forceinline__ Pos classify(const TileTable& tt, const int64_t* s_off, const int64_t* s_end,
+                                        const int64_t* offset, const int64_t* numel, int64_t p, int64_t p1,
+                                        int64_t count) {
+  Pos q{p, -1, 0, POS_NONE};
+  if (p >= p1) return q;
+  const int j = lookup(tt, s_off, offset, p);
+  const int64_t t = tt.t0 + j;
+  const int64_t beg = t >= 0 ? tensor_begin(tt, s_off, offset, j) : INT64_MIN;
+  const int64_t end = t >= 0 ? tensor_end(tt, s_end, offset, numel, j) : INT64_MIN;
+  q.cls = POS_EDGE;
+  if (p + V <= count) {
+    if (t >= 0 && p + V <= end) {
+      q.cls = POS_VEC;
+      q.t = t;
+      q.li = p - beg;
+    } else if (p >= end && lookup(tt, s_off, offset, p + V - 1) == j) {
+      q.cls = POS_ZERO;  // no tensor element anywhere in the vector
+    }
+  }
+  return q;
+}
+
+
+// The tile's (rank, tensor) pointers, staged in LDS when they fit so that the data
+// loads do not wait behind dependent pointer loads.
+struct PtrTable {
+  const void* const* g;  // rank-major device table
+  const void* const* s;  // LDS copy, s[(r - r0) * nt + j], or null
+  int64_t t0, ntensors;
+  int nt, r0;
+  __device__ __forceinline__ const void* get(int r, int64_t t) const {
+    return s ? s[(r - r0) * nt + (int)(t - t0)] : g[(int64_t)r * ntensors + t];
+  }
+};
+
+// Pointers of ranks [r0, r1) for the tile's tensors.
+__device__ PtrTable stage_ptrs(const void* const* g, const TileTable& tt, int ntensors, int r0, int r1,
+                               const void** s_ptr) {
+  PtrTable pt{g, nullptr, tt.t0, ntensors, tt.nt, r0};
+  const int nr = r1 - r0;
+  if (tt.in_lds && (int64_t)tt.nt * nr <= kLdsPtrs) {
+    for (int idx = threadIdx.x; idx < tt.nt * nr; idx += kBlock) {
+      const int rr = idx / tt.nt;
+      const int64_t t = tt.t0 + (idx - rr * tt.nt);
+      s_ptr[idx] = t >= 0 ? g[(int64_t)(r0 + rr) * ntensors + t] : nullptr;
+    }
+    pt.s = s_ptr;
+  }
+  __syncthreads();
+  return pt;
+}
+
+template <typename TT, typename TB, typename Cfg>
 __global__ __launch_bounds__(kBlock) void pack_kernel(const void* const* __restrict__ srcs,
                                                       const int64_t* __restrict__ numel,
                                                       const int64_t* __restrict__ offset, int ntensors, RankPtrs bufs,
-                                                      int64_t count, int nranks) {
+                                                      int64_t count, int nranks, int rpb) {
   constexpr int V = BufVec<TB>::n;
-  __shared__ int64_t s_off[kLdsTensors], s_end[kLdsTensors], s_meta[2];
-  __shared__ const TT* s_ptr[kLdsTensors];
+  using VB = typename Mover<TT, TB>::buf_vec;
+  constexpr int kPosPerLane = Cfg::POS, kRankBatch = Cfg::RB, kTileVecs = Cfg::kTileVecs;
+  __shared__ int64_t s_off[Cfg::kLdsTensors], s_end[Cfg::kLdsTensors], s_meta[2];
+  __shared__ const void* s_ptr[kLdsPtrs];
   const int64_t p0 = (int64_t)blockIdx.x * kTileVecs * V;
   const int64_t p1 = p0 + (int64_t)kTileVecs * V < count ? p0 + (int64_t)kTileVecs * V : count;
-  const TileTable tt = stage_tile(offset, numel, ntensors, p0, p1, s_off, s_end, s_meta);
+  const TileTable tt = stage_tile<Cfg::kLdsTensors>(offset, numel, ntensors, p0, p1, s_off, s_end, s_meta);
+  const int rbeg = blockIdx.y * rpb, rend = rbeg + rpb < nranks ? rbeg + rpb : nranks;
+  const PtrTable pt = stage_ptrs(srcs, tt, ntensors, rbeg, rend, s_ptr);
 
-  for (int r = 0; r < nranks; ++r) {
-    if (tt.in_lds) {
-      for (int j = threadIdx.x; j < tt.nt; j += kBlock) {
-        const int64_t t = tt.t0 + j;
-        s_ptr[j] = t >= 0 ? static_cast<const TT*>(srcs[(int64_t)r * ntensors + t]) : nullptr;
-      }
-      __syncthreads();
+  Pos pos[kPosPerLane];
+#pragma unroll
+  for (int u = 0; u < kPosPerLane; ++u)
+    pos[u] = classify<V>(tt, s_off, s_end, offset, numel, p0 + (int64_t)(u * kBlock + threadIdx.x) * V, p1, count);
+
+  for (int r0 = rbeg; r0 < rend; r0 += kRankBatch) {
+    VB v[kRankBatch][kPosPerLane];
+#pragma unroll
+    for (int rr = 0; rr < kRankBatch; ++rr) {
+      const int r = r0 + rr;
+#pragma unroll
+      for (int u = 0; u < kPosPerLane; ++u)
+        if (r < rend && pos[u].cls == POS_VEC)
+          v[rr][u] = Mover<TT, TB>::template load<Cfg::NTL>(static_cast<const TT*>(pt.get(r, pos[u].t)) + pos[u].li);
     }
-    TB* __restrict__ buf = static_cast<TB*>(bufs.p[r]);
-    for (int u = 0; u < kTileVecs / kBlock; ++u) {
-      const int64_t p = p0 + (int64_t)(u * kBlock + threadIdx.x) * V;
-      if (p >= p1) break;
-      const int j = lookup(tt, s_off, offset, p);
-      const int64_t beg = j >= 0 ? tensor_begin(tt, s_off, offset, j) : INT64_MIN;
-      const int64_t end = j >= 0 ? tensor_end(tt, s_end, offset, numel, j) : INT64_MIN;
-      const TT* src = nullptr;
-      if (j >= 0 && tt.t0 + j >= 0)
-        src = tt.in_lds ? s_ptr[j] : static_cast<const TT*>(srcs[(int64_t)r * ntensors + tt.t0 + j]);
-      if (j >= 0 && p + V <= end && p + V <= count &&
-          (reinterpret_cast<uintptr_t>(src + (p - beg)) & 15) == 0) {
-        Mover<TT, TB>::to_buf(src + (p - beg), buf + p);
-        continue;
-      }
-      if (j >= 0 && p >= end && p + V <= count) {
-        // the whole vector may be padding: check that no later tensor starts inside it
-        const int jn = lookup(tt, s_off, offset, p + V - 1);
-        if (jn == j) {
-          store_zero(buf + p);
-          continue;
+#pragma unroll
+    for (int rr = 0; rr < kRankBatch; ++rr) {
+      const int r = r0 + rr;
+      if (r >= rend) break;
+      TB* __restrict__ buf = static_cast<TB*>(bufs.p[r]);
+#pragma unroll
+      for (int u = 0; u < kPosPerLane; ++u) {
+        const Pos& q = pos[u];
+        if (q.cls == POS_VEC) {
+          st16<Cfg::NTS>(reinterpret_cast<VB*>(buf + q.p), v[rr][u]);
+        } else if (q.cls == POS_ZERO) {
+          store_zero(buf + q.p);
+        } else if (q.cls == POS_EDGE) {
+          for (int k = 0; k < V; ++k) {
+            const int64_t pe = q.p + k;
+            if (pe >= count) break;
+            const int jk = lookup(tt, s_off, offset, pe);
+            const int64_t tk = tt.t0 + jk;
+            TB val = (TB)0;
+            if (tk >= 0 && pe < tensor_end(tt, s_end, offset, numel, jk)) {
+              const TT* sk = static_cast<const TT*>(pt.get(r, tk));
+              val = Mover<TT, TB>::cvt_in(sk[pe - tensor_begin(tt, s_off, offset, jk)]);
+            }
+            buf[pe] = val;
+          }
         }
       }
-      for (int k = 0; k < V; ++k) {  // tails, padding, unaligned tensors
-        const int64_t pe = p + k;
-        if (pe >= count) break;
-        const int jk = lookup(tt, s_off, offset, pe);
-        TB v = (TB)0;
-        if (jk >= 0 && pe < tensor_end(tt, s_end, offset, numel, jk)) {
-          const TT* sk = tt.in_lds ? s_ptr[jk] : static_cast<const TT*>(srcs[(int64_t)r * ntensors + tt.t0 + jk]);
-          v = Mover<TT, TB>::cvt_in(sk[pe - tensor_begin(tt, s_off, offset, jk)]);
-        }
-        buf[pe] = v;
-      }
     }
-    if (tt.in_lds) __syncthreads();  // s_ptr is rewritten for the next rank
   }
 }
 
-template <typename TT, typename TB>
+template <typename TT, typename TB, typename Cfg>
 __global__ __launch_bounds__(kBlock) void unpack_kernel(RankPtrs bufs, int64_t count, void* const* __restrict__ dsts,
                                                         const int64_t* __restrict__ numel,
                                                         const int64_t* __restrict__ offset, int ntensors,
-                                                        int nranks) {
+                                                        int nranks, int rpb) {
   constexpr int V = BufVec<TB>::n;
-  __shared__ int64_t s_off[kLdsTensors], s_end[kLdsTensors], s_meta[2];
-  __shared__ TT* s_ptr[kLdsTensors];
+  using VB = typename Mover<TT, TB>::buf_vec;
+  constexpr int kPosPerLane = Cfg::POS, kRankBatch = Cfg::RB, kTileVecs = Cfg::kTileVecs;
+  __shared__ int64_t s_off[Cfg::kLdsTensors], s_end[Cfg::kLdsTensors], s_meta[2];
+  __shared__ const void* s_ptr[kLdsPtrs];
   const int64_t p0 = (int64_t)blockIdx.x * kTileVecs * V;
   const int64_t p1 = p0 + (int64_t)kTileVecs * V < count ? p0 + (int64_t)kTileVecs * V : count;
-  const TileTable tt = stage_tile(offset, numel, ntensors, p0, p1, s_off, s_end, s_meta);
+  const TileTable tt = stage_tile<Cfg::kLdsTensors>(offset, numel, ntensors, p0, p1, s_off, s_end, s_meta);
+  const int rbeg = blockIdx.y * rpb, rend = rbeg + rpb < nranks ? rbeg + rpb : nranks;
+  const PtrTable pt = stage_ptrs(dsts, tt, ntensors, rbeg, rend, s_ptr);
 
-  for (int r = 0; r < nranks; ++r) {
-    if (tt.in_lds) {
-      for (int j = threadIdx.x; j < tt.nt; j += kBlock) {
-        const int64_t t = tt.t0 + j;
-        s_ptr[j] = t >= 0 ? static_cast<TT*>(dsts[(int64_t)r * ntensors + t]) : nullptr;
-      }
-      __syncthreads();
+  Pos pos[kPosPerLane];
+#pragma unroll
+  for (int u = 0; u < kPosPerLane; ++u)
+    pos[u] = classify<V>(tt, s_off, s_end, offset, numel, p0 + (int64_t)(u * kBlock + threadIdx.x) * V, p1, count);
+
+  for (int r0 = rbeg; r0 < rend; r0 += kRankBatch) {
+    VB v[kRankBatch][kPosPerLane];
+#pragma unroll
+    for (int rr = 0; rr < kRankBatch; ++rr) {
+      const int r = r0 + rr;
+      const TB* __restrict__ buf = static_cast<const TB*>(bufs.p[r < rend ? r : rbeg]);
+#pragma unroll
+      for (int u = 0; u < kPosPerLane; ++u)
+        if (r < rend && pos[u].cls == POS_VEC) v[rr][u] = ld16<Cfg::NTL>(reinterpret_cast<const VB*>(buf + pos[u].p));
     }
-    const TB* __restrict__ buf = static_cast<const TB*>(bufs.p[r]);
-    for (int u = 0; u < kTileVecs / kBlock; ++u) {
-      const int64_t p = p0 + (int64_t)(u * kBlock + threadIdx.x) * V;
-      if (p >= p1) break;
-      const int j = lookup(tt, s_off, offset, p);
-      if (j >= 0 && tt.t0 + j >= 0) {
-        const int64_t beg = tensor_begin(tt, s_off, offset, j);
-        const int64_t end = tensor_end(tt, s_end, offset, numel, j);
-        TT* dst = tt.in_lds ? s_ptr[j] : static_cast<TT*>(dsts[(int64_t)r * ntensors + tt.t0 + j]);
-        if (p + V <= end && (reinterpret_cast<uintptr_t>(dst + (p - beg)) & 15) == 0) {
-          Mover<TT, TB>::from_buf(buf + p, dst + (p - beg));
-          continue;
+#pragma unroll
+    for (int rr = 0; rr < kRankBatch; ++rr) {
+      const int r = r0 + rr;
+      if (r >= rend) break;
+      const TB* __restrict__ buf = static_cast<const TB*>(bufs.p[r]);
+#pragma unroll
+      for (int u = 0; u < kPosPerLane; ++u) {
+        const Pos& q = pos[u];
+        if (q.cls == POS_VEC) {
+          Mover<TT, TB>::template store<Cfg::NTS>(static_cast<TT*>(const_cast<void*>(pt.get(r, q.t))) + q.li, v[rr][u]);
+        } else if (q.cls == POS_EDGE) {
+          for (int k = 0; k < V; ++k) {
+            const int64_t pe = q.p + k;
+            if (pe >= count) break;
+            const int jk = lookup(tt, s_off, offset, pe);
+            const int64_t tk = tt.t0 + jk;
+            if (tk >= 0 && pe < tensor_end(tt, s_end, offset, numel, jk)) {
+              TT* dk = static_cast<TT*>(const_cast<void*>(pt.get(r, tk)));
+              dk[pe - tensor_begin(tt, s_off, offset, jk)] = Mover<TT, TB>::cvt_out(buf[pe]);
+            }
+          }
         }
       }
-      for (int k = 0; k < V; ++k) {  // tails, padding, unaligned tensors
-        const int64_t pe = p + k;
-        if (pe >= count) break;
-        const int jk = lookup(tt, s_off, offset, pe);
-        if (jk >= 0 && pe < tensor_end(tt, s_end, offset, numel, jk)) {
-          TT* dk = tt.in_lds ? s_ptr[jk] : static_cast<TT*>(dsts[(int64_t)r * ntensors + tt.t0 + jk]);
-          dk[pe - tensor_begin(tt, s_off, offset, jk)] = Mover<TT, TB>::cvt_out(buf[pe]);
-        }
-      }
     }
-    if (tt.in_lds) __syncthreads();
   }
 }
 
+template <typename Cfg>
 unsigned tiles_for(int64_t count, int buf_dtype) {
   const int64_t v = buf_dtype == HVDX_FLOAT32 ? 4 : 8;
-  const int64_t per = (int64_t)kTileVecs * v;
+  const int64_t per = (int64_t)Cfg::kTileVecs * v;
   return (unsigned)((count + per - 1) / per);
 }
 
 }  // namespace
 
+template <typename Cfg>
+int ranks_per_block(int nranks) { return Cfg::RPB > 0 && Cfg::RPB < nranks ? Cfg::RPB : nranks; }
+
 hipError_t launch_pack(const void* const* srcs, const int64_t* numel, const int64_t* offset, int ntensors,
                        int src_dtype, const RankPtrs& bufs, int64_t count, int buf_dtype, int nranks,
                        hipStream_t stream) {
-  const dim3 grid(tiles_for(count, buf_dtype));
+  const int rpb = ranks_per_block<PackCfg>(nranks);
+  const dim3 grid(tiles_for<PackCfg>(count, buf_dtype), (nranks + rpb - 1) / rpb);
   if (src_dtype == HVDX_FLOAT32 && buf_dtype == HVDX_FLOAT32)
-    hipLaunchKernelGGL((pack_kernel<float, float>), grid, dim3(kBlock), 0, stream, srcs, numel, offset, ntensors,
-                       bufs, count, nranks);
+    hipLaunchKernelGGL((pack_kernel<float, float, PackCfg>), grid, dim3(kBlock), 0, stream, srcs, numel, offset, ntensors,
+                       bufs, count, nranks, rpb);
   else if (src_dtype == HVDX_FLOAT32 && buf_dtype == HVDX_FLOAT16)
-    hipLaunchKernelGGL((pack_kernel<float, _Float16>), grid, dim3(kBlock), 0, stream, srcs, numel, offset,
-                       ntensors, bufs, count, nranks);
+    hipLaunchKernelGGL((pack_kernel<float, _Float16, PackCfg>), grid, dim3(kBlock), 0, stream, srcs, numel, offset,
+                       ntensors, bufs, count, nranks, rpb);
   else
-    hipLaunchKernelGGL((pack_kernel<_Float16, _Float16>), grid, dim3(kBlock), 0, stream, srcs, numel, offset,
-                       ntensors, bufs, count, nranks);
+    hipLaunchKernelGGL((pack_kernel<_Float16, _Float16, PackCfg>), grid, dim3(kBlock), 0, stream, srcs, numel, offset,
+                       ntensors, bufs, count, nranks, rpb);
   return hipGetLastError();
 }
 
 hipError_t launch_unpack(const RankPtrs& bufs, int64_t count, int buf_dtype, void* const* dsts,
                          const int64_t* numel, const int64_t* offset, int ntensors, int dst_dtype, int nranks,
                          hipStream_t stream) {
-  const dim3 grid(tiles_for(count, buf_dtype));
+  const int rpb = ranks_per_block<UnpackCfg>(nranks);
+  const dim3 grid(tiles_for<UnpackCfg>(count, buf_dtype), (nranks + rpb - 1) / rpb);
   if (dst_dtype == HVDX_FLOAT32 && buf_dtype == HVDX_FLOAT32)
-    hipLaunchKernelGGL((unpack_kernel<float, float>), grid, dim3(kBlock), 0, stream, bufs, count, dsts, numel,
-                       offset, ntensors, nranks);
+    hipLaunchKernelGGL((unpack_kernel<float, float, UnpackCfg>), grid, dim3(kBlock), 0, stream, bufs, count, dsts, numel,
+                       offset, ntensors, nranks, rpb);
   else if (dst_dtype == HVDX_FLOAT32 && buf_dtype == HVDX_FLOAT16)
-    hipLaunchKernelGGL((unpack_kernel<float, _Float16>), grid, dim3(kBlock), 0, stream, bufs, count, dsts, numel,
-                       offset, ntensors, nranks);
+    hipLaunchKernelGGL((unpack_kernel<float, _Float16, UnpackCfg>), grid, dim3(kBlock), 0, stream, bufs, count, dsts, numel,
+                       offset, ntensors, nranks, rpb);
   else
-    hipLaunchKernelGGL((unpack_kernel<_Float16, _Float16>), grid, dim3(kBlock), 0, stream, bufs, count, dsts,
-                       numel, offset, ntensors, nranks);
+    hipLaunchKernelGGL((unpack_kernel<_Float16, _Float16, UnpackCfg>), grid, dim3(kBlock), 0, stream, bufs, count, dsts,
+                       numel, offset, ntensors, nranks, rpb);
   return hipGetLastError();
 }
 

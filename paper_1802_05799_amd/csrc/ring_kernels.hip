@@ -35,7 +35,6 @@ struct Vec<_Float16> {
   static constexpr int n = 8;
 };
 
-constexpr int kUnroll = 4;  // 16-byte vectors in flight per lane and stream
 
 template <int DIV>
 __device__ __forceinline__ float finish(float v, const RingArgs& a) {
@@ -96,12 +95,47 @@ __device__ __forceinline__ int64_t head_elems(const void* p, int64_t len) {
   return h < len ? h : len;
 }
 
+// ---- launch policies ---------------------------------------------------------------
+//
+// Two shapes, chosen by the size of one rank buffer.  Measured on MI355X: when a
+// step's working set (about 3x a rank buffer) fits the 256 MB Infinity Cache the
+// best reduce-scatter keeps loads cached and streams its stores non-temporally
+// (the next step re-reads what this one wrote from the cache), and the best
+// all-gather is plain with two vectors per lane; when it does not fit, one vector
+// per lane with every access non-temporal streams closest to the HBM limit.
+template <int U_, int BS_, bool NTL_, bool NTS_>
+struct Policy {
+  static constexpr int U = U_;      // 16-byte vectors per lane and stream
+  static constexpr int BS = BS_;    // threads per block
+  static constexpr bool NTL = NTL_; // non-temporal loads
+  static constexpr bool NTS = NTS_; // non-temporal stores
+};
+using RsCached = Policy<4, 256, false, true>;
+using RsStream = Policy<1, 256, true, true>;
+using AgCached = Policy<2, 512, false, false>;
+using AgStream = Policy<1, 256, true, true>;
+using C16Cached = Policy<2, 256, false, false>;
+using C16Stream = Policy<1, 256, true, true>;
+constexpr int64_t kStreamBytes = 128ll << 20;  // rank buffers at least this large stream
+
+template <bool NT, typename V>
+__device__ __forceinline__ V vload(const V* p) {
+  if constexpr (NT) return __builtin_nontemporal_load(p);
+  return *p;
+}
+template <bool NT, typename V>
+__device__ __forceinline__ void vstore(V* p, V v) {
+  if constexpr (NT) __builtin_nontemporal_store(v, p);
+  else *p = v;
+}
+
 // ---- plain ring (buffers of type T) ---------------------------------------------------
 
-template <typename T, int DIV, bool VEC_OK>
-__global__ __launch_bounds__(kBlock) void rs_step_kernel(RankPtrs bufs, RingArgs a) {
+template <typename T, int DIV, bool VEC_OK, typename P>
+__global__ __launch_bounds__(P::BS) void rs_step_kernel(RankPtrs bufs, RingArgs a) {
   using VT = typename Vec<T>::type;
   constexpr int V = Vec<T>::n;
+  constexpr int BS = P::BS, U = P::U;
   const int c = blockIdx.y;
   const Chunk ch = chunk_of(c, a);
   const int snd = rs_sender(c, a.step, a.n);
@@ -112,37 +146,37 @@ __global__ __launch_bounds__(kBlock) void rs_step_kernel(RankPtrs bufs, RingArgs
   const int64_t head = VEC_OK ? head_elems<T>(dst, ch.len) : ch.len;
   const int64_t nvec = (ch.len - head) / V;
   const int64_t tail = head + nvec * V;
-  const int64_t gtid = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-  const int64_t gthreads = (int64_t)gridDim.x * kBlock;
+  const int64_t gtid = (int64_t)blockIdx.x * BS + threadIdx.x;
+  const int64_t gthreads = (int64_t)gridDim.x * BS;
   for (int64_t e = gtid; e < head; e += gthreads) dst[e] = combine1<DIV>(dst[e], src[e], a);
   for (int64_t e = tail + gtid; e < ch.len; e += gthreads) dst[e] = combine1<DIV>(dst[e], src[e], a);
 
   const VT* __restrict__ s4 = reinterpret_cast<const VT*>(src + head);
   VT* __restrict__ d4 = reinterpret_cast<VT*>(dst + head);
-  for (int64_t base = (int64_t)blockIdx.x * kBlock * kUnroll + threadIdx.x; base < nvec;
-       base += gthreads * kUnroll) {
-    VT x[kUnroll], y[kUnroll];
-    if (base + (kUnroll - 1) * kBlock < nvec) {  // whole tile: all loads in flight at once
+  for (int64_t base = (int64_t)blockIdx.x * BS * U + threadIdx.x; base < nvec; base += gthreads * U) {
+    VT x[U], y[U];
+    if (base + (U - 1) * BS < nvec) {  // whole tile: all loads in flight at once
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
-        x[u] = s4[base + u * kBlock];
-        y[u] = d4[base + u * kBlock];
+      for (int u = 0; u < U; ++u) {
+        x[u] = vload<P::NTL>(s4 + base + u * BS);
+        y[u] = vload<P::NTL>(d4 + base + u * BS);
       }
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u) d4[base + u * kBlock] = combine<DIV>(y[u], x[u], a);
+      for (int u = 0; u < U; ++u) vstore<P::NTS>(d4 + base + u * BS, combine<DIV>(y[u], x[u], a));
       continue;
     }
-    for (int u = 0; u < kUnroll; ++u) {
-      const int64_t i = base + u * kBlock;
+    for (int u = 0; u < U; ++u) {
+      const int64_t i = base + u * BS;
       if (i < nvec) d4[i] = combine<DIV>(d4[i], s4[i], a);
     }
   }
 }
 
-template <typename T, bool VEC_OK>
-__global__ __launch_bounds__(kBlock) void ag_step_kernel(RankPtrs bufs, RingArgs a) {
+template <typename T, bool VEC_OK, typename P>
+__global__ __launch_bounds__(P::BS) void ag_step_kernel(RankPtrs bufs, RingArgs a) {
   using VT = typename Vec<T>::type;
   constexpr int V = Vec<T>::n;
+  constexpr int BS = P::BS, U = P::U;
   const int c = blockIdx.y;
   const Chunk ch = chunk_of(c, a);
   const int snd = ag_sender(c, a.step, a.n);
@@ -153,25 +187,24 @@ __global__ __launch_bounds__(kBlock) void ag_step_kernel(RankPtrs bufs, RingArgs
   const int64_t head = VEC_OK ? head_elems<T>(dst, ch.len) : ch.len;
   const int64_t nvec = (ch.len - head) / V;
   const int64_t tail = head + nvec * V;
-  const int64_t gtid = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-  const int64_t gthreads = (int64_t)gridDim.x * kBlock;
+  const int64_t gtid = (int64_t)blockIdx.x * BS + threadIdx.x;
+  const int64_t gthreads = (int64_t)gridDim.x * BS;
   for (int64_t e = gtid; e < head; e += gthreads) dst[e] = src[e];
   for (int64_t e = tail + gtid; e < ch.len; e += gthreads) dst[e] = src[e];
 
   const VT* __restrict__ s4 = reinterpret_cast<const VT*>(src + head);
   VT* __restrict__ d4 = reinterpret_cast<VT*>(dst + head);
-  for (int64_t base = (int64_t)blockIdx.x * kBlock * kUnroll + threadIdx.x; base < nvec;
-       base += gthreads * kUnroll) {
-    VT x[kUnroll];
-    if (base + (kUnroll - 1) * kBlock < nvec) {
+  for (int64_t base = (int64_t)blockIdx.x * BS * U + threadIdx.x; base < nvec; base += gthreads * U) {
+    VT x[U];
+    if (base + (U - 1) * BS < nvec) {
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u) x[u] = s4[base + u * kBlock];
+      for (int u = 0; u < U; ++u) x[u] = vload<P::NTL>(s4 + base + u * BS);
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u) d4[base + u * kBlock] = x[u];
+      for (int u = 0; u < U; ++u) vstore<P::NTS>(d4 + base + u * BS, x[u]);
       continue;
     }
-    for (int u = 0; u < kUnroll; ++u) {
-      const int64_t i = base + u * kBlock;
+    for (int u = 0; u < U; ++u) {
+      const int64_t i = base + u * BS;
       if (i < nvec) d4[i] = s4[i];
     }
   }
@@ -204,8 +237,9 @@ __device__ __forceinline__ void from_f16x8(f16x8 h, f32x4& lo, f32x4& hi) {
   }
 }
 
-template <int DIV, bool FIRST, bool VEC_OK>
-__global__ __launch_bounds__(kBlock) void rs_step_c16_kernel(RankPtrs x, _Float16* wire, RingArgs a) {
+template <int DIV, bool FIRST, bool VEC_OK, typename P>
+__global__ __launch_bounds__(P::BS) void rs_step_c16_kernel(RankPtrs x, _Float16* wire, RingArgs a) {
+  constexpr int BS = P::BS, U = P::U;
   const int c = blockIdx.y;
   const Chunk ch = chunk_of(c, a);
   const int snd = rs_sender(c, a.step, a.n);
@@ -218,8 +252,8 @@ __global__ __launch_bounds__(kBlock) void rs_step_c16_kernel(RankPtrs x, _Float1
   const int64_t head = VEC_OK ? head_elems<_Float16>(wr, ch.len) : ch.len;
   const int64_t nvec = (ch.len - head) / 8;
   const int64_t tail = head + nvec * 8;
-  const int64_t gtid = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-  const int64_t gthreads = (int64_t)gridDim.x * kBlock;
+  const int64_t gtid = (int64_t)blockIdx.x * BS + threadIdx.x;
+  const int64_t gthreads = (int64_t)gridDim.x * BS;
   auto one = [&](int64_t e) {
     const _Float16 sent = FIRST ? (_Float16)xs[e] : ws[e];
     wr[e] = combine1<DIV>((_Float16)xr[e], sent, a);
@@ -231,26 +265,28 @@ __global__ __launch_bounds__(kBlock) void rs_step_c16_kernel(RankPtrs x, _Float1
   const f32x4* __restrict__ xr4 = reinterpret_cast<const f32x4*>(xr + head);
   const f16x8* __restrict__ ws8 = reinterpret_cast<const f16x8*>(ws + head);
   f16x8* __restrict__ wr8 = reinterpret_cast<f16x8*>(wr + head);
-  for (int64_t base = (int64_t)blockIdx.x * kBlock * 2 + threadIdx.x; base < nvec; base += gthreads * 2) {
-    f16x8 sent[2], mine[2];
+  for (int64_t base = (int64_t)blockIdx.x * BS * U + threadIdx.x; base < nvec; base += gthreads * U) {
+    f16x8 sent[U], mine[U];
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int64_t i = base + u * kBlock;
+    for (int u = 0; u < U; ++u) {
+      const int64_t i = base + u * BS;
       if (i < nvec) {
-        mine[u] = to_f16x8(xr4[2 * i], xr4[2 * i + 1]);
-        sent[u] = FIRST ? to_f16x8(xs4[2 * i], xs4[2 * i + 1]) : ws8[i];
+        mine[u] = to_f16x8(vload<P::NTL>(xr4 + 2 * i), vload<P::NTL>(xr4 + 2 * i + 1));
+        sent[u] = FIRST ? to_f16x8(vload<P::NTL>(xs4 + 2 * i), vload<P::NTL>(xs4 + 2 * i + 1))
+                        : vload<P::NTL>(ws8 + i);
       }
     }
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int64_t i = base + u * kBlock;
-      if (i < nvec) wr8[i] = combine<DIV>(mine[u], sent[u], a);
+    for (int u = 0; u < U; ++u) {
+      const int64_t i = base + u * BS;
+      if (i < nvec) vstore<P::NTS>(wr8 + i, combine<DIV>(mine[u], sent[u], a));
     }
   }
 }
 
-template <bool FIRST, bool LAST, bool VEC_OK>
-__global__ __launch_bounds__(kBlock) void ag_step_c16_kernel(RankPtrs x, _Float16* wire, RingArgs a) {
+template <bool FIRST, bool LAST, bool VEC_OK, typename P>
+__global__ __launch_bounds__(P::BS) void ag_step_c16_kernel(RankPtrs x, _Float16* wire, RingArgs a) {
+  constexpr int BS = P::BS, U = P::U;
   const int c = blockIdx.y;
   const Chunk ch = chunk_of(c, a);
   const int snd = ag_sender(c, a.step, a.n);
@@ -263,8 +299,8 @@ __global__ __launch_bounds__(kBlock) void ag_step_c16_kernel(RankPtrs x, _Float1
   const int64_t head = VEC_OK ? head_elems<_Float16>(wr, ch.len) : ch.len;
   const int64_t nvec = (ch.len - head) / 8;
   const int64_t tail = head + nvec * 8;
-  const int64_t gtid = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-  const int64_t gthreads = (int64_t)gridDim.x * kBlock;
+  const int64_t gtid = (int64_t)blockIdx.x * BS + threadIdx.x;
+  const int64_t gthreads = (int64_t)gridDim.x * BS;
   auto one = [&](int64_t e) {
     const _Float16 h = ws[e];
     const float f = (float)h;
@@ -279,27 +315,26 @@ __global__ __launch_bounds__(kBlock) void ag_step_c16_kernel(RankPtrs x, _Float1
   f32x4* __restrict__ xr4 = reinterpret_cast<f32x4*>(xr + head);
   const f16x8* __restrict__ ws8 = reinterpret_cast<const f16x8*>(ws + head);
   f16x8* __restrict__ wr8 = reinterpret_cast<f16x8*>(wr + head);
-  for (int64_t base = (int64_t)blockIdx.x * kBlock * kUnroll + threadIdx.x; base < nvec;
-       base += gthreads * kUnroll) {
-    f16x8 h[kUnroll];
+  for (int64_t base = (int64_t)blockIdx.x * BS * U + threadIdx.x; base < nvec; base += gthreads * U) {
+    f16x8 h[U];
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      const int64_t i = base + u * kBlock;
-      if (i < nvec) h[u] = ws8[i];
+    for (int u = 0; u < U; ++u) {
+      const int64_t i = base + u * BS;
+      if (i < nvec) h[u] = vload<P::NTL>(ws8 + i);
     }
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      const int64_t i = base + u * kBlock;
+    for (int u = 0; u < U; ++u) {
+      const int64_t i = base + u * BS;
       if (i < nvec) {
         f32x4 lo, hi;
         from_f16x8(h[u], lo, hi);
         if (FIRST) {
-          xs4[2 * i] = lo;
-          xs4[2 * i + 1] = hi;
+          vstore<P::NTS>(xs4 + 2 * i, lo);
+          vstore<P::NTS>(xs4 + 2 * i + 1, hi);
         }
-        xr4[2 * i] = lo;
-        xr4[2 * i + 1] = hi;
-        if (!LAST) wr8[i] = h[u];
+        vstore<P::NTS>(xr4 + 2 * i, lo);
+        vstore<P::NTS>(xr4 + 2 * i + 1, hi);
+        if (!LAST) vstore<P::NTS>(wr8 + i, h[u]);
       }
     }
   }
@@ -312,22 +347,24 @@ __global__ __launch_bounds__(kBlock) void roundtrip_c16_kernel(float* x, int64_t
     x[e] = (float)(_Float16)x[e];
 }
 
-// ---- grid sizing ----------------------------------------------------------------------
+// ---- grid sizing and dispatch --------------------------------------------------------
 
-// Blocks per chunk: enough for one pass with kUnroll vectors per lane, at least 1.
-dim3 step_grid(const RingArgs& a, int elems_per_vec, int unroll) {
+// Blocks per chunk: enough for one pass over the longest chunk, at least 1.
+dim3 step_grid(const RingArgs& a, int elems_per_vec, int unroll, int bs) {
   const int64_t longest = a.q + (a.rem ? 1 : 0);
   const int64_t vecs = longest / elems_per_vec + 2;
-  int64_t bx = (vecs + (int64_t)kBlock * unroll - 1) / ((int64_t)kBlock * unroll);
+  int64_t bx = (vecs + (int64_t)bs * unroll - 1) / ((int64_t)bs * unroll);
   if (bx < 1) bx = 1;
   if (bx > (1 << 20)) bx = 1 << 20;
   return dim3((unsigned)bx, (unsigned)a.n, 1);
 }
 
-template <typename T>
-hipError_t rs_dispatch(const RankPtrs& bufs, const RingArgs& a, int divmode, bool vec_ok, hipStream_t st) {
-  const dim3 grid = step_grid(a, Vec<T>::n, kUnroll);
-#define HVDX_RS(DIV, VOK) hipLaunchKernelGGL((rs_step_kernel<T, DIV, VOK>), grid, dim3(kBlock), 0, st, bufs, a)
+bool streams(const RingArgs& a, int esize) { return (a.q + 1) * a.n * (int64_t)esize >= kStreamBytes; }
+
+template <typename T, typename P>
+void rs_launch(const RankPtrs& bufs, const RingArgs& a, int divmode, bool vec_ok, hipStream_t st) {
+  const dim3 grid = step_grid(a, Vec<T>::n, P::U, P::BS);
+#define HVDX_RS(DIV, VOK) hipLaunchKernelGGL((rs_step_kernel<T, DIV, VOK, P>), grid, dim3(P::BS), 0, st, bufs, a)
   if (vec_ok) {
     if (divmode == DIV_NONE) HVDX_RS(DIV_NONE, true);
     else if (divmode == DIV_POW2) HVDX_RS(DIV_POW2, true);
@@ -338,17 +375,73 @@ hipError_t rs_dispatch(const RankPtrs& bufs, const RingArgs& a, int divmode, boo
     else HVDX_RS(DIV_TRUE, false);
   }
 #undef HVDX_RS
+}
+
+template <typename T>
+hipError_t rs_dispatch(const RankPtrs& bufs, const RingArgs& a, int divmode, bool vec_ok, hipStream_t st) {
+  if (streams(a, sizeof(T))) rs_launch<T, RsStream>(bufs, a, divmode, vec_ok, st);
+  else rs_launch<T, RsCached>(bufs, a, divmode, vec_ok, st);
   return hipGetLastError();
+}
+
+template <typename T, typename P>
+void ag_launch(const RankPtrs& bufs, const RingArgs& a, bool vec_ok, hipStream_t st) {
+  const dim3 grid = step_grid(a, Vec<T>::n, P::U, P::BS);
+  if (vec_ok)
+    hipLaunchKernelGGL((ag_step_kernel<T, true, P>), grid, dim3(P::BS), 0, st, bufs, a);
+  else
+    hipLaunchKernelGGL((ag_step_kernel<T, false, P>), grid, dim3(P::BS), 0, st, bufs, a);
 }
 
 template <typename T>
 hipError_t ag_dispatch(const RankPtrs& bufs, const RingArgs& a, bool vec_ok, hipStream_t st) {
-  const dim3 grid = step_grid(a, Vec<T>::n, kUnroll);
-  if (vec_ok)
-    hipLaunchKernelGGL((ag_step_kernel<T, true>), grid, dim3(kBlock), 0, st, bufs, a);
-  else
-    hipLaunchKernelGGL((ag_step_kernel<T, false>), grid, dim3(kBlock), 0, st, bufs, a);
+  if (streams(a, sizeof(T))) ag_launch<T, AgStream>(bufs, a, vec_ok, st);
+  else ag_launch<T, AgCached>(bufs, a, vec_ok, st);
   return hipGetLastError();
+}
+
+template <typename P>
+void rs_c16_launch(const RankPtrs& x, _Float16* w, const RingArgs& a, int divmode, bool vector_ok,
+                   hipStream_t stream) {
+  const dim3 grid = step_grid(a, 8, P::U, P::BS);
+  const bool first = a.step == 0;
+#define HVDX_RSC(DIV, F, VOK) \
+  hipLaunchKernelGGL((rs_step_c16_kernel<DIV, F, VOK, P>), grid, dim3(P::BS), 0, stream, x, w, a)
+#define HVDX_RSC_V(DIV, F) \
+  if (vector_ok) HVDX_RSC(DIV, F, true); else HVDX_RSC(DIV, F, false)
+#define HVDX_RSC_F(DIV) \
+  if (first) { HVDX_RSC_V(DIV, true); } else { HVDX_RSC_V(DIV, false); }
+  if (divmode == DIV_NONE) {
+    HVDX_RSC_F(DIV_NONE)
+  } else if (divmode == DIV_POW2) {
+    HVDX_RSC_F(DIV_POW2)
+  } else {
+    HVDX_RSC_F(DIV_TRUE)
+  }
+#undef HVDX_RSC_F
+#undef HVDX_RSC_V
+#undef HVDX_RSC
+}
+
+template <typename P>
+void ag_c16_launch(const RankPtrs& x, _Float16* w, const RingArgs& a, bool vector_ok, hipStream_t stream) {
+  const dim3 grid = step_grid(a, 8, P::U, P::BS);
+  const bool first = a.step == 0, last = a.step == a.n - 2;
+#define HVDX_AGC(F, L, VOK) \
+  hipLaunchKernelGGL((ag_step_c16_kernel<F, L, VOK, P>), grid, dim3(P::BS), 0, stream, x, w, a)
+#define HVDX_AGC_V(F, L) \
+  if (vector_ok) HVDX_AGC(F, L, true); else HVDX_AGC(F, L, false)
+  if (first && last) {
+    HVDX_AGC_V(true, true);
+  } else if (first) {
+    HVDX_AGC_V(true, false);
+  } else if (last) {
+    HVDX_AGC_V(false, true);
+  } else {
+    HVDX_AGC_V(false, false);
+  }
+#undef HVDX_AGC_V
+#undef HVDX_AGC
 }
 
 }  // namespace
@@ -366,47 +459,16 @@ hipError_t launch_ag_step(const RankPtrs& bufs, const RingArgs& a, int dtype, bo
 
 hipError_t launch_rs_step_c16(const RankPtrs& x, void* wire, const RingArgs& a, int divmode, bool vector_ok,
                               hipStream_t stream) {
-  const dim3 grid = step_grid(a, 8, 2);
   _Float16* w = static_cast<_Float16*>(wire);
-  const bool first = a.step == 0;
-#define HVDX_RSC(DIV, F, VOK) \
-  hipLaunchKernelGGL((rs_step_c16_kernel<DIV, F, VOK>), grid, dim3(kBlock), 0, stream, x, w, a)
-#define HVDX_RSC_V(DIV, F) \
-  if (vector_ok) HVDX_RSC(DIV, F, true); else HVDX_RSC(DIV, F, false)
-#define HVDX_RSC_F(DIV) \
-  if (first) { HVDX_RSC_V(DIV, true); } else { HVDX_RSC_V(DIV, false); }
-  if (divmode == DIV_NONE) {
-    HVDX_RSC_F(DIV_NONE)
-  } else if (divmode == DIV_POW2) {
-    HVDX_RSC_F(DIV_POW2)
-  } else {
-    HVDX_RSC_F(DIV_TRUE)
-  }
-#undef HVDX_RSC_F
-#undef HVDX_RSC_V
-#undef HVDX_RSC
+  if (streams(a, 4)) rs_c16_launch<C16Stream>(x, w, a, divmode, vector_ok, stream);
+  else rs_c16_launch<C16Cached>(x, w, a, divmode, vector_ok, stream);
   return hipGetLastError();
 }
 
 hipError_t launch_ag_step_c16(const RankPtrs& x, void* wire, const RingArgs& a, bool vector_ok, hipStream_t stream) {
-  const dim3 grid = step_grid(a, 8, kUnroll);
   _Float16* w = static_cast<_Float16*>(wire);
-  const bool first = a.step == 0, last = a.step == a.n - 2;
-#define HVDX_AGC(F, L, VOK) \
-  hipLaunchKernelGGL((ag_step_c16_kernel<F, L, VOK>), grid, dim3(kBlock), 0, stream, x, w, a)
-#define HVDX_AGC_V(F, L) \
-  if (vector_ok) HVDX_AGC(F, L, true); else HVDX_AGC(F, L, false)
-  if (first && last) {
-    HVDX_AGC_V(true, true);
-  } else if (first) {
-    HVDX_AGC_V(true, false);
-  } else if (last) {
-    HVDX_AGC_V(false, true);
-  } else {
-    HVDX_AGC_V(false, false);
-  }
-#undef HVDX_AGC_V
-#undef HVDX_AGC
+  if (streams(a, 4)) ag_c16_launch<C16Stream>(x, w, a, vector_ok, stream);
+  else ag_c16_launch<C16Cached>(x, w, a, vector_ok, stream);
   return hipGetLastError();
 }
 
