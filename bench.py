@@ -38,6 +38,9 @@ def parse():
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="target oracle time for the CPU baseline")
     p.add_argument("--calibration-copy-mib", type=int, default=0,
                    help="first run 3 plain device copies of this many MiB (a known-traffic kernel for counters)")
+    p.add_argument("--summarize-profiles", metavar="DIR",
+                   help="no GPU: summarize rocprofv3 output under DIR (prof_*/ kernel stats, pmc_fetch/, pmc_write/) "
+                        "into profiles/")
     return p.parse_args()
 
 
@@ -102,19 +105,22 @@ def measure(name, steps, warmup):
     wall = time.perf_counter() - t0
     ms = e0.elapsed_time(e1) / steps
 
-    # the same steps once more, with an event pair around each run of consecutive
-    # launches of one kernel (e.g. the N-1 reduce-scatter steps of a bucket), so the
-    # events add little to what they measure
-    launches = ar.launches(sid)
+    # the same steps once more with one HIP event pair around each library call: the
+    # copy-in, the N-1 reduce-scatter steps, the N-1 all-gather steps and the copy-out
+    # of every bucket (a phase's launches leave the C library back to back, so its
+    # events cost little and average over N-1 launches of one kernel)
     groups = []
-    for kind, bi, s, fn in launches:
-        key = (kernel_name(ar, kind, bi), bi, kind)
-        if groups and groups[-1][0] == key:
-            groups[-1][1].append((kind, bi, s, fn))
-        else:
-            groups.append((key, [(kind, bi, s, fn)]))
-    # every step's events are created up front and read after one final sync, so the
-    # host never stalls the GPU between an event pair; one untimed traced step first
+    for bi, b in enumerate(ar.buckets):
+        if not b.direct:
+            groups.append(("pack", bi, [-1], lambda b=b: ar.pack(b, sid)))
+        if ar.nranks > 1:
+            steps_ = list(range(ar.nranks - 1))
+            groups.append(("rs", bi, steps_, lambda b=b: ar.ring_phase(b, hv.PHASE_REDUCE_SCATTER, sid)))
+            groups.append(("ag", bi, steps_, lambda b=b: ar.ring_phase(b, hv.PHASE_ALLGATHER, sid)))
+        elif b.direct and ar.compress:
+            groups.append(("ring", bi, [-1], lambda b=b: ar.ring(b, sid)))
+        if not b.direct:
+            groups.append(("unpack", bi, [-1], lambda b=b: ar.unpack(b, sid)))
     evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in groups]
            for _ in range(steps + 1)]
     for step_evs in evs:  # torch creates the HIP events on first record: do that outside the timing
@@ -123,21 +129,20 @@ def measure(name, steps, warmup):
             b.record(stream)
     torch.cuda.synchronize()
     if hasattr(torch.cuda, "_sleep"):  # a bounded spin lets the host enqueue ahead of the GPU
-        torch.cuda._sleep(50_000_000)
+        torch.cuda._sleep(20_000_000)
     for step_evs in evs:
-        for (key, items), (a, b) in zip(groups, step_evs):
+        for (kind, bi, ss, fn), (a, b) in zip(groups, step_evs):
             a.record(stream)
-            for _kind, _bi, _s, fn in items:
-                fn()
+            fn()
             b.record(stream)
     torch.cuda.synchronize()
     per_kernel = {}
-    for step_evs in evs[1:]:
-        for (key, items), (a, b) in zip(groups, step_evs):
-            d = per_kernel.setdefault(key[0], {"launches": 0, "ms": 0.0, "bytes": 0})
-            d["launches"] += len(items)
+    for step_evs in evs[1:]:  # the first traced step is a warm-up
+        for (kind, bi, ss, fn), (a, b) in zip(groups, step_evs):
+            d = per_kernel.setdefault(kernel_name(ar, kind, bi), {"launches": 0, "ms": 0.0, "bytes": 0})
+            d["launches"] += len(ss)
             d["ms"] += a.elapsed_time(b)
-            d["bytes"] += sum(kernel_bytes(ar, kind, bi, s) for kind, bi, s, _fn in items)
+            d["bytes"] += sum(kernel_bytes(ar, kind, bi, s) for s in ss)
     traced_ms = sum(d["ms"] for d in per_kernel.values()) / steps
     for d in per_kernel.values():
         d["avg_us"] = 1000.0 * d["ms"] / d["launches"]
@@ -181,6 +186,75 @@ def traffic_for(kernel, workload):
     return rec.get("per_launch_bytes", {}).get(f"{workload}/{kernel}")
 
 
+def short_kernel_name(full):
+    """rocprofv3 kernel name -> the names bench.py reports."""
+    base = full.replace("(anonymous namespace)", "anon").split("(")[0]
+    for key, short in (("rs_step_c16_kernel", "rs_step_c16"), ("ag_step_c16_kernel", "ag_step_c16"),
+                       ("roundtrip_c16_kernel", "ring")):
+        if key in base:
+            return short
+    for key in ("rs_step_kernel", "ag_step_kernel"):
+        if key in base:
+            return key.replace("_kernel", "") + ("_f16" if "<_Float16" in base else "_f32")
+    if "unpack_kernel" in base:
+        return "unpack"
+    if "pack_kernel" in base:
+        return "pack"
+    return None
+
+
+def summarize_profiles(d):
+    """Per-kernel average duration (kernel trace) and HBM bytes per dispatch (FETCH_SIZE,
+    WRITE_SIZE), each counter scaled by what it reads for a plain 1 GiB device copy."""
+    import csv
+    import glob
+
+    out_lines, traffic = [], {}
+    stats = sorted(glob.glob(os.path.join(d, "prof_*", "*_kernel_stats.csv")))
+    for f in stats:
+        workload = os.path.basename(os.path.dirname(f))[len("prof_"):]
+        rows = list(csv.DictReader(open(f)))
+        out_lines.append(f"## kernel trace: {workload}\n")
+        out_lines.append("| kernel | instantiation | calls | average us | total ms |\n|---|---|---|---|---|")
+        for r in rows:
+            k = short_kernel_name(r["Name"])
+            if k:
+                name = r["Name"].replace("(anonymous namespace)::", "").split("(")[0].replace("void hvdx::", "")
+                out_lines.append(f"| {k} | `{name}` | {r['Calls']} | "
+                                 f"{float(r['AverageNs']) / 1e3:.2f} | {float(r['TotalDurationNs']) / 1e6:.2f} |")
+        out_lines.append("")
+    pmc = {}
+    for counter, sub in (("FETCH_SIZE", "pmc_fetch"), ("WRITE_SIZE", "pmc_write")):
+        files = glob.glob(os.path.join(d, sub, "*_counter_collection.csv"))
+        if not files:
+            continue
+        rows = [r for r in csv.DictReader(open(files[0])) if r["Counter_Name"] == counter]
+        cal = [float(r["Counter_Value"]) for r in rows
+               if "copyBuffer" in r["Kernel_Name"] and int(r["Grid_Size"]) >= (1 << 17)]
+        if not cal:
+            continue
+        factor = (1 << 20) / (sum(cal) / len(cal))  # a 1 GiB copy reads and writes 2^20 KiB
+        per = {}
+        for r in rows:
+            k = short_kernel_name(r["Kernel_Name"])
+            if k:
+                per.setdefault(k, []).append(float(r["Counter_Value"]) * factor * 1024)
+        pmc[counter] = (factor, {k: sum(v) / len(v) for k, v in per.items()})
+    if len(pmc) == 2:
+        (ff, fetch), (fw, write) = pmc["FETCH_SIZE"], pmc["WRITE_SIZE"]
+        out_lines.append("## HBM traffic per dispatch (resnet50 workload)\n")
+        out_lines.append(f"calibration: a 1 GiB device copy reads FETCH_SIZE x {ff:.3f} and WRITE_SIZE x {fw:.3f}\n")
+        out_lines.append("| kernel | fetch MB | write MB | total MB |\n|---|---|---|---|")
+        for k in sorted(fetch):
+            tot = fetch[k] + write.get(k, 0.0)
+            traffic[f"resnet50/{k}"] = round(tot)
+            out_lines.append(f"| {k} | {fetch[k] / 1e6:.1f} | {write.get(k, 0.0) / 1e6:.1f} | {tot / 1e6:.1f} |")
+        with open(TRAFFIC_FILE, "w") as f:
+            json.dump({"source_hash": kernel_source_hash(), "per_launch_bytes": traffic,
+                       "calibration": {"FETCH_SIZE": ff, "WRITE_SIZE": fw}}, f, indent=1)
+    return "\n".join(out_lines)
+
+
 def cpu_baseline(name, target_s):
     """The oracle (plan, copy-in, ring, copy-out) on a bounded sample of the workload:
     all N ranks, the last tensors of the ready list (the network's first layers, many
@@ -221,6 +295,9 @@ def cpu_baseline(name, target_s):
 
 def main():
     args = parse()
+    if args.summarize_profiles:
+        print(summarize_profiles(args.summarize_profiles))
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print(
             "bench.py runs on one GPU: the N simulated ranks live side by side in that GPU's memory, "

@@ -167,6 +167,27 @@ int hvdx_ring_allreduce(void* const* bufs, int nranks, int64_t count, int dtype,
                         void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * hvdx_ring_reduce_scatter / hvdx_ring_allgather -- the two halves of
+ * hvdx_ring_allreduce (paper section 3: the N-1 adding iterations, then the N-1
+ * replacing iterations), each one call.  Running the first and then the second
+ * with the same arguments and workspace is hvdx_ring_allreduce.
+ *
+ * After the reduce-scatter half, rank (c-1) mod N holds chunk c of the reduced
+ * result (with AVERAGE already divided) -- in its buffer, or, when compressing,
+ * in its binary16 wire copy inside `workspace`, which the all-gather half then
+ * needs unchanged.  The other chunks of every rank hold intermediate values.
+ * The all-gather half copies each such chunk around the ring so every rank ends
+ * with all of them; used on its own (no compression) it gathers rank r's chunk
+ * (r+1) mod N into every rank.  With nranks = 1 both are no-ops, except that the
+ * compressed reduce-scatter rounds the buffer through binary16.
+ * Arguments and errors as hvdx_ring_allreduce.
+ */
+int hvdx_ring_reduce_scatter(void* const* bufs, int nranks, int64_t count, int dtype, int op, int compress,
+                             void* workspace, size_t workspace_bytes, void* stream);
+int hvdx_ring_allgather(void* const* bufs, int nranks, int64_t count, int dtype, int op, int compress,
+                        void* workspace, size_t workspace_bytes, void* stream);
+
+/*
  * hvdx_ring_step -- one step of hvdx_ring_allreduce (all N transfers of adding or
  * replacing step `step`, 0 <= step < nranks-1), for tracing and for checking
  * intermediate states.  Running phase REDUCE_SCATTER steps 0..N-2 then
@@ -184,6 +205,44 @@ size_t hvdx_ring_workspace_bytes(int nranks, int64_t count, int dtype, int compr
  * start = c*q + min(c, r), len = q + (c < r) with q, r = count / nranks,
  * count % nranks.  Host only.  HVDX_ERR_INVALID for bad arguments. */
 int hvdx_ring_chunk(int64_t count, int nranks, int c, int64_t* start, int64_t* len);
+
+/*
+ * Timeline (paper section 6: a per-node record of what the collective did at each
+ * step, viewable in Chrome's about:tracing).  Between hvdx_timeline_begin and
+ * hvdx_timeline_end every kernel this library launches, from any thread and on any
+ * stream, is bracketed by a pair of HIP events that the library owns; no device
+ * memory is allocated.
+ *
+ *   hvdx_timeline_begin(capacity)  start recording up to `capacity` (>= 1)
+ *       launches; launches past that are counted as dropped.  Returns
+ *       HVDX_ERR_INVALID if a timeline is already recording or capacity < 1,
+ *       HVDX_ERR_HIP if the events cannot be created.
+ *   hvdx_timeline_end(out, capacity, nrecords, ndropped)  wait for the recorded
+ *       launches to finish, write up to `capacity` records to the host array
+ *       `out` in launch order, set *nrecords and *ndropped, stop recording and
+ *       release the events.  Times are microseconds from the start of the first
+ *       recorded launch.  HVDX_ERR_INVALID if no timeline is recording.
+ */
+#define HVDX_KERNEL_PACK 0
+#define HVDX_KERNEL_REDUCE_SCATTER 1
+#define HVDX_KERNEL_ALLGATHER 2
+#define HVDX_KERNEL_UNPACK 3
+#define HVDX_KERNEL_ROUNDTRIP 4 /* one-rank compressed ring: round to binary16 and back */
+
+typedef struct hvdx_trace_record {
+  int32_t kind;     /* HVDX_KERNEL_* */
+  int32_t step;     /* ring step for REDUCE_SCATTER / ALLGATHER, else -1 */
+  int32_t nranks;
+  int32_t dtype;    /* buffer element type */
+  int32_t compress; /* HVDX_COMPRESS_* of the ring */
+  int32_t reserved;
+  int64_t count;    /* buffer elements per rank */
+  double start_us;
+  double duration_us;
+} hvdx_trace_record;
+
+int hvdx_timeline_begin(int capacity);
+int hvdx_timeline_end(hvdx_trace_record* out, int capacity, int* nrecords, int* ndropped);
 
 /* Text for a status code (static storage). */
 const char* hvdx_strerror(int status);

@@ -33,14 +33,19 @@ from ._lib import (  # noqa: F401
     hvdx_fuse_plan,
     hvdx_fuse_unpack,
     hvdx_last_error,
+    hvdx_ring_allgather,
     hvdx_ring_allreduce,
     hvdx_ring_chunk,
+    hvdx_ring_reduce_scatter,
     hvdx_ring_step,
     hvdx_ring_workspace_bytes,
     hvdx_strerror,
+    hvdx_timeline_begin,
+    hvdx_timeline_end,
     hvdx_version,
 )
 from .cycle import FusedAllreduce  # noqa: F401
+from .timeline import Timeline  # noqa: F401
 
 
 def allreduce_(per_rank, op: str = "average", compress: bool = False,

@@ -36,12 +36,34 @@ _SIGNATURES = {
     "hvdx_fuse_unpack": (_i, [_pp, _i64, _i, _p, _p, _p, _i, _i, _i, _p]),
     "hvdx_ring_allreduce": (_i, [_pp, _i, _i64, _i, _i, _i, _p, _sz, _p]),
     "hvdx_ring_step": (_i, [_pp, _i, _i64, _i, _i, _i, _i, _i, _p, _sz, _p]),
+    "hvdx_ring_reduce_scatter": (_i, [_pp, _i, _i64, _i, _i, _i, _p, _sz, _p]),
+    "hvdx_ring_allgather": (_i, [_pp, _i, _i64, _i, _i, _i, _p, _sz, _p]),
     "hvdx_ring_workspace_bytes": (_sz, [_i, _i64, _i, _i]),
     "hvdx_ring_chunk": (_i, [_i64, _i, _i, _pi64, _pi64]),
     "hvdx_strerror": (ctypes.c_char_p, [_i]),
     "hvdx_last_error": (ctypes.c_char_p, []),
     "hvdx_version": (_i, []),
+    "hvdx_timeline_begin": (_i, [_i]),
+    "hvdx_timeline_end": (_i, [_p, _i, ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_int)]),
 }
+
+KERNEL_PACK, KERNEL_REDUCE_SCATTER, KERNEL_ALLGATHER, KERNEL_UNPACK, KERNEL_ROUNDTRIP = 0, 1, 2, 3, 4
+
+
+class TraceRecord(ctypes.Structure):
+    """hvdx_trace_record"""
+
+    _fields_ = [
+        ("kind", ctypes.c_int32),
+        ("step", ctypes.c_int32),
+        ("nranks", ctypes.c_int32),
+        ("dtype", ctypes.c_int32),
+        ("compress", ctypes.c_int32),
+        ("reserved", ctypes.c_int32),
+        ("count", ctypes.c_int64),
+        ("start_us", ctypes.c_double),
+        ("duration_us", ctypes.c_double),
+    ]
 
 
 class HvdxError(RuntimeError):
@@ -52,7 +74,7 @@ class HvdxError(RuntimeError):
 
 def _load():
     if not os.path.exists(LIB_PATH):
-        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_1802_05799_amd.build`")
+        raise ImportError(f"{LIB_PATH} is not built; run `python paper_1802_05799_amd/build.py`")
     lib = ctypes.CDLL(LIB_PATH)
     for name, (res, args) in _SIGNATURES.items():
         fn = getattr(lib, name)
@@ -133,8 +155,33 @@ def hvdx_ring_allreduce(bufs, nranks: int, count: int, dtype: int, op: int, comp
     _check(lib.hvdx_ring_allreduce(pb, nranks, count, dtype, op, compress, workspace, workspace_bytes, stream))
 
 
+def hvdx_ring_reduce_scatter(bufs, nranks: int, count: int, dtype: int, op: int, compress: int = COMPRESS_NONE,
+                             workspace: int = 0, workspace_bytes: int = 0, stream: int = 0) -> None:
+    pb, _keep = _ptr_array(bufs)
+    _check(lib.hvdx_ring_reduce_scatter(pb, nranks, count, dtype, op, compress, workspace, workspace_bytes, stream))
+
+
+def hvdx_ring_allgather(bufs, nranks: int, count: int, dtype: int, op: int, compress: int = COMPRESS_NONE,
+                        workspace: int = 0, workspace_bytes: int = 0, stream: int = 0) -> None:
+    pb, _keep = _ptr_array(bufs)
+    _check(lib.hvdx_ring_allgather(pb, nranks, count, dtype, op, compress, workspace, workspace_bytes, stream))
+
+
 def hvdx_ring_step(bufs, nranks: int, count: int, dtype: int, op: int, compress: int, phase: int, step: int,
                    workspace: int = 0, workspace_bytes: int = 0, stream: int = 0) -> None:
     pb, _keep = _ptr_array(bufs)
     _check(lib.hvdx_ring_step(pb, nranks, count, dtype, op, compress, phase, step, workspace, workspace_bytes,
                               stream))
+
+
+def hvdx_timeline_begin(capacity: int) -> None:
+    _check(lib.hvdx_timeline_begin(capacity))
+
+
+def hvdx_timeline_end(capacity: int):
+    """Return (records as dicts, number dropped)."""
+    arr = (TraceRecord * max(1, capacity))()
+    n, dropped = ctypes.c_int(), ctypes.c_int()
+    _check(lib.hvdx_timeline_end(ctypes.cast(arr, ctypes.c_void_p), capacity, ctypes.byref(n), ctypes.byref(dropped)))
+    recs = [{f: getattr(arr[i], f) for f, _ in TraceRecord._fields_ if f != "reserved"} for i in range(n.value)]
+    return recs, dropped.value

@@ -1,6 +1,8 @@
 """Build libhvdx.so for gfx950 with hipcc (in-tree, next to this file).
 
-    python -m paper_1802_05799_amd.build
+    python paper_1802_05799_amd/build.py
+
+(Run it as a file: importing the package loads the library being rebuilt.)
 """
 from __future__ import annotations
 

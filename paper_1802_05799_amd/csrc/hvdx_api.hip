@@ -6,6 +6,7 @@
 #include <stdio.h>
 
 #include <algorithm>
+#include <mutex>
 #include <utility>
 #include <vector>
 
@@ -14,6 +15,67 @@
 namespace {
 
 thread_local char g_last_error[512] = "";
+
+// ---- timeline state ----------------------------------------------------------------
+struct TimelineEntry {
+  hvdx_trace_record rec;
+  hipEvent_t start, end;
+};
+
+struct Timeline {
+  std::mutex mu;
+  bool on = false;
+  int capacity = 0;
+  int dropped = 0;
+  std::vector<hipEvent_t> pool;  // 2 * capacity events, created at begin
+  std::vector<TimelineEntry> entries;
+};
+
+Timeline& timeline() {
+  static Timeline t;
+  return t;
+}
+
+// Brackets one kernel launch with timeline events when a timeline is recording.
+class TimedLaunch {
+ public:
+  TimedLaunch(int kind, int step, int nranks, int dtype, int compress, int64_t count, hipStream_t st)
+      : st_(st) {
+    Timeline& t = timeline();
+    lock_ = std::unique_lock<std::mutex>(t.mu);
+    if (!t.on) {
+      lock_.unlock();
+      return;
+    }
+    if ((int)t.entries.size() >= t.capacity) {
+      ++t.dropped;
+      lock_.unlock();
+      return;
+    }
+    TimelineEntry e{};
+    e.rec.kind = kind;
+    e.rec.step = step;
+    e.rec.nranks = nranks;
+    e.rec.dtype = dtype;
+    e.rec.compress = compress;
+    e.rec.count = count;
+    e.start = t.pool[2 * t.entries.size()];
+    e.end = t.pool[2 * t.entries.size() + 1];
+    if (hipEventRecord(e.start, st_) == hipSuccess) {
+      t.entries.push_back(e);
+      end_ = e.end;
+    }
+  }
+  // The lock is still held here: recording ends before another launch can start one.
+  ~TimedLaunch() {
+    if (end_) (void)hipEventRecord(end_, st_);
+  }
+
+ private:
+  hipStream_t st_;
+  hipEvent_t end_ = nullptr;
+  std::unique_lock<std::mutex> lock_;
+};
 
 int fail(int code, const char* fmt, ...) {
   va_list ap;
@@ -135,6 +197,8 @@ int run_step(void* const* bufs, int nranks, int64_t count, int dtype, int op, in
   const hvdx::RankPtrs p = rank_ptrs(bufs, nranks);
   const bool vok = vectors_ok(bufs, nranks, workspace);
   const int dm = step == nranks - 2 ? div_mode(op, nranks) : hvdx::DIV_NONE;
+  TimedLaunch timed(phase == HVDX_PHASE_REDUCE_SCATTER ? HVDX_KERNEL_REDUCE_SCATTER : HVDX_KERNEL_ALLGATHER, step,
+                    nranks, dtype, compress, count, st);
   hipError_t e;
   if (compress == HVDX_COMPRESS_FP16) {
     e = phase == HVDX_PHASE_REDUCE_SCATTER ? hvdx::launch_rs_step_c16(p, workspace, a, dm, vok, st)
@@ -171,6 +235,63 @@ int check_fusion(const void* const* tensors, const int64_t* numel, const int64_t
 extern "C" {
 
 int hvdx_version(void) { return HVDX_VERSION; }
+
+int hvdx_timeline_begin(int capacity) {
+  if (capacity < 1 || capacity > (1 << 24)) return fail(HVDX_ERR_INVALID, "hvdx_timeline_begin: bad capacity %d", capacity);
+  Timeline& t = timeline();
+  std::lock_guard<std::mutex> g(t.mu);
+  if (t.on) return fail(HVDX_ERR_INVALID, "hvdx_timeline_begin: a timeline is already recording");
+  t.pool.assign(2 * (size_t)capacity, nullptr);
+  for (auto& ev : t.pool) {
+    const hipError_t e = hipEventCreate(&ev);
+    if (e != hipSuccess) {
+      for (auto& x : t.pool)
+        if (x) (void)hipEventDestroy(x);
+      t.pool.clear();
+      return hip_fail(e, "hvdx_timeline_begin: hipEventCreate");
+    }
+  }
+  t.entries.clear();
+  t.entries.reserve(capacity);
+  t.capacity = capacity;
+  t.dropped = 0;
+  t.on = true;
+  return HVDX_OK;
+}
+
+int hvdx_timeline_end(hvdx_trace_record* out, int capacity, int* nrecords, int* ndropped) {
+  if (!nrecords || !ndropped || capacity < 0 || (capacity > 0 && !out))
+    return fail(HVDX_ERR_INVALID, "hvdx_timeline_end: bad arguments");
+  Timeline& t = timeline();
+  std::lock_guard<std::mutex> g(t.mu);
+  if (!t.on) return fail(HVDX_ERR_INVALID, "hvdx_timeline_end: no timeline is recording");
+  t.on = false;
+  int rc = HVDX_OK;
+  const int n = (int)t.entries.size();
+  hipError_t e = hipSuccess;
+  for (int i = 0; i < n && e == hipSuccess; ++i) e = hipEventSynchronize(t.entries[i].end);
+  if (e != hipSuccess) rc = hip_fail(e, "hvdx_timeline_end: hipEventSynchronize");
+  int written = 0;
+  for (int i = 0; i < n && written < capacity && rc == HVDX_OK; ++i) {
+    float t0 = 0.f, dur = 0.f;
+    e = hipEventElapsedTime(&t0, t.entries[0].start, t.entries[i].start);
+    if (e == hipSuccess) e = hipEventElapsedTime(&dur, t.entries[i].start, t.entries[i].end);
+    if (e != hipSuccess) {
+      rc = hip_fail(e, "hvdx_timeline_end: hipEventElapsedTime");
+      break;
+    }
+    out[written] = t.entries[i].rec;
+    out[written].start_us = 1000.0 * t0;
+    out[written].duration_us = 1000.0 * dur;
+    ++written;
+  }
+  *nrecords = written;
+  *ndropped = t.dropped + (n - written);
+  for (auto& ev : t.pool) (void)hipEventDestroy(ev);
+  t.pool.clear();
+  t.entries.clear();
+  return rc;
+}
 
 const char* hvdx_last_error(void) { return g_last_error; }
 
@@ -260,6 +381,8 @@ int hvdx_fuse_pack(const void* const* srcs, const int64_t* numel, const int64_t*
                         "hvdx_fuse_pack");
   if (rc) return rc;
   if (buf_count == 0) return HVDX_OK;
+  TimedLaunch timed(HVDX_KERNEL_PACK, -1, nranks, buf_dtype, HVDX_COMPRESS_NONE, buf_count,
+                    static_cast<hipStream_t>(stream));
   const hipError_t e = hvdx::launch_pack(srcs, numel, offset, ntensors, src_dtype, rank_ptrs(bufs, nranks),
                                          buf_count, buf_dtype, nranks, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? HVDX_OK : hip_fail(e, "pack launch");
@@ -272,6 +395,8 @@ int hvdx_fuse_unpack(const void* const* bufs, int64_t buf_count, int buf_dtype, 
                         "hvdx_fuse_unpack");
   if (rc) return rc;
   if (buf_count == 0) return HVDX_OK;
+  TimedLaunch timed(HVDX_KERNEL_UNPACK, -1, nranks, buf_dtype, HVDX_COMPRESS_NONE, buf_count,
+                    static_cast<hipStream_t>(stream));
   const hipError_t e =
       hvdx::launch_unpack(rank_ptrs(const_cast<void* const*>(bufs), nranks), buf_count, buf_dtype, dsts, numel,
                           offset, ntensors, dst_dtype, nranks, static_cast<hipStream_t>(stream));
@@ -291,23 +416,45 @@ int hvdx_ring_step(void* const* bufs, int nranks, int64_t count, int dtype, int 
                   static_cast<hipStream_t>(stream));
 }
 
-int hvdx_ring_allreduce(void* const* bufs, int nranks, int64_t count, int dtype, int op, int compress,
-                        void* workspace, size_t workspace_bytes, void* stream) {
-  int rc = check_ring(bufs, nranks, count, dtype, op, compress, workspace, workspace_bytes, "hvdx_ring_allreduce");
+// The N-1 steps of one phase; the one-rank compressed ring rounds in the adding phase.
+static int run_phase(void* const* bufs, int nranks, int64_t count, int dtype, int op, int compress, int phase,
+                     void* workspace, size_t workspace_bytes, void* stream, const char* what) {
+  int rc = check_ring(bufs, nranks, count, dtype, op, compress, workspace, workspace_bytes, what);
   if (rc) return rc;
   if (count == 0) return HVDX_OK;
   hipStream_t st = static_cast<hipStream_t>(stream);
   if (nranks == 1) {  // no messages; AVERAGE divides by 1; compression still rounds
-    if (compress != HVDX_COMPRESS_FP16) return HVDX_OK;
+    if (compress != HVDX_COMPRESS_FP16 || phase != HVDX_PHASE_REDUCE_SCATTER) return HVDX_OK;
+    TimedLaunch timed(HVDX_KERNEL_ROUNDTRIP, -1, 1, dtype, compress, count, st);
     const hipError_t e = hvdx::launch_roundtrip_c16(bufs[0], count, st);
     return e == hipSuccess ? HVDX_OK : hip_fail(e, "fp16 round-trip launch");
   }
-  for (int phase = HVDX_PHASE_REDUCE_SCATTER; phase <= HVDX_PHASE_ALLGATHER; ++phase)
-    for (int s = 0; s < nranks - 1; ++s) {
-      rc = run_step(bufs, nranks, count, dtype, op, compress, phase, s, workspace, st);
-      if (rc) return rc;
-    }
+  for (int s = 0; s < nranks - 1; ++s) {
+    rc = run_step(bufs, nranks, count, dtype, op, compress, phase, s, workspace, st);
+    if (rc) return rc;
+  }
   return HVDX_OK;
+}
+
+int hvdx_ring_reduce_scatter(void* const* bufs, int nranks, int64_t count, int dtype, int op, int compress,
+                             void* workspace, size_t workspace_bytes, void* stream) {
+  return run_phase(bufs, nranks, count, dtype, op, compress, HVDX_PHASE_REDUCE_SCATTER, workspace,
+                   workspace_bytes, stream, "hvdx_ring_reduce_scatter");
+}
+
+int hvdx_ring_allgather(void* const* bufs, int nranks, int64_t count, int dtype, int op, int compress,
+                        void* workspace, size_t workspace_bytes, void* stream) {
+  return run_phase(bufs, nranks, count, dtype, op, compress, HVDX_PHASE_ALLGATHER, workspace, workspace_bytes,
+                   stream, "hvdx_ring_allgather");
+}
+
+int hvdx_ring_allreduce(void* const* bufs, int nranks, int64_t count, int dtype, int op, int compress,
+                        void* workspace, size_t workspace_bytes, void* stream) {
+  int rc = run_phase(bufs, nranks, count, dtype, op, compress, HVDX_PHASE_REDUCE_SCATTER, workspace,
+                     workspace_bytes, stream, "hvdx_ring_allreduce");
+  if (rc) return rc;
+  return run_phase(bufs, nranks, count, dtype, op, compress, HVDX_PHASE_ALLGATHER, workspace, workspace_bytes,
+                   stream, "hvdx_ring_allreduce");
 }
 
 }  // extern "C"

@@ -20,6 +20,7 @@ from dataclasses import dataclass
 import torch
 
 from . import _lib as L
+from . import timeline as _timeline
 
 _TORCH_DTYPE = {L.FLOAT32: torch.float32, L.FLOAT16: torch.float16}
 _HVDX_DTYPE = {torch.float32: L.FLOAT32, torch.float16: L.FLOAT16}
@@ -90,6 +91,7 @@ class FusedAllreduce:
             b.ptrs_dev = torch.tensor([self.tensors[r][t].data_ptr() for r in range(n) for t in b.tensors],
                                       dtype=torch.int64, device=dev)
         self._buf_ptrs = [x.data_ptr() for x in self.bufs]
+        _timeline.start_from_env()
 
     # ---- the steps, exposed separately for tracing ------------------------------------
     def pack(self, b: Bucket, stream: int) -> None:
@@ -112,6 +114,12 @@ class FusedAllreduce:
         ptrs, count, dtype, compress, ws, wsb = self.ring_args(b)
         L.hvdx_ring_allreduce(ptrs, self.nranks, count, dtype, self.op, compress, ws, wsb, stream)
 
+    def ring_phase(self, b: Bucket, phase: int, stream: int) -> None:
+        """All N-1 steps of one half of the ring (one C call)."""
+        ptrs, count, dtype, compress, ws, wsb = self.ring_args(b)
+        fn = L.hvdx_ring_reduce_scatter if phase == L.PHASE_REDUCE_SCATTER else L.hvdx_ring_allgather
+        fn(ptrs, self.nranks, count, dtype, self.op, compress, ws, wsb, stream)
+
     def ring_step(self, b: Bucket, phase: int, step: int, stream: int) -> None:
         ptrs, count, dtype, compress, ws, wsb = self.ring_args(b)
         L.hvdx_ring_step(ptrs, self.nranks, count, dtype, self.op, compress, phase, step, ws, wsb, stream)
@@ -119,14 +127,15 @@ class FusedAllreduce:
     def launches(self, stream: int):
         """The allreduce as its separate kernel launches, in order:
         (kind, bucket index, step, zero-argument callable).  kind is "pack", "rs",
-        "ag", "unpack", or "ring" (a whole one-rank ring).  Running them all in order
-        is one call of this object."""
+        "ag", "unpack", or "ring" (the one-rank compressed ring, a round trip through
+        binary16).  Running them all in order is one call of this object."""
         out = []
         for bi, b in enumerate(self.buckets):
             if not b.direct:
                 out.append(("pack", bi, -1, lambda b=b: self.pack(b, stream)))
             if self.nranks == 1:
-                out.append(("ring", bi, -1, lambda b=b: self.ring(b, stream)))
+                if b.direct and self.compress:  # the only one-rank ring that launches a kernel
+                    out.append(("ring", bi, -1, lambda b=b: self.ring(b, stream)))
             else:
                 for ph, kind in ((L.PHASE_REDUCE_SCATTER, "rs"), (L.PHASE_ALLGATHER, "ag")):
                     for s in range(self.nranks - 1):

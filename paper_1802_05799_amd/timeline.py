@@ -1,0 +1,104 @@
+"""Timeline of the allreduce's kernel launches (paper section 6, Horovod Timeline).
+
+The paper's timeline shows what every node did at each time step in Chrome's
+about:tracing viewer and is switched on by one environment variable.  Here the
+library brackets each kernel it launches with HIP events while a timeline
+records (hvdx_timeline_begin / hvdx_timeline_end); this module turns the records
+into Chrome trace JSON with one track per simulated rank, naming for every ring
+step the chunk the rank sends to its right neighbour and the chunk it receives
+from its left one, plus one track for the GPU kernels themselves.
+
+    with Timeline() as tl:
+        allreduce()
+    tl.save("trace.json")
+
+or set HVDX_TIMELINE=trace.json before the first FusedAllreduce is built: every
+allreduce of the process is then recorded and the trace written at exit.
+"""
+from __future__ import annotations
+
+import atexit
+import json
+import os
+
+from . import _lib as L
+
+KIND_NAMES = {
+    L.KERNEL_PACK: "copy in",
+    L.KERNEL_REDUCE_SCATTER: "reduce-scatter",
+    L.KERNEL_ALLGATHER: "allgather",
+    L.KERNEL_UNPACK: "copy out",
+    L.KERNEL_ROUNDTRIP: "fp16 round trip",
+}
+
+
+def chunks_of_step(kind: int, step: int, rank: int, n: int):
+    """(chunk sent to rank+1, chunk received from rank-1) in one ring step: in adding
+    step s rank r sends chunk (r - s) mod N, in replacing step s chunk (r + 1 - s) mod N."""
+    if kind == L.KERNEL_REDUCE_SCATTER:
+        return (rank - step) % n, (rank - 1 - step) % n
+    return (rank + 1 - step) % n, (rank - step) % n
+
+
+class Timeline:
+    def __init__(self, capacity: int = 1 << 16):
+        self.capacity = capacity
+        self.records: list = []
+        self.dropped = 0
+
+    def __enter__(self):
+        L.hvdx_timeline_begin(self.capacity)
+        return self
+
+    def __exit__(self, *exc):
+        self.records, self.dropped = L.hvdx_timeline_end(self.capacity)
+        return False
+
+    def chrome_trace(self) -> dict:
+        events = [
+            {"ph": "M", "pid": 0, "tid": 0, "name": "process_name", "args": {"name": "hvdx (one MI355X)"}},
+            {"ph": "M", "pid": 0, "tid": 0, "name": "thread_name", "args": {"name": "GPU kernels"}},
+        ]
+        named = set()
+        for rec in self.records:
+            kind, n, step = rec["kind"], rec["nranks"], rec["step"]
+            name = KIND_NAMES.get(kind, str(kind)) + (f" {step}" if step >= 0 else "")
+            common = {"ph": "X", "pid": 0, "ts": rec["start_us"], "dur": rec["duration_us"], "cat": "hvdx"}
+            events.append(dict(common, tid=0, name=name, args={"elements_per_rank": rec["count"], "ranks": n}))
+            for r in range(n):
+                if r not in named:
+                    named.add(r)
+                    events.append({"ph": "M", "pid": 0, "tid": r + 1, "name": "thread_name",
+                                   "args": {"name": f"rank {r}"}})
+                args = {}
+                if kind in (L.KERNEL_REDUCE_SCATTER, L.KERNEL_ALLGATHER):
+                    sent, recv = chunks_of_step(kind, step, r, n)
+                    args = {"send chunk": sent, "to": (r + 1) % n, "recv chunk": recv, "from": (r - 1) % n,
+                            "received values": "added" if kind == L.KERNEL_REDUCE_SCATTER else "replace"}
+                events.append(dict(common, tid=r + 1, name=name, args=args))
+        return {"traceEvents": events, "displayTimeUnit": "ms",
+                "otherData": {"dropped_launches": self.dropped}}
+
+    def save(self, path: str) -> None:
+        with open(path, "w") as f:
+            json.dump(self.chrome_trace(), f)
+
+
+_env_timeline: Timeline | None = None
+
+
+def start_from_env() -> None:
+    """Record every launch of this process into $HVDX_TIMELINE (written at exit)."""
+    global _env_timeline
+    path = os.environ.get("HVDX_TIMELINE")
+    if not path or _env_timeline is not None:
+        return
+    tl = Timeline(int(os.environ.get("HVDX_TIMELINE_CAPACITY", 1 << 20)))
+    tl.__enter__()
+    _env_timeline = tl
+
+    def finish():
+        tl.__exit__(None, None, None)
+        tl.save(path)
+
+    atexit.register(finish)

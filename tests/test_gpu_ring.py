@@ -151,3 +151,43 @@ def test_streams_and_repeat_calls():
     s.synchronize()
     want = ring.ring_allreduce(ring.ring_allreduce(x.copy(), "sum"), "sum")
     assert_bits_equal(from_gpu_rows(rows), want, "twice")
+
+
+def test_reduce_scatter_and_allgather_halves():
+    """hvdx_ring_reduce_scatter leaves rank (c-1) holding chunk c of the result (the
+    oracle's state after the adding half); hvdx_ring_allgather then completes the
+    allreduce; alone, the all-gather spreads rank r's chunk (r+1) to every rank."""
+    rng = np.random.default_rng(107)
+    for n, count, dtype, compress in ((3, 7, np.float32, False), (5, 10007, np.float32, False),
+                                      (8, 33001, np.float16, False), (6, 4099, np.float32, True)):
+        say(f"halves n={n} count={count} {np.dtype(dtype).name} compress={compress}")
+        x = inputs(rng, n, count, dtype)
+        states = []
+        base = fusion.cast(x, np.float16) if compress else x.copy()
+        ring.ring_allreduce(base, "average", observe=lambda ph, s, b: states.append(b.copy()))
+        rows, keep = to_gpu_rows(x)
+        ptrs = [r.data_ptr() for r in rows]
+        dt = hv.FLOAT32 if dtype == np.float32 else hv.FLOAT16
+        cmp = hv.COMPRESS_FP16 if compress else hv.COMPRESS_NONE
+        wsb = hv.hvdx_ring_workspace_bytes(n, count, dt, cmp)
+        ws = torch.zeros(max(wsb, 1), dtype=torch.uint8, device="cuda")
+        hv.hvdx_ring_reduce_scatter(ptrs, n, count, dt, hv.AVERAGE, cmp, ws.data_ptr() if wsb else 0, wsb)
+        starts, lengths = ring.chunk_bounds(count, n)
+        if not compress:
+            got = from_gpu_rows(rows)
+            for c in range(n):
+                sl = slice(starts[c], starts[c] + lengths[c])
+                assert_bits_equal(got[(c - 1) % n, sl], states[n - 2][(c - 1) % n, sl], f"owner of chunk {c}")
+        hv.hvdx_ring_allgather(ptrs, n, count, dt, hv.AVERAGE, cmp, ws.data_ptr() if wsb else 0, wsb)
+        want = fusion.cast(states[-1], np.float32) if compress else states[-1]
+        assert_bits_equal(from_gpu_rows(rows), want, "after both halves")
+    # the all-gather half alone
+    n, count = 5, 1003
+    x = inputs(rng, n, count, np.float32)
+    rows, keep = to_gpu_rows(x)
+    hv.hvdx_ring_allgather([r.data_ptr() for r in rows], n, count, hv.FLOAT32, hv.SUM)
+    starts, lengths = ring.chunk_bounds(count, n)
+    want = np.empty(count, np.float32)
+    for c in range(n):
+        want[starts[c] : starts[c] + lengths[c]] = x[(c - 1) % n, starts[c] : starts[c] + lengths[c]]
+    assert_bits_equal(from_gpu_rows(rows), np.broadcast_to(want, (n, count)).copy(), "allgather alone")

@@ -1,0 +1,68 @@
+"""The timeline on the GPU: one record per launch, in launch order, and a Chrome trace."""
+import json
+import os
+import subprocess
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import paper_1802_05799_amd as hv
+from _gpu import say
+
+pytestmark = pytest.mark.gpu
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def tensors(n, numel, seed=0):
+    g = np.random.default_rng(seed)
+    return [[torch.from_numpy((g.standard_normal(k) * 0.01).astype(np.float32)).cuda() for k in numel] for _ in range(n)]
+
+
+def test_records_follow_launches():
+    say("timeline records")
+    per_rank = tensors(5, [7, 4000, 100, 30000, 5])
+    ar = hv.FusedAllreduce(per_rank, op="average", threshold_bytes=40000)
+    sid = torch.cuda.current_stream().cuda_stream
+    launches = ar.launches(sid)
+    with hv.Timeline(capacity=1000) as tl:
+        ar(sid)
+        ar(sid)
+    assert tl.dropped == 0 and len(tl.records) == 2 * len(launches)
+    code = {"pack": 0, "rs": 1, "ag": 2, "unpack": 3}
+    for rec, (kind, bi, s, _fn) in zip(tl.records, launches + launches):
+        assert rec["kind"] == code[kind] and rec["step"] == s and rec["nranks"] == 5
+        assert rec["count"] == ar.buckets[bi].count and rec["duration_us"] > 0
+    starts = [r["start_us"] for r in tl.records]
+    assert starts[0] == 0 and starts == sorted(starts)
+    trace = tl.chrome_trace()
+    json.dumps(trace)
+    ranks = {e["tid"] for e in trace["traceEvents"] if e["ph"] == "X"}
+    assert ranks == set(range(6))  # GPU track + 5 ranks
+
+
+def test_capacity_counts_dropped_launches():
+    per_rank = tensors(3, [1000, 2000])
+    ar = hv.FusedAllreduce(per_rank)
+    with hv.Timeline(capacity=2) as tl:
+        ar()
+    assert len(tl.records) == 2 and tl.dropped == len(ar.launches(0)) - 2
+
+
+def test_environment_variable_writes_trace(tmp_path):
+    path = tmp_path / "trace.json"
+    code = (
+        "import sys; sys.path.insert(0, %r)\n"
+        "import torch, paper_1802_05799_amd as hv\n"
+        "xs = [[torch.ones(1000, device='cuda'), torch.ones(77, device='cuda')] for _ in range(4)]\n"
+        "ar = hv.FusedAllreduce(xs)\n"
+        "ar(); ar(); torch.cuda.synchronize()\n" % ROOT
+    )
+    say("timeline env subprocess")
+    env = dict(os.environ, HVDX_TIMELINE=str(path))
+    subprocess.run([sys.executable, "-c", code], env=env, check=True, timeout=120)
+    trace = json.loads(path.read_text())
+    names = [e["name"] for e in trace["traceEvents"] if e["ph"] == "X" and e["tid"] == 0]
+    assert names == ["copy in", "reduce-scatter 0", "reduce-scatter 1", "reduce-scatter 2", "allgather 0",
+                     "allgather 1", "allgather 2", "copy out"] * 2
