@@ -35,6 +35,8 @@ def parse():
     p.add_argument("--workload", default="resnet50")
     p.add_argument("--no-per-config", action="store_true", help="time only the headline workload")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-ablation", action="store_true", help="skip the fusion-threshold sweep")
+    p.add_argument("--no-broadcast", action="store_true", help="skip the broadcast measurement")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="target oracle time for the CPU baseline")
     p.add_argument("--calibration-copy-mib", type=int, default=0,
                    help="first run 3 plain device copies of this many MiB (a known-traffic kernel for counters)")
@@ -56,6 +58,8 @@ def kernel_bytes(ar, kind, bi, step):
     if kind == "unpack":
         return n * (es_b + es_t) * data
     compressed = b.direct and ar.compress
+    if kind == "rs_ag":  # read owner and sender, write owner and the next rank
+        return 16 * b.count if compressed else 4 * (es_t if b.direct else es_b) * b.count
     if kind == "rs":
         if compressed:
             return (10 if step == 0 else 8) * b.count
@@ -69,16 +73,41 @@ def kernel_bytes(ar, kind, bi, step):
     return 0
 
 
+KIND_OF_CODE = {0: "pack", 1: "rs", 2: "ag", 3: "unpack", 4: "ring", 6: "rs_ag"}
+
+
+def phase_sequence(ar):
+    """(timeline kind code, bucket, first step, launches) of each per-phase record one
+    call of `ar` produces."""
+    out = []
+    n = ar.nranks
+    for bi, b in enumerate(ar.buckets):
+        if not b.direct:
+            out.append((0, bi, -1, 1))
+        if n == 1:
+            if b.direct and ar.compress:
+                out.append((4, bi, -1, 1))
+        else:
+            if n > 2:
+                out.append((1, bi, 0, n - 2))
+            out.append((6, bi, n - 2, 1))
+            if n > 2:
+                out.append((2, bi, 1, n - 2))
+        if not b.direct:
+            out.append((3, bi, -1, 1))
+    return out
+
+
 def kernel_name(ar, kind, bi):
     b = ar.buckets[bi]
-    if kind in ("rs", "ag"):
+    if kind in ("rs", "ag", "rs_ag"):
         if b.direct and ar.compress:
             return f"{kind}_step_c16"
         return f"{kind}_step_{'f16' if (ar.buf_dtype == 1 and not b.direct) else 'f32'}"
     return kind
 
 
-def measure(name, steps, warmup):
+def measure(name, steps, warmup, threshold=64 << 20, per_kernel_pass=True, schedule="ring"):
     import torch
 
     import paper_1802_05799_amd as hv
@@ -87,7 +116,7 @@ def measure(name, steps, warmup):
 
     w = configs.get(name)
     per_rank, storage, starts = wgpu.make_rank_tensors(w)
-    ar = hv.FusedAllreduce(per_rank, op=w.op, compress=w.compress)
+    ar = hv.FusedAllreduce(per_rank, op=w.op, compress=w.compress, threshold_bytes=threshold, schedule=schedule)
     stream = torch.cuda.current_stream()
     sid = stream.cuda_stream
     for _ in range(warmup):
@@ -104,45 +133,39 @@ def measure(name, steps, warmup):
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms = e0.elapsed_time(e1) / steps
+    if not per_kernel_pass:
+        res = {"ms_per_step": ms, "algbw_GBps": w.rank_bytes / (ms * 1e-3) / 1e9, "buckets": len(ar.buckets),
+               "launches_per_step": len(ar.kernel_sequence())}
+        del ar, per_rank, storage
+        torch.cuda.empty_cache()
+        return res
 
-    # the same steps once more with one HIP event pair around each library call: the
-    # copy-in, the N-1 reduce-scatter steps, the N-1 all-gather steps and the copy-out
-    # of every bucket (a phase's launches leave the C library back to back, so its
-    # events cost little and average over N-1 launches of one kernel)
-    groups = []
-    for bi, b in enumerate(ar.buckets):
-        if not b.direct:
-            groups.append(("pack", bi, [-1], lambda b=b: ar.pack(b, sid)))
-        if ar.nranks > 1:
-            steps_ = list(range(ar.nranks - 1))
-            groups.append(("rs", bi, steps_, lambda b=b: ar.ring_phase(b, hv.PHASE_REDUCE_SCATTER, sid)))
-            groups.append(("ag", bi, steps_, lambda b=b: ar.ring_phase(b, hv.PHASE_ALLGATHER, sid)))
-        elif b.direct and ar.compress:
-            groups.append(("ring", bi, [-1], lambda b=b: ar.ring(b, sid)))
-        if not b.direct:
-            groups.append(("unpack", bi, [-1], lambda b=b: ar.unpack(b, sid)))
-    evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in groups]
-           for _ in range(steps + 1)]
-    for step_evs in evs:  # torch creates the HIP events on first record: do that outside the timing
-        for a, b in step_evs:
-            a.record(stream)
-            b.record(stream)
-    torch.cuda.synchronize()
-    if hasattr(torch.cuda, "_sleep"):  # a bounded spin lets the host enqueue ahead of the GPU
-        torch.cuda._sleep(20_000_000)
-    for step_evs in evs:
-        for (kind, bi, ss, fn), (a, b) in zip(groups, step_evs):
-            a.record(stream)
-            fn()
-            b.record(stream)
-    torch.cuda.synchronize()
+    # the same steps once more under the library's per-phase timeline: HIP events
+    # recorded inside the C library around each run of one kernel (a bucket's
+    # copy-in, its plain adding steps, the fused adding/replacing step, its plain
+    # replacing steps, its copy-out).  Each record's median over the timed steps is
+    # kept: a sample the host stalled is an outlier, not a kernel duration.
+    with hv.Timeline(capacity=64 * (steps + 1) * max(1, len(ar.buckets)), per_phase=True) as tl:
+        for _ in range(steps + 1):
+            ar(sid)
+    recs = tl.records
+    per_step = len(recs) // (steps + 1)
+    if tl.dropped or per_step * (steps + 1) != len(recs):
+        raise RuntimeError(f"timeline recorded {len(recs)} records for {steps + 1} steps")
+    seq = phase_sequence(ar)
+    if [(k, st, la) for k, _bi, st, la in seq] != [(r["kind"], r["step"], r["launches"]) for r in recs[:per_step]]:
+        raise RuntimeError("timeline records do not follow the expected launch order")
     per_kernel = {}
-    for step_evs in evs[1:]:  # the first traced step is a warm-up
-        for (kind, bi, ss, fn), (a, b) in zip(groups, step_evs):
-            d = per_kernel.setdefault(kernel_name(ar, kind, bi), {"launches": 0, "ms": 0.0, "bytes": 0})
-            d["launches"] += len(ss)
-            d["ms"] += a.elapsed_time(b)
-            d["bytes"] += sum(kernel_bytes(ar, kind, bi, s) for s in ss)
+    outliers = 0
+    for i, (kcode, bi, st, la) in enumerate(seq):
+        samples = sorted(recs[j * per_step + i]["duration_us"] / 1000.0 for j in range(1, steps + 1))
+        med = samples[len(samples) // 2]
+        outliers += sum(1 for x in samples if x > 1.5 * med)
+        kind = KIND_OF_CODE[kcode]
+        d = per_kernel.setdefault(kernel_name(ar, kind, bi), {"launches": 0, "ms": 0.0, "bytes": 0})
+        d["launches"] += la * steps
+        d["ms"] += med * steps
+        d["bytes"] += sum(kernel_bytes(ar, kind, bi, s_) for s_ in range(st, st + la)) * steps
     traced_ms = sum(d["ms"] for d in per_kernel.values()) / steps
     for d in per_kernel.values():
         d["avg_us"] = 1000.0 * d["ms"] / d["launches"]
@@ -159,9 +182,55 @@ def measure(name, steps, warmup):
         "busbw_GBps": w.rank_bytes / (ms * 1e-3) / 1e9 * 2 * (w.nranks - 1) / w.nranks,
         "wall_ms_per_step": 1000.0 * wall / steps,
         "kernels": per_kernel,
+        "timing_outliers": outliers,
         "buckets": [(b.count, len(b.tensors), b.direct) for b in ar.buckets],
     }
     del ar, per_rank, storage
+    torch.cuda.empty_cache()
+    return res
+
+
+def measure_broadcast(name, steps, warmup=2):
+    """Rank 0's parameters to every rank (paper sections 4 and 5): one broadcast call
+    per tensor, and one call over each rank's whole contiguous parameter storage."""
+    import torch
+
+    import paper_1802_05799_amd as hv
+    from workloads import configs
+    from workloads import gpu as wgpu
+
+    w = configs.get(name)
+    per_rank, storage, starts = wgpu.make_rank_tensors(w)
+    stream = torch.cuda.current_stream()
+    sid = stream.cuda_stream
+    flat_ptrs = [x.data_ptr() for x in storage]
+    flat_bytes = storage[0].numel() * 4
+
+    def timed(fn):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(steps):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / steps
+
+    ms_tensors = timed(lambda: hv.broadcast_(per_rank, 0))
+    ms_flat = timed(lambda: hv.hvdx_broadcast(flat_ptrs, w.nranks, flat_bytes, 0, sid))
+    moved = 2 * (w.nranks - 1) * flat_bytes  # every non-root rank reads and writes each byte once
+    res = {
+        "workload": name,
+        "per_tensor_ms": round(ms_tensors, 4),
+        "per_tensor_algbw_GBps": round(w.rank_bytes / (ms_tensors * 1e-3) / 1e9, 2),
+        "flat_ms": round(ms_flat, 4),
+        "flat_algbw_GBps": round(flat_bytes / (ms_flat * 1e-3) / 1e9, 2),
+        "flat_hbm_GBps": round(moved / (ms_flat * 1e-3) / 1e9, 1),
+        "launches_per_tensor_call": 2 * w.nranks - 2,
+    }
+    del per_rank, storage
     torch.cuda.empty_cache()
     return res
 
@@ -189,11 +258,12 @@ def traffic_for(kernel, workload):
 def short_kernel_name(full):
     """rocprofv3 kernel name -> the names bench.py reports."""
     base = full.replace("(anonymous namespace)", "anon").split("(")[0]
-    for key, short in (("rs_step_c16_kernel", "rs_step_c16"), ("ag_step_c16_kernel", "ag_step_c16"),
-                       ("roundtrip_c16_kernel", "ring")):
+    for key, short in (("rs_ag_step_c16_kernel", "rs_ag_step_c16"), ("rs_step_c16_kernel", "rs_step_c16"),
+                       ("ag_step_c16_kernel", "ag_step_c16"), ("roundtrip_c16_kernel", "ring"),
+                       ("fold_kernel", "fold")):
         if key in base:
             return short
-    for key in ("rs_step_kernel", "ag_step_kernel"):
+    for key in ("rs_ag_step_kernel", "rs_step_kernel", "ag_step_kernel"):
         if key in base:
             return key.replace("_kernel", "") + ("_f16" if "<_Float16" in base else "_f32")
     if "unpack_kernel" in base:
@@ -345,6 +415,32 @@ def main():
                                 "share": round(v["share"], 4)} for k, v in r["kernels"].items()},
             }
 
+    # fusion ablation (paper section 7): the same workload with other buffer sizes;
+    # threshold 0 reduces every tensor with its own ring (no fusion)
+    ablation = {}
+    if not args.no_ablation:
+        for thr in (0, 1 << 20, 4 << 20, 16 << 20, 64 << 20, 256 << 20):
+            r = measure(args.workload, max(3, args.steps // 4), 2, threshold=thr, per_kernel_pass=False)
+            ablation[str(thr)] = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in r.items()}
+            print(f"# fusion threshold {thr}: {r['ms_per_step']:.3f} ms/step", file=sys.stderr, flush=True)
+
+    # the ring's fold computed directly (same bits, no per-step messages): a bound for
+    # one GPU, reported beside the ring, never as the headline value
+    fold = {}
+    if not args.no_per_config:
+        from workloads import configs
+
+        for name in configs.WORKLOADS:
+            r = measure(name, max(3, args.steps // 2), 2, per_kernel_pass=False, schedule="fold")
+            fold[name] = {"ms_per_step": round(r["ms_per_step"], 4), "algbw_GBps": round(r["algbw_GBps"], 2)}
+            print(f"# fold schedule {name}: {r['ms_per_step']:.3f} ms/step", file=sys.stderr, flush=True)
+
+    bcast = None
+    if not args.no_broadcast:
+        bcast = measure_broadcast(args.workload, max(3, args.steps // 2))
+        print(f"# broadcast: {bcast['flat_ms']:.3f} ms flat, {bcast['per_tensor_ms']:.3f} ms per tensor",
+              file=sys.stderr, flush=True)
+
     dom_name, dom = max(head["kernels"].items(), key=lambda kv: kv[1]["share"])
     roofline = {
         "bound": "hbm",
@@ -356,6 +452,8 @@ def main():
         "traffic": traffic_for(dom_name, args.workload),
         "avg_launch_us": round(dom["avg_us"], 2),
         "launches_per_step": dom["launches"] // args.steps,
+        "timing": "median over the timed steps of the library's per-phase timeline events, / launches in the phase",
+        "timing_outlier_samples": head["timing_outliers"],
         "algorithmic_bytes_per_step": dom["bytes"] // args.steps,
     }
     out = {
@@ -381,6 +479,9 @@ def main():
         "busbw_GBps": round(head["busbw_GBps"], 2),
         "roofline": roofline,
         "per_config": per_config,
+        "fusion_ablation": {"workload": args.workload, "by_threshold_bytes": ablation},
+        "broadcast": bcast,
+        "fold_schedule": fold,
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(args.workload, args.cpu_seconds)

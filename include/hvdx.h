@@ -158,7 +158,8 @@ int hvdx_fuse_unpack(const void* const* bufs, int64_t buf_count, int buf_dtype, 
  * Schedule: chunk c (of N near-equal contiguous chunks, the first count mod N
  * one element longer) moves from rank (c+s) mod N to (c+s+1) mod N in adding
  * step s and from rank (c-1+s) mod N to (c+s) mod N in replacing step s, so the
- * sum of chunk c is formed in ring order starting at rank c.  Each addition is
+ * sum of chunk c is formed in ring order starting at rank c.  (Adding step N-2
+ * and replacing step 0 run as one kernel here; the buffers end the same.)  Each addition is
  * rounded to nearest even in dtype (binary16 when compressed); AVERAGE divides
  * the complete sum by nranks once, correctly rounded, at the last adding step.
  * Errors: HVDX_ERR_INVALID, HVDX_ERR_ALIAS, HVDX_ERR_WORKSPACE, HVDX_ERR_HIP.
@@ -197,6 +198,37 @@ int hvdx_ring_allgather(void* const* bufs, int nranks, int64_t count, int dtype,
 int hvdx_ring_step(void* const* bufs, int nranks, int64_t count, int dtype, int op, int compress, int phase,
                    int step, void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * hvdx_broadcast -- copy rank `root`'s buffer into every other rank's buffer (paper
+ * section 4, the broadcast that gives every worker the same initial model;
+ * section 5, broadcasting the variables from the first process to all others).
+ * The bytes travel as a pipelined chain along the ring: the buffer is cut into N
+ * chunks of whole 16-byte units (the first (units mod N) chunks one unit longer;
+ * the last unit may be short), and in step s rank root+k forwards chunk s-k to rank
+ * root+k+1 (k = 0..N-2, when 0 <= s-k < N): 2N-2 steps.  Bytes are copied, not
+ * interpreted, so any element type works.
+ *
+ *   bufs[nranks]  host array of device pointers, each nbytes long, pairwise
+ *                 non-overlapping (16-byte alignment of all of them enables the
+ *                 vector path)
+ *   nbytes        >= 0 (0 is a no-op); root in 0..nranks-1
+ * hvdx_broadcast_step runs step `step` (0 <= step < 2*nranks-2) alone.
+ * Errors: HVDX_ERR_INVALID, HVDX_ERR_ALIAS, HVDX_ERR_HIP.
+ */
+int hvdx_broadcast(void* const* bufs, int nranks, int64_t nbytes, int root, void* stream);
+int hvdx_broadcast_step(void* const* bufs, int nranks, int64_t nbytes, int root, int step, void* stream);
+
+/*
+ * hvdx_fold_allreduce -- the same result as hvdx_ring_allreduce, bit for bit,
+ * computed without the ring's messages: each element's N values are read once and
+ * added in the ring's order (starting at the rank whose chunk holds the element,
+ * paper section 3), divided once for AVERAGE, and written to all N buffers.  It
+ * moves 2N elements per element instead of the ring's 5(N-1), so it bounds what a
+ * one-GPU schedule can do; it is not a simulation of the ring's transport.
+ * Arguments as hvdx_ring_allreduce; compression needs no workspace here.
+ */
+int hvdx_fold_allreduce(void* const* bufs, int nranks, int64_t count, int dtype, int op, int compress, void* stream);
+
 /* Workspace bytes hvdx_ring_allreduce needs: 0 unless compressing binary32 data,
  * then nranks * (count rounded up to 128) * 2.  Host only. */
 size_t hvdx_ring_workspace_bytes(int nranks, int64_t count, int dtype, int compress);
@@ -209,39 +241,47 @@ int hvdx_ring_chunk(int64_t count, int nranks, int c, int64_t* start, int64_t* l
 /*
  * Timeline (paper section 6: a per-node record of what the collective did at each
  * step, viewable in Chrome's about:tracing).  Between hvdx_timeline_begin and
- * hvdx_timeline_end every kernel this library launches, from any thread and on any
- * stream, is bracketed by a pair of HIP events that the library owns; no device
- * memory is allocated.
+ * hvdx_timeline_end the library brackets its kernel launches, from any thread and
+ * on any stream, with pairs of HIP events it owns; no device memory is allocated.
  *
- *   hvdx_timeline_begin(capacity)  start recording up to `capacity` (>= 1)
- *       launches; launches past that are counted as dropped.  Returns
- *       HVDX_ERR_INVALID if a timeline is already recording or capacity < 1,
- *       HVDX_ERR_HIP if the events cannot be created.
+ *   hvdx_timeline_begin(capacity, per_phase)  start recording up to `capacity`
+ *       (>= 1) records; records past that are counted as dropped.  per_phase = 0
+ *       records every launch; per_phase = 1 records each run of launches of one
+ *       kernel inside one call (e.g. the N-2 plain adding steps of a ring) as one
+ *       record whose `launches` says how many.  Returns HVDX_ERR_INVALID if a
+ *       timeline is already recording or capacity < 1, HVDX_ERR_HIP if the events
+ *       cannot be created.
  *   hvdx_timeline_end(out, capacity, nrecords, ndropped)  wait for the recorded
- *       launches to finish, write up to `capacity` records to the host array
- *       `out` in launch order, set *nrecords and *ndropped, stop recording and
- *       release the events.  Times are microseconds from the start of the first
- *       recorded launch.  HVDX_ERR_INVALID if no timeline is recording.
+ *       work to finish, write up to `capacity` records to the host array `out` in
+ *       launch order, set *nrecords and *ndropped, stop recording and release the
+ *       events.  Times are microseconds from the start of the first record.
+ *       HVDX_ERR_INVALID if no timeline is recording.  Call it when no other
+ *       thread is launching library work.
  */
 #define HVDX_KERNEL_PACK 0
 #define HVDX_KERNEL_REDUCE_SCATTER 1
 #define HVDX_KERNEL_ALLGATHER 2
 #define HVDX_KERNEL_UNPACK 3
 #define HVDX_KERNEL_ROUNDTRIP 4 /* one-rank compressed ring: round to binary16 and back */
+#define HVDX_KERNEL_BROADCAST 5 /* one step of hvdx_broadcast */
+#define HVDX_KERNEL_RS_AG 6     /* last adding step and first replacing step in one launch */
+#define HVDX_KERNEL_FOLD 7      /* hvdx_fold_allreduce */
 
 typedef struct hvdx_trace_record {
   int32_t kind;     /* HVDX_KERNEL_* */
-  int32_t step;     /* ring step for REDUCE_SCATTER / ALLGATHER, else -1 */
+  int32_t step;     /* first ring or broadcast step of the record, else -1 */
+  int32_t launches; /* kernel launches the record covers */
   int32_t nranks;
-  int32_t dtype;    /* buffer element type */
+  int32_t dtype;    /* buffer element type (-1 for a broadcast, which copies bytes) */
   int32_t compress; /* HVDX_COMPRESS_* of the ring */
+  int32_t root;     /* broadcast root, else -1 */
   int32_t reserved;
-  int64_t count;    /* buffer elements per rank */
+  int64_t count;    /* buffer elements per rank (bytes for a broadcast) */
   double start_us;
   double duration_us;
 } hvdx_trace_record;
 
-int hvdx_timeline_begin(int capacity);
+int hvdx_timeline_begin(int capacity, int per_phase);
 int hvdx_timeline_end(hvdx_trace_record* out, int capacity, int* nrecords, int* ndropped);
 
 /* Text for a status code (static storage). */

@@ -15,6 +15,8 @@ Plain, slow, written to be checked against the paper by eye:
 * ``allreduce`` -- the two composed: one averaging allreduce over every rank's
                    list of gradient tensors (paper section 5, the optimizer wrapper
                    that averages gradients).
+* ``broadcast`` -- the root's variables copied to every rank (paper sections 4
+                   and 5), as a pipelined chain along the ring.
 
 Arithmetic is in the buffer's precision (binary32, or binary16 when compressed),
 because the result of the method is defined by that arithmetic in ring order; an
@@ -22,4 +24,4 @@ fp64 sum is used only by the tests that bound the oracle's error.  Where the pap
 is silent the readings are documented in ``ring`` and ``fusion``.  Every function
 here is pinned by tests in ``tests/test_oracle_*.py``; none is "parity unpinned".
 """
-from . import allreduce, fusion, ring  # noqa: F401
+from . import allreduce, broadcast, fusion, ring  # noqa: F401

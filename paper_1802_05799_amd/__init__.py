@@ -29,6 +29,9 @@ from ._lib import (  # noqa: F401
     PHASE_REDUCE_SCATTER,
     SUM,
     HvdxError,
+    hvdx_broadcast,
+    hvdx_broadcast_step,
+    hvdx_fold_allreduce,
     hvdx_fuse_pack,
     hvdx_fuse_plan,
     hvdx_fuse_unpack,
@@ -46,6 +49,20 @@ from ._lib import (  # noqa: F401
 )
 from .cycle import FusedAllreduce  # noqa: F401
 from .timeline import Timeline  # noqa: F401
+
+
+def broadcast_(per_rank, root: int = 0) -> None:
+    """Copy rank `root`'s tensors into every other rank's, tensor by tensor (paper
+    sections 4 and 5: consistent initial variables).  Tensors must be contiguous GPU
+    tensors of matching shapes and dtypes across ranks."""
+    n = len(per_rank)
+    for ts in zip(*per_rank):
+        ref = ts[0]
+        for x in ts:
+            if x.shape != ref.shape or x.dtype != ref.dtype or not x.is_contiguous() or x.device.type != "cuda":
+                raise ValueError("broadcast needs contiguous GPU tensors matching across ranks")
+        stream = torch.cuda.current_stream(ref.device).cuda_stream
+        hvdx_broadcast([x.data_ptr() for x in ts], n, ref.numel() * ref.element_size(), root, stream)
 
 
 def allreduce_(per_rank, op: str = "average", compress: bool = False,

@@ -43,11 +43,15 @@ _SIGNATURES = {
     "hvdx_strerror": (ctypes.c_char_p, [_i]),
     "hvdx_last_error": (ctypes.c_char_p, []),
     "hvdx_version": (_i, []),
-    "hvdx_timeline_begin": (_i, [_i]),
+    "hvdx_broadcast": (_i, [_pp, _i, _i64, _i, _p]),
+    "hvdx_broadcast_step": (_i, [_pp, _i, _i64, _i, _i, _p]),
+    "hvdx_fold_allreduce": (_i, [_pp, _i, _i64, _i, _i, _i, _p]),
+    "hvdx_timeline_begin": (_i, [_i, _i]),
     "hvdx_timeline_end": (_i, [_p, _i, ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_int)]),
 }
 
 KERNEL_PACK, KERNEL_REDUCE_SCATTER, KERNEL_ALLGATHER, KERNEL_UNPACK, KERNEL_ROUNDTRIP = 0, 1, 2, 3, 4
+KERNEL_BROADCAST, KERNEL_RS_AG, KERNEL_FOLD = 5, 6, 7
 
 
 class TraceRecord(ctypes.Structure):
@@ -56,9 +60,11 @@ class TraceRecord(ctypes.Structure):
     _fields_ = [
         ("kind", ctypes.c_int32),
         ("step", ctypes.c_int32),
+        ("launches", ctypes.c_int32),
         ("nranks", ctypes.c_int32),
         ("dtype", ctypes.c_int32),
         ("compress", ctypes.c_int32),
+        ("root", ctypes.c_int32),
         ("reserved", ctypes.c_int32),
         ("count", ctypes.c_int64),
         ("start_us", ctypes.c_double),
@@ -174,8 +180,8 @@ def hvdx_ring_step(bufs, nranks: int, count: int, dtype: int, op: int, compress:
                               stream))
 
 
-def hvdx_timeline_begin(capacity: int) -> None:
-    _check(lib.hvdx_timeline_begin(capacity))
+def hvdx_timeline_begin(capacity: int, per_phase: bool = False) -> None:
+    _check(lib.hvdx_timeline_begin(capacity, 1 if per_phase else 0))
 
 
 def hvdx_timeline_end(capacity: int):
@@ -185,3 +191,19 @@ def hvdx_timeline_end(capacity: int):
     _check(lib.hvdx_timeline_end(ctypes.cast(arr, ctypes.c_void_p), capacity, ctypes.byref(n), ctypes.byref(dropped)))
     recs = [{f: getattr(arr[i], f) for f, _ in TraceRecord._fields_ if f != "reserved"} for i in range(n.value)]
     return recs, dropped.value
+
+
+def hvdx_broadcast(bufs, nranks: int, nbytes: int, root: int, stream: int = 0) -> None:
+    pb, _keep = _ptr_array(bufs)
+    _check(lib.hvdx_broadcast(pb, nranks, nbytes, root, stream))
+
+
+def hvdx_broadcast_step(bufs, nranks: int, nbytes: int, root: int, step: int, stream: int = 0) -> None:
+    pb, _keep = _ptr_array(bufs)
+    _check(lib.hvdx_broadcast_step(pb, nranks, nbytes, root, step, stream))
+
+
+def hvdx_fold_allreduce(bufs, nranks: int, count: int, dtype: int, op: int, compress: int = COMPRESS_NONE,
+                        stream: int = 0) -> None:
+    pb, _keep = _ptr_array(bufs)
+    _check(lib.hvdx_fold_allreduce(pb, nranks, count, dtype, op, compress, stream))

@@ -37,8 +37,16 @@ struct CopyCfg {
 #ifndef HVDX_UNPACK_CFG
 #define HVDX_UNPACK_CFG CopyCfg<4, 2, 2, true, true>
 #endif
-using PackCfg = HVDX_PACK_CFG;
+#ifndef HVDX_PACK16_CFG
+#define HVDX_PACK16_CFG HVDX_PACK_CFG
+#endif
+#ifndef HVDX_UNPACK16_CFG  // binary16 -> binary32 writes twice what it reads: cached stores win
+#define HVDX_UNPACK16_CFG CopyCfg<2, 2, 2, false, false>
+#endif
+using PackCfg = HVDX_PACK_CFG;      // binary32 buffers
 using UnpackCfg = HVDX_UNPACK_CFG;
+using Pack16Cfg = HVDX_PACK16_CFG;  // binary16 buffers
+using Unpack16Cfg = HVDX_UNPACK16_CFG;
 constexpr int kLdsPtrs = 2048;  // (rank, tensor) pointers a tile can stage in LDS
 
 template <typename TB>
@@ -452,42 +460,60 @@ unsigned tiles_for(int64_t count, int buf_dtype) {
   return (unsigned)((count + per - 1) / per);
 }
 
-}  // namespace
-
 template <typename Cfg>
 int ranks_per_block(int nranks) { return Cfg::RPB > 0 && Cfg::RPB < nranks ? Cfg::RPB : nranks; }
+
+template <typename Cfg>
+void pack_with(const void* const* srcs, const int64_t* numel, const int64_t* offset, int ntensors, int src_dtype,
+               const RankPtrs& bufs, int64_t count, int buf_dtype, int nranks, hipStream_t stream) {
+  const int rpb = ranks_per_block<Cfg>(nranks);
+  const dim3 grid(tiles_for<Cfg>(count, buf_dtype), (nranks + rpb - 1) / rpb);
+  if (src_dtype == HVDX_FLOAT32 && buf_dtype == HVDX_FLOAT32)
+    hipLaunchKernelGGL((pack_kernel<float, float, Cfg>), grid, dim3(kBlock), 0, stream, srcs, numel, offset,
+                       ntensors, bufs, count, nranks, rpb);
+  else if (src_dtype == HVDX_FLOAT32 && buf_dtype == HVDX_FLOAT16)
+    hipLaunchKernelGGL((pack_kernel<float, _Float16, Cfg>), grid, dim3(kBlock), 0, stream, srcs, numel, offset,
+                       ntensors, bufs, count, nranks, rpb);
+  else
+    hipLaunchKernelGGL((pack_kernel<_Float16, _Float16, Cfg>), grid, dim3(kBlock), 0, stream, srcs, numel, offset,
+                       ntensors, bufs, count, nranks, rpb);
+}
+
+template <typename Cfg>
+void unpack_with(const RankPtrs& bufs, int64_t count, int buf_dtype, void* const* dsts, const int64_t* numel,
+                 const int64_t* offset, int ntensors, int dst_dtype, int nranks, hipStream_t stream) {
+  const int rpb = ranks_per_block<Cfg>(nranks);
+  const dim3 grid(tiles_for<Cfg>(count, buf_dtype), (nranks + rpb - 1) / rpb);
+  if (dst_dtype == HVDX_FLOAT32 && buf_dtype == HVDX_FLOAT32)
+    hipLaunchKernelGGL((unpack_kernel<float, float, Cfg>), grid, dim3(kBlock), 0, stream, bufs, count, dsts, numel,
+                       offset, ntensors, nranks, rpb);
+  else if (dst_dtype == HVDX_FLOAT32 && buf_dtype == HVDX_FLOAT16)
+    hipLaunchKernelGGL((unpack_kernel<float, _Float16, Cfg>), grid, dim3(kBlock), 0, stream, bufs, count, dsts,
+                       numel, offset, ntensors, nranks, rpb);
+  else
+    hipLaunchKernelGGL((unpack_kernel<_Float16, _Float16, Cfg>), grid, dim3(kBlock), 0, stream, bufs, count, dsts,
+                       numel, offset, ntensors, nranks, rpb);
+}
+
+}  // namespace
 
 hipError_t launch_pack(const void* const* srcs, const int64_t* numel, const int64_t* offset, int ntensors,
                        int src_dtype, const RankPtrs& bufs, int64_t count, int buf_dtype, int nranks,
                        hipStream_t stream) {
-  const int rpb = ranks_per_block<PackCfg>(nranks);
-  const dim3 grid(tiles_for<PackCfg>(count, buf_dtype), (nranks + rpb - 1) / rpb);
-  if (src_dtype == HVDX_FLOAT32 && buf_dtype == HVDX_FLOAT32)
-    hipLaunchKernelGGL((pack_kernel<float, float, PackCfg>), grid, dim3(kBlock), 0, stream, srcs, numel, offset, ntensors,
-                       bufs, count, nranks, rpb);
-  else if (src_dtype == HVDX_FLOAT32 && buf_dtype == HVDX_FLOAT16)
-    hipLaunchKernelGGL((pack_kernel<float, _Float16, PackCfg>), grid, dim3(kBlock), 0, stream, srcs, numel, offset,
-                       ntensors, bufs, count, nranks, rpb);
+  if (buf_dtype == HVDX_FLOAT32)
+    pack_with<PackCfg>(srcs, numel, offset, ntensors, src_dtype, bufs, count, buf_dtype, nranks, stream);
   else
-    hipLaunchKernelGGL((pack_kernel<_Float16, _Float16, PackCfg>), grid, dim3(kBlock), 0, stream, srcs, numel, offset,
-                       ntensors, bufs, count, nranks, rpb);
+    pack_with<Pack16Cfg>(srcs, numel, offset, ntensors, src_dtype, bufs, count, buf_dtype, nranks, stream);
   return hipGetLastError();
 }
 
 hipError_t launch_unpack(const RankPtrs& bufs, int64_t count, int buf_dtype, void* const* dsts,
                          const int64_t* numel, const int64_t* offset, int ntensors, int dst_dtype, int nranks,
                          hipStream_t stream) {
-  const int rpb = ranks_per_block<UnpackCfg>(nranks);
-  const dim3 grid(tiles_for<UnpackCfg>(count, buf_dtype), (nranks + rpb - 1) / rpb);
-  if (dst_dtype == HVDX_FLOAT32 && buf_dtype == HVDX_FLOAT32)
-    hipLaunchKernelGGL((unpack_kernel<float, float, UnpackCfg>), grid, dim3(kBlock), 0, stream, bufs, count, dsts, numel,
-                       offset, ntensors, nranks, rpb);
-  else if (dst_dtype == HVDX_FLOAT32 && buf_dtype == HVDX_FLOAT16)
-    hipLaunchKernelGGL((unpack_kernel<float, _Float16, UnpackCfg>), grid, dim3(kBlock), 0, stream, bufs, count, dsts, numel,
-                       offset, ntensors, nranks, rpb);
+  if (buf_dtype == HVDX_FLOAT32)
+    unpack_with<UnpackCfg>(bufs, count, buf_dtype, dsts, numel, offset, ntensors, dst_dtype, nranks, stream);
   else
-    hipLaunchKernelGGL((unpack_kernel<_Float16, _Float16, UnpackCfg>), grid, dim3(kBlock), 0, stream, bufs, count, dsts,
-                       numel, offset, ntensors, nranks, rpb);
+    unpack_with<Unpack16Cfg>(bufs, count, buf_dtype, dsts, numel, offset, ntensors, dst_dtype, nranks, stream);
   return hipGetLastError();
 }
 

@@ -23,8 +23,9 @@ struct TimelineEntry {
 };
 
 struct Timeline {
-  std::mutex mu;
+  std::recursive_mutex mu;  // a phase record wraps the launches it covers
   bool on = false;
+  bool per_phase = false;
   int capacity = 0;
   int dropped = 0;
   std::vector<hipEvent_t> pool;  // 2 * capacity events, created at begin
@@ -36,28 +37,28 @@ Timeline& timeline() {
   return t;
 }
 
-// Brackets one kernel launch with timeline events when a timeline is recording.
+// Brackets kernel launches with timeline events when a timeline is recording at
+// this granularity: a phase record (phase = true) covers several launches and is
+// taken only in per-phase mode, a launch record only in per-launch mode.
 class TimedLaunch {
  public:
-  TimedLaunch(int kind, int step, int nranks, int dtype, int compress, int64_t count, hipStream_t st)
-      : st_(st) {
+  TimedLaunch(int kind, int step, int nranks, int dtype, int compress, int64_t count, hipStream_t st, int root = -1,
+              bool phase = false, int launches = 1)
+      : st_(st), lock_(timeline().mu) {
     Timeline& t = timeline();
-    lock_ = std::unique_lock<std::mutex>(t.mu);
-    if (!t.on) {
-      lock_.unlock();
-      return;
-    }
+    if (!t.on || t.per_phase != phase) return;
     if ((int)t.entries.size() >= t.capacity) {
       ++t.dropped;
-      lock_.unlock();
       return;
     }
     TimelineEntry e{};
     e.rec.kind = kind;
     e.rec.step = step;
+    e.rec.launches = launches;
     e.rec.nranks = nranks;
     e.rec.dtype = dtype;
     e.rec.compress = compress;
+    e.rec.root = root;
     e.rec.count = count;
     e.start = t.pool[2 * t.entries.size()];
     e.end = t.pool[2 * t.entries.size() + 1];
@@ -66,15 +67,15 @@ class TimedLaunch {
       end_ = e.end;
     }
   }
-  // The lock is still held here: recording ends before another launch can start one.
+  // The lock is still held here: no other thread's launch lands inside the record.
   ~TimedLaunch() {
     if (end_) (void)hipEventRecord(end_, st_);
   }
 
  private:
   hipStream_t st_;
+  std::unique_lock<std::recursive_mutex> lock_;
   hipEvent_t end_ = nullptr;
-  std::unique_lock<std::mutex> lock_;
 };
 
 int fail(int code, const char* fmt, ...) {
@@ -190,17 +191,23 @@ bool vectors_ok(void* const* bufs, int nranks, const void* workspace) {
   return aligned16(workspace);
 }
 
-// One step, arguments already checked, nranks >= 2, count > 0.
+// One step, arguments already checked, nranks >= 2, count > 0.  `fused` runs adding
+// step N-2 together with replacing step 0.
 int run_step(void* const* bufs, int nranks, int64_t count, int dtype, int op, int compress, int phase, int step,
-             void* workspace, hipStream_t st) {
+             void* workspace, hipStream_t st, bool fused = false) {
   const hvdx::RingArgs a = ring_args(nranks, count, step);
   const hvdx::RankPtrs p = rank_ptrs(bufs, nranks);
   const bool vok = vectors_ok(bufs, nranks, workspace);
-  const int dm = step == nranks - 2 ? div_mode(op, nranks) : hvdx::DIV_NONE;
-  TimedLaunch timed(phase == HVDX_PHASE_REDUCE_SCATTER ? HVDX_KERNEL_REDUCE_SCATTER : HVDX_KERNEL_ALLGATHER, step,
-                    nranks, dtype, compress, count, st);
+  const int dm = (fused || step == nranks - 2) && phase == HVDX_PHASE_REDUCE_SCATTER ? div_mode(op, nranks)
+                                                                                  : hvdx::DIV_NONE;
+  const int kind = fused ? HVDX_KERNEL_RS_AG
+                         : (phase == HVDX_PHASE_REDUCE_SCATTER ? HVDX_KERNEL_REDUCE_SCATTER : HVDX_KERNEL_ALLGATHER);
+  TimedLaunch timed(kind, step, nranks, dtype, compress, count, st);
   hipError_t e;
-  if (compress == HVDX_COMPRESS_FP16) {
+  if (fused) {
+    e = compress == HVDX_COMPRESS_FP16 ? hvdx::launch_rs_ag_step_c16(p, workspace, a, dm, vok, st)
+                                       : hvdx::launch_rs_ag_step(p, a, dtype, dm, vok, st);
+  } else if (compress == HVDX_COMPRESS_FP16) {
     e = phase == HVDX_PHASE_REDUCE_SCATTER ? hvdx::launch_rs_step_c16(p, workspace, a, dm, vok, st)
                                            : hvdx::launch_ag_step_c16(p, workspace, a, vok, st);
   } else {
@@ -208,7 +215,22 @@ int run_step(void* const* bufs, int nranks, int64_t count, int dtype, int op, in
                                            : hvdx::launch_ag_step(p, a, dtype, vok, st);
   }
   if (e != hipSuccess)
-    return hip_fail(e, phase == HVDX_PHASE_REDUCE_SCATTER ? "reduce-scatter step launch" : "allgather step launch");
+    return hip_fail(e, fused ? "fused step launch"
+                             : (phase == HVDX_PHASE_REDUCE_SCATTER ? "reduce-scatter step launch"
+                                                                   : "allgather step launch"));
+  return HVDX_OK;
+}
+
+// Steps [s0, s1) of one phase, as one timeline phase record.
+int run_steps(void* const* bufs, int nranks, int64_t count, int dtype, int op, int compress, int phase, int s0,
+              int s1, void* workspace, hipStream_t st) {
+  if (s1 <= s0) return HVDX_OK;
+  TimedLaunch timed(phase == HVDX_PHASE_REDUCE_SCATTER ? HVDX_KERNEL_REDUCE_SCATTER : HVDX_KERNEL_ALLGATHER, s0,
+                    nranks, dtype, compress, count, st, -1, true, s1 - s0);
+  for (int s = s0; s < s1; ++s) {
+    const int rc = run_step(bufs, nranks, count, dtype, op, compress, phase, s, workspace, st);
+    if (rc) return rc;
+  }
   return HVDX_OK;
 }
 
@@ -236,10 +258,10 @@ extern "C" {
 
 int hvdx_version(void) { return HVDX_VERSION; }
 
-int hvdx_timeline_begin(int capacity) {
+int hvdx_timeline_begin(int capacity, int per_phase) {
   if (capacity < 1 || capacity > (1 << 24)) return fail(HVDX_ERR_INVALID, "hvdx_timeline_begin: bad capacity %d", capacity);
   Timeline& t = timeline();
-  std::lock_guard<std::mutex> g(t.mu);
+  std::lock_guard<std::recursive_mutex> g(t.mu);
   if (t.on) return fail(HVDX_ERR_INVALID, "hvdx_timeline_begin: a timeline is already recording");
   t.pool.assign(2 * (size_t)capacity, nullptr);
   for (auto& ev : t.pool) {
@@ -255,6 +277,7 @@ int hvdx_timeline_begin(int capacity) {
   t.entries.reserve(capacity);
   t.capacity = capacity;
   t.dropped = 0;
+  t.per_phase = per_phase != 0;
   t.on = true;
   return HVDX_OK;
 }
@@ -263,7 +286,7 @@ int hvdx_timeline_end(hvdx_trace_record* out, int capacity, int* nrecords, int* 
   if (!nrecords || !ndropped || capacity < 0 || (capacity > 0 && !out))
     return fail(HVDX_ERR_INVALID, "hvdx_timeline_end: bad arguments");
   Timeline& t = timeline();
-  std::lock_guard<std::mutex> g(t.mu);
+  std::lock_guard<std::recursive_mutex> g(t.mu);
   if (!t.on) return fail(HVDX_ERR_INVALID, "hvdx_timeline_end: no timeline is recording");
   t.on = false;
   int rc = HVDX_OK;
@@ -383,6 +406,8 @@ int hvdx_fuse_pack(const void* const* srcs, const int64_t* numel, const int64_t*
   if (buf_count == 0) return HVDX_OK;
   TimedLaunch timed(HVDX_KERNEL_PACK, -1, nranks, buf_dtype, HVDX_COMPRESS_NONE, buf_count,
                     static_cast<hipStream_t>(stream));
+  TimedLaunch timed_phase(HVDX_KERNEL_PACK, -1, nranks, buf_dtype, HVDX_COMPRESS_NONE, buf_count,
+                          static_cast<hipStream_t>(stream), -1, true);
   const hipError_t e = hvdx::launch_pack(srcs, numel, offset, ntensors, src_dtype, rank_ptrs(bufs, nranks),
                                          buf_count, buf_dtype, nranks, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? HVDX_OK : hip_fail(e, "pack launch");
@@ -397,6 +422,8 @@ int hvdx_fuse_unpack(const void* const* bufs, int64_t buf_count, int buf_dtype, 
   if (buf_count == 0) return HVDX_OK;
   TimedLaunch timed(HVDX_KERNEL_UNPACK, -1, nranks, buf_dtype, HVDX_COMPRESS_NONE, buf_count,
                     static_cast<hipStream_t>(stream));
+  TimedLaunch timed_phase(HVDX_KERNEL_UNPACK, -1, nranks, buf_dtype, HVDX_COMPRESS_NONE, buf_count,
+                          static_cast<hipStream_t>(stream), -1, true);
   const hipError_t e =
       hvdx::launch_unpack(rank_ptrs(const_cast<void* const*>(bufs), nranks), buf_count, buf_dtype, dsts, numel,
                           offset, ntensors, dst_dtype, nranks, static_cast<hipStream_t>(stream));
@@ -426,14 +453,11 @@ static int run_phase(void* const* bufs, int nranks, int64_t count, int dtype, in
   if (nranks == 1) {  // no messages; AVERAGE divides by 1; compression still rounds
     if (compress != HVDX_COMPRESS_FP16 || phase != HVDX_PHASE_REDUCE_SCATTER) return HVDX_OK;
     TimedLaunch timed(HVDX_KERNEL_ROUNDTRIP, -1, 1, dtype, compress, count, st);
+    TimedLaunch timed_phase(HVDX_KERNEL_ROUNDTRIP, -1, 1, dtype, compress, count, st, -1, true);
     const hipError_t e = hvdx::launch_roundtrip_c16(bufs[0], count, st);
     return e == hipSuccess ? HVDX_OK : hip_fail(e, "fp16 round-trip launch");
   }
-  for (int s = 0; s < nranks - 1; ++s) {
-    rc = run_step(bufs, nranks, count, dtype, op, compress, phase, s, workspace, st);
-    if (rc) return rc;
-  }
-  return HVDX_OK;
+  return run_steps(bufs, nranks, count, dtype, op, compress, phase, 0, nranks - 1, workspace, st);
 }
 
 int hvdx_ring_reduce_scatter(void* const* bufs, int nranks, int64_t count, int dtype, int op, int compress,
@@ -450,11 +474,83 @@ int hvdx_ring_allgather(void* const* bufs, int nranks, int64_t count, int dtype,
 
 int hvdx_ring_allreduce(void* const* bufs, int nranks, int64_t count, int dtype, int op, int compress,
                         void* workspace, size_t workspace_bytes, void* stream) {
-  int rc = run_phase(bufs, nranks, count, dtype, op, compress, HVDX_PHASE_REDUCE_SCATTER, workspace,
-                     workspace_bytes, stream, "hvdx_ring_allreduce");
+  int rc = check_ring(bufs, nranks, count, dtype, op, compress, workspace, workspace_bytes, "hvdx_ring_allreduce");
   if (rc) return rc;
-  return run_phase(bufs, nranks, count, dtype, op, compress, HVDX_PHASE_ALLGATHER, workspace, workspace_bytes,
-                   stream, "hvdx_ring_allreduce");
+  if (count == 0) return HVDX_OK;
+  if (nranks == 1)
+    return run_phase(bufs, nranks, count, dtype, op, compress, HVDX_PHASE_REDUCE_SCATTER, workspace,
+                     workspace_bytes, stream, "hvdx_ring_allreduce");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int last = nranks - 2;
+  rc = run_steps(bufs, nranks, count, dtype, op, compress, HVDX_PHASE_REDUCE_SCATTER, 0, last, workspace, st);
+  if (rc) return rc;
+  {
+    TimedLaunch timed_phase(HVDX_KERNEL_RS_AG, last, nranks, dtype, compress, count, st, -1, true);
+    rc = run_step(bufs, nranks, count, dtype, op, compress, HVDX_PHASE_REDUCE_SCATTER, last, workspace, st, true);
+    if (rc) return rc;
+  }
+  return run_steps(bufs, nranks, count, dtype, op, compress, HVDX_PHASE_ALLGATHER, 1, nranks - 1, workspace, st);
+}
+
+int hvdx_fold_allreduce(void* const* bufs, int nranks, int64_t count, int dtype, int op, int compress,
+                        void* stream) {
+  int rc = check_ring(bufs, nranks, count, dtype, op, HVDX_COMPRESS_NONE, nullptr, 0, "hvdx_fold_allreduce");
+  if (rc) return rc;
+  if (compress != HVDX_COMPRESS_NONE && compress != HVDX_COMPRESS_FP16)
+    return fail(HVDX_ERR_INVALID, "hvdx_fold_allreduce: unknown compression %d", compress);
+  if (compress == HVDX_COMPRESS_FP16 && dtype != HVDX_FLOAT32)
+    return fail(HVDX_ERR_INVALID, "hvdx_fold_allreduce: fp16 compression needs float32 buffers");
+  if (count == 0) return HVDX_OK;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const hvdx::RingArgs a = ring_args(nranks, count, 0);
+  TimedLaunch timed(HVDX_KERNEL_FOLD, -1, nranks, dtype, compress, count, st);
+  TimedLaunch timed_phase(HVDX_KERNEL_FOLD, -1, nranks, dtype, compress, count, st, -1, true);
+  const hipError_t e = hvdx::launch_fold(rank_ptrs(bufs, nranks), a, count, dtype, compress, div_mode(op, nranks),
+                                         vectors_ok(bufs, nranks, nullptr), st);
+  return e == hipSuccess ? HVDX_OK : hip_fail(e, "fold launch");
+}
+
+static int check_bcast(void* const* bufs, int nranks, int64_t nbytes, int root, const char* what) {
+  int rc = check_rank_buffers(bufs, nranks, nbytes, 1, what);
+  if (rc) return rc;
+  if (root < 0 || root >= nranks) return fail(HVDX_ERR_INVALID, "%s: root %d outside 0..%d", what, root, nranks - 1);
+  return HVDX_OK;
+}
+
+static int bcast_step(void* const* bufs, int nranks, int64_t nbytes, int root, int step, hipStream_t st) {
+  hvdx::BcastArgs a{};
+  a.n = nranks;
+  a.root = root;
+  a.step = step;
+  a.nbytes = nbytes;
+  const int64_t units = (nbytes + 15) / 16;
+  a.q = units / nranks;
+  a.rem = units % nranks;
+  bool vok = true;
+  for (int r = 0; r < nranks; ++r) vok = vok && aligned16(bufs[r]);
+  TimedLaunch timed(HVDX_KERNEL_BROADCAST, step, nranks, -1, HVDX_COMPRESS_NONE, nbytes, st, root);
+  TimedLaunch timed_phase(HVDX_KERNEL_BROADCAST, step, nranks, -1, HVDX_COMPRESS_NONE, nbytes, st, root, true);
+  const hipError_t e = hvdx::launch_bcast_step(rank_ptrs(bufs, nranks), a, vok, st);
+  return e == hipSuccess ? HVDX_OK : hip_fail(e, "broadcast step launch");
+}
+
+int hvdx_broadcast_step(void* const* bufs, int nranks, int64_t nbytes, int root, int step, void* stream) {
+  int rc = check_bcast(bufs, nranks, nbytes, root, "hvdx_broadcast_step");
+  if (rc) return rc;
+  if (step < 0 || step > 2 * nranks - 3)
+    return fail(HVDX_ERR_INVALID, "hvdx_broadcast_step: step %d outside 0..%d", step, 2 * nranks - 3);
+  if (nbytes == 0) return HVDX_OK;
+  return bcast_step(bufs, nranks, nbytes, root, step, static_cast<hipStream_t>(stream));
+}
+
+int hvdx_broadcast(void* const* bufs, int nranks, int64_t nbytes, int root, void* stream) {
+  int rc = check_bcast(bufs, nranks, nbytes, root, "hvdx_broadcast");
+  if (rc) return rc;
+  for (int s = 0; nbytes > 0 && s < 2 * nranks - 2; ++s) {
+    rc = bcast_step(bufs, nranks, nbytes, root, s, static_cast<hipStream_t>(stream));
+    if (rc) return rc;
+  }
+  return HVDX_OK;
 }
 
 }  // extern "C"

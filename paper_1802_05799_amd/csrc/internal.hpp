@@ -38,6 +38,22 @@ hipError_t launch_rs_step_c16(const RankPtrs& x, void* wire, const RingArgs& a, 
                               hipStream_t stream);
 hipError_t launch_ag_step_c16(const RankPtrs& x, void* wire, const RingArgs& a, bool vector_ok, hipStream_t stream);
 hipError_t launch_roundtrip_c16(void* x, int64_t count, hipStream_t stream);
+// Adding step N-2 and replacing step 0 in one launch.
+hipError_t launch_rs_ag_step(const RankPtrs& bufs, const RingArgs& a, int dtype, int divmode, bool vector_ok,
+                             hipStream_t stream);
+hipError_t launch_rs_ag_step_c16(const RankPtrs& x, void* wire, const RingArgs& a, int divmode, bool vector_ok,
+                                 hipStream_t stream);
+// The ring's per-element fold in one pass (same bits, no per-step messages).
+hipError_t launch_fold(const RankPtrs& bufs, const RingArgs& a, int64_t count, int dtype, int compress, int divmode,
+                       bool vector_ok, hipStream_t stream);
+
+// Broadcast chain step (broadcast_kernels.hip).
+struct BcastArgs {
+  int n, root, step;
+  int64_t nbytes;
+  int64_t q, rem;  // 16-byte units per chunk: q, the first rem chunks one more
+};
+hipError_t launch_bcast_step(const RankPtrs& bufs, const BcastArgs& a, bool vector_ok, hipStream_t stream);
 
 // Launchers (fusion_kernels.hip).
 hipError_t launch_pack(const void* const* srcs, const int64_t* numel, const int64_t* offset, int ntensors,

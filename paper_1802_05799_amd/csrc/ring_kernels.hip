@@ -43,6 +43,16 @@ __device__ __forceinline__ float finish(float v, const RingArgs& a) {
   return v;
 }
 
+// binary16 finish: scaling by 1/N = 2^-k is done in binary16 itself (one rounding of
+// the exact product, the same bits as through binary32); going through binary32
+// lets the compiler select v_fma_mix with a +0 addend, which turns -0 into +0.
+template <int DIV>
+__device__ __forceinline__ _Float16 finish16(_Float16 v, const RingArgs& a) {
+  if constexpr (DIV == DIV_POW2) return v * (_Float16)a.inv;
+  if constexpr (DIV == DIV_TRUE) return (_Float16)((float)v / a.nf);
+  return v;
+}
+
 // receiver's value + sender's value, and the AVERAGE divide when DIV says so
 template <int DIV>
 __device__ __forceinline__ float combine1(float local, float recv, const RingArgs& a) {
@@ -50,9 +60,7 @@ __device__ __forceinline__ float combine1(float local, float recv, const RingArg
 }
 template <int DIV>
 __device__ __forceinline__ _Float16 combine1(_Float16 local, _Float16 recv, const RingArgs& a) {
-  _Float16 s = local + recv;
-  if constexpr (DIV == DIV_NONE) return s;
-  return (_Float16)finish<DIV>((float)s, a);
+  return finish16<DIV>(local + recv, a);
 }
 template <int DIV>
 __device__ __forceinline__ f32x4 combine(f32x4 local, f32x4 recv, const RingArgs& a) {
@@ -66,9 +74,10 @@ __device__ __forceinline__ f32x4 combine(f32x4 local, f32x4 recv, const RingArgs
 template <int DIV>
 __device__ __forceinline__ f16x8 combine(f16x8 local, f16x8 recv, const RingArgs& a) {
   f16x8 s = local + recv;
-  if constexpr (DIV != DIV_NONE) {
+  if constexpr (DIV == DIV_POW2) s = s * (f16x8)((_Float16)a.inv);
+  if constexpr (DIV == DIV_TRUE) {
 #pragma unroll
-    for (int k = 0; k < 8; ++k) s[k] = (_Float16)finish<DIV>((float)s[k], a);
+    for (int k = 0; k < 8; ++k) s[k] = finish16<DIV>(s[k], a);
   }
   return s;
 }
@@ -115,7 +124,14 @@ using RsStream = Policy<1, 256, true, true>;
 using AgCached = Policy<2, 512, false, false>;
 using AgStream = Policy<1, 256, true, true>;
 using C16Cached = Policy<2, 256, false, false>;
-using C16Stream = Policy<1, 256, true, true>;
+#ifndef HVDX_C16_RS_STREAM
+#define HVDX_C16_RS_STREAM Policy<1, 256, true, true>
+#endif
+#ifndef HVDX_C16_AG_STREAM  // writes 3x what it reads: cached stores measured 1.4x faster
+#define HVDX_C16_AG_STREAM Policy<2, 256, false, false>
+#endif
+using C16RsStream = HVDX_C16_RS_STREAM;
+using C16AgStream = HVDX_C16_AG_STREAM;
 constexpr int64_t kStreamBytes = 128ll << 20;  // rank buffers at least this large stream
 
 template <bool NT, typename V>
@@ -340,6 +356,228 @@ __global__ __launch_bounds__(P::BS) void ag_step_c16_kernel(RankPtrs x, _Float16
   }
 }
 
+// ---- the last adding step fused with the first replacing step -----------------------
+//
+// In adding step N-2 the owner (c-1) of chunk c completes its sum from the sender
+// (c-2); in replacing step 0 the owner sends it on to rank c.  One kernel does both:
+// it writes the finished (averaged) chunk to the owner and to rank c, which saves
+// reading it back.  The buffers end exactly as after the two steps.
+
+template <typename T, int DIV, bool VEC_OK, typename P>
+__global__ __launch_bounds__(P::BS) void rs_ag_step_kernel(RankPtrs bufs, RingArgs a) {
+  using VT = typename Vec<T>::type;
+  constexpr int V = Vec<T>::n;
+  constexpr int BS = P::BS, U = P::U;
+  const int c = blockIdx.y;
+  const Chunk ch = chunk_of(c, a);
+  const int snd = rs_sender(c, a.n - 2, a.n);
+  const int own = (snd + 1) % a.n;
+  // with N = 2 the sender is rank c itself, so src and nxt alias (each element is
+  // read before the same lane writes it): no __restrict__ on them
+  const T* src = static_cast<const T*>(bufs.p[snd]) + ch.start;
+  T* __restrict__ dst = static_cast<T*>(bufs.p[own]) + ch.start;
+  T* nxt = static_cast<T*>(bufs.p[c]) + ch.start;
+
+  const int64_t head = VEC_OK ? head_elems<T>(dst, ch.len) : ch.len;
+  const int64_t nvec = (ch.len - head) / V;
+  const int64_t tail = head + nvec * V;
+  const int64_t gtid = (int64_t)blockIdx.x * BS + threadIdx.x;
+  const int64_t gthreads = (int64_t)gridDim.x * BS;
+  auto one = [&](int64_t e) {
+    const T v = combine1<DIV>(dst[e], src[e], a);
+    dst[e] = v;
+    nxt[e] = v;
+  };
+  for (int64_t e = gtid; e < head; e += gthreads) one(e);
+  for (int64_t e = tail + gtid; e < ch.len; e += gthreads) one(e);
+
+  const VT* s4 = reinterpret_cast<const VT*>(src + head);
+  VT* __restrict__ d4 = reinterpret_cast<VT*>(dst + head);
+  VT* n4 = reinterpret_cast<VT*>(nxt + head);
+  for (int64_t base = (int64_t)blockIdx.x * BS * U + threadIdx.x; base < nvec; base += gthreads * U) {
+    VT x[U], y[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int64_t i = base + u * BS;
+      if (i < nvec) {
+        x[u] = vload<P::NTL>(s4 + i);
+        y[u] = vload<P::NTL>(d4 + i);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int64_t i = base + u * BS;
+      if (i < nvec) {
+        const VT v = combine<DIV>(y[u], x[u], a);
+        vstore<P::NTS>(d4 + i, v);
+        vstore<P::NTS>(n4 + i, v);
+      }
+    }
+  }
+}
+
+// Compressed: the owner's wire copy is not read again, so only rank c's is written.
+template <int DIV, bool FIRST, bool LAST, bool VEC_OK, typename P>
+__global__ __launch_bounds__(P::BS) void rs_ag_step_c16_kernel(RankPtrs x, _Float16* wire, RingArgs a) {
+  constexpr int BS = P::BS, U = P::U;
+  const int c = blockIdx.y;
+  const Chunk ch = chunk_of(c, a);
+  const int snd = rs_sender(c, a.n - 2, a.n);
+  const int own = (snd + 1) % a.n;
+  // with N = 2 the sender is rank c itself: xs/xn and ws/wn alias (read before written)
+  const float* xs = static_cast<const float*>(x.p[snd]) + ch.start;
+  float* __restrict__ xo = static_cast<float*>(x.p[own]) + ch.start;
+  float* xn = static_cast<float*>(x.p[c]) + ch.start;
+  const _Float16* ws = wire + (int64_t)snd * a.wire_stride + ch.start;
+  _Float16* wn = wire + (int64_t)c * a.wire_stride + ch.start;
+
+  const int64_t head = VEC_OK ? head_elems<_Float16>(wn, ch.len) : ch.len;
+  const int64_t nvec = (ch.len - head) / 8;
+  const int64_t tail = head + nvec * 8;
+  const int64_t gtid = (int64_t)blockIdx.x * BS + threadIdx.x;
+  const int64_t gthreads = (int64_t)gridDim.x * BS;
+  auto one = [&](int64_t e) {
+    const _Float16 sent = FIRST ? (_Float16)xs[e] : ws[e];
+    const _Float16 h = combine1<DIV>((_Float16)xo[e], sent, a);
+    const float f = (float)h;
+    xo[e] = f;
+    xn[e] = f;
+    if (!LAST) wn[e] = h;
+  };
+  for (int64_t e = gtid; e < head; e += gthreads) one(e);
+  for (int64_t e = tail + gtid; e < ch.len; e += gthreads) one(e);
+
+  const f32x4* xs4 = reinterpret_cast<const f32x4*>(xs + head);
+  f32x4* __restrict__ xo4 = reinterpret_cast<f32x4*>(xo + head);
+  f32x4* xn4 = reinterpret_cast<f32x4*>(xn + head);
+  const f16x8* ws8 = reinterpret_cast<const f16x8*>(ws + head);
+  f16x8* wn8 = reinterpret_cast<f16x8*>(wn + head);
+  for (int64_t base = (int64_t)blockIdx.x * BS * U + threadIdx.x; base < nvec; base += gthreads * U) {
+    f16x8 sent[U], mine[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int64_t i = base + u * BS;
+      if (i < nvec) {
+        mine[u] = to_f16x8(vload<P::NTL>(xo4 + 2 * i), vload<P::NTL>(xo4 + 2 * i + 1));
+        sent[u] = FIRST ? to_f16x8(vload<P::NTL>(xs4 + 2 * i), vload<P::NTL>(xs4 + 2 * i + 1))
+                        : vload<P::NTL>(ws8 + i);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int64_t i = base + u * BS;
+      if (i < nvec) {
+        const f16x8 h = combine<DIV>(mine[u], sent[u], a);
+        f32x4 lo, hi;
+        from_f16x8(h, lo, hi);
+        vstore<P::NTS>(xo4 + 2 * i, lo);
+        vstore<P::NTS>(xo4 + 2 * i + 1, hi);
+        vstore<P::NTS>(xn4 + 2 * i, lo);
+        vstore<P::NTS>(xn4 + 2 * i + 1, hi);
+        if (!LAST) vstore<P::NTS>(wn8 + i, h);
+      }
+    }
+  }
+}
+
+// ---- the ring's fold computed directly -----------------------------------------------
+//
+// Element e of chunk c ends as FIN(((x_c + x_{c+1}) + ...) + x_{c+N-1}) on every rank,
+// the ring's summation order.  One kernel reads the N values of each element once,
+// adds them in that order in registers (binary16 after rounding each input when
+// compressing) and writes the result to all N ranks: 2N element reads and writes
+// instead of the ring's 5(N-1), with identical bits, but without the per-step
+// messages of a real ring.
+
+__device__ __forceinline__ int64_t chunk_index(int64_t e, const RingArgs& a) {
+  const int64_t big = a.rem * (a.q + 1);  // elements in the first rem (longer) chunks
+  return e < big ? e / (a.q + 1) : a.rem + (e - big) / a.q;
+}
+
+template <typename T, bool COMP>
+struct FoldTypes;
+template <>
+struct FoldTypes<float, false> {
+  using acc = float;
+  __device__ static float in(float v) { return v; }
+  __device__ static float out(float v) { return v; }
+};
+template <>
+struct FoldTypes<_Float16, false> {
+  using acc = _Float16;
+  __device__ static _Float16 in(_Float16 v) { return v; }
+  __device__ static _Float16 out(_Float16 v) { return v; }
+};
+template <>
+struct FoldTypes<float, true> {  // binary32 data, binary16 arithmetic
+  using acc = _Float16;
+  __device__ static _Float16 in(float v) { return (_Float16)v; }
+  __device__ static float out(_Float16 v) { return (float)v; }
+};
+
+constexpr int kFoldBatch = 8;  // ranks whose loads are in flight together
+
+template <int DIV>
+__device__ __forceinline__ float fold_finish(float v, const RingArgs& a) {
+  return finish<DIV>(v, a);
+}
+template <int DIV>
+__device__ __forceinline__ _Float16 fold_finish(_Float16 v, const RingArgs& a) {
+  return finish16<DIV>(v, a);
+}
+
+template <typename T, int DIV, bool COMP, bool VEC_OK>
+__global__ __launch_bounds__(kBlock) void fold_kernel(RankPtrs bufs, RingArgs a, int64_t count) {
+  using F = FoldTypes<T, COMP>;
+  using A = typename F::acc;
+  constexpr int V = 4;  // elements per lane (16 bytes of binary32, 8 of binary16)
+  const int64_t nv = (count + V - 1) / V;
+  const int n = a.n;
+  for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < nv; i += (int64_t)gridDim.x * kBlock) {
+    const int64_t e0 = i * V;
+    const int64_t c0 = chunk_index(e0, a);
+    const bool whole = VEC_OK && e0 + V <= count && chunk_index(e0 + V - 1, a) == c0;
+    if (whole) {
+      A acc[V];
+      T v[kFoldBatch][V];
+      for (int k0 = 0; k0 < n; k0 += kFoldBatch) {
+#pragma unroll
+        for (int kk = 0; kk < kFoldBatch; ++kk) {
+          const int k = k0 + kk;
+          if (k < n) {
+            const T* p = static_cast<const T*>(bufs.p[(c0 + k) % n]) + e0;
+#pragma unroll
+            for (int j = 0; j < V; ++j) v[kk][j] = p[j];
+          }
+        }
+#pragma unroll
+        for (int kk = 0; kk < kFoldBatch; ++kk) {
+          const int k = k0 + kk;
+          if (k < n) {
+#pragma unroll
+            for (int j = 0; j < V; ++j) acc[j] = k == 0 ? F::in(v[kk][j]) : (A)(acc[j] + F::in(v[kk][j]));
+          }
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < V; ++j) acc[j] = fold_finish<DIV>(acc[j], a);
+      for (int r = 0; r < n; ++r) {
+        T* p = static_cast<T*>(bufs.p[r]) + e0;
+#pragma unroll
+        for (int j = 0; j < V; ++j) p[j] = F::out(acc[j]);
+      }
+      continue;
+    }
+    for (int64_t e = e0; e < e0 + V && e < count; ++e) {  // vectors that cross a chunk edge
+      const int64_t c = chunk_index(e, a);
+      A acc = F::in(static_cast<const T*>(bufs.p[c])[e]);
+      for (int k = 1; k < n; ++k) acc = (A)(acc + F::in(static_cast<const T*>(bufs.p[(c + k) % n])[e]));
+      acc = fold_finish<DIV>(acc, a);
+      for (int r = 0; r < n; ++r) static_cast<T*>(bufs.p[r])[e] = F::out(acc);
+    }
+  }
+}
+
 // One rank, compressed: the result is the value rounded to binary16 and widened.
 __global__ __launch_bounds__(kBlock) void roundtrip_c16_kernel(float* x, int64_t count) {
   const int64_t gthreads = (int64_t)gridDim.x * kBlock;
@@ -460,14 +698,14 @@ hipError_t launch_ag_step(const RankPtrs& bufs, const RingArgs& a, int dtype, bo
 hipError_t launch_rs_step_c16(const RankPtrs& x, void* wire, const RingArgs& a, int divmode, bool vector_ok,
                               hipStream_t stream) {
   _Float16* w = static_cast<_Float16*>(wire);
-  if (streams(a, 4)) rs_c16_launch<C16Stream>(x, w, a, divmode, vector_ok, stream);
+  if (streams(a, 4)) rs_c16_launch<C16RsStream>(x, w, a, divmode, vector_ok, stream);
   else rs_c16_launch<C16Cached>(x, w, a, divmode, vector_ok, stream);
   return hipGetLastError();
 }
 
 hipError_t launch_ag_step_c16(const RankPtrs& x, void* wire, const RingArgs& a, bool vector_ok, hipStream_t stream) {
   _Float16* w = static_cast<_Float16*>(wire);
-  if (streams(a, 4)) ag_c16_launch<C16Stream>(x, w, a, vector_ok, stream);
+  if (streams(a, 4)) ag_c16_launch<C16AgStream>(x, w, a, vector_ok, stream);
   else ag_c16_launch<C16Cached>(x, w, a, vector_ok, stream);
   return hipGetLastError();
 }
@@ -478,6 +716,86 @@ hipError_t launch_roundtrip_c16(void* x, int64_t count, hipStream_t stream) {
   if (blocks > 65536) blocks = 65536;
   hipLaunchKernelGGL(roundtrip_c16_kernel, dim3((unsigned)blocks), dim3(kBlock), 0, stream, static_cast<float*>(x),
                      count);
+  return hipGetLastError();
+}
+
+hipError_t launch_rs_ag_step(const RankPtrs& bufs, const RingArgs& a, int dtype, int divmode, bool vector_ok,
+                             hipStream_t stream) {
+#define HVDX_RSAG(T, P, DIV, VOK) \
+  hipLaunchKernelGGL((rs_ag_step_kernel<T, DIV, VOK, P>), step_grid(a, Vec<T>::n, P::U, P::BS), dim3(P::BS), 0, \
+                     stream, bufs, a)
+#define HVDX_RSAG_V(T, P, DIV) \
+  if (vector_ok) HVDX_RSAG(T, P, DIV, true); else HVDX_RSAG(T, P, DIV, false)
+#define HVDX_RSAG_D(T, P) \
+  if (divmode == DIV_NONE) { HVDX_RSAG_V(T, P, DIV_NONE); } \
+  else if (divmode == DIV_POW2) { HVDX_RSAG_V(T, P, DIV_POW2); } \
+  else { HVDX_RSAG_V(T, P, DIV_TRUE); }
+  if (dtype == HVDX_FLOAT32) {
+    if (streams(a, 4)) { HVDX_RSAG_D(float, RsStream) } else { HVDX_RSAG_D(float, RsCached) }
+  } else {
+    if (streams(a, 2)) { HVDX_RSAG_D(_Float16, RsStream) } else { HVDX_RSAG_D(_Float16, RsCached) }
+  }
+#undef HVDX_RSAG_D
+#undef HVDX_RSAG_V
+#undef HVDX_RSAG
+  return hipGetLastError();
+}
+
+namespace {
+template <typename P>
+void rs_ag_c16_launch(const RankPtrs& x, _Float16* w, const RingArgs& a, int divmode, bool vector_ok,
+                      hipStream_t stream) {
+  const dim3 grid = step_grid(a, 8, P::U, P::BS);
+  const bool first = a.n == 2, last = a.n == 2;  // step N-2 is also the first adding step when N = 2
+#define HVDX_RAC(DIV, F, L, VOK) \
+  hipLaunchKernelGGL((rs_ag_step_c16_kernel<DIV, F, L, VOK, P>), grid, dim3(P::BS), 0, stream, x, w, a)
+#define HVDX_RAC_V(DIV, F, L) \
+  if (vector_ok) HVDX_RAC(DIV, F, L, true); else HVDX_RAC(DIV, F, L, false)
+#define HVDX_RAC_D(F, L) \
+  if (divmode == DIV_NONE) { HVDX_RAC_V(DIV_NONE, F, L); } \
+  else if (divmode == DIV_POW2) { HVDX_RAC_V(DIV_POW2, F, L); } \
+  else { HVDX_RAC_V(DIV_TRUE, F, L); }
+  if (first && last) {
+    HVDX_RAC_D(true, true)
+  } else {
+    HVDX_RAC_D(false, false)
+  }
+#undef HVDX_RAC_D
+#undef HVDX_RAC_V
+#undef HVDX_RAC
+}
+}  // namespace
+
+hipError_t launch_rs_ag_step_c16(const RankPtrs& x, void* wire, const RingArgs& a, int divmode, bool vector_ok,
+                                 hipStream_t stream) {
+  _Float16* w = static_cast<_Float16*>(wire);
+  if (streams(a, 4)) rs_ag_c16_launch<C16RsStream>(x, w, a, divmode, vector_ok, stream);
+  else rs_ag_c16_launch<C16Cached>(x, w, a, divmode, vector_ok, stream);
+  return hipGetLastError();
+}
+
+hipError_t launch_fold(const RankPtrs& bufs, const RingArgs& a, int64_t count, int dtype, int compress, int divmode,
+                       bool vector_ok, hipStream_t stream) {
+  int64_t blocks = (count / 4 + kBlock) / kBlock;
+  if (blocks < 1) blocks = 1;
+  if (blocks > (1 << 20)) blocks = 1 << 20;
+  const dim3 grid((unsigned)blocks), block(kBlock);
+#define HVDX_FOLD(T, C, DIV) \
+  if (vector_ok) hipLaunchKernelGGL((fold_kernel<T, DIV, C, true>), grid, block, 0, stream, bufs, a, count); \
+  else hipLaunchKernelGGL((fold_kernel<T, DIV, C, false>), grid, block, 0, stream, bufs, a, count)
+#define HVDX_FOLD_D(T, C) \
+  if (divmode == DIV_NONE) { HVDX_FOLD(T, C, DIV_NONE); } \
+  else if (divmode == DIV_POW2) { HVDX_FOLD(T, C, DIV_POW2); } \
+  else { HVDX_FOLD(T, C, DIV_TRUE); }
+  if (compress == HVDX_COMPRESS_FP16) {
+    HVDX_FOLD_D(float, true)
+  } else if (dtype == HVDX_FLOAT32) {
+    HVDX_FOLD_D(float, false)
+  } else {
+    HVDX_FOLD_D(_Float16, false)
+  }
+#undef HVDX_FOLD_D
+#undef HVDX_FOLD
   return hipGetLastError();
 }
 

@@ -42,7 +42,13 @@ class FusedAllreduce:
     """In-place allreduce of N ranks' gradient lists (SUM or AVERAGE)."""
 
     def __init__(self, per_rank, op: str = "average", compress: bool = False,
-                 threshold_bytes: int = L.DEFAULT_FUSION_THRESHOLD, align_bytes: int = L.DEFAULT_FUSION_ALIGN):
+                 threshold_bytes: int = L.DEFAULT_FUSION_THRESHOLD, align_bytes: int = L.DEFAULT_FUSION_ALIGN,
+                 schedule: str = "ring"):
+        """schedule "ring" runs the ring's 2(N-1) steps; "fold" computes the same bits
+        with hvdx_fold_allreduce (no per-step messages: a one-GPU bound, not the ring)."""
+        if schedule not in ("ring", "fold"):
+            raise ValueError("schedule must be 'ring' or 'fold'")
+        self.schedule = schedule
         if not per_rank or len(per_rank) > L.MAX_RANKS:
             raise ValueError(f"need 1..{L.MAX_RANKS} ranks")
         if op not in _OPS:
@@ -112,7 +118,10 @@ class FusedAllreduce:
 
     def ring(self, b: Bucket, stream: int) -> None:
         ptrs, count, dtype, compress, ws, wsb = self.ring_args(b)
-        L.hvdx_ring_allreduce(ptrs, self.nranks, count, dtype, self.op, compress, ws, wsb, stream)
+        if self.schedule == "fold":
+            L.hvdx_fold_allreduce(ptrs, self.nranks, count, dtype, self.op, compress, stream)
+        else:
+            L.hvdx_ring_allreduce(ptrs, self.nranks, count, dtype, self.op, compress, ws, wsb, stream)
 
     def ring_phase(self, b: Bucket, phase: int, stream: int) -> None:
         """All N-1 steps of one half of the ring (one C call)."""
@@ -124,24 +133,24 @@ class FusedAllreduce:
         ptrs, count, dtype, compress, ws, wsb = self.ring_args(b)
         L.hvdx_ring_step(ptrs, self.nranks, count, dtype, self.op, compress, phase, step, ws, wsb, stream)
 
-    def launches(self, stream: int):
-        """The allreduce as its separate kernel launches, in order:
-        (kind, bucket index, step, zero-argument callable).  kind is "pack", "rs",
-        "ag", "unpack", or "ring" (the one-rank compressed ring, a round trip through
-        binary16).  Running them all in order is one call of this object."""
+    def kernel_sequence(self):
+        """The kernels one call launches, in order: (kind, bucket index, step) with
+        kind "pack", "rs", "rs_ag" (adding step N-2 fused with replacing step 0),
+        "ag", "unpack", or "ring" (the one-rank compressed round trip)."""
         out = []
+        n = self.nranks
         for bi, b in enumerate(self.buckets):
             if not b.direct:
-                out.append(("pack", bi, -1, lambda b=b: self.pack(b, stream)))
-            if self.nranks == 1:
+                out.append(("pack", bi, -1))
+            if n == 1:
                 if b.direct and self.compress:  # the only one-rank ring that launches a kernel
-                    out.append(("ring", bi, -1, lambda b=b: self.ring(b, stream)))
+                    out.append(("ring", bi, -1))
             else:
-                for ph, kind in ((L.PHASE_REDUCE_SCATTER, "rs"), (L.PHASE_ALLGATHER, "ag")):
-                    for s in range(self.nranks - 1):
-                        out.append((kind, bi, s, lambda b=b, ph=ph, s=s: self.ring_step(b, ph, s, stream)))
+                out += [("rs", bi, s) for s in range(n - 2)]
+                out.append(("rs_ag", bi, n - 2))
+                out += [("ag", bi, s) for s in range(1, n - 1)]
             if not b.direct:
-                out.append(("unpack", bi, -1, lambda b=b: self.unpack(b, stream)))
+                out.append(("unpack", bi, -1))
         return out
 
     def __call__(self, stream: int | None = None) -> None:

@@ -29,6 +29,9 @@ KIND_NAMES = {
     L.KERNEL_ALLGATHER: "allgather",
     L.KERNEL_UNPACK: "copy out",
     L.KERNEL_ROUNDTRIP: "fp16 round trip",
+    L.KERNEL_BROADCAST: "broadcast",
+    L.KERNEL_RS_AG: "reduce-scatter + allgather",
+    L.KERNEL_FOLD: "fold",
 }
 
 
@@ -40,14 +43,32 @@ def chunks_of_step(kind: int, step: int, rank: int, n: int):
     return (rank + 1 - step) % n, (rank - step) % n
 
 
+def broadcast_step_args(step: int, rank: int, root: int, n: int) -> dict:
+    """What `rank` does in broadcast step `step`: rank root+k forwards chunk step-k to
+    its right neighbour (k = 0..N-2) and received chunk step-k+1 from its left one."""
+    k = (rank - root) % n
+    args = {}
+    if k <= n - 2 and 0 <= step - k < n:
+        args["send chunk"] = step - k
+        args["to"] = (rank + 1) % n
+    if k >= 1 and 0 <= step - k + 1 < n:
+        args["recv chunk"] = step - k + 1
+        args["from"] = (rank - 1) % n
+    return args
+
+
 class Timeline:
-    def __init__(self, capacity: int = 1 << 16):
+    """per_phase=False records every launch; True records each run of launches of one
+    kernel inside a library call as one record (see hvdx_timeline_begin)."""
+
+    def __init__(self, capacity: int = 1 << 16, per_phase: bool = False):
         self.capacity = capacity
+        self.per_phase = per_phase
         self.records: list = []
         self.dropped = 0
 
     def __enter__(self):
-        L.hvdx_timeline_begin(self.capacity)
+        L.hvdx_timeline_begin(self.capacity, self.per_phase)
         return self
 
     def __exit__(self, *exc):
@@ -63,6 +84,8 @@ class Timeline:
         for rec in self.records:
             kind, n, step = rec["kind"], rec["nranks"], rec["step"]
             name = KIND_NAMES.get(kind, str(kind)) + (f" {step}" if step >= 0 else "")
+            if rec["launches"] > 1:
+                name += f"-{step + rec['launches'] - 1}"
             common = {"ph": "X", "pid": 0, "ts": rec["start_us"], "dur": rec["duration_us"], "cat": "hvdx"}
             events.append(dict(common, tid=0, name=name, args={"elements_per_rank": rec["count"], "ranks": n}))
             for r in range(n):
@@ -71,7 +94,13 @@ class Timeline:
                     events.append({"ph": "M", "pid": 0, "tid": r + 1, "name": "thread_name",
                                    "args": {"name": f"rank {r}"}})
                 args = {}
-                if kind in (L.KERNEL_REDUCE_SCATTER, L.KERNEL_ALLGATHER):
+                if kind == L.KERNEL_BROADCAST:
+                    args = broadcast_step_args(step, r, rec["root"], n)
+                if kind == L.KERNEL_RS_AG:  # adding step N-2, then replacing step 0
+                    args = {"send chunks": [(r + 2) % n, (r + 1) % n], "to": (r + 1) % n,
+                            "recv chunks": [(r + 1) % n, r], "from": (r - 1) % n,
+                            "received values": "added, then replace"}
+                if kind in (L.KERNEL_REDUCE_SCATTER, L.KERNEL_ALLGATHER) and rec["launches"] == 1:
                     sent, recv = chunks_of_step(kind, step, r, n)
                     args = {"send chunk": sent, "to": (r + 1) % n, "recv chunk": recv, "from": (r - 1) % n,
                             "received values": "added" if kind == L.KERNEL_REDUCE_SCATTER else "replace"}

@@ -55,7 +55,7 @@ def gpu_ring(x: np.ndarray, op: str, compress: bool = False, offset_elems: int =
 
 def bits(a: np.ndarray) -> np.ndarray:
     a = np.ascontiguousarray(a)
-    return a.view({2: np.uint16, 4: np.uint32, 8: np.uint64}[a.dtype.itemsize])
+    return a.view({1: np.uint8, 2: np.uint16, 4: np.uint32, 8: np.uint64}[a.dtype.itemsize])
 
 
 def assert_bits_equal(got: np.ndarray, want: np.ndarray, what: str = "") -> None:

@@ -157,3 +157,25 @@ def test_plan_argument_errors():
     with pytest.raises(hv.HvdxError):
         hv.hvdx_fuse_plan([1], hv.FLOAT32, -1)
     assert hv.hvdx_fuse_plan([], hv.FLOAT32) == ([], [], [], [])
+
+
+def test_broadcast_argument_errors():
+    bc = hv.hvdx_broadcast
+    assert status_of(bc, bufs(3, 64), 3, 64, 3) == hv.ERR_INVALID  # root out of range
+    assert status_of(bc, bufs(3, 64), 3, 64, -1) == hv.ERR_INVALID
+    assert status_of(bc, bufs(3, 64), 3, -1, 0) == hv.ERR_INVALID
+    assert status_of(bc, [FAKE, FAKE + 32, FAKE + 4096], 3, 64, 0) == hv.ERR_ALIAS
+    assert status_of(bc, bufs(3, 64), 0, 64, 0) == hv.ERR_INVALID
+    assert status_of(bc, bufs(3, 0), 3, 0, 1) == hv.OK  # nothing to copy
+    st = hv.hvdx_broadcast_step
+    assert status_of(st, bufs(3, 64), 3, 64, 0, 4) == hv.ERR_INVALID  # steps are 0..2N-3
+    assert status_of(st, bufs(1, 64), 1, 64, 0, 0) == hv.ERR_INVALID  # no steps with one rank
+
+
+def test_fold_argument_errors():
+    fo = hv.hvdx_fold_allreduce
+    assert status_of(fo, bufs(2, 8), 0, 8, hv.FLOAT32, hv.SUM) == hv.ERR_INVALID
+    assert status_of(fo, bufs(2, 8), 2, 8, hv.FLOAT16, hv.SUM, hv.COMPRESS_FP16) == hv.ERR_INVALID
+    assert status_of(fo, bufs(2, 8), 2, 8, hv.FLOAT32, hv.SUM, 7) == hv.ERR_INVALID
+    assert status_of(fo, [FAKE, FAKE + 16], 2, 8, hv.FLOAT32, hv.SUM) == hv.ERR_ALIAS
+    assert status_of(fo, bufs(2, 0), 2, 0, hv.FLOAT32, hv.AVERAGE) == hv.OK

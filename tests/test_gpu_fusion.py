@@ -115,13 +115,14 @@ CYCLE_CASES = [
 ]
 
 
+@pytest.mark.parametrize("schedule", ["ring", "fold"])
 @pytest.mark.parametrize("case", range(len(CYCLE_CASES)))
-def test_fused_allreduce_matches_oracle(case):
+def test_fused_allreduce_matches_oracle(case, schedule):
     numel, n, threshold, compress, op = CYCLE_CASES[case]
     rng = np.random.default_rng(300 + case)
     host, dev, keep = make_tensors(rng, n, numel, np.float32)
-    say(f"cycle case={case} n={n} threshold={threshold} compress={compress}")
-    ar = hv.FusedAllreduce(dev, op=op, compress=compress, threshold_bytes=threshold)
+    say(f"cycle case={case} n={n} threshold={threshold} compress={compress} schedule={schedule}")
+    ar = hv.FusedAllreduce(dev, op=op, compress=compress, threshold_bytes=threshold, schedule=schedule)
     ar()
     torch.cuda.synchronize()
     want = allreduce.allreduce(host, op, compress=compress, threshold=threshold)

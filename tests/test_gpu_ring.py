@@ -70,12 +70,34 @@ def test_special_values():
     x32[:, :8] = np.array([0.0, -0.0, 1.0, 2.0 ** -24, 65504.0, 65520.0, np.inf, -np.inf], np.float32)
     x32[1, 8:16] = 2.0 ** 24
     x32[:, 16:24] = 1.0
-    for op in ("sum", "average"):
-        say(f"special values op={op}")
-        assert_bits_equal(gpu_ring(x32, op), oracle_ring(x32, op), "f32")
-        x16 = fusion.cast(x32, np.float16)
-        assert_bits_equal(gpu_ring(x16, op), oracle_ring(x16, op), "f16")
-        assert_bits_equal(gpu_ring(x32, op, True), oracle_ring(x32, op, True), "compressed")
+    def fold(x, op, compress=False):
+        rows, keep = to_gpu_rows(x)
+        dt = hv.FLOAT32 if x.dtype == np.float32 else hv.FLOAT16
+        hv.hvdx_fold_allreduce([r.data_ptr() for r in rows], x.shape[0], x.shape[1], dt, OPS[op],
+                               hv.COMPRESS_FP16 if compress else hv.COMPRESS_NONE)
+        return from_gpu_rows(rows)
+
+    def halves(x, op, compress=False):
+        n, count = x.shape
+        rows, keep = to_gpu_rows(x)
+        dt = hv.FLOAT32 if x.dtype == np.float32 else hv.FLOAT16
+        cmp = hv.COMPRESS_FP16 if compress else hv.COMPRESS_NONE
+        wsb = hv.hvdx_ring_workspace_bytes(n, count, dt, cmp)
+        ws = torch.zeros(max(wsb, 1), dtype=torch.uint8, device="cuda")
+        ptrs = [r.data_ptr() for r in rows]
+        hv.hvdx_ring_reduce_scatter(ptrs, n, count, dt, OPS[op], cmp, ws.data_ptr() if wsb else 0, wsb)
+        hv.hvdx_ring_allgather(ptrs, n, count, dt, OPS[op], cmp, ws.data_ptr() if wsb else 0, wsb)
+        return from_gpu_rows(rows)
+
+    x16 = fusion.cast(x32, np.float16)
+    for nr in (4, 3, 2):
+        for op in ("sum", "average"):
+            say(f"special values n={nr} op={op}")
+            a32, a16 = x32[:nr].copy(), x16[:nr].copy()
+            for path in (gpu_ring, fold, halves):
+                assert_bits_equal(path(a32, op), oracle_ring(a32, op), f"f32 {path.__name__}")
+                assert_bits_equal(path(a16, op), oracle_ring(a16, op), f"f16 {path.__name__}")
+                assert_bits_equal(path(a32, op, True), oracle_ring(a32, op, True), f"compressed {path.__name__}")
 
 
 def test_each_step_matches_oracle_states():
@@ -191,3 +213,23 @@ def test_reduce_scatter_and_allgather_halves():
     for c in range(n):
         want[starts[c] : starts[c] + lengths[c]] = x[(c - 1) % n, starts[c] : starts[c] + lengths[c]]
     assert_bits_equal(from_gpu_rows(rows), np.broadcast_to(want, (n, count)).copy(), "allgather alone")
+
+
+def test_fold_matches_the_ring_bit_for_bit():
+    """hvdx_fold_allreduce computes the ring's fold directly: same bits as the oracle's ring."""
+    rng = np.random.default_rng(108)
+    for n, count in CASES[::3] + [(8, 1 << 20), (64, 100003), (3, 7)]:
+        for dtype, compress in ((np.float32, False), (np.float16, False), (np.float32, True)):
+            for op in ("sum", "average"):
+                say(f"fold n={n} count={count} {np.dtype(dtype).name} compress={compress} {op}")
+                x = inputs(rng, n, count, dtype)
+                rows, keep = to_gpu_rows(x)
+                dt = hv.FLOAT32 if dtype == np.float32 else hv.FLOAT16
+                hv.hvdx_fold_allreduce([r.data_ptr() for r in rows], n, count, dt, OPS[op],
+                                       hv.COMPRESS_FP16 if compress else hv.COMPRESS_NONE)
+                assert_bits_equal(from_gpu_rows(rows), oracle_ring(x, op, compress), f"n={n} count={count}")
+    # unaligned buffers take the per-element path
+    x = inputs(rng, 5, 1001, np.float32)
+    rows, keep = to_gpu_rows(x, offset_elems=1)
+    hv.hvdx_fold_allreduce([r.data_ptr() for r in rows], 5, 1001, hv.FLOAT32, hv.AVERAGE)
+    assert_bits_equal(from_gpu_rows(rows), oracle_ring(x, "average"), "unaligned")

@@ -25,14 +25,14 @@ def test_records_follow_launches():
     per_rank = tensors(5, [7, 4000, 100, 30000, 5])
     ar = hv.FusedAllreduce(per_rank, op="average", threshold_bytes=40000)
     sid = torch.cuda.current_stream().cuda_stream
-    launches = ar.launches(sid)
+    launches = ar.kernel_sequence()
     with hv.Timeline(capacity=1000) as tl:
         ar(sid)
         ar(sid)
     assert tl.dropped == 0 and len(tl.records) == 2 * len(launches)
-    code = {"pack": 0, "rs": 1, "ag": 2, "unpack": 3}
-    for rec, (kind, bi, s, _fn) in zip(tl.records, launches + launches):
-        assert rec["kind"] == code[kind] and rec["step"] == s and rec["nranks"] == 5
+    code = {"pack": 0, "rs": 1, "ag": 2, "unpack": 3, "rs_ag": 6}
+    for rec, (kind, bi, s) in zip(tl.records, launches + launches):
+        assert rec["kind"] == code[kind] and rec["step"] == s and rec["nranks"] == 5 and rec["launches"] == 1
         assert rec["count"] == ar.buckets[bi].count and rec["duration_us"] > 0
     starts = [r["start_us"] for r in tl.records]
     assert starts[0] == 0 and starts == sorted(starts)
@@ -47,7 +47,7 @@ def test_capacity_counts_dropped_launches():
     ar = hv.FusedAllreduce(per_rank)
     with hv.Timeline(capacity=2) as tl:
         ar()
-    assert len(tl.records) == 2 and tl.dropped == len(ar.launches(0)) - 2
+    assert len(tl.records) == 2 and tl.dropped == len(ar.kernel_sequence()) - 2
 
 
 def test_environment_variable_writes_trace(tmp_path):
@@ -64,5 +64,21 @@ def test_environment_variable_writes_trace(tmp_path):
     subprocess.run([sys.executable, "-c", code], env=env, check=True, timeout=120)
     trace = json.loads(path.read_text())
     names = [e["name"] for e in trace["traceEvents"] if e["ph"] == "X" and e["tid"] == 0]
-    assert names == ["copy in", "reduce-scatter 0", "reduce-scatter 1", "reduce-scatter 2", "allgather 0",
+    assert names == ["copy in", "reduce-scatter 0", "reduce-scatter 1", "reduce-scatter + allgather 2",
                      "allgather 1", "allgather 2", "copy out"] * 2
+
+
+def test_per_phase_records():
+    per_rank = tensors(6, [7, 4000, 100, 30000, 5])
+    ar = hv.FusedAllreduce(per_rank, op="average", threshold_bytes=40000)
+    with hv.Timeline(capacity=100, per_phase=True) as tl:
+        ar()
+    got = [(r["kind"], r["step"], r["launches"]) for r in tl.records]
+    want = []
+    for bi, b in enumerate(ar.buckets):
+        if not b.direct:
+            want.append((0, -1, 1))
+        want += [(1, 0, 4), (6, 4, 1), (2, 1, 4)]
+        if not b.direct:
+            want.append((3, -1, 1))
+    assert got == want

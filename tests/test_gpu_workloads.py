@@ -56,24 +56,30 @@ def test_tiny_workload_full_parity():
             assert_bits_equal(per_rank[r][t].cpu().numpy(), want[r][t], f"rank {r} tensor {t}")
 
 
-@pytest.mark.parametrize("name", ["resnet50", "inceptionv3", "vgg16", "vgg16fp16"])
-def test_full_workload(name):
+@pytest.mark.parametrize(
+    "name,threshold",
+    [("resnet50", 64 << 20), ("inceptionv3", 64 << 20), ("vgg16", 64 << 20), ("vgg16fp16", 64 << 20),
+     ("resnet50", 0), ("inceptionv3", 1 << 20)],
+    ids=["resnet50", "inceptionv3", "vgg16", "vgg16fp16", "resnet50-unfused", "inceptionv3-1MiB"],
+)
+def test_full_workload(name, threshold):
+    """Threshold 0 is the unfused ablation: every tensor reduced by its own ring."""
     w = configs.get(name)
     n = w.nranks
-    say(f"workload {name}: generate")
+    say(f"workload {name} threshold {threshold}: generate")
     per_rank, storage, starts = wgpu.make_rank_tensors(w)
     numel, prefix = w.numel(), w.prefix()
     say(f"workload {name}: allreduce")
-    ar = hv.FusedAllreduce(per_rank, op=w.op, compress=w.compress)
+    ar = hv.FusedAllreduce(per_rank, op=w.op, compress=w.compress, threshold_bytes=threshold)
     ar()
     torch.cuda.synchronize()
 
     # sampled positions of every bucket against the oracle's ring, bit for bit
-    plan = fusion.fuse_plan(numel, 2 if w.compress else 4)
+    plan = fusion.fuse_plan(numel, 2 if w.compress else 4, threshold)
     assert [(b.count, b.direct) for b in plan] == [(b.count, b.direct) for b in ar.buckets]
     value_of = lambda r, t, i: rng.values(w.dist, w.key(r), prefix[t] + np.asarray(i), w.sigma)  # noqa: E731
     for bi, b in enumerate(plan):
-        elems = sample_positions(b, numel, n, seed=bi)
+        elems = sample_positions(b, numel, n, seed=bi, nrandom=4096 if len(plan) < 20 else 64)
         say(f"workload {name}: bucket {bi} count={b.count} samples={len(elems)}")
         want, tensor, local = allreduce.ring_columns(b, numel, elems, value_of, n, w.op, w.compress)
         keep = tensor >= 0
