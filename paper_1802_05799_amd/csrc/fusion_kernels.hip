@@ -5,8 +5,8 @@
 // 16-byte vector of the buffer, so load balance does not depend on how ragged the
 // tensors are (Inception-V3 mixes 32-element batch-norm vectors with 2M-element
 // weights).  A block finds the tensors that overlap its tile once, stages their
-// offsets and ends in LDS, and reuses them for all N ranks; per rank it stages the
-// N tensor pointers of that rank.  A lane binary-searches the LDS table for its
+// offsets and ends in LDS, together with the tensor pointers of the ranks it
+// serves, and reuses them for all of those ranks.  A lane binary-searches the LDS table for its
 // vector's tensor.  Vectors entirely inside one tensor with a 16-byte aligned
 // source take the vector path; tensor tails, padding and unaligned tensors take a
 // per-element path.  Padding is written as zero by the copy-in and skipped by the
@@ -23,19 +23,26 @@ typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 // Shape of a copy kernel: POS 16-byte buffer vectors per lane (a tile is kBlock*POS
 // vectors), RB ranks whose loads are in flight together, RPB ranks per block (0 =
 // all), and non-temporal loads/stores.  Measured on MI355X with the workloads'
-// buckets (both stream their data once, so every access is non-temporal).
+// buckets (both stream their data once, so every access is non-temporal).  Two
+// ranks per block and small LDS tables (3 KiB a block) gave the most blocks in
+// flight and the best rate for both directions.
+#ifndef HVDX_LDS_TENSORS
+#define HVDX_LDS_TENSORS 64
+#endif
 template <int POS_, int RB_, int RPB_, bool NTL_, bool NTS_>
 struct CopyCfg {
   static constexpr int POS = POS_, RB = RB_, RPB = RPB_;
   static constexpr bool NTL = NTL_, NTS = NTS_;
   static constexpr int kTileVecs = kBlock * POS_;
-  static constexpr int kLdsTensors = kBlock * POS_ + 8;  // a tile's tensors staged in LDS
+  // A tile's tensors staged in LDS; a tile that spans more looks its tensors up in
+  // global memory instead.
+  static constexpr int kLdsTensors = kBlock * POS_ + 8 < HVDX_LDS_TENSORS ? kBlock * POS_ + 8 : HVDX_LDS_TENSORS;
 };
 #ifndef HVDX_PACK_CFG
-#define HVDX_PACK_CFG CopyCfg<2, 4, 4, true, true>
+#define HVDX_PACK_CFG CopyCfg<2, 2, 2, true, true>
 #endif
 #ifndef HVDX_UNPACK_CFG
-#define HVDX_UNPACK_CFG CopyCfg<4, 2, 2, true, true>
+#define HVDX_UNPACK_CFG CopyCfg<2, 2, 2, true, true>
 #endif
 #ifndef HVDX_PACK16_CFG
 #define HVDX_PACK16_CFG HVDX_PACK_CFG
@@ -47,7 +54,10 @@ using PackCfg = HVDX_PACK_CFG;      // binary32 buffers
 using UnpackCfg = HVDX_UNPACK_CFG;
 using Pack16Cfg = HVDX_PACK16_CFG;  // binary16 buffers
 using Unpack16Cfg = HVDX_UNPACK16_CFG;
-constexpr int kLdsPtrs = 2048;  // (rank, tensor) pointers a tile can stage in LDS
+#ifndef HVDX_LDS_PTRS
+#define HVDX_LDS_PTRS 256
+#endif
+constexpr int kLdsPtrs = HVDX_LDS_PTRS;  // (rank, tensor) pointers a tile can stage in LDS
 
 template <typename TB>
 struct BufVec {
@@ -206,35 +216,39 @@ __device__ int64_t find_tensor_wave(const int64_t* offset, int64_t lo, int64_t h
   return lo - 1;
 }
 
-// The first wavefront locates the tile's tensors; everyone stages their offsets and ends.
+// Waves 0 and 1 locate the tile's first and last tensor at the same time; then the
+// whole block stages their offsets and ends, and the tile's (rank, tensor) pointers
+// of ranks [r0, r1), in one pass: two rounds of global loads per block in all.
 template <int LDS_TENSORS>
 __device__ TileTable stage_tile(const int64_t* offset, const int64_t* numel, int ntensors, int64_t p0, int64_t p1,
-                                int64_t* s_off, int64_t* s_end, int64_t* s_meta) {
-  if (threadIdx.x < 64) {
-    const int64_t t0 = find_tensor_wave(offset, 0, ntensors, p0);
-    const int64_t t1 = find_tensor_wave(offset, t0 < 0 ? 0 : t0, ntensors, p1 - 1);
-    if (threadIdx.x == 0) {
-      s_meta[0] = t0;
-      s_meta[1] = t1 - t0 + 1;
-    }
+                                const void* const* ptrs, int r0, int r1, int64_t* s_off, int64_t* s_end,
+                                int64_t* s_meta, const void** s_ptr, bool* ptrs_in_lds) {
+  const int wave = threadIdx.x >> 6;
+  if (wave < 2) {
+    const int64_t t = find_tensor_wave(offset, 0, ntensors, wave == 0 ? p0 : p1 - 1);
+    if ((threadIdx.x & 63) == 0) s_meta[wave] = t;
   }
   __syncthreads();
   TileTable tt;
   tt.t0 = s_meta[0];
-  tt.nt = (int)s_meta[1];
+  tt.nt = (int)(s_meta[1] - s_meta[0] + 1);
   tt.in_lds = tt.nt <= LDS_TENSORS;
-  if (tt.in_lds) {
-    for (int j = threadIdx.x; j < tt.nt; j += kBlock) {
-      const int64_t t = tt.t0 + j;
-      if (t >= 0) {
-        s_off[j] = offset[t];
-        s_end[j] = offset[t] + numel[t];
-      } else {  // positions before the first tensor are padding
-        s_off[j] = INT64_MIN;
-        s_end[j] = INT64_MIN;
-      }
+  const int nr = r1 - r0;
+  const bool pin = tt.in_lds && (int64_t)tt.nt * nr <= kLdsPtrs;
+  const int work = pin ? tt.nt * nr : (tt.in_lds ? tt.nt : 0);
+  for (int idx = threadIdx.x; idx < work; idx += kBlock) {
+    if (idx < tt.nt) {
+      const int64_t t = tt.t0 + idx;
+      s_off[idx] = t >= 0 ? offset[t] : INT64_MIN;  // positions before the first tensor are padding
+      s_end[idx] = t >= 0 ? offset[t] + numel[t] : INT64_MIN;
+    }
+    if (pin) {
+      const int rr = idx / tt.nt;
+      const int64_t t = tt.t0 + (idx - rr * tt.nt);
+      s_ptr[idx] = t >= 0 ? ptrs[(int64_t)(r0 + rr) * ntensors + t] : nullptr;
     }
   }
+  *ptrs_in_lds = pin;
   __syncthreads();
   return tt;
 }
@@ -316,23 +330,6 @@ struct PtrTable {
   }
 };
 
-// Pointers of ranks [r0, r1) for the tile's tensors.
-__device__ PtrTable stage_ptrs(const void* const* g, const TileTable& tt, int ntensors, int r0, int r1,
-                               const void** s_ptr) {
-  PtrTable pt{g, nullptr, tt.t0, ntensors, tt.nt, r0};
-  const int nr = r1 - r0;
-  if (tt.in_lds && (int64_t)tt.nt * nr <= kLdsPtrs) {
-    for (int idx = threadIdx.x; idx < tt.nt * nr; idx += kBlock) {
-      const int rr = idx / tt.nt;
-      const int64_t t = tt.t0 + (idx - rr * tt.nt);
-      s_ptr[idx] = t >= 0 ? g[(int64_t)(r0 + rr) * ntensors + t] : nullptr;
-    }
-    pt.s = s_ptr;
-  }
-  __syncthreads();
-  return pt;
-}
-
 template <typename TT, typename TB, typename Cfg>
 __global__ __launch_bounds__(kBlock) void pack_kernel(const void* const* __restrict__ srcs,
                                                       const int64_t* __restrict__ numel,
@@ -345,9 +342,11 @@ __global__ __launch_bounds__(kBlock) void pack_kernel(const void* const* __restr
   __shared__ const void* s_ptr[kLdsPtrs];
   const int64_t p0 = (int64_t)blockIdx.x * kTileVecs * V;
   const int64_t p1 = p0 + (int64_t)kTileVecs * V < count ? p0 + (int64_t)kTileVecs * V : count;
-  const TileTable tt = stage_tile<Cfg::kLdsTensors>(offset, numel, ntensors, p0, p1, s_off, s_end, s_meta);
   const int rbeg = blockIdx.y * rpb, rend = rbeg + rpb < nranks ? rbeg + rpb : nranks;
-  const PtrTable pt = stage_ptrs(srcs, tt, ntensors, rbeg, rend, s_ptr);
+  bool pin;
+  const TileTable tt = stage_tile<Cfg::kLdsTensors>(offset, numel, ntensors, p0, p1, srcs, rbeg, rend, s_off, s_end,
+                                                    s_meta, s_ptr, &pin);
+  const PtrTable pt{srcs, pin ? s_ptr : nullptr, tt.t0, ntensors, tt.nt, rbeg};
 
   Pos pos[kPosPerLane];
 #pragma unroll
@@ -407,9 +406,11 @@ __global__ __launch_bounds__(kBlock) void unpack_kernel(RankPtrs bufs, int64_t c
   __shared__ const void* s_ptr[kLdsPtrs];
   const int64_t p0 = (int64_t)blockIdx.x * kTileVecs * V;
   const int64_t p1 = p0 + (int64_t)kTileVecs * V < count ? p0 + (int64_t)kTileVecs * V : count;
-  const TileTable tt = stage_tile<Cfg::kLdsTensors>(offset, numel, ntensors, p0, p1, s_off, s_end, s_meta);
   const int rbeg = blockIdx.y * rpb, rend = rbeg + rpb < nranks ? rbeg + rpb : nranks;
-  const PtrTable pt = stage_ptrs(dsts, tt, ntensors, rbeg, rend, s_ptr);
+  bool pin;
+  const TileTable tt = stage_tile<Cfg::kLdsTensors>(offset, numel, ntensors, p0, p1, dsts, rbeg, rend, s_off, s_end,
+                                                    s_meta, s_ptr, &pin);
+  const PtrTable pt{dsts, pin ? s_ptr : nullptr, tt.t0, ntensors, tt.nt, rbeg};
 
   Pos pos[kPosPerLane];
 #pragma unroll
