@@ -53,9 +53,9 @@ def kernel_bytes(ar, kind, bi, step):
     es_t = 4 if ar.dtype == 0 else 2  # tensor element size
     es_b = 4 if ar.buf_dtype == 0 else 2  # buffer element size
     data = sum(ar.numel[t] for t in b.tensors)
-    if kind == "pack":
+    if kind in ("pack", "pack_rs"):  # the fused adding step reuses the values it packs
         return n * (es_t * data + es_b * b.count)
-    if kind == "unpack":
+    if kind in ("unpack", "ag_unpack"):  # the fused replacing step only changes which buffer is read
         return n * (es_b + es_t) * data
     compressed = b.direct and ar.compress
     if kind == "rs_ag":  # read owner and sender, write owner and the next rank
@@ -73,7 +73,8 @@ def kernel_bytes(ar, kind, bi, step):
     return 0
 
 
-KIND_OF_CODE = {0: "pack", 1: "rs", 2: "ag", 3: "unpack", 4: "ring", 6: "rs_ag"}
+KIND_OF_CODE = {0: "pack", 1: "rs", 2: "ag", 3: "unpack", 4: "ring", 6: "rs_ag", 7: "fold", 8: "pack_rs",
+                9: "ag_unpack"}
 
 
 def phase_sequence(ar):
@@ -82,6 +83,17 @@ def phase_sequence(ar):
     out = []
     n = ar.nranks
     for bi, b in enumerate(ar.buckets):
+        if b.count == 0:
+            continue
+        if ar.fuse_boundary and not b.direct and n >= 3:
+            out.append((8, bi, 0, 1))
+            if n > 3:
+                out.append((1, bi, 1, n - 3))
+            out.append((6, bi, n - 2, 1))
+            if n > 3:
+                out.append((2, bi, 1, n - 3))
+            out.append((9, bi, n - 2, 1))
+            continue
         if not b.direct:
             out.append((0, bi, -1, 1))
         if n == 1:
@@ -107,7 +119,25 @@ def kernel_name(ar, kind, bi):
     return kind
 
 
-def measure(name, steps, warmup, threshold=64 << 20, per_kernel_pass=True, schedule="ring"):
+def time_graph(ar, steps, stream):
+    """ms per allreduce replaying one HIP graph of the whole cycle `steps` times."""
+    import torch
+
+    graph = ar.capture()
+    for _ in range(2):
+        graph.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(steps):
+        graph.replay()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    del graph
+    return e0.elapsed_time(e1) / steps
+
+
+def measure(name, steps, warmup, threshold=64 << 20, per_kernel_pass=True, schedule="ring", graph_pass=True):
     import torch
 
     import paper_1802_05799_amd as hv
@@ -133,9 +163,11 @@ def measure(name, steps, warmup, threshold=64 << 20, per_kernel_pass=True, sched
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms = e0.elapsed_time(e1) / steps
+    # the same cycle submitted as one HIP graph per step (launch overhead removed)
+    graph_ms = time_graph(ar, steps, stream) if graph_pass else None
     if not per_kernel_pass:
         res = {"ms_per_step": ms, "algbw_GBps": w.rank_bytes / (ms * 1e-3) / 1e9, "buckets": len(ar.buckets),
-               "launches_per_step": len(ar.kernel_sequence())}
+               "launches_per_step": len(ar.kernel_sequence()), "graph_ms_per_step": graph_ms}
         del ar, per_rank, storage
         torch.cuda.empty_cache()
         return res
@@ -177,10 +209,12 @@ def measure(name, steps, warmup, threshold=64 << 20, per_kernel_pass=True, sched
     res = {
         "workload": name,
         "nranks": w.nranks,
+        "steps": steps,
         "ms_per_step": ms,
         "algbw_GBps": w.rank_bytes / (ms * 1e-3) / 1e9,
         "busbw_GBps": w.rank_bytes / (ms * 1e-3) / 1e9 * 2 * (w.nranks - 1) / w.nranks,
         "wall_ms_per_step": 1000.0 * wall / steps,
+        "graph_ms_per_step": graph_ms,
         "kernels": per_kernel,
         "timing_outliers": outliers,
         "buckets": [(b.count, len(b.tensors), b.direct) for b in ar.buckets],
@@ -266,10 +300,11 @@ def short_kernel_name(full):
     for key in ("rs_ag_step_kernel", "rs_step_kernel", "ag_step_kernel"):
         if key in base:
             return key.replace("_kernel", "") + ("_f16" if "<_Float16" in base else "_f32")
+    ring = base.rstrip().endswith(", true>")  # the copy kernels' last template argument: fused with a ring step
     if "unpack_kernel" in base:
-        return "unpack"
+        return "ag_unpack" if ring else "unpack"
     if "pack_kernel" in base:
-        return "pack"
+        return "pack_rs" if ring else "pack"
     return None
 
 
@@ -392,7 +427,8 @@ def main():
         torch.cuda.empty_cache()
 
     head = measure(args.workload, args.steps, args.warmup)
-    print(f"# {args.workload}: {head['ms_per_step']:.3f} ms/step, {head['algbw_GBps']:.1f} GB/s", file=sys.stderr,
+    print(f"# {args.workload}: {head['ms_per_step']:.3f} ms/step, {head['algbw_GBps']:.1f} GB/s, "
+          f"graph {head['graph_ms_per_step']:.3f} ms/step", file=sys.stderr,
           flush=True)
     per_config = {}
     if not args.no_per_config:
@@ -403,11 +439,20 @@ def main():
                 r = head
             else:
                 r = measure(name, max(3, args.steps // 2), 2)
-                print(f"# {name}: {r['ms_per_step']:.3f} ms/step, {r['algbw_GBps']:.1f} GB/s", file=sys.stderr,
+                print(f"# {name}: {r['ms_per_step']:.3f} ms/step, {r['algbw_GBps']:.1f} GB/s, "
+                      f"graph {r['graph_ms_per_step']:.3f} ms/step", file=sys.stderr,
                       flush=True)
+            ring = [v for k, v in r["kernels"].items() if k.startswith(("rs_step", "ag_step", "rs_ag_step"))]
+            ring_bytes = sum(v["bytes"] for v in ring) / r["steps"]  # per step
+            ring_ms = sum(v["ms_per_step"] for v in ring)
+            path_bytes = sum(v["bytes"] for v in r["kernels"].values()) / r["steps"]
             per_config[name] = {
                 "nranks": r["nranks"],
                 "ms_per_step": round(r["ms_per_step"], 4),
+                "graph_ms_per_step": r["graph_ms_per_step"] and round(r["graph_ms_per_step"], 4),
+                # algorithmic bytes over time: the ring's kernels alone, and the whole step
+                "ring_hbm_frac": round(ring_bytes / (ring_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4) if ring_ms else None,
+                "path_hbm_frac": round(path_bytes / (r["ms_per_step"] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
                 "algbw_GBps": round(r["algbw_GBps"], 2),
                 "busbw_GBps": round(r["busbw_GBps"], 2),
                 "kernels": {k: {"avg_us": round(v["avg_us"], 2), "GBps": v["GBps"] and round(v["GBps"], 1),
@@ -422,7 +467,8 @@ def main():
         for thr in (0, 1 << 20, 4 << 20, 16 << 20, 64 << 20, 256 << 20):
             r = measure(args.workload, max(3, args.steps // 4), 2, threshold=thr, per_kernel_pass=False)
             ablation[str(thr)] = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in r.items()}
-            print(f"# fusion threshold {thr}: {r['ms_per_step']:.3f} ms/step", file=sys.stderr, flush=True)
+            print(f"# fusion threshold {thr}: {r['ms_per_step']:.3f} ms/step, graph {r['graph_ms_per_step']:.3f}",
+                  file=sys.stderr, flush=True)
 
     # the ring's fold computed directly (same bits, no per-step messages): a bound for
     # one GPU, reported beside the ring, never as the headline value
@@ -431,7 +477,7 @@ def main():
         from workloads import configs
 
         for name in configs.WORKLOADS:
-            r = measure(name, max(3, args.steps // 2), 2, per_kernel_pass=False, schedule="fold")
+            r = measure(name, max(3, args.steps // 2), 2, per_kernel_pass=False, schedule="fold", graph_pass=False)
             fold[name] = {"ms_per_step": round(r["ms_per_step"], 4), "algbw_GBps": round(r["algbw_GBps"], 2)}
             print(f"# fold schedule {name}: {r['ms_per_step']:.3f} ms/step", file=sys.stderr, flush=True)
 

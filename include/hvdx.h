@@ -136,6 +136,56 @@ int hvdx_fuse_unpack(const void* const* bufs, int64_t buf_count, int buf_dtype, 
                      void* stream);
 
 /*
+ * hvdx_fuse_pack_rs -- hvdx_fuse_pack and the ring's adding step 0 (paper section 3,
+ * the first iteration whose received values are added) in one launch: the buffers
+ * end exactly as hvdx_fuse_pack followed by hvdx_ring_step(REDUCE_SCATTER, step 0)
+ * on buf_dtype leaves them (chunk c of rank c+1 holds rank c+1's packed values
+ * plus rank c's, added in buf_dtype), without reading any buffer back.  Needs
+ * nranks >= 3, so that step 0 is not the step that divides for AVERAGE.
+ * Arguments as hvdx_fuse_pack.
+ * Errors: as hvdx_fuse_pack; HVDX_ERR_UNSUPPORTED for nranks < 3.
+ */
+int hvdx_fuse_pack_rs(const void* const* srcs, const int64_t* numel, const int64_t* offset, int ntensors,
+                      int src_dtype, void* const* bufs, int64_t buf_count, int buf_dtype, int nranks, void* stream);
+
+/*
+ * hvdx_fuse_ag_unpack -- the ring's last replacing step (step N-2) and
+ * hvdx_fuse_unpack in one launch: every tensor receives what hvdx_ring_step
+ * (ALLGATHER, step N-2) followed by hvdx_fuse_unpack would give it.  In chunk c
+ * that step hands rank c-3's values to rank c-2 (mod N); here rank c-2 copies them
+ * out of rank c-3's buffer directly, so rank c-2's buffer keeps that chunk's
+ * previous contents (the buffers are left as before the step).  Needs
+ * nranks >= 3 (for fewer ranks the last replacing step is step 0).
+ * Arguments as hvdx_fuse_unpack.
+ * Errors: as hvdx_fuse_unpack; HVDX_ERR_UNSUPPORTED for nranks < 3.
+ */
+int hvdx_fuse_ag_unpack(const void* const* bufs, int64_t buf_count, int buf_dtype, void* const* dsts,
+                        const int64_t* numel, const int64_t* offset, int ntensors, int dst_dtype, int nranks,
+                        void* stream);
+
+/*
+ * hvdx_fuse_allreduce -- one fusion buffer's whole cycle (paper section 7, steps 3
+ * to 5, around the ring-allreduce of section 3), in place on the tensors: their
+ * values end exactly as hvdx_fuse_pack, hvdx_ring_allreduce (buf_dtype, no
+ * compression) and hvdx_fuse_unpack would leave them.  For nranks >= 3 it launches
+ * hvdx_fuse_pack_rs, adding steps 1..N-3, the fused adding step N-2 / replacing
+ * step 0, replacing steps 1..N-3, and hvdx_fuse_ag_unpack: 2N-3 launches and five
+ * buffer passes fewer than the separate calls.  For nranks <= 2 it makes the
+ * separate calls.  The fusion buffers are scratch: their contents afterwards are
+ * unspecified.
+ *
+ *   tensors[nranks*ntensors]  DEVICE array of device pointers, rank-major, read
+ *                             and then written at [0, numel[t]), tensor_dtype
+ *   numel, offset, bufs       as for hvdx_fuse_pack; tensors must not overlap bufs
+ *                             (not checked: the table is device data)
+ *   op                        HVDX_SUM or HVDX_AVERAGE
+ * Errors: as hvdx_fuse_pack, and HVDX_ERR_INVALID for an unknown op.
+ */
+int hvdx_fuse_allreduce(void* const* tensors, const int64_t* numel, const int64_t* offset, int ntensors,
+                        int tensor_dtype, void* const* bufs, int64_t buf_count, int buf_dtype, int nranks, int op,
+                        void* stream);
+
+/*
  * hvdx_ring_allreduce -- the ring-allreduce of paper section 3: N-1 steps in which
  * every rank adds the chunk received from its left neighbour into its own buffer,
  * then N-1 steps in which the received chunk replaces its own.  In place on all
@@ -266,6 +316,8 @@ int hvdx_ring_chunk(int64_t count, int nranks, int c, int64_t* start, int64_t* l
 #define HVDX_KERNEL_BROADCAST 5 /* one step of hvdx_broadcast */
 #define HVDX_KERNEL_RS_AG 6     /* last adding step and first replacing step in one launch */
 #define HVDX_KERNEL_FOLD 7      /* hvdx_fold_allreduce */
+#define HVDX_KERNEL_PACK_RS 8   /* copy-in with adding step 0 (step = 0) */
+#define HVDX_KERNEL_AG_UNPACK 9 /* replacing step N-2 with copy-out (step = N-2) */
 
 typedef struct hvdx_trace_record {
   int32_t kind;     /* HVDX_KERNEL_* */

@@ -32,7 +32,10 @@ from ._lib import (  # noqa: F401
     hvdx_broadcast,
     hvdx_broadcast_step,
     hvdx_fold_allreduce,
+    hvdx_fuse_ag_unpack,
+    hvdx_fuse_allreduce,
     hvdx_fuse_pack,
+    hvdx_fuse_pack_rs,
     hvdx_fuse_plan,
     hvdx_fuse_unpack,
     hvdx_last_error,

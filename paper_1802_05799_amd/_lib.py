@@ -34,6 +34,9 @@ _SIGNATURES = {
     "hvdx_fuse_plan": (_i, [_pi64, _i, _i, _i64, _i64, _pi32, _pi64, _pi64, _pi32, _pi32]),
     "hvdx_fuse_pack": (_i, [_p, _p, _p, _i, _i, _pp, _i64, _i, _i, _p]),
     "hvdx_fuse_unpack": (_i, [_pp, _i64, _i, _p, _p, _p, _i, _i, _i, _p]),
+    "hvdx_fuse_pack_rs": (_i, [_p, _p, _p, _i, _i, _pp, _i64, _i, _i, _p]),
+    "hvdx_fuse_ag_unpack": (_i, [_pp, _i64, _i, _p, _p, _p, _i, _i, _i, _p]),
+    "hvdx_fuse_allreduce": (_i, [_p, _p, _p, _i, _i, _pp, _i64, _i, _i, _i, _p]),
     "hvdx_ring_allreduce": (_i, [_pp, _i, _i64, _i, _i, _i, _p, _sz, _p]),
     "hvdx_ring_step": (_i, [_pp, _i, _i64, _i, _i, _i, _i, _i, _p, _sz, _p]),
     "hvdx_ring_reduce_scatter": (_i, [_pp, _i, _i64, _i, _i, _i, _p, _sz, _p]),
@@ -52,6 +55,7 @@ _SIGNATURES = {
 
 KERNEL_PACK, KERNEL_REDUCE_SCATTER, KERNEL_ALLGATHER, KERNEL_UNPACK, KERNEL_ROUNDTRIP = 0, 1, 2, 3, 4
 KERNEL_BROADCAST, KERNEL_RS_AG, KERNEL_FOLD = 5, 6, 7
+KERNEL_PACK_RS, KERNEL_AG_UNPACK = 8, 9
 
 
 class TraceRecord(ctypes.Structure):
@@ -153,6 +157,27 @@ def hvdx_fuse_unpack(bufs, buf_count: int, buf_dtype: int, dsts_dev: int, numel_
     pb, _keep = _ptr_array(bufs)
     _check(lib.hvdx_fuse_unpack(pb, buf_count, buf_dtype, dsts_dev, numel_dev, offset_dev, ntensors, dst_dtype,
                                 nranks, stream))
+
+
+def hvdx_fuse_pack_rs(srcs_dev: int, numel_dev: int, offset_dev: int, ntensors: int, src_dtype: int, bufs,
+                      buf_count: int, buf_dtype: int, nranks: int, stream: int = 0) -> None:
+    pb, _keep = _ptr_array(bufs)
+    _check(lib.hvdx_fuse_pack_rs(srcs_dev, numel_dev, offset_dev, ntensors, src_dtype, pb, buf_count, buf_dtype,
+                                 nranks, stream))
+
+
+def hvdx_fuse_ag_unpack(bufs, buf_count: int, buf_dtype: int, dsts_dev: int, numel_dev: int, offset_dev: int,
+                        ntensors: int, dst_dtype: int, nranks: int, stream: int = 0) -> None:
+    pb, _keep = _ptr_array(bufs)
+    _check(lib.hvdx_fuse_ag_unpack(pb, buf_count, buf_dtype, dsts_dev, numel_dev, offset_dev, ntensors, dst_dtype,
+                                   nranks, stream))
+
+
+def hvdx_fuse_allreduce(tensors_dev: int, numel_dev: int, offset_dev: int, ntensors: int, tensor_dtype: int, bufs,
+                        buf_count: int, buf_dtype: int, nranks: int, op: int, stream: int = 0) -> None:
+    pb, _keep = _ptr_array(bufs)
+    _check(lib.hvdx_fuse_allreduce(tensors_dev, numel_dev, offset_dev, ntensors, tensor_dtype, pb, buf_count,
+                                   buf_dtype, nranks, op, stream))
 
 
 def hvdx_ring_allreduce(bufs, nranks: int, count: int, dtype: int, op: int, compress: int = COMPRESS_NONE,

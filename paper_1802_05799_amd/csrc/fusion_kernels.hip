@@ -218,11 +218,12 @@ __device__ int64_t find_tensor_wave(const int64_t* offset, int64_t lo, int64_t h
 
 // Waves 0 and 1 locate the tile's first and last tensor at the same time; then the
 // whole block stages their offsets and ends, and the tile's (rank, tensor) pointers
-// of ranks [r0, r1), in one pass: two rounds of global loads per block in all.
+// of slots [r0, r1) (slot v is rank (v + rot) mod n), in one pass: two rounds of
+// global loads per block in all.
 template <int LDS_TENSORS>
 __device__ TileTable stage_tile(const int64_t* offset, const int64_t* numel, int ntensors, int64_t p0, int64_t p1,
-                                const void* const* ptrs, int r0, int r1, int64_t* s_off, int64_t* s_end,
-                                int64_t* s_meta, const void** s_ptr, bool* ptrs_in_lds) {
+                                const void* const* ptrs, int r0, int r1, int rot, int n, int64_t* s_off,
+                                int64_t* s_end, int64_t* s_meta, const void** s_ptr, bool* ptrs_in_lds) {
   const int wave = threadIdx.x >> 6;
   if (wave < 2) {
     const int64_t t = find_tensor_wave(offset, 0, ntensors, wave == 0 ? p0 : p1 - 1);
@@ -245,7 +246,8 @@ __device__ TileTable stage_tile(const int64_t* offset, const int64_t* numel, int
     if (pin) {
       const int rr = idx / tt.nt;
       const int64_t t = tt.t0 + (idx - rr * tt.nt);
-      s_ptr[idx] = t >= 0 ? ptrs[(int64_t)(r0 + rr) * ntensors + t] : nullptr;
+      const int rank = (r0 + rr + rot) % n;
+      s_ptr[idx] = t >= 0 ? ptrs[(int64_t)rank * ntensors + t] : nullptr;
     }
   }
   *ptrs_in_lds = pin;
@@ -287,28 +289,31 @@ enum PosClass { POS_NONE = 0, POS_VEC = 1, POS_ZERO = 2, POS_EDGE = 3 };
 
 struct Pos {
   int64_t p;    // buffer position of the vector's first element
-  int64_t t;    // tensor owning it (POS_VEC)
+  int t;        // tensor owning it (POS_VEC); tensor counts are int
   int64_t li;   // index of that element inside the tensor (POS_VEC)
   int cls;
 };
 
 // Classify buffer vector [p, p+V): inside one tensor, all padding, or an edge that
-// needs the element-by-element path (tensor tails, unaligned tensor offsets).
+// needs the element-by-element path (tensor tails, unaligned tensor offsets).  Only
+// positions in [cs, ce) belong to the block: the kernels fused with a ring step work
+// on one ring chunk per block, and a vector that reaches outside it takes the
+// element path, which skips the positions of the neighbouring chunk.
 template <int V>
 __device__ __forceinline__ Pos classify(const TileTable& tt, const int64_t* s_off, const int64_t* s_end,
                                         const int64_t* offset, const int64_t* numel, int64_t p, int64_t p1,
-                                        int64_t count) {
+                                        int64_t cs, int64_t ce) {
   Pos q{p, -1, 0, POS_NONE};
-  if (p >= p1) return q;
+  if (p >= p1 || p + V <= cs) return q;  // past the tile, or wholly before the block's chunk
   const int j = lookup(tt, s_off, offset, p);
   const int64_t t = tt.t0 + j;
   const int64_t beg = t >= 0 ? tensor_begin(tt, s_off, offset, j) : INT64_MIN;
   const int64_t end = t >= 0 ? tensor_end(tt, s_end, offset, numel, j) : INT64_MIN;
   q.cls = POS_EDGE;
-  if (p + V <= count) {
+  if (p >= cs && p + V <= ce) {
     if (t >= 0 && p + V <= end) {
       q.cls = POS_VEC;
-      q.t = t;
+      q.t = (int)t;
       q.li = p - beg;
     } else if (p >= end && lookup(tt, s_off, offset, p + V - 1) == j) {
       q.cls = POS_ZERO;  // no tensor element anywhere in the vector
@@ -317,74 +322,134 @@ __device__ __forceinline__ Pos classify(const TileTable& tt, const int64_t* s_of
   return q;
 }
 
+// The ring's chunk partition: chunk c starts at c*q + min(c, rem) and holds q
+// elements, one more for the first rem chunks.
+__device__ __forceinline__ int64_t chunk_start(int c, int64_t q, int64_t rem) { return c * q + (c < rem ? c : rem); }
+
+// Which buffer positions and ranks a block serves.  Plain copies: grid (tiles, rank
+// groups), tile x covers [x*T, x*T + T) of the buffer.  Fused with a ring step: grid
+// (tiles per chunk, chunks, rank groups); chunk c's tiles are the buffer's own tiles
+// from the one holding its first position on (so every access keeps the alignment
+// of the plain copy), and the block serves only [cs, ce) of its tile.
+struct BlockSpan {
+  int64_t p0, p1, cs, ce;
+  int c;  // ring chunk (fused kernels), else 0
+  int rbeg, rend;
+};
+
+template <bool RING>
+__device__ __forceinline__ BlockSpan block_span(int64_t tile_elems, int64_t count, int nranks, int rpb, int64_t q,
+                                                int64_t rem) {
+  BlockSpan b;
+  int group;
+  if constexpr (RING) {
+    b.c = blockIdx.y;
+    b.cs = chunk_start(b.c, q, rem);
+    b.ce = b.cs + q + (b.c < rem ? 1 : 0);
+    b.p0 = (b.cs & ~(tile_elems - 1)) + (int64_t)blockIdx.x * tile_elems;  // tile_elems is a power of two
+    b.p1 = b.p0 + tile_elems < b.ce ? b.p0 + tile_elems : b.ce;
+    group = blockIdx.z;
+  } else {
+    b.c = 0;
+    b.cs = 0;
+    b.ce = count;
+    b.p0 = (int64_t)blockIdx.x * tile_elems;
+    b.p1 = b.p0 + tile_elems < count ? b.p0 + tile_elems : count;
+    group = blockIdx.y;
+  }
+  b.rbeg = group * rpb;
+  b.rend = b.rbeg + rpb < nranks ? b.rbeg + rpb : nranks;
+  return b;
+}
 
 // The tile's (rank, tensor) pointers, staged in LDS when they fit so that the data
-// loads do not wait behind dependent pointer loads.
+// loads do not wait behind dependent pointer loads.  A block serves "slots" [r0, r0+nr);
+// slot v is rank (v + rot) mod n (rot = 0 except in the copy-in fused with a ring step).
 struct PtrTable {
   const void* const* g;  // rank-major device table
-  const void* const* s;  // LDS copy, s[(r - r0) * nt + j], or null
+  const void* const* s;  // LDS copy, s[(v - r0) * nt + j], or null
   int64_t t0, ntensors;
-  int nt, r0;
-  __device__ __forceinline__ const void* get(int r, int64_t t) const {
-    return s ? s[(r - r0) * nt + (int)(t - t0)] : g[(int64_t)r * ntensors + t];
+  int nt, r0, rot, n;
+  __device__ __forceinline__ int rank(int v) const { return v + rot < n ? v + rot : v + rot - n; }
+  __device__ __forceinline__ const void* get(int v, int64_t t) const {
+    return s ? s[(v - r0) * nt + (int)(t - t0)] : g[(int64_t)rank(v) * ntensors + t];
   }
 };
 
-template <typename TT, typename TB, typename Cfg>
+// Copy-in.  With RING it is fused with the ring's first adding step (paper section 3,
+// the first of the N-1 iterations whose received values are added): in chunk c the
+// receiving rank c+1 stores its own value plus rank c's, so the buffers end in the
+// state the copy-in and that step leave, without reading the sender's buffer back.
+// A block's slots start at its chunk's sender, so slot 0 (sender) and slot 1
+// (receiver) are one load batch of the first rank group.
+template <typename TT, typename TB, typename Cfg, bool RING>
 __global__ __launch_bounds__(kBlock) void pack_kernel(const void* const* __restrict__ srcs,
                                                       const int64_t* __restrict__ numel,
                                                       const int64_t* __restrict__ offset, int ntensors, RankPtrs bufs,
-                                                      int64_t count, int nranks, int rpb) {
+                                                      int64_t count, int nranks, int rpb, int64_t q, int64_t rem) {
+  static_assert(!RING || (Cfg::RB >= 2 && (Cfg::RPB == 0 || Cfg::RPB >= 2)),
+                "the fused copy-in needs the sender and receiver in one load batch");
   constexpr int V = BufVec<TB>::n;
   using VB = typename Mover<TT, TB>::buf_vec;
   constexpr int kPosPerLane = Cfg::POS, kRankBatch = Cfg::RB, kTileVecs = Cfg::kTileVecs;
   __shared__ int64_t s_off[Cfg::kLdsTensors], s_end[Cfg::kLdsTensors], s_meta[2];
   __shared__ const void* s_ptr[kLdsPtrs];
-  const int64_t p0 = (int64_t)blockIdx.x * kTileVecs * V;
-  const int64_t p1 = p0 + (int64_t)kTileVecs * V < count ? p0 + (int64_t)kTileVecs * V : count;
-  const int rbeg = blockIdx.y * rpb, rend = rbeg + rpb < nranks ? rbeg + rpb : nranks;
+  static_assert((kTileVecs & (kTileVecs - 1)) == 0, "tiles are a power of two vectors");
+  const BlockSpan bs = block_span<RING>((int64_t)kTileVecs * V, count, nranks, rpb, q, rem);
+  if (bs.p0 >= bs.p1) return;  // past the end of a shorter chunk: the whole block leaves
+  const int rot = bs.c;
   bool pin;
-  const TileTable tt = stage_tile<Cfg::kLdsTensors>(offset, numel, ntensors, p0, p1, srcs, rbeg, rend, s_off, s_end,
-                                                    s_meta, s_ptr, &pin);
-  const PtrTable pt{srcs, pin ? s_ptr : nullptr, tt.t0, ntensors, tt.nt, rbeg};
+  const TileTable tt = stage_tile<Cfg::kLdsTensors>(offset, numel, ntensors, bs.p0, bs.p1, srcs, bs.rbeg, bs.rend,
+                                                    rot, nranks, s_off, s_end, s_meta, s_ptr, &pin);
+  const PtrTable pt{srcs, pin ? s_ptr : nullptr, tt.t0, ntensors, tt.nt, bs.rbeg, rot, nranks};
+  const int receiver = bs.c + 1 == nranks ? 0 : bs.c + 1;  // of chunk c in adding step 0
 
   Pos pos[kPosPerLane];
 #pragma unroll
   for (int u = 0; u < kPosPerLane; ++u)
-    pos[u] = classify<V>(tt, s_off, s_end, offset, numel, p0 + (int64_t)(u * kBlock + threadIdx.x) * V, p1, count);
+    pos[u] = classify<V>(tt, s_off, s_end, offset, numel, bs.p0 + (int64_t)(u * kBlock + threadIdx.x) * V, bs.p1,
+                         bs.cs, bs.ce);
 
-  for (int r0 = rbeg; r0 < rend; r0 += kRankBatch) {
+  for (int v0 = bs.rbeg; v0 < bs.rend; v0 += kRankBatch) {
     VB v[kRankBatch][kPosPerLane];
 #pragma unroll
     for (int rr = 0; rr < kRankBatch; ++rr) {
-      const int r = r0 + rr;
+      const int slot = v0 + rr;
 #pragma unroll
       for (int u = 0; u < kPosPerLane; ++u)
-        if (r < rend && pos[u].cls == POS_VEC)
-          v[rr][u] = Mover<TT, TB>::template load<Cfg::NTL>(static_cast<const TT*>(pt.get(r, pos[u].t)) + pos[u].li);
+        if (slot < bs.rend && pos[u].cls == POS_VEC)
+          v[rr][u] = Mover<TT, TB>::template load<Cfg::NTL>(static_cast<const TT*>(pt.get(slot, pos[u].t)) +
+                                                            pos[u].li);
     }
 #pragma unroll
     for (int rr = 0; rr < kRankBatch; ++rr) {
-      const int r = r0 + rr;
-      if (r >= rend) break;
+      const int slot = v0 + rr;
+      if (slot >= bs.rend) break;
+      const int r = pt.rank(slot);
       TB* __restrict__ buf = static_cast<TB*>(bufs.p[r]);
 #pragma unroll
       for (int u = 0; u < kPosPerLane; ++u) {
-        const Pos& q = pos[u];
-        if (q.cls == POS_VEC) {
-          st16<Cfg::NTS>(reinterpret_cast<VB*>(buf + q.p), v[rr][u]);
-        } else if (q.cls == POS_ZERO) {
-          store_zero(buf + q.p);
-        } else if (q.cls == POS_EDGE) {
+        const Pos& ps = pos[u];
+        if (ps.cls == POS_VEC) {
+          VB x = v[rr][u];
+          if (RING && rr > 0 && slot == 1) x = x + v[rr > 0 ? rr - 1 : 0][u];  // receiver: own + sender's
+          st16<Cfg::NTS>(reinterpret_cast<VB*>(buf + ps.p), x);
+        } else if (ps.cls == POS_ZERO) {
+          store_zero(buf + ps.p);  // padding: zero, and zero + zero for a receiver
+        } else if (ps.cls == POS_EDGE) {
           for (int k = 0; k < V; ++k) {
-            const int64_t pe = q.p + k;
-            if (pe >= count) break;
+            const int64_t pe = ps.p + k;
+            if (pe >= bs.ce) break;
+            if (pe < bs.cs) continue;
             const int jk = lookup(tt, s_off, offset, pe);
             const int64_t tk = tt.t0 + jk;
+            const bool in_tensor = tk >= 0 && pe < tensor_end(tt, s_end, offset, numel, jk);
+            const int64_t li = in_tensor ? pe - tensor_begin(tt, s_off, offset, jk) : 0;
             TB val = (TB)0;
-            if (tk >= 0 && pe < tensor_end(tt, s_end, offset, numel, jk)) {
-              const TT* sk = static_cast<const TT*>(pt.get(r, tk));
-              val = Mover<TT, TB>::cvt_in(sk[pe - tensor_begin(tt, s_off, offset, jk)]);
+            if (in_tensor) {
+              val = Mover<TT, TB>::cvt_in(static_cast<const TT*>(pt.get(slot, tk))[li]);
+              if (RING && r == receiver)
+                val = val + Mover<TT, TB>::cvt_in(static_cast<const TT*>(srcs[(int64_t)bs.c * ntensors + tk])[li]);
             }
             buf[pe] = val;
           }
@@ -394,53 +459,64 @@ __global__ __launch_bounds__(kBlock) void pack_kernel(const void* const* __restr
   }
 }
 
-template <typename TT, typename TB, typename Cfg>
+// Copy-out.  With RING it is fused with the ring's last replacing step: in chunk c
+// that step hands rank c-3's final values to rank c-2, so rank c-2 copies them out
+// from rank c-3's buffer (mod N) and its own buffer keeps the chunk's older values.
+template <typename TT, typename TB, typename Cfg, bool RING>
 __global__ __launch_bounds__(kBlock) void unpack_kernel(RankPtrs bufs, int64_t count, void* const* __restrict__ dsts,
                                                         const int64_t* __restrict__ numel,
                                                         const int64_t* __restrict__ offset, int ntensors,
-                                                        int nranks, int rpb) {
+                                                        int nranks, int rpb, int64_t q, int64_t rem) {
   constexpr int V = BufVec<TB>::n;
   using VB = typename Mover<TT, TB>::buf_vec;
   constexpr int kPosPerLane = Cfg::POS, kRankBatch = Cfg::RB, kTileVecs = Cfg::kTileVecs;
   __shared__ int64_t s_off[Cfg::kLdsTensors], s_end[Cfg::kLdsTensors], s_meta[2];
   __shared__ const void* s_ptr[kLdsPtrs];
-  const int64_t p0 = (int64_t)blockIdx.x * kTileVecs * V;
-  const int64_t p1 = p0 + (int64_t)kTileVecs * V < count ? p0 + (int64_t)kTileVecs * V : count;
-  const int rbeg = blockIdx.y * rpb, rend = rbeg + rpb < nranks ? rbeg + rpb : nranks;
+  static_assert((kTileVecs & (kTileVecs - 1)) == 0, "tiles are a power of two vectors");
+  const BlockSpan bs = block_span<RING>((int64_t)kTileVecs * V, count, nranks, rpb, q, rem);
+  if (bs.p0 >= bs.p1) return;  // past the end of a shorter chunk: the whole block leaves
+  // the rank that receives chunk c in the last replacing step, which reads its sender's buffer
+  const int receiver = RING ? (bs.c + nranks - 2) % nranks : -1;
   bool pin;
-  const TileTable tt = stage_tile<Cfg::kLdsTensors>(offset, numel, ntensors, p0, p1, dsts, rbeg, rend, s_off, s_end,
-                                                    s_meta, s_ptr, &pin);
-  const PtrTable pt{dsts, pin ? s_ptr : nullptr, tt.t0, ntensors, tt.nt, rbeg};
+  const TileTable tt = stage_tile<Cfg::kLdsTensors>(offset, numel, ntensors, bs.p0, bs.p1, dsts, bs.rbeg, bs.rend, 0,
+                                                    nranks, s_off, s_end, s_meta, s_ptr, &pin);
+  const PtrTable pt{dsts, pin ? s_ptr : nullptr, tt.t0, ntensors, tt.nt, bs.rbeg, 0, nranks};
 
   Pos pos[kPosPerLane];
 #pragma unroll
   for (int u = 0; u < kPosPerLane; ++u)
-    pos[u] = classify<V>(tt, s_off, s_end, offset, numel, p0 + (int64_t)(u * kBlock + threadIdx.x) * V, p1, count);
+    pos[u] = classify<V>(tt, s_off, s_end, offset, numel, bs.p0 + (int64_t)(u * kBlock + threadIdx.x) * V, bs.p1,
+                         bs.cs, bs.ce);
 
-  for (int r0 = rbeg; r0 < rend; r0 += kRankBatch) {
+  for (int r0 = bs.rbeg; r0 < bs.rend; r0 += kRankBatch) {
     VB v[kRankBatch][kPosPerLane];
 #pragma unroll
     for (int rr = 0; rr < kRankBatch; ++rr) {
-      const int r = r0 + rr;
-      const TB* __restrict__ buf = static_cast<const TB*>(bufs.p[r < rend ? r : rbeg]);
+      const int r = r0 + rr < bs.rend ? r0 + rr : bs.rbeg;
+      const int from = r == receiver ? (r == 0 ? nranks - 1 : r - 1) : r;
+      const TB* __restrict__ buf = static_cast<const TB*>(bufs.p[from]);
 #pragma unroll
       for (int u = 0; u < kPosPerLane; ++u)
-        if (r < rend && pos[u].cls == POS_VEC) v[rr][u] = ld16<Cfg::NTL>(reinterpret_cast<const VB*>(buf + pos[u].p));
+        if (r0 + rr < bs.rend && pos[u].cls == POS_VEC)
+          v[rr][u] = ld16<Cfg::NTL>(reinterpret_cast<const VB*>(buf + pos[u].p));
     }
 #pragma unroll
     for (int rr = 0; rr < kRankBatch; ++rr) {
       const int r = r0 + rr;
-      if (r >= rend) break;
-      const TB* __restrict__ buf = static_cast<const TB*>(bufs.p[r]);
+      if (r >= bs.rend) break;
+      const int from = r == receiver ? (r == 0 ? nranks - 1 : r - 1) : r;
+      const TB* __restrict__ buf = static_cast<const TB*>(bufs.p[from]);
 #pragma unroll
       for (int u = 0; u < kPosPerLane; ++u) {
-        const Pos& q = pos[u];
-        if (q.cls == POS_VEC) {
-          Mover<TT, TB>::template store<Cfg::NTS>(static_cast<TT*>(const_cast<void*>(pt.get(r, q.t))) + q.li, v[rr][u]);
-        } else if (q.cls == POS_EDGE) {
+        const Pos& ps = pos[u];
+        if (ps.cls == POS_VEC) {
+          Mover<TT, TB>::template store<Cfg::NTS>(static_cast<TT*>(const_cast<void*>(pt.get(r, ps.t))) + ps.li,
+                                                  v[rr][u]);
+        } else if (ps.cls == POS_EDGE) {
           for (int k = 0; k < V; ++k) {
-            const int64_t pe = q.p + k;
-            if (pe >= count) break;
+            const int64_t pe = ps.p + k;
+            if (pe >= bs.ce) break;
+            if (pe < bs.cs) continue;
             const int jk = lookup(tt, s_off, offset, pe);
             const int64_t tk = tt.t0 + jk;
             if (tk >= 0 && pe < tensor_end(tt, s_end, offset, numel, jk)) {
@@ -464,57 +540,85 @@ unsigned tiles_for(int64_t count, int buf_dtype) {
 template <typename Cfg>
 int ranks_per_block(int nranks) { return Cfg::RPB > 0 && Cfg::RPB < nranks ? Cfg::RPB : nranks; }
 
-template <typename Cfg>
+// Plain: (tiles, rank groups).  Fused with a ring step: (tiles a chunk can meet --
+// its length plus up to a tile of slack before its start -- chunks, rank groups).
+template <typename Cfg, bool RING>
+dim3 copy_grid(int64_t count, int buf_dtype, int nranks) {
+  const int rpb = ranks_per_block<Cfg>(nranks);
+  const unsigned groups = (unsigned)((nranks + rpb - 1) / rpb);
+  if (!RING) return dim3(tiles_for<Cfg>(count, buf_dtype), groups);
+  const int64_t tile = (int64_t)Cfg::kTileVecs * (buf_dtype == HVDX_FLOAT32 ? 4 : 8);
+  const int64_t longest = count / nranks + (count % nranks ? 1 : 0);
+  return dim3(tiles_for<Cfg>(longest + tile - 1, buf_dtype), (unsigned)nranks, groups);
+}
+
+template <typename Cfg, bool RING>
 void pack_with(const void* const* srcs, const int64_t* numel, const int64_t* offset, int ntensors, int src_dtype,
                const RankPtrs& bufs, int64_t count, int buf_dtype, int nranks, hipStream_t stream) {
   const int rpb = ranks_per_block<Cfg>(nranks);
-  const dim3 grid(tiles_for<Cfg>(count, buf_dtype), (nranks + rpb - 1) / rpb);
+  const dim3 grid = copy_grid<Cfg, RING>(count, buf_dtype, nranks);
+  const int64_t q = count / nranks, rem = count % nranks;
   if (src_dtype == HVDX_FLOAT32 && buf_dtype == HVDX_FLOAT32)
-    hipLaunchKernelGGL((pack_kernel<float, float, Cfg>), grid, dim3(kBlock), 0, stream, srcs, numel, offset,
-                       ntensors, bufs, count, nranks, rpb);
+    hipLaunchKernelGGL((pack_kernel<float, float, Cfg, RING>), grid, dim3(kBlock), 0, stream, srcs, numel, offset,
+                       ntensors, bufs, count, nranks, rpb, q, rem);
   else if (src_dtype == HVDX_FLOAT32 && buf_dtype == HVDX_FLOAT16)
-    hipLaunchKernelGGL((pack_kernel<float, _Float16, Cfg>), grid, dim3(kBlock), 0, stream, srcs, numel, offset,
-                       ntensors, bufs, count, nranks, rpb);
+    hipLaunchKernelGGL((pack_kernel<float, _Float16, Cfg, RING>), grid, dim3(kBlock), 0, stream, srcs, numel,
+                       offset, ntensors, bufs, count, nranks, rpb, q, rem);
   else
-    hipLaunchKernelGGL((pack_kernel<_Float16, _Float16, Cfg>), grid, dim3(kBlock), 0, stream, srcs, numel, offset,
-                       ntensors, bufs, count, nranks, rpb);
+    hipLaunchKernelGGL((pack_kernel<_Float16, _Float16, Cfg, RING>), grid, dim3(kBlock), 0, stream, srcs, numel,
+                       offset, ntensors, bufs, count, nranks, rpb, q, rem);
 }
 
-template <typename Cfg>
+template <typename Cfg, bool RING>
 void unpack_with(const RankPtrs& bufs, int64_t count, int buf_dtype, void* const* dsts, const int64_t* numel,
                  const int64_t* offset, int ntensors, int dst_dtype, int nranks, hipStream_t stream) {
   const int rpb = ranks_per_block<Cfg>(nranks);
-  const dim3 grid(tiles_for<Cfg>(count, buf_dtype), (nranks + rpb - 1) / rpb);
+  const dim3 grid = copy_grid<Cfg, RING>(count, buf_dtype, nranks);
+  const int64_t q = count / nranks, rem = count % nranks;
   if (dst_dtype == HVDX_FLOAT32 && buf_dtype == HVDX_FLOAT32)
-    hipLaunchKernelGGL((unpack_kernel<float, float, Cfg>), grid, dim3(kBlock), 0, stream, bufs, count, dsts, numel,
-                       offset, ntensors, nranks, rpb);
+    hipLaunchKernelGGL((unpack_kernel<float, float, Cfg, RING>), grid, dim3(kBlock), 0, stream, bufs, count, dsts,
+                       numel, offset, ntensors, nranks, rpb, q, rem);
   else if (dst_dtype == HVDX_FLOAT32 && buf_dtype == HVDX_FLOAT16)
-    hipLaunchKernelGGL((unpack_kernel<float, _Float16, Cfg>), grid, dim3(kBlock), 0, stream, bufs, count, dsts,
-                       numel, offset, ntensors, nranks, rpb);
+    hipLaunchKernelGGL((unpack_kernel<float, _Float16, Cfg, RING>), grid, dim3(kBlock), 0, stream, bufs, count,
+                       dsts, numel, offset, ntensors, nranks, rpb, q, rem);
   else
-    hipLaunchKernelGGL((unpack_kernel<_Float16, _Float16, Cfg>), grid, dim3(kBlock), 0, stream, bufs, count, dsts,
-                       numel, offset, ntensors, nranks, rpb);
+    hipLaunchKernelGGL((unpack_kernel<_Float16, _Float16, Cfg, RING>), grid, dim3(kBlock), 0, stream, bufs, count,
+                       dsts, numel, offset, ntensors, nranks, rpb, q, rem);
 }
 
 }  // namespace
 
 hipError_t launch_pack(const void* const* srcs, const int64_t* numel, const int64_t* offset, int ntensors,
-                       int src_dtype, const RankPtrs& bufs, int64_t count, int buf_dtype, int nranks,
+                       int src_dtype, const RankPtrs& bufs, int64_t count, int buf_dtype, int nranks, bool ring,
                        hipStream_t stream) {
-  if (buf_dtype == HVDX_FLOAT32)
-    pack_with<PackCfg>(srcs, numel, offset, ntensors, src_dtype, bufs, count, buf_dtype, nranks, stream);
-  else
-    pack_with<Pack16Cfg>(srcs, numel, offset, ntensors, src_dtype, bufs, count, buf_dtype, nranks, stream);
+  if (buf_dtype == HVDX_FLOAT32) {
+    if (ring) pack_with<PackCfg, true>(srcs, numel, offset, ntensors, src_dtype, bufs, count, buf_dtype, nranks, stream);
+    else pack_with<PackCfg, false>(srcs, numel, offset, ntensors, src_dtype, bufs, count, buf_dtype, nranks, stream);
+  } else {
+    if (ring)
+      pack_with<Pack16Cfg, true>(srcs, numel, offset, ntensors, src_dtype, bufs, count, buf_dtype, nranks, stream);
+    else
+      pack_with<Pack16Cfg, false>(srcs, numel, offset, ntensors, src_dtype, bufs, count, buf_dtype, nranks, stream);
+  }
   return hipGetLastError();
 }
 
 hipError_t launch_unpack(const RankPtrs& bufs, int64_t count, int buf_dtype, void* const* dsts,
                          const int64_t* numel, const int64_t* offset, int ntensors, int dst_dtype, int nranks,
-                         hipStream_t stream) {
-  if (buf_dtype == HVDX_FLOAT32)
-    unpack_with<UnpackCfg>(bufs, count, buf_dtype, dsts, numel, offset, ntensors, dst_dtype, nranks, stream);
-  else
-    unpack_with<Unpack16Cfg>(bufs, count, buf_dtype, dsts, numel, offset, ntensors, dst_dtype, nranks, stream);
+                         bool ring, hipStream_t stream) {
+  if (buf_dtype == HVDX_FLOAT32) {
+    if (ring)
+      unpack_with<UnpackCfg, true>(bufs, count, buf_dtype, dsts, numel, offset, ntensors, dst_dtype, nranks, stream);
+    else
+      unpack_with<UnpackCfg, false>(bufs, count, buf_dtype, dsts, numel, offset, ntensors, dst_dtype, nranks, stream);
+  } else {
+    if (ring)
+      unpack_with<Unpack16Cfg, true>(bufs, count, buf_dtype, dsts, numel, offset, ntensors, dst_dtype, nranks,
+                                     stream);
+    else
+      unpack_with<Unpack16Cfg, false>(bufs, count, buf_dtype, dsts, numel, offset, ntensors, dst_dtype, nranks,
+                                      stream);
+  }
   return hipGetLastError();
 }
 

@@ -47,6 +47,9 @@ class TimedLaunch {
       : st_(st), lock_(timeline().mu) {
     Timeline& t = timeline();
     if (!t.on || t.per_phase != phase) return;
+    // Launches recorded into a HIP graph run later, at each replay: they get no record.
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(st_, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone) return;
     if ((int)t.entries.size() >= t.capacity) {
       ++t.dropped;
       return;
@@ -409,8 +412,56 @@ int hvdx_fuse_pack(const void* const* srcs, const int64_t* numel, const int64_t*
   TimedLaunch timed_phase(HVDX_KERNEL_PACK, -1, nranks, buf_dtype, HVDX_COMPRESS_NONE, buf_count,
                           static_cast<hipStream_t>(stream), -1, true);
   const hipError_t e = hvdx::launch_pack(srcs, numel, offset, ntensors, src_dtype, rank_ptrs(bufs, nranks),
-                                         buf_count, buf_dtype, nranks, static_cast<hipStream_t>(stream));
+                                         buf_count, buf_dtype, nranks, false, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? HVDX_OK : hip_fail(e, "pack launch");
+}
+
+// The copy-in fused with adding step 0, or the copy-out fused with replacing step N-2
+// (arguments already checked, nranks >= 3, buf_count > 0).
+static int run_pack_rs(const void* const* srcs, const int64_t* numel, const int64_t* offset, int ntensors,
+                       int src_dtype, void* const* bufs, int64_t buf_count, int buf_dtype, int nranks,
+                       hipStream_t st) {
+  TimedLaunch timed(HVDX_KERNEL_PACK_RS, 0, nranks, buf_dtype, HVDX_COMPRESS_NONE, buf_count, st);
+  TimedLaunch timed_phase(HVDX_KERNEL_PACK_RS, 0, nranks, buf_dtype, HVDX_COMPRESS_NONE, buf_count, st, -1, true);
+  const hipError_t e = hvdx::launch_pack(srcs, numel, offset, ntensors, src_dtype, rank_ptrs(bufs, nranks), buf_count,
+                                         buf_dtype, nranks, true, st);
+  return e == hipSuccess ? HVDX_OK : hip_fail(e, "fused copy-in launch");
+}
+
+static int run_ag_unpack(const void* const* bufs, int64_t buf_count, int buf_dtype, void* const* dsts,
+                         const int64_t* numel, const int64_t* offset, int ntensors, int dst_dtype, int nranks,
+                         hipStream_t st) {
+  TimedLaunch timed(HVDX_KERNEL_AG_UNPACK, nranks - 2, nranks, buf_dtype, HVDX_COMPRESS_NONE, buf_count, st);
+  TimedLaunch timed_phase(HVDX_KERNEL_AG_UNPACK, nranks - 2, nranks, buf_dtype, HVDX_COMPRESS_NONE, buf_count, st,
+                          -1, true);
+  const hipError_t e = hvdx::launch_unpack(rank_ptrs(const_cast<void* const*>(bufs), nranks), buf_count, buf_dtype,
+                                           dsts, numel, offset, ntensors, dst_dtype, nranks, true, st);
+  return e == hipSuccess ? HVDX_OK : hip_fail(e, "fused copy-out launch");
+}
+
+int hvdx_fuse_pack_rs(const void* const* srcs, const int64_t* numel, const int64_t* offset, int ntensors,
+                      int src_dtype, void* const* bufs, int64_t buf_count, int buf_dtype, int nranks, void* stream) {
+  int rc = check_fusion(srcs, numel, offset, ntensors, src_dtype, bufs, buf_count, buf_dtype, nranks,
+                        "hvdx_fuse_pack_rs");
+  if (rc) return rc;
+  if (nranks < 3)
+    return fail(HVDX_ERR_UNSUPPORTED, "hvdx_fuse_pack_rs: needs 3 or more ranks (adding step 0 is the last one)");
+  if (buf_count == 0) return HVDX_OK;
+  return run_pack_rs(srcs, numel, offset, ntensors, src_dtype, bufs, buf_count, buf_dtype, nranks,
+                     static_cast<hipStream_t>(stream));
+}
+
+int hvdx_fuse_ag_unpack(const void* const* bufs, int64_t buf_count, int buf_dtype, void* const* dsts,
+                        const int64_t* numel, const int64_t* offset, int ntensors, int dst_dtype, int nranks,
+                        void* stream) {
+  int rc = check_fusion(dsts, numel, offset, ntensors, dst_dtype, bufs, buf_count, buf_dtype, nranks,
+                        "hvdx_fuse_ag_unpack");
+  if (rc) return rc;
+  if (nranks < 3)
+    return fail(HVDX_ERR_UNSUPPORTED, "hvdx_fuse_ag_unpack: needs 3 or more ranks (replacing step N-2 is step 0)");
+  if (buf_count == 0) return HVDX_OK;
+  return run_ag_unpack(bufs, buf_count, buf_dtype, dsts, numel, offset, ntensors, dst_dtype, nranks,
+                       static_cast<hipStream_t>(stream));
 }
 
 int hvdx_fuse_unpack(const void* const* bufs, int64_t buf_count, int buf_dtype, void* const* dsts,
@@ -426,7 +477,7 @@ int hvdx_fuse_unpack(const void* const* bufs, int64_t buf_count, int buf_dtype, 
                           static_cast<hipStream_t>(stream), -1, true);
   const hipError_t e =
       hvdx::launch_unpack(rank_ptrs(const_cast<void* const*>(bufs), nranks), buf_count, buf_dtype, dsts, numel,
-                          offset, ntensors, dst_dtype, nranks, static_cast<hipStream_t>(stream));
+                          offset, ntensors, dst_dtype, nranks, false, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? HVDX_OK : hip_fail(e, "unpack launch");
 }
 
@@ -490,6 +541,45 @@ int hvdx_ring_allreduce(void* const* bufs, int nranks, int64_t count, int dtype,
     if (rc) return rc;
   }
   return run_steps(bufs, nranks, count, dtype, op, compress, HVDX_PHASE_ALLGATHER, 1, nranks - 1, workspace, st);
+}
+
+int hvdx_fuse_allreduce(void* const* tensors, const int64_t* numel, const int64_t* offset, int ntensors,
+                        int tensor_dtype, void* const* bufs, int64_t buf_count, int buf_dtype, int nranks, int op,
+                        void* stream) {
+  int rc = check_fusion(tensors, numel, offset, ntensors, tensor_dtype, bufs, buf_count, buf_dtype, nranks,
+                        "hvdx_fuse_allreduce");
+  if (rc) return rc;
+  if (op != HVDX_SUM && op != HVDX_AVERAGE) return fail(HVDX_ERR_INVALID, "hvdx_fuse_allreduce: unknown op %d", op);
+  if (buf_count == 0) return HVDX_OK;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const void* const* srcs = const_cast<const void* const*>(tensors);
+  if (nranks < 3) {  // no adding step before the last, no replacing step after the first
+    rc = hvdx_fuse_pack(srcs, numel, offset, ntensors, tensor_dtype, bufs, buf_count, buf_dtype, nranks, stream);
+    if (!rc && nranks == 2) {
+      TimedLaunch timed_phase(HVDX_KERNEL_RS_AG, 0, nranks, buf_dtype, HVDX_COMPRESS_NONE, buf_count, st, -1, true);
+      rc = run_step(bufs, nranks, buf_count, buf_dtype, op, HVDX_COMPRESS_NONE, HVDX_PHASE_REDUCE_SCATTER, 0,
+                    nullptr, st, true);
+    }
+    if (rc) return rc;
+    return hvdx_fuse_unpack(bufs, buf_count, buf_dtype, tensors, numel, offset, ntensors, tensor_dtype, nranks,
+                            stream);
+  }
+  const int last = nranks - 2;
+  rc = run_pack_rs(srcs, numel, offset, ntensors, tensor_dtype, bufs, buf_count, buf_dtype, nranks, st);
+  if (!rc)
+    rc = run_steps(bufs, nranks, buf_count, buf_dtype, op, HVDX_COMPRESS_NONE, HVDX_PHASE_REDUCE_SCATTER, 1, last,
+                   nullptr, st);
+  if (rc) return rc;
+  {
+    TimedLaunch timed_phase(HVDX_KERNEL_RS_AG, last, nranks, buf_dtype, HVDX_COMPRESS_NONE, buf_count, st, -1, true);
+    rc = run_step(bufs, nranks, buf_count, buf_dtype, op, HVDX_COMPRESS_NONE, HVDX_PHASE_REDUCE_SCATTER, last,
+                  nullptr, st, true);
+    if (rc) return rc;
+  }
+  rc = run_steps(bufs, nranks, buf_count, buf_dtype, op, HVDX_COMPRESS_NONE, HVDX_PHASE_ALLGATHER, 1, last, nullptr,
+                 st);
+  if (rc) return rc;
+  return run_ag_unpack(bufs, buf_count, buf_dtype, tensors, numel, offset, ntensors, tensor_dtype, nranks, st);
 }
 
 int hvdx_fold_allreduce(void* const* bufs, int nranks, int64_t count, int dtype, int op, int compress,

@@ -43,12 +43,17 @@ class FusedAllreduce:
 
     def __init__(self, per_rank, op: str = "average", compress: bool = False,
                  threshold_bytes: int = L.DEFAULT_FUSION_THRESHOLD, align_bytes: int = L.DEFAULT_FUSION_ALIGN,
-                 schedule: str = "ring"):
+                 schedule: str = "ring", fuse_boundary: bool = True):
         """schedule "ring" runs the ring's 2(N-1) steps; "fold" computes the same bits
-        with hvdx_fold_allreduce (no per-step messages: a one-GPU bound, not the ring)."""
+        with hvdx_fold_allreduce (no per-step messages: a one-GPU bound, not the ring).
+        With fuse_boundary (ring schedule, N >= 3) a fusion buffer's copy-in runs with
+        the ring's first adding step and its copy-out with the last replacing step
+        (hvdx_fuse_allreduce); otherwise copy-in, ring and copy-out are separate calls.
+        Both give the same bits."""
         if schedule not in ("ring", "fold"):
             raise ValueError("schedule must be 'ring' or 'fold'")
         self.schedule = schedule
+        self.fuse_boundary = fuse_boundary and schedule == "ring"
         if not per_rank or len(per_rank) > L.MAX_RANKS:
             raise ValueError(f"need 1..{L.MAX_RANKS} ranks")
         if op not in _OPS:
@@ -133,13 +138,35 @@ class FusedAllreduce:
         ptrs, count, dtype, compress, ws, wsb = self.ring_args(b)
         L.hvdx_ring_step(ptrs, self.nranks, count, dtype, self.op, compress, phase, step, ws, wsb, stream)
 
+    def fused_cycle(self, b: Bucket, stream: int) -> None:
+        """A fusion buffer's copy-in, ring and copy-out with the boundary steps fused."""
+        L.hvdx_fuse_allreduce(b.ptrs_dev.data_ptr(), b.numel_dev.data_ptr(), b.offset_dev.data_ptr(), len(b.tensors),
+                              self.dtype, self._buf_ptrs, b.count, self.buf_dtype, self.nranks, self.op, stream)
+
     def kernel_sequence(self):
         """The kernels one call launches, in order: (kind, bucket index, step) with
-        kind "pack", "rs", "rs_ag" (adding step N-2 fused with replacing step 0),
-        "ag", "unpack", or "ring" (the one-rank compressed round trip)."""
+        kind "pack", "pack_rs" (copy-in with adding step 0), "rs", "rs_ag" (adding
+        step N-2 fused with replacing step 0), "ag", "ag_unpack" (replacing step N-2
+        with copy-out), "unpack", "fold", or "ring" (the one-rank compressed round trip)."""
         out = []
         n = self.nranks
         for bi, b in enumerate(self.buckets):
+            if b.count == 0:
+                continue
+            if self.schedule == "fold":
+                if not b.direct:
+                    out.append(("pack", bi, -1))
+                out.append(("fold", bi, -1))
+                if not b.direct:
+                    out.append(("unpack", bi, -1))
+                continue
+            if self.fuse_boundary and not b.direct and n >= 3:
+                out.append(("pack_rs", bi, 0))
+                out += [("rs", bi, s) for s in range(1, n - 2)]
+                out.append(("rs_ag", bi, n - 2))
+                out += [("ag", bi, s) for s in range(1, n - 2)]
+                out.append(("ag_unpack", bi, n - 2))
+                continue
             if not b.direct:
                 out.append(("pack", bi, -1))
             if n == 1:
@@ -153,12 +180,31 @@ class FusedAllreduce:
                 out.append(("unpack", bi, -1))
         return out
 
+    def capture(self) -> "torch.cuda.CUDAGraph":
+        """Record one call's launches (every bucket's copy-in, ring steps and copy-out)
+        in a HIP graph and return it without running them.  ``graph.replay()`` then
+        reduces the same tensors, in place, with one submission instead of one launch
+        per kernel, which is what decides the time of small buckets.  The tensors,
+        fusion buffers and descriptors the graph points at are this object's; the graph
+        holds a reference to it.  Launches inside the capture get no
+        timeline records."""
+        graph = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream(self.device)  # default priority
+        side.wait_stream(torch.cuda.current_stream(self.device))
+        with torch.cuda.graph(graph, stream=side):
+            self(side.cuda_stream)
+        torch.cuda.current_stream(self.device).wait_stream(side)
+        graph.owner = self  # the memory the graph points at lives as long as the graph
+        return graph
+
     def __call__(self, stream: int | None = None) -> None:
         if stream is None:
             stream = torch.cuda.current_stream(self.device).cuda_stream
         for b in self.buckets:
             if b.direct:
                 self.ring(b, stream)
+            elif self.fuse_boundary:
+                self.fused_cycle(b, stream)
             else:
                 self.pack(b, stream)
                 self.ring(b, stream)

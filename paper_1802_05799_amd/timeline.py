@@ -32,6 +32,8 @@ KIND_NAMES = {
     L.KERNEL_BROADCAST: "broadcast",
     L.KERNEL_RS_AG: "reduce-scatter + allgather",
     L.KERNEL_FOLD: "fold",
+    L.KERNEL_PACK_RS: "copy in + reduce-scatter",
+    L.KERNEL_AG_UNPACK: "allgather + copy out",
 }
 
 
@@ -100,10 +102,12 @@ class Timeline:
                     args = {"send chunks": [(r + 2) % n, (r + 1) % n], "to": (r + 1) % n,
                             "recv chunks": [(r + 1) % n, r], "from": (r - 1) % n,
                             "received values": "added, then replace"}
-                if kind in (L.KERNEL_REDUCE_SCATTER, L.KERNEL_ALLGATHER) and rec["launches"] == 1:
-                    sent, recv = chunks_of_step(kind, step, r, n)
+                ring_kind = {L.KERNEL_PACK_RS: L.KERNEL_REDUCE_SCATTER, L.KERNEL_AG_UNPACK: L.KERNEL_ALLGATHER}.get(
+                    kind, kind)
+                if ring_kind in (L.KERNEL_REDUCE_SCATTER, L.KERNEL_ALLGATHER) and rec["launches"] == 1:
+                    sent, recv = chunks_of_step(ring_kind, step, r, n)
                     args = {"send chunk": sent, "to": (r + 1) % n, "recv chunk": recv, "from": (r - 1) % n,
-                            "received values": "added" if kind == L.KERNEL_REDUCE_SCATTER else "replace"}
+                            "received values": "added" if ring_kind == L.KERNEL_REDUCE_SCATTER else "replace"}
                 events.append(dict(common, tid=r + 1, name=name, args=args))
         return {"traceEvents": events, "displayTimeUnit": "ms",
                 "otherData": {"dropped_launches": self.dropped}}

@@ -145,6 +145,25 @@ def test_fusion_argument_errors():
     assert status_of(pk, FAKE, FAKE, FAKE, 3, hv.FLOAT32, b, 0, hv.FLOAT32, 2) == hv.OK
 
 
+def test_fused_boundary_argument_errors():
+    pr, au, fa = hv.hvdx_fuse_pack_rs, hv.hvdx_fuse_ag_unpack, hv.hvdx_fuse_allreduce
+    b2, b3 = bufs(2, 64), bufs(3, 64)
+    # the fused copy kernels need a first adding step that is not the last one
+    assert status_of(pr, FAKE, FAKE, FAKE, 3, hv.FLOAT32, b2, 64, hv.FLOAT32, 2) == hv.ERR_UNSUPPORTED
+    assert status_of(au, b2, 64, hv.FLOAT32, FAKE, FAKE, FAKE, 3, hv.FLOAT32, 2) == hv.ERR_UNSUPPORTED
+    assert status_of(pr, 0, FAKE, FAKE, 3, hv.FLOAT32, b3, 64, hv.FLOAT32, 3) == hv.ERR_INVALID
+    assert status_of(au, b3, 64, hv.FLOAT32, 0, FAKE, FAKE, 3, hv.FLOAT32, 3) == hv.ERR_INVALID
+    assert status_of(fa, FAKE, FAKE, FAKE, 3, hv.FLOAT32, b3, 64, hv.FLOAT32, 3, 7) == hv.ERR_INVALID  # op
+    assert status_of(fa, 0, FAKE, FAKE, 3, hv.FLOAT32, b3, 64, hv.FLOAT32, 3, hv.SUM) == hv.ERR_INVALID
+    assert status_of(fa, FAKE, FAKE, FAKE, 3, hv.FLOAT16, b3, 64, hv.FLOAT32, 3, hv.SUM) == hv.ERR_UNSUPPORTED
+    assert status_of(fa, FAKE, FAKE, FAKE, 3, hv.FLOAT32, [FAKE, FAKE + 64, FAKE + 4096], 64, hv.FLOAT32, 3,
+                     hv.SUM) == hv.ERR_ALIAS
+    # empty buffers are a no-op
+    assert status_of(pr, FAKE, FAKE, FAKE, 3, hv.FLOAT32, b3, 0, hv.FLOAT32, 3) == hv.OK
+    assert status_of(au, b3, 0, hv.FLOAT32, FAKE, FAKE, FAKE, 3, hv.FLOAT32, 3) == hv.OK
+    assert status_of(fa, FAKE, FAKE, FAKE, 3, hv.FLOAT32, b3, 0, hv.FLOAT32, 3, hv.AVERAGE) == hv.OK
+
+
 def test_plan_argument_errors():
     with pytest.raises(hv.HvdxError):
         hv.hvdx_fuse_plan([1, -2], hv.FLOAT32)

@@ -5,7 +5,7 @@ import torch
 
 import paper_1802_05799_amd as hv
 from _gpu import NP_TO_HV, NP_TO_TORCH, assert_bits_equal, say
-from oracle import allreduce, fusion
+from oracle import allreduce, fusion, ring
 
 pytestmark = pytest.mark.gpu
 
@@ -115,17 +115,74 @@ CYCLE_CASES = [
 ]
 
 
-@pytest.mark.parametrize("schedule", ["ring", "fold"])
+@pytest.mark.parametrize("mode", ["ring", "ring-separate", "fold"])
 @pytest.mark.parametrize("case", range(len(CYCLE_CASES)))
-def test_fused_allreduce_matches_oracle(case, schedule):
+def test_fused_allreduce_matches_oracle(case, mode):
     numel, n, threshold, compress, op = CYCLE_CASES[case]
     rng = np.random.default_rng(300 + case)
     host, dev, keep = make_tensors(rng, n, numel, np.float32)
-    say(f"cycle case={case} n={n} threshold={threshold} compress={compress} schedule={schedule}")
-    ar = hv.FusedAllreduce(dev, op=op, compress=compress, threshold_bytes=threshold, schedule=schedule)
+    say(f"cycle case={case} n={n} threshold={threshold} compress={compress} mode={mode}")
+    ar = hv.FusedAllreduce(dev, op=op, compress=compress, threshold_bytes=threshold,
+                           schedule="fold" if mode == "fold" else "ring", fuse_boundary=mode == "ring")
     ar()
     torch.cuda.synchronize()
     want = allreduce.allreduce(host, op, compress=compress, threshold=threshold)
     for r in range(n):
         for t in range(len(numel)):
             assert_bits_equal(dev[r][t].cpu().numpy(), want[r][t], f"rank {r} tensor {t}")
+
+
+FUSED_CASES = [
+    # (numel list, nranks, buffer dtype, align bytes)
+    ([7, 64, 100, 1000, 4608, 4096, 513, 10000], 3, np.float32, 16),
+    ([7, 64, 100, 1000, 4608, 4096, 513, 10000], 4, np.float32, 16),
+    ([1] * 3000 + [5000], 5, np.float32, 16),  # many tensors per tile
+    ([33, 31, 1, 2, 3, 4, 5, 6, 7, 8, 9, 100000], 7, np.float32, 4),  # no padding: vectors cross chunk ends
+    ([257] * 40 + [70000, 3, 9000], 6, np.float16, 16),  # binary16 buffer
+    ([1, 0, 2], 8, np.float32, 16),  # fewer buffer elements than ranks: empty chunks
+    ([3000, 1, 2, 50000, 64, 64, 64, 128 * 1024, 9], 13, np.float16, 2),
+]
+
+
+@pytest.mark.parametrize("misalign", [False, True], ids=["aligned", "misaligned"])
+@pytest.mark.parametrize("case", range(len(FUSED_CASES)))
+def test_copy_kernels_fused_with_ring_steps(case, misalign):
+    """hvdx_fuse_pack_rs leaves the buffers as the copy-in and adding step 0 do;
+    hvdx_fuse_ag_unpack, started from the state before replacing step N-2, gives every
+    tensor what that step and the copy-out give it, and writes no buffer."""
+    numel, n, buf_np, align = FUSED_CASES[case]
+    rng = np.random.default_rng(400 + case)
+    host, dev, keep = make_tensors(rng, n, numel, np.float32, misalign)
+    (b,) = fusion.fuse_plan(numel, np.dtype(buf_np).itemsize, threshold=1 << 30, align=align)
+    say(f"fused copy case={case} misalign={misalign} count={b.count} n={n}")
+    hv_buf = NP_TO_HV[np.dtype(buf_np)]
+    ptrs, nm, off = descriptors(dev, b, numel)
+    bufs = [torch.full((b.count + 64,), 7.0, dtype=NP_TO_TORCH[np.dtype(buf_np)], device="cuda") for _ in range(n)]
+    st = torch.cuda.current_stream().cuda_stream
+    hv.hvdx_fuse_pack_rs(ptrs.data_ptr(), nm.data_ptr(), off.data_ptr(), len(b.tensors), hv.FLOAT32,
+                         [x.data_ptr() for x in bufs], b.count, hv_buf, n, st)
+    torch.cuda.synchronize()
+
+    states = {}
+    work = np.stack([fusion.pack(host[r], b, buf_np) for r in range(n)])
+    ring.ring_allreduce(work, "average", observe=lambda ph, s_, x: states.__setitem__((ph, s_), x.copy()))
+    got = np.stack([x.cpu().numpy() for x in bufs])
+    assert_bits_equal(got[:, : b.count], states[("rs", 0)], "copy-in + adding step 0")
+    assert np.all(got[:, b.count :] == 7.0), "wrote past the buffer"
+
+    before = states[("ag", n - 3)]
+    for r in range(n):
+        bufs[r][: b.count].copy_(torch.from_numpy(before[r]))
+        for x in dev[r]:
+            x.fill_(-3.0)
+    torch.cuda.synchronize()
+    hv.hvdx_fuse_ag_unpack([x.data_ptr() for x in bufs], b.count, hv_buf, ptrs.data_ptr(), nm.data_ptr(),
+                           off.data_ptr(), len(b.tensors), hv.FLOAT32, n, st)
+    torch.cuda.synchronize()
+    final = states[("ag", n - 2)]
+    for r in range(n):
+        want = fusion.unpack(final[r], b, numel, np.float32)
+        for t in b.tensors:
+            assert_bits_equal(dev[r][t].cpu().numpy(), want[t], f"rank {r} tensor {t}")
+        assert_bits_equal(bufs[r][: b.count].cpu().numpy(), before[r], f"buffer of rank {r}")
+

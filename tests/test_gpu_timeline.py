@@ -20,17 +20,18 @@ def tensors(n, numel, seed=0):
     return [[torch.from_numpy((g.standard_normal(k) * 0.01).astype(np.float32)).cuda() for k in numel] for _ in range(n)]
 
 
-def test_records_follow_launches():
-    say("timeline records")
+@pytest.mark.parametrize("fuse_boundary", [True, False], ids=["fused-boundary", "separate"])
+def test_records_follow_launches(fuse_boundary):
+    say(f"timeline records fuse_boundary={fuse_boundary}")
     per_rank = tensors(5, [7, 4000, 100, 30000, 5])
-    ar = hv.FusedAllreduce(per_rank, op="average", threshold_bytes=40000)
+    ar = hv.FusedAllreduce(per_rank, op="average", threshold_bytes=40000, fuse_boundary=fuse_boundary)
     sid = torch.cuda.current_stream().cuda_stream
     launches = ar.kernel_sequence()
     with hv.Timeline(capacity=1000) as tl:
         ar(sid)
         ar(sid)
     assert tl.dropped == 0 and len(tl.records) == 2 * len(launches)
-    code = {"pack": 0, "rs": 1, "ag": 2, "unpack": 3, "rs_ag": 6}
+    code = {"pack": 0, "rs": 1, "ag": 2, "unpack": 3, "rs_ag": 6, "pack_rs": 8, "ag_unpack": 9}
     for rec, (kind, bi, s) in zip(tl.records, launches + launches):
         assert rec["kind"] == code[kind] and rec["step"] == s and rec["nranks"] == 5 and rec["launches"] == 1
         assert rec["count"] == ar.buckets[bi].count and rec["duration_us"] > 0
@@ -64,21 +65,26 @@ def test_environment_variable_writes_trace(tmp_path):
     subprocess.run([sys.executable, "-c", code], env=env, check=True, timeout=120)
     trace = json.loads(path.read_text())
     names = [e["name"] for e in trace["traceEvents"] if e["ph"] == "X" and e["tid"] == 0]
-    assert names == ["copy in", "reduce-scatter 0", "reduce-scatter 1", "reduce-scatter + allgather 2",
-                     "allgather 1", "allgather 2", "copy out"] * 2
+    assert names == ["copy in + reduce-scatter 0", "reduce-scatter 1", "reduce-scatter + allgather 2",
+                     "allgather 1", "allgather + copy out 2"] * 2
 
 
-def test_per_phase_records():
+@pytest.mark.parametrize("fuse_boundary", [True, False], ids=["fused-boundary", "separate"])
+def test_per_phase_records(fuse_boundary):
     per_rank = tensors(6, [7, 4000, 100, 30000, 5])
-    ar = hv.FusedAllreduce(per_rank, op="average", threshold_bytes=40000)
+    ar = hv.FusedAllreduce(per_rank, op="average", threshold_bytes=40000, fuse_boundary=fuse_boundary)
     with hv.Timeline(capacity=100, per_phase=True) as tl:
         ar()
     got = [(r["kind"], r["step"], r["launches"]) for r in tl.records]
     want = []
     for bi, b in enumerate(ar.buckets):
+        if fuse_boundary and not b.direct:  # copy-in + step 0, steps 1-3, 4 + 0, steps 1-3, 4 + copy-out
+            want += [(8, 0, 1), (1, 1, 3), (6, 4, 1), (2, 1, 3), (9, 4, 1)]
+            continue
         if not b.direct:
             want.append((0, -1, 1))
         want += [(1, 0, 4), (6, 4, 1), (2, 1, 4)]
         if not b.direct:
             want.append((3, -1, 1))
+    assert any(not b.direct for b in ar.buckets) and any(b.direct for b in ar.buckets)
     assert got == want

@@ -57,20 +57,24 @@ def test_tiny_workload_full_parity():
 
 
 @pytest.mark.parametrize(
-    "name,threshold",
-    [("resnet50", 64 << 20), ("inceptionv3", 64 << 20), ("vgg16", 64 << 20), ("vgg16fp16", 64 << 20),
-     ("resnet50", 0), ("inceptionv3", 1 << 20)],
-    ids=["resnet50", "inceptionv3", "vgg16", "vgg16fp16", "resnet50-unfused", "inceptionv3-1MiB"],
+    "name,threshold,fuse_boundary",
+    [("resnet50", 64 << 20, True), ("inceptionv3", 64 << 20, True), ("vgg16", 64 << 20, True),
+     ("vgg16fp16", 64 << 20, True), ("resnet50", 0, True), ("inceptionv3", 1 << 20, True),
+     ("resnet50", 64 << 20, False), ("vgg16fp16", 64 << 20, False)],
+    ids=["resnet50", "inceptionv3", "vgg16", "vgg16fp16", "resnet50-unfused", "inceptionv3-1MiB",
+         "resnet50-separate-boundary", "vgg16fp16-separate-boundary"],
 )
-def test_full_workload(name, threshold):
-    """Threshold 0 is the unfused ablation: every tensor reduced by its own ring."""
+def test_full_workload(name, threshold, fuse_boundary):
+    """Threshold 0 is the unfused ablation: every tensor reduced by its own ring.  With
+    fuse_boundary=False copy-in, ring and copy-out run as separate calls."""
     w = configs.get(name)
     n = w.nranks
     say(f"workload {name} threshold {threshold}: generate")
     per_rank, storage, starts = wgpu.make_rank_tensors(w)
     numel, prefix = w.numel(), w.prefix()
     say(f"workload {name}: allreduce")
-    ar = hv.FusedAllreduce(per_rank, op=w.op, compress=w.compress, threshold_bytes=threshold)
+    ar = hv.FusedAllreduce(per_rank, op=w.op, compress=w.compress, threshold_bytes=threshold,
+                           fuse_boundary=fuse_boundary)
     ar()
     torch.cuda.synchronize()
 
