@@ -137,3 +137,61 @@ def test_unmutated_fusion_passes():
     from oracle import fusion
 
     assert fusion_pins_fail(fusion) is None
+
+
+# ---- broadcast -------------------------------------------------------------------------
+def broadcast_pins_fail(bmod):
+    import test_oracle_broadcast as tb
+
+    try:
+        for n in (1, 2, 3, 5, 8):
+            for nbytes in (0, 1, 17, 16 * n, 1000):
+                for root in {0, n - 1, n // 2}:
+                    x = tb.distinct(n, nbytes)
+                    if not np.array_equal(bmod.chain_broadcast(x.copy(), root), np.broadcast_to(x[root], x.shape)):
+                        return "result"
+        if bmod.chunk_bytes(40, 3) != [(0, 16), (16, 32), (32, 40)]:
+            return "chunks"
+        # 80 bytes = 5 units = 3 * 1 + 2: the first two chunks take two units each
+        if bmod.chunk_bytes(80, 3) != [(0, 32), (32, 64), (64, 80)]:
+            return "chunk remainder"
+        for n in (2, 3, 5):
+            tr = bmod.new_traffic(n)
+            bmod.chain_broadcast(tb.distinct(n, 1000), 1 % n, traffic=tr)
+            if any(tr["recvd"][r] != (0 if r == 1 % n else 1000) for r in range(n)):
+                return "traffic"
+        # hand-worked intermediate states (root 1, three ranks)
+        x = tb.distinct(3, 40)
+        seen = {}
+        bmod.chain_broadcast(x.copy(), 1, observe=lambda s, b: seen.__setitem__(s, b.copy()))
+        want_step0 = x.copy()
+        want_step0[2, 0:16] = x[1, 0:16]  # step 0: only chunk 0 leaves the root
+        if not np.array_equal(seen[0], want_step0):
+            return "schedule"
+    except Exception as exc:
+        return type(exc).__name__
+    return None
+
+
+BROADCAST_MUTANTS = [
+    ("chunks not in whole units", "units = -(-nbytes // UNIT)", "units = nbytes"),
+    ("long chunks last", "n = q + (1 if j < rem else 0)", "n = q + (1 if j >= nranks - rem else 0)"),
+    ("last link dropped", "for k in range(n - 1):  # link", "for k in range(n - 2):  # link"),
+    ("one step short", "for step in range(2 * n - 2):", "for step in range(2 * n - 3):"),
+    ("chunk schedule not staggered", "j = step - k", "j = step"),
+    ("root ignored", "src, dst = (root + k) % n, (root + k + 1) % n", "src, dst = k % n, (k + 1) % n"),
+    ("copy reversed", "bufs[dst, lo:hi] = bufs[src, lo:hi]", "bufs[src, lo:hi] = bufs[dst, lo:hi]"),
+    ("traffic counts sender as receiver", 'traffic["recvd"][dst] += hi - lo', 'traffic["recvd"][src] += hi - lo'),
+]
+
+
+@pytest.mark.parametrize("label,old,new", BROADCAST_MUTANTS, ids=[m[0] for m in BROADCAST_MUTANTS])
+def test_broadcast_mutant_is_caught(label, old, new):
+    mod = load_mutant("broadcast", old, new)
+    assert broadcast_pins_fail(mod) is not None, f"no pin caught mutant: {label}"
+
+
+def test_unmutated_broadcast_passes():
+    from oracle import broadcast
+
+    assert broadcast_pins_fail(broadcast) is None
