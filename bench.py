@@ -137,7 +137,15 @@ def time_graph(ar, steps, stream):
     return e0.elapsed_time(e1) / steps
 
 
-def measure(name, steps, warmup, threshold=64 << 20, per_kernel_pass=True, schedule="ring", graph_pass=True):
+MALL_FLUSH_BYTES = 1 << 30  # written between allreduces: 4x the 256 MB Infinity Cache
+
+
+def measure(name, steps, warmup, threshold=64 << 20, per_kernel_pass=True, schedule="ring", graph_pass=True,
+            flush_bytes=0):
+    """Time `steps` allreduces of workload `name`.  With flush_bytes, a buffer that
+    large is overwritten before every allreduce (outside its timing), so each one
+    starts with none of its data in the Infinity Cache; each allreduce then has its
+    own event pair and the median is reported."""
     import torch
 
     import paper_1802_05799_amd as hv
@@ -149,22 +157,39 @@ def measure(name, steps, warmup, threshold=64 << 20, per_kernel_pass=True, sched
     ar = hv.FusedAllreduce(per_rank, op=w.op, compress=w.compress, threshold_bytes=threshold, schedule=schedule)
     stream = torch.cuda.current_stream()
     sid = stream.cuda_stream
-    for _ in range(warmup):
+    scratch = torch.empty(flush_bytes // 4, dtype=torch.float32, device="cuda") if flush_bytes else None
+
+    def flush(i):
+        if scratch is not None:
+            scratch.fill_(float(i))
+
+    for i in range(warmup):
+        flush(i)
         ar(sid)
     torch.cuda.synchronize()
 
-    # timed region: exactly `steps` whole allreduces, one event pair around them
     t0 = time.perf_counter()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record(stream)
-    for _ in range(steps):
-        ar(sid)
-    e1.record(stream)
-    torch.cuda.synchronize()
+    if scratch is None:
+        # timed region: exactly `steps` whole allreduces, one event pair around them
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(steps):
+            ar(sid)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / steps
+    else:
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+        for i, (a, b) in enumerate(ev):
+            flush(i)
+            a.record(stream)
+            ar(sid)
+            b.record(stream)
+        torch.cuda.synchronize()
+        ms = sorted(a.elapsed_time(b) for a, b in ev)[steps // 2]
     wall = time.perf_counter() - t0
-    ms = e0.elapsed_time(e1) / steps
     # the same cycle submitted as one HIP graph per step (launch overhead removed)
-    graph_ms = time_graph(ar, steps, stream) if graph_pass else None
+    graph_ms = time_graph(ar, steps, stream) if graph_pass and scratch is None else None
     if not per_kernel_pass:
         res = {"ms_per_step": ms, "algbw_GBps": w.rank_bytes / (ms * 1e-3) / 1e9, "buckets": len(ar.buckets),
                "launches_per_step": len(ar.kernel_sequence()), "graph_ms_per_step": graph_ms}
@@ -178,7 +203,8 @@ def measure(name, steps, warmup, threshold=64 << 20, per_kernel_pass=True, sched
     # replacing steps, its copy-out).  Each record's median over the timed steps is
     # kept: a sample the host stalled is an outlier, not a kernel duration.
     with hv.Timeline(capacity=64 * (steps + 1) * max(1, len(ar.buckets)), per_phase=True) as tl:
-        for _ in range(steps + 1):
+        for i in range(steps + 1):
+            flush(i)  # not a library launch: no timeline record
             ar(sid)
     recs = tl.records
     per_step = len(recs) // (steps + 1)
@@ -219,9 +245,20 @@ def measure(name, steps, warmup, threshold=64 << 20, per_kernel_pass=True, sched
         "timing_outliers": outliers,
         "buckets": [(b.count, len(b.tensors), b.direct) for b in ar.buckets],
     }
-    del ar, per_rank, storage
+    del ar, per_rank, storage, scratch
     torch.cuda.empty_cache()
     return res
+
+
+def hbm_fracs(r):
+    """HBM fraction (algorithmic bytes over time) of the ring's kernels alone and of
+    the whole step."""
+    ring = [v for k, v in r["kernels"].items() if k.startswith(("rs_step", "ag_step", "rs_ag_step"))]
+    ring_bytes = sum(v["bytes"] for v in ring) / r["steps"]  # per step
+    ring_ms = sum(v["ms_per_step"] for v in ring)
+    path_bytes = sum(v["bytes"] for v in r["kernels"].values()) / r["steps"]
+    return (round(ring_bytes / (ring_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4) if ring_ms else None,
+            round(path_bytes / (r["ms_per_step"] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4))
 
 
 def measure_broadcast(name, steps, warmup=2):
@@ -442,17 +479,24 @@ def main():
                 print(f"# {name}: {r['ms_per_step']:.3f} ms/step, {r['algbw_GBps']:.1f} GB/s, "
                       f"graph {r['graph_ms_per_step']:.3f} ms/step", file=sys.stderr,
                       flush=True)
-            ring = [v for k, v in r["kernels"].items() if k.startswith(("rs_step", "ag_step", "rs_ag_step"))]
-            ring_bytes = sum(v["bytes"] for v in ring) / r["steps"]  # per step
-            ring_ms = sum(v["ms_per_step"] for v in ring)
-            path_bytes = sum(v["bytes"] for v in r["kernels"].values()) / r["steps"]
+            ring_frac, path_frac = hbm_fracs(r)
+            # the same allreduce started with the Infinity Cache flushed
+            f = measure(name, max(3, args.steps // 2), 1, graph_pass=False, flush_bytes=MALL_FLUSH_BYTES)
+            f_ring, f_path = hbm_fracs(f)
+            print(f"# {name} (cache flushed): {f['ms_per_step']:.3f} ms/step, ring {f_ring}", file=sys.stderr,
+                  flush=True)
             per_config[name] = {
                 "nranks": r["nranks"],
                 "ms_per_step": round(r["ms_per_step"], 4),
                 "graph_ms_per_step": r["graph_ms_per_step"] and round(r["graph_ms_per_step"], 4),
                 # algorithmic bytes over time: the ring's kernels alone, and the whole step
-                "ring_hbm_frac": round(ring_bytes / (ring_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4) if ring_ms else None,
-                "path_hbm_frac": round(path_bytes / (r["ms_per_step"] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                "ring_hbm_frac": ring_frac,
+                "path_hbm_frac": path_frac,
+                "mall_flushed": {"ms_per_step": round(f["ms_per_step"], 4),
+                                 "algbw_GBps": round(f["algbw_GBps"], 2),
+                                 "ring_hbm_frac": f_ring, "path_hbm_frac": f_path,
+                                 "kernels_hbm_frac": {k: v["hbm_frac"] and round(v["hbm_frac"], 4)
+                                                      for k, v in f["kernels"].items()}},
                 "algbw_GBps": round(r["algbw_GBps"], 2),
                 "busbw_GBps": round(r["busbw_GBps"], 2),
                 "kernels": {k: {"avg_us": round(v["avg_us"], 2), "GBps": v["GBps"] and round(v["GBps"], 1),

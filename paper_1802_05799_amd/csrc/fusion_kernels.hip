@@ -20,23 +20,32 @@ namespace {
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 
-// Shape of a copy kernel: POS 16-byte buffer vectors per lane (a tile is kBlock*POS
-// vectors), RB ranks whose loads are in flight together, RPB ranks per block (0 =
-// all), and non-temporal loads/stores.  Measured on MI355X with the workloads'
-// buckets (both stream their data once, so every access is non-temporal).  Two
-// ranks per block and small LDS tables (3 KiB a block) gave the most blocks in
-// flight and the best rate for both directions.
+// Shape of a copy kernel: POS 16-byte buffer vectors per lane in a row (a row is
+// kBlock*POS vectors), SUB rows per block (one tensor lookup serves them all), RB
+// ranks whose loads are in flight together, RPB ranks per block (0 = all),
+// non-temporal loads/stores, and the lane layout.  Measured on MI355X with the
+// workloads' buckets: a block's prologue (two rounds of dependent loads to find its
+// tensors) has to be amortized over enough data in flight.  Two ranks per block with
+// two block-strided vectors per lane and one row (four loads in flight per lane,
+// 16 KiB read and written per block, 3 KiB of LDS) was best in both directions.
+// One rank per block with one vector per lane (the best pattern for a plain copy
+// between many buffers, tried with the receiver's block loading the sender's values
+// too) lost to the prologue even with 8 rows; more rows, more ranks per batch or
+// wavefront-contiguous lanes did not help either.
 #ifndef HVDX_LDS_TENSORS
 #define HVDX_LDS_TENSORS 64
 #endif
-template <int POS_, int RB_, int RPB_, bool NTL_, bool NTS_>
+template <int POS_, int RB_, int RPB_, bool NTL_, bool NTS_, bool WAVE_ = false, int SUB_ = 1>
 struct CopyCfg {
   static constexpr int POS = POS_, RB = RB_, RPB = RPB_;
   static constexpr bool NTL = NTL_, NTS = NTS_;
-  static constexpr int kTileVecs = kBlock * POS_;
+  static constexpr bool WAVE = WAVE_;  // a wavefront's POS vectors are contiguous (else block-strided)
+  static constexpr int SUB = SUB_;     // rows of kBlock*POS vectors a block moves one after another
+  static constexpr int kRowVecs = kBlock * POS_;
+  static constexpr int kTileVecs = kRowVecs * SUB_;  // a block's tile: one tensor lookup serves all its rows
   // A tile's tensors staged in LDS; a tile that spans more looks its tensors up in
   // global memory instead.
-  static constexpr int kLdsTensors = kBlock * POS_ + 8 < HVDX_LDS_TENSORS ? kBlock * POS_ + 8 : HVDX_LDS_TENSORS;
+  static constexpr int kLdsTensors = kTileVecs + 8 < HVDX_LDS_TENSORS ? kTileVecs + 8 : HVDX_LDS_TENSORS;
 };
 #ifndef HVDX_PACK_CFG
 #define HVDX_PACK_CFG CopyCfg<2, 2, 2, true, true>
@@ -54,10 +63,20 @@ using PackCfg = HVDX_PACK_CFG;      // binary32 buffers
 using UnpackCfg = HVDX_UNPACK_CFG;
 using Pack16Cfg = HVDX_PACK16_CFG;  // binary16 buffers
 using Unpack16Cfg = HVDX_UNPACK16_CFG;
+#ifndef HVDX_COPY_ATTR
+#define HVDX_COPY_ATTR
+#endif
 #ifndef HVDX_LDS_PTRS
 #define HVDX_LDS_PTRS 256
 #endif
 constexpr int kLdsPtrs = HVDX_LDS_PTRS;  // (rank, tensor) pointers a tile can stage in LDS
+
+// Vector u of this lane within its block's tile.
+template <typename Cfg>
+__device__ __forceinline__ int tile_vec(int u) {
+  if constexpr (Cfg::WAVE) return (threadIdx.x >> 6) * 64 * Cfg::POS + u * 64 + (threadIdx.x & 63);
+  return u * kBlock + threadIdx.x;
+}
 
 template <typename TB>
 struct BufVec {
@@ -382,11 +401,17 @@ struct PtrTable {
 // state the copy-in and that step leave, without reading the sender's buffer back.
 // A block's slots start at its chunk's sender, so slot 0 (sender) and slot 1
 // (receiver) are one load batch of the first rank group.
+//
+// Each row of the tile is moved in two passes: whole vectors (and all-padding ones)
+// first, for every rank, then the rare edge vectors element by element.  Keeping the
+// element path out of the vector pass keeps the vector pass's registers low enough
+// for full occupancy.
 template <typename TT, typename TB, typename Cfg, bool RING>
-__global__ __launch_bounds__(kBlock) void pack_kernel(const void* const* __restrict__ srcs,
-                                                      const int64_t* __restrict__ numel,
-                                                      const int64_t* __restrict__ offset, int ntensors, RankPtrs bufs,
-                                                      int64_t count, int nranks, int rpb, int64_t q, int64_t rem) {
+__global__ __launch_bounds__(kBlock) HVDX_COPY_ATTR void pack_kernel(const void* const* __restrict__ srcs,
+                                                                    const int64_t* __restrict__ numel,
+                                                                    const int64_t* __restrict__ offset, int ntensors,
+                                                                    RankPtrs bufs, int64_t count, int nranks, int rpb,
+                                                                    int64_t q, int64_t rem) {
   static_assert(!RING || (Cfg::RB >= 2 && (Cfg::RPB == 0 || Cfg::RPB >= 2)),
                 "the fused copy-in needs the sender and receiver in one load batch");
   constexpr int V = BufVec<TB>::n;
@@ -404,55 +429,67 @@ __global__ __launch_bounds__(kBlock) void pack_kernel(const void* const* __restr
   const PtrTable pt{srcs, pin ? s_ptr : nullptr, tt.t0, ntensors, tt.nt, bs.rbeg, rot, nranks};
   const int receiver = bs.c + 1 == nranks ? 0 : bs.c + 1;  // of chunk c in adding step 0
 
-  Pos pos[kPosPerLane];
+  for (int row = 0; row < Cfg::SUB; ++row) {
+    const int64_t r0 = bs.p0 + (int64_t)row * Cfg::kRowVecs * V;
+    if (r0 >= bs.p1) break;
+    Pos pos[kPosPerLane];
+    bool edges = false;
 #pragma unroll
-  for (int u = 0; u < kPosPerLane; ++u)
-    pos[u] = classify<V>(tt, s_off, s_end, offset, numel, bs.p0 + (int64_t)(u * kBlock + threadIdx.x) * V, bs.p1,
-                         bs.cs, bs.ce);
-
-  for (int v0 = bs.rbeg; v0 < bs.rend; v0 += kRankBatch) {
-    VB v[kRankBatch][kPosPerLane];
-#pragma unroll
-    for (int rr = 0; rr < kRankBatch; ++rr) {
-      const int slot = v0 + rr;
-#pragma unroll
-      for (int u = 0; u < kPosPerLane; ++u)
-        if (slot < bs.rend && pos[u].cls == POS_VEC)
-          v[rr][u] = Mover<TT, TB>::template load<Cfg::NTL>(static_cast<const TT*>(pt.get(slot, pos[u].t)) +
-                                                            pos[u].li);
+    for (int u = 0; u < kPosPerLane; ++u) {
+      pos[u] = classify<V>(tt, s_off, s_end, offset, numel, r0 + (int64_t)tile_vec<Cfg>(u) * V, bs.p1, bs.cs, bs.ce);
+      edges |= pos[u].cls == POS_EDGE;
     }
+
+    for (int v0 = bs.rbeg; v0 < bs.rend; v0 += kRankBatch) {
+      VB v[kRankBatch][kPosPerLane];
 #pragma unroll
-    for (int rr = 0; rr < kRankBatch; ++rr) {
-      const int slot = v0 + rr;
-      if (slot >= bs.rend) break;
+      for (int rr = 0; rr < kRankBatch; ++rr) {
+        const int slot = v0 + rr;
+#pragma unroll
+        for (int u = 0; u < kPosPerLane; ++u)
+          if (slot < bs.rend && pos[u].cls == POS_VEC)
+            v[rr][u] = Mover<TT, TB>::template load<Cfg::NTL>(static_cast<const TT*>(pt.get(slot, pos[u].t)) +
+                                                              pos[u].li);
+      }
+#pragma unroll
+      for (int rr = 0; rr < kRankBatch; ++rr) {
+        const int slot = v0 + rr;
+        if (slot >= bs.rend) break;
+        TB* __restrict__ buf = static_cast<TB*>(bufs.p[pt.rank(slot)]);
+#pragma unroll
+        for (int u = 0; u < kPosPerLane; ++u) {
+          if (pos[u].cls == POS_VEC) {
+            VB x = v[rr][u];
+            if (RING && rr > 0 && slot == 1) x = x + v[rr > 0 ? rr - 1 : 0][u];  // receiver: own + sender's
+            st16<Cfg::NTS>(reinterpret_cast<VB*>(buf + pos[u].p), x);
+          } else if (pos[u].cls == POS_ZERO) {
+            store_zero(buf + pos[u].p);  // padding: zero, and zero + zero for a receiver
+          }
+        }
+      }
+    }
+
+    if (!edges) continue;
+    for (int slot = bs.rbeg; slot < bs.rend; ++slot) {
       const int r = pt.rank(slot);
       TB* __restrict__ buf = static_cast<TB*>(bufs.p[r]);
-#pragma unroll
       for (int u = 0; u < kPosPerLane; ++u) {
-        const Pos& ps = pos[u];
-        if (ps.cls == POS_VEC) {
-          VB x = v[rr][u];
-          if (RING && rr > 0 && slot == 1) x = x + v[rr > 0 ? rr - 1 : 0][u];  // receiver: own + sender's
-          st16<Cfg::NTS>(reinterpret_cast<VB*>(buf + ps.p), x);
-        } else if (ps.cls == POS_ZERO) {
-          store_zero(buf + ps.p);  // padding: zero, and zero + zero for a receiver
-        } else if (ps.cls == POS_EDGE) {
-          for (int k = 0; k < V; ++k) {
-            const int64_t pe = ps.p + k;
-            if (pe >= bs.ce) break;
-            if (pe < bs.cs) continue;
-            const int jk = lookup(tt, s_off, offset, pe);
-            const int64_t tk = tt.t0 + jk;
-            const bool in_tensor = tk >= 0 && pe < tensor_end(tt, s_end, offset, numel, jk);
-            const int64_t li = in_tensor ? pe - tensor_begin(tt, s_off, offset, jk) : 0;
-            TB val = (TB)0;
-            if (in_tensor) {
-              val = Mover<TT, TB>::cvt_in(static_cast<const TT*>(pt.get(slot, tk))[li]);
-              if (RING && r == receiver)
-                val = val + Mover<TT, TB>::cvt_in(static_cast<const TT*>(srcs[(int64_t)bs.c * ntensors + tk])[li]);
-            }
-            buf[pe] = val;
+        if (pos[u].cls != POS_EDGE) continue;
+        for (int k = 0; k < V; ++k) {
+          const int64_t pe = pos[u].p + k;
+          if (pe >= bs.ce) break;
+          if (pe < bs.cs) continue;
+          const int jk = lookup(tt, s_off, offset, pe);
+          const int64_t tk = tt.t0 + jk;
+          const bool in_tensor = tk >= 0 && pe < tensor_end(tt, s_end, offset, numel, jk);
+          const int64_t li = in_tensor ? pe - tensor_begin(tt, s_off, offset, jk) : 0;
+          TB val = (TB)0;
+          if (in_tensor) {
+            val = Mover<TT, TB>::cvt_in(static_cast<const TT*>(pt.get(slot, tk))[li]);
+            if (RING && r == receiver)
+              val = val + Mover<TT, TB>::cvt_in(static_cast<const TT*>(srcs[(int64_t)bs.c * ntensors + tk])[li]);
           }
+          buf[pe] = val;
         }
       }
     }
@@ -462,11 +499,13 @@ __global__ __launch_bounds__(kBlock) void pack_kernel(const void* const* __restr
 // Copy-out.  With RING it is fused with the ring's last replacing step: in chunk c
 // that step hands rank c-3's final values to rank c-2, so rank c-2 copies them out
 // from rank c-3's buffer (mod N) and its own buffer keeps the chunk's older values.
+// Two passes per row, as in the copy-in.
 template <typename TT, typename TB, typename Cfg, bool RING>
-__global__ __launch_bounds__(kBlock) void unpack_kernel(RankPtrs bufs, int64_t count, void* const* __restrict__ dsts,
-                                                        const int64_t* __restrict__ numel,
-                                                        const int64_t* __restrict__ offset, int ntensors,
-                                                        int nranks, int rpb, int64_t q, int64_t rem) {
+__global__ __launch_bounds__(kBlock) HVDX_COPY_ATTR void unpack_kernel(RankPtrs bufs, int64_t count,
+                                                                      void* const* __restrict__ dsts,
+                                                                      const int64_t* __restrict__ numel,
+                                                                      const int64_t* __restrict__ offset, int ntensors,
+                                                                      int nranks, int rpb, int64_t q, int64_t rem) {
   constexpr int V = BufVec<TB>::n;
   using VB = typename Mover<TT, TB>::buf_vec;
   constexpr int kPosPerLane = Cfg::POS, kRankBatch = Cfg::RB, kTileVecs = Cfg::kTileVecs;
@@ -482,47 +521,57 @@ __global__ __launch_bounds__(kBlock) void unpack_kernel(RankPtrs bufs, int64_t c
                                                     nranks, s_off, s_end, s_meta, s_ptr, &pin);
   const PtrTable pt{dsts, pin ? s_ptr : nullptr, tt.t0, ntensors, tt.nt, bs.rbeg, 0, nranks};
 
-  Pos pos[kPosPerLane];
+  for (int row = 0; row < Cfg::SUB; ++row) {
+    const int64_t r0 = bs.p0 + (int64_t)row * Cfg::kRowVecs * V;
+    if (r0 >= bs.p1) break;
+    Pos pos[kPosPerLane];
+    bool edges = false;
 #pragma unroll
-  for (int u = 0; u < kPosPerLane; ++u)
-    pos[u] = classify<V>(tt, s_off, s_end, offset, numel, bs.p0 + (int64_t)(u * kBlock + threadIdx.x) * V, bs.p1,
-                         bs.cs, bs.ce);
-
-  for (int r0 = bs.rbeg; r0 < bs.rend; r0 += kRankBatch) {
-    VB v[kRankBatch][kPosPerLane];
-#pragma unroll
-    for (int rr = 0; rr < kRankBatch; ++rr) {
-      const int r = r0 + rr < bs.rend ? r0 + rr : bs.rbeg;
-      const int from = r == receiver ? (r == 0 ? nranks - 1 : r - 1) : r;
-      const TB* __restrict__ buf = static_cast<const TB*>(bufs.p[from]);
-#pragma unroll
-      for (int u = 0; u < kPosPerLane; ++u)
-        if (r0 + rr < bs.rend && pos[u].cls == POS_VEC)
-          v[rr][u] = ld16<Cfg::NTL>(reinterpret_cast<const VB*>(buf + pos[u].p));
+    for (int u = 0; u < kPosPerLane; ++u) {
+      pos[u] = classify<V>(tt, s_off, s_end, offset, numel, r0 + (int64_t)tile_vec<Cfg>(u) * V, bs.p1, bs.cs, bs.ce);
+      edges |= pos[u].cls == POS_EDGE;
     }
+
+    for (int rb = bs.rbeg; rb < bs.rend; rb += kRankBatch) {
+      VB v[kRankBatch][kPosPerLane];
 #pragma unroll
-    for (int rr = 0; rr < kRankBatch; ++rr) {
-      const int r = r0 + rr;
-      if (r >= bs.rend) break;
+      for (int rr = 0; rr < kRankBatch; ++rr) {
+        const int r = rb + rr;
+        const int from = r == receiver ? (r == 0 ? nranks - 1 : r - 1) : r;
+        const TB* __restrict__ buf = static_cast<const TB*>(bufs.p[r < bs.rend ? from : bs.rbeg]);
+#pragma unroll
+        for (int u = 0; u < kPosPerLane; ++u)
+          if (r < bs.rend && pos[u].cls == POS_VEC)
+            v[rr][u] = ld16<Cfg::NTL>(reinterpret_cast<const VB*>(buf + pos[u].p));
+      }
+#pragma unroll
+      for (int rr = 0; rr < kRankBatch; ++rr) {
+        const int r = rb + rr;
+        if (r >= bs.rend) break;
+#pragma unroll
+        for (int u = 0; u < kPosPerLane; ++u)
+          if (pos[u].cls == POS_VEC)
+            Mover<TT, TB>::template store<Cfg::NTS>(static_cast<TT*>(const_cast<void*>(pt.get(r, pos[u].t))) +
+                                                        pos[u].li,
+                                                    v[rr][u]);
+      }
+    }
+
+    if (!edges) continue;
+    for (int r = bs.rbeg; r < bs.rend; ++r) {
       const int from = r == receiver ? (r == 0 ? nranks - 1 : r - 1) : r;
       const TB* __restrict__ buf = static_cast<const TB*>(bufs.p[from]);
-#pragma unroll
       for (int u = 0; u < kPosPerLane; ++u) {
-        const Pos& ps = pos[u];
-        if (ps.cls == POS_VEC) {
-          Mover<TT, TB>::template store<Cfg::NTS>(static_cast<TT*>(const_cast<void*>(pt.get(r, ps.t))) + ps.li,
-                                                  v[rr][u]);
-        } else if (ps.cls == POS_EDGE) {
-          for (int k = 0; k < V; ++k) {
-            const int64_t pe = ps.p + k;
-            if (pe >= bs.ce) break;
-            if (pe < bs.cs) continue;
-            const int jk = lookup(tt, s_off, offset, pe);
-            const int64_t tk = tt.t0 + jk;
-            if (tk >= 0 && pe < tensor_end(tt, s_end, offset, numel, jk)) {
-              TT* dk = static_cast<TT*>(const_cast<void*>(pt.get(r, tk)));
-              dk[pe - tensor_begin(tt, s_off, offset, jk)] = Mover<TT, TB>::cvt_out(buf[pe]);
-            }
+        if (pos[u].cls != POS_EDGE) continue;
+        for (int k = 0; k < V; ++k) {
+          const int64_t pe = pos[u].p + k;
+          if (pe >= bs.ce) break;
+          if (pe < bs.cs) continue;
+          const int jk = lookup(tt, s_off, offset, pe);
+          const int64_t tk = tt.t0 + jk;
+          if (tk >= 0 && pe < tensor_end(tt, s_end, offset, numel, jk)) {
+            TT* dk = static_cast<TT*>(const_cast<void*>(pt.get(r, tk)));
+            dk[pe - tensor_begin(tt, s_off, offset, jk)] = Mover<TT, TB>::cvt_out(buf[pe]);
           }
         }
       }

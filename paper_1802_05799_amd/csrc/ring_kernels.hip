@@ -111,21 +111,47 @@ __device__ __forceinline__ int64_t head_elems(const void* p, int64_t len) {
 // best reduce-scatter keeps loads cached and streams its stores non-temporally
 // (the next step re-reads what this one wrote from the cache), and the best
 // all-gather is plain with two vectors per lane; when it does not fit, one vector
-// per lane with every access non-temporal streams closest to the HBM limit.
-template <int U_, int BS_, bool NTL_, bool NTS_>
+// per lane with every access non-temporal streams closest to the HBM limit.  The
+// fused step N-2/0 (two reads, two writes) does best with one vector per lane in
+// both regimes.  Each shape can be replaced at build time (-DHVDX_RS_CACHED=...).
+template <int U_, int BS_, bool NTL_, bool NTS_, bool WAVE_ = false>
 struct Policy {
   static constexpr int U = U_;      // 16-byte vectors per lane and stream
   static constexpr int BS = BS_;    // threads per block
   static constexpr bool NTL = NTL_; // non-temporal loads
   static constexpr bool NTS = NTS_; // non-temporal stores
+  static constexpr bool WAVE = WAVE_;  // a wavefront's U vectors are contiguous (else block-strided)
 };
-using RsCached = Policy<4, 256, false, true>;
-using RsStream = Policy<1, 256, true, true>;
-using AgCached = Policy<2, 512, false, false>;
-using AgStream = Policy<1, 256, true, true>;
-using C16Cached = Policy<2, 256, false, false>;
+#ifndef HVDX_RS_CACHED
+#define HVDX_RS_CACHED Policy<4, 256, false, true>
+#endif
+#ifndef HVDX_RS_STREAM
+#define HVDX_RS_STREAM Policy<1, 256, true, true>
+#endif
+#ifndef HVDX_AG_CACHED
+#define HVDX_AG_CACHED Policy<2, 512, false, false>
+#endif
+#ifndef HVDX_AG_STREAM
+#define HVDX_AG_STREAM Policy<1, 256, true, true>
+#endif
+#ifndef HVDX_RSAG_CACHED  // two reads and two writes per vector: one vector per lane measured best
+#define HVDX_RSAG_CACHED Policy<1, 256, false, true>
+#endif
+#ifndef HVDX_RSAG_STREAM
+#define HVDX_RSAG_STREAM HVDX_RS_STREAM
+#endif
+#ifndef HVDX_C16_CACHED
+#define HVDX_C16_CACHED Policy<2, 256, false, false>
+#endif
+using RsCached = HVDX_RS_CACHED;
+using RsStream = HVDX_RS_STREAM;
+using AgCached = HVDX_AG_CACHED;
+using AgStream = HVDX_AG_STREAM;
+using RsAgCached = HVDX_RSAG_CACHED;
+using RsAgStream = HVDX_RSAG_STREAM;
+using C16Cached = HVDX_C16_CACHED;
 #ifndef HVDX_C16_RS_STREAM
-#define HVDX_C16_RS_STREAM Policy<1, 256, true, true>
+#define HVDX_C16_RS_STREAM Policy<1, 64, true, true>
 #endif
 #ifndef HVDX_C16_AG_STREAM  // writes 3x what it reads: cached stores measured 1.4x faster
 #define HVDX_C16_AG_STREAM Policy<2, 256, false, false>
@@ -133,6 +159,13 @@ using C16Cached = Policy<2, 256, false, false>;
 using C16RsStream = HVDX_C16_RS_STREAM;
 using C16AgStream = HVDX_C16_AG_STREAM;
 constexpr int64_t kStreamBytes = 128ll << 20;  // rank buffers at least this large stream
+
+// Vector u of this lane in a block's span of BS*U vectors starting at blk.
+template <typename P>
+__device__ __forceinline__ int64_t lane_vec(int64_t blk, int u) {
+  if constexpr (P::WAVE) return blk + (int64_t)(threadIdx.x >> 6) * 64 * P::U + u * 64 + (threadIdx.x & 63);
+  return blk + (int64_t)u * P::BS + threadIdx.x;
+}
 
 template <bool NT, typename V>
 __device__ __forceinline__ V vload(const V* p) {
@@ -169,20 +202,20 @@ __global__ __launch_bounds__(P::BS) void rs_step_kernel(RankPtrs bufs, RingArgs 
 
   const VT* __restrict__ s4 = reinterpret_cast<const VT*>(src + head);
   VT* __restrict__ d4 = reinterpret_cast<VT*>(dst + head);
-  for (int64_t base = (int64_t)blockIdx.x * BS * U + threadIdx.x; base < nvec; base += gthreads * U) {
+  for (int64_t blk = (int64_t)blockIdx.x * BS * U; blk < nvec; blk += gthreads * U) {
     VT x[U], y[U];
-    if (base + (U - 1) * BS < nvec) {  // whole tile: all loads in flight at once
+    if (blk + BS * U <= nvec) {  // whole tile: all loads in flight at once
 #pragma unroll
       for (int u = 0; u < U; ++u) {
-        x[u] = vload<P::NTL>(s4 + base + u * BS);
-        y[u] = vload<P::NTL>(d4 + base + u * BS);
+        x[u] = vload<P::NTL>(s4 + lane_vec<P>(blk, u));
+        y[u] = vload<P::NTL>(d4 + lane_vec<P>(blk, u));
       }
 #pragma unroll
-      for (int u = 0; u < U; ++u) vstore<P::NTS>(d4 + base + u * BS, combine<DIV>(y[u], x[u], a));
+      for (int u = 0; u < U; ++u) vstore<P::NTS>(d4 + lane_vec<P>(blk, u), combine<DIV>(y[u], x[u], a));
       continue;
     }
     for (int u = 0; u < U; ++u) {
-      const int64_t i = base + u * BS;
+      const int64_t i = lane_vec<P>(blk, u);
       if (i < nvec) d4[i] = combine<DIV>(d4[i], s4[i], a);
     }
   }
@@ -210,17 +243,17 @@ __global__ __launch_bounds__(P::BS) void ag_step_kernel(RankPtrs bufs, RingArgs 
 
   const VT* __restrict__ s4 = reinterpret_cast<const VT*>(src + head);
   VT* __restrict__ d4 = reinterpret_cast<VT*>(dst + head);
-  for (int64_t base = (int64_t)blockIdx.x * BS * U + threadIdx.x; base < nvec; base += gthreads * U) {
+  for (int64_t blk = (int64_t)blockIdx.x * BS * U; blk < nvec; blk += gthreads * U) {
     VT x[U];
-    if (base + (U - 1) * BS < nvec) {
+    if (blk + BS * U <= nvec) {
 #pragma unroll
-      for (int u = 0; u < U; ++u) x[u] = vload<P::NTL>(s4 + base + u * BS);
+      for (int u = 0; u < U; ++u) x[u] = vload<P::NTL>(s4 + lane_vec<P>(blk, u));
 #pragma unroll
-      for (int u = 0; u < U; ++u) vstore<P::NTS>(d4 + base + u * BS, x[u]);
+      for (int u = 0; u < U; ++u) vstore<P::NTS>(d4 + lane_vec<P>(blk, u), x[u]);
       continue;
     }
     for (int u = 0; u < U; ++u) {
-      const int64_t i = base + u * BS;
+      const int64_t i = lane_vec<P>(blk, u);
       if (i < nvec) d4[i] = s4[i];
     }
   }
@@ -281,11 +314,11 @@ __global__ __launch_bounds__(P::BS) void rs_step_c16_kernel(RankPtrs x, _Float16
   const f32x4* __restrict__ xr4 = reinterpret_cast<const f32x4*>(xr + head);
   const f16x8* __restrict__ ws8 = reinterpret_cast<const f16x8*>(ws + head);
   f16x8* __restrict__ wr8 = reinterpret_cast<f16x8*>(wr + head);
-  for (int64_t base = (int64_t)blockIdx.x * BS * U + threadIdx.x; base < nvec; base += gthreads * U) {
+  for (int64_t blk = (int64_t)blockIdx.x * BS * U; blk < nvec; blk += gthreads * U) {
     f16x8 sent[U], mine[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int64_t i = base + u * BS;
+      const int64_t i = lane_vec<P>(blk, u);
       if (i < nvec) {
         mine[u] = to_f16x8(vload<P::NTL>(xr4 + 2 * i), vload<P::NTL>(xr4 + 2 * i + 1));
         sent[u] = FIRST ? to_f16x8(vload<P::NTL>(xs4 + 2 * i), vload<P::NTL>(xs4 + 2 * i + 1))
@@ -294,7 +327,7 @@ __global__ __launch_bounds__(P::BS) void rs_step_c16_kernel(RankPtrs x, _Float16
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int64_t i = base + u * BS;
+      const int64_t i = lane_vec<P>(blk, u);
       if (i < nvec) vstore<P::NTS>(wr8 + i, combine<DIV>(mine[u], sent[u], a));
     }
   }
@@ -331,16 +364,16 @@ __global__ __launch_bounds__(P::BS) void ag_step_c16_kernel(RankPtrs x, _Float16
   f32x4* __restrict__ xr4 = reinterpret_cast<f32x4*>(xr + head);
   const f16x8* __restrict__ ws8 = reinterpret_cast<const f16x8*>(ws + head);
   f16x8* __restrict__ wr8 = reinterpret_cast<f16x8*>(wr + head);
-  for (int64_t base = (int64_t)blockIdx.x * BS * U + threadIdx.x; base < nvec; base += gthreads * U) {
+  for (int64_t blk = (int64_t)blockIdx.x * BS * U; blk < nvec; blk += gthreads * U) {
     f16x8 h[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int64_t i = base + u * BS;
+      const int64_t i = lane_vec<P>(blk, u);
       if (i < nvec) h[u] = vload<P::NTL>(ws8 + i);
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int64_t i = base + u * BS;
+      const int64_t i = lane_vec<P>(blk, u);
       if (i < nvec) {
         f32x4 lo, hi;
         from_f16x8(h[u], lo, hi);
@@ -394,11 +427,11 @@ __global__ __launch_bounds__(P::BS) void rs_ag_step_kernel(RankPtrs bufs, RingAr
   const VT* s4 = reinterpret_cast<const VT*>(src + head);
   VT* __restrict__ d4 = reinterpret_cast<VT*>(dst + head);
   VT* n4 = reinterpret_cast<VT*>(nxt + head);
-  for (int64_t base = (int64_t)blockIdx.x * BS * U + threadIdx.x; base < nvec; base += gthreads * U) {
+  for (int64_t blk = (int64_t)blockIdx.x * BS * U; blk < nvec; blk += gthreads * U) {
     VT x[U], y[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int64_t i = base + u * BS;
+      const int64_t i = lane_vec<P>(blk, u);
       if (i < nvec) {
         x[u] = vload<P::NTL>(s4 + i);
         y[u] = vload<P::NTL>(d4 + i);
@@ -406,7 +439,7 @@ __global__ __launch_bounds__(P::BS) void rs_ag_step_kernel(RankPtrs bufs, RingAr
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int64_t i = base + u * BS;
+      const int64_t i = lane_vec<P>(blk, u);
       if (i < nvec) {
         const VT v = combine<DIV>(y[u], x[u], a);
         vstore<P::NTS>(d4 + i, v);
@@ -452,11 +485,11 @@ __global__ __launch_bounds__(P::BS) void rs_ag_step_c16_kernel(RankPtrs x, _Floa
   f32x4* xn4 = reinterpret_cast<f32x4*>(xn + head);
   const f16x8* ws8 = reinterpret_cast<const f16x8*>(ws + head);
   f16x8* wn8 = reinterpret_cast<f16x8*>(wn + head);
-  for (int64_t base = (int64_t)blockIdx.x * BS * U + threadIdx.x; base < nvec; base += gthreads * U) {
+  for (int64_t blk = (int64_t)blockIdx.x * BS * U; blk < nvec; blk += gthreads * U) {
     f16x8 sent[U], mine[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int64_t i = base + u * BS;
+      const int64_t i = lane_vec<P>(blk, u);
       if (i < nvec) {
         mine[u] = to_f16x8(vload<P::NTL>(xo4 + 2 * i), vload<P::NTL>(xo4 + 2 * i + 1));
         sent[u] = FIRST ? to_f16x8(vload<P::NTL>(xs4 + 2 * i), vload<P::NTL>(xs4 + 2 * i + 1))
@@ -465,7 +498,7 @@ __global__ __launch_bounds__(P::BS) void rs_ag_step_c16_kernel(RankPtrs x, _Floa
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int64_t i = base + u * BS;
+      const int64_t i = lane_vec<P>(blk, u);
       if (i < nvec) {
         const f16x8 h = combine<DIV>(mine[u], sent[u], a);
         f32x4 lo, hi;
@@ -731,9 +764,9 @@ hipError_t launch_rs_ag_step(const RankPtrs& bufs, const RingArgs& a, int dtype,
   else if (divmode == DIV_POW2) { HVDX_RSAG_V(T, P, DIV_POW2); } \
   else { HVDX_RSAG_V(T, P, DIV_TRUE); }
   if (dtype == HVDX_FLOAT32) {
-    if (streams(a, 4)) { HVDX_RSAG_D(float, RsStream) } else { HVDX_RSAG_D(float, RsCached) }
+    if (streams(a, 4)) { HVDX_RSAG_D(float, RsAgStream) } else { HVDX_RSAG_D(float, RsAgCached) }
   } else {
-    if (streams(a, 2)) { HVDX_RSAG_D(_Float16, RsStream) } else { HVDX_RSAG_D(_Float16, RsCached) }
+    if (streams(a, 2)) { HVDX_RSAG_D(_Float16, RsAgStream) } else { HVDX_RSAG_D(_Float16, RsAgCached) }
   }
 #undef HVDX_RSAG_D
 #undef HVDX_RSAG_V
