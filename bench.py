@@ -59,16 +59,16 @@ def kernel_bytes(ar, kind, bi, step):
         return n * (es_b + es_t) * data
     compressed = b.direct and ar.compress
     if kind == "rs_ag":  # read owner and sender, write owner and the next rank
-        return 16 * b.count if compressed else 4 * (es_t if b.direct else es_b) * b.count
+        if compressed:  # binary32 owner, binary16 sender (binary32 when N = 2: its first touch)
+            return (16 if n == 2 else 14) * b.count
+        return 4 * (es_t if b.direct else es_b) * b.count
     if kind == "rs":
         if compressed:
             return (10 if step == 0 else 8) * b.count
         return 3 * es_b * b.count if not b.direct else 3 * es_t * b.count
     if kind == "ag":
-        if compressed:
-            first, last = step == 0, step == n - 2
-            per = 2 + 4 + (4 if first else 0) + (0 if last else 2)
-            return per * b.count
+        if compressed:  # step 0 widens the owner's binary16 into two buffers; later steps copy binary32
+            return (10 if step == 0 else 8) * b.count
         return 2 * es_b * b.count if not b.direct else 2 * es_t * b.count
     return 0
 

@@ -199,7 +199,9 @@ int hvdx_fuse_allreduce(void* const* tensors, const int64_t* numel, const int64_
  *   compress         HVDX_COMPRESS_NONE, or HVDX_COMPRESS_FP16 (dtype FLOAT32
  *                    only): values are rounded to binary16 when first sent,
  *                    added and averaged in binary16, and widened back into the
- *                    binary32 buffers by the replacing steps
+ *                    binary32 buffers by the replacing steps (the first one
+ *                    widens the owner's binary16 result; the later ones forward
+ *                    it as the binary32 value that holds it exactly)
  *   workspace        device memory of at least hvdx_ring_workspace_bytes(...)
  *                    bytes, 256-byte aligned, disjoint from bufs; only used with
  *                    compression (may be NULL otherwise); contents afterwards

@@ -153,7 +153,7 @@ using C16Cached = HVDX_C16_CACHED;
 #ifndef HVDX_C16_RS_STREAM
 #define HVDX_C16_RS_STREAM Policy<1, 64, true, true>
 #endif
-#ifndef HVDX_C16_AG_STREAM  // writes 3x what it reads: cached stores measured 1.4x faster
+#ifndef HVDX_C16_AG_STREAM  // replacing step 0 writes 4x what it reads: cached stores measured faster
 #define HVDX_C16_AG_STREAM Policy<2, 256, false, false>
 #endif
 using C16RsStream = HVDX_C16_RS_STREAM;
@@ -333,29 +333,31 @@ __global__ __launch_bounds__(P::BS) void rs_step_c16_kernel(RankPtrs x, _Float16
   }
 }
 
-template <bool FIRST, bool LAST, bool VEC_OK, typename P>
-__global__ __launch_bounds__(P::BS) void ag_step_c16_kernel(RankPtrs x, _Float16* wire, RingArgs a) {
+// Replacing step 0: the owner (c-1) of chunk c widens its binary16 result into its
+// own binary32 buffer and into rank c's.  The later replacing steps forward values
+// that are binary16 numbers held exactly in binary32, so they are plain binary32
+// copies (ag_step_kernel<float>): the same bits as narrowing, sending and widening
+// again, moved 4 bytes in and 4 out per element.
+template <bool VEC_OK, typename P>
+__global__ __launch_bounds__(P::BS) void ag_first_c16_kernel(RankPtrs x, const _Float16* wire, RingArgs a) {
   constexpr int BS = P::BS, U = P::U;
   const int c = blockIdx.y;
   const Chunk ch = chunk_of(c, a);
-  const int snd = ag_sender(c, a.step, a.n);
+  const int snd = ag_sender(c, 0, a.n);
   const int rcv = (snd + 1) % a.n;
   float* __restrict__ xs = static_cast<float*>(x.p[snd]) + ch.start;
   float* __restrict__ xr = static_cast<float*>(x.p[rcv]) + ch.start;
   const _Float16* __restrict__ ws = wire + (int64_t)snd * a.wire_stride + ch.start;
-  _Float16* __restrict__ wr = wire + (int64_t)rcv * a.wire_stride + ch.start;
 
-  const int64_t head = VEC_OK ? head_elems<_Float16>(wr, ch.len) : ch.len;
+  const int64_t head = VEC_OK ? head_elems<_Float16>(ws, ch.len) : ch.len;
   const int64_t nvec = (ch.len - head) / 8;
   const int64_t tail = head + nvec * 8;
   const int64_t gtid = (int64_t)blockIdx.x * BS + threadIdx.x;
   const int64_t gthreads = (int64_t)gridDim.x * BS;
   auto one = [&](int64_t e) {
-    const _Float16 h = ws[e];
-    const float f = (float)h;
-    if (FIRST) xs[e] = f;
+    const float f = (float)ws[e];
+    xs[e] = f;
     xr[e] = f;
-    if (!LAST) wr[e] = h;
   };
   for (int64_t e = gtid; e < head; e += gthreads) one(e);
   for (int64_t e = tail + gtid; e < ch.len; e += gthreads) one(e);
@@ -363,7 +365,6 @@ __global__ __launch_bounds__(P::BS) void ag_step_c16_kernel(RankPtrs x, _Float16
   f32x4* __restrict__ xs4 = reinterpret_cast<f32x4*>(xs + head);
   f32x4* __restrict__ xr4 = reinterpret_cast<f32x4*>(xr + head);
   const f16x8* __restrict__ ws8 = reinterpret_cast<const f16x8*>(ws + head);
-  f16x8* __restrict__ wr8 = reinterpret_cast<f16x8*>(wr + head);
   for (int64_t blk = (int64_t)blockIdx.x * BS * U; blk < nvec; blk += gthreads * U) {
     f16x8 h[U];
 #pragma unroll
@@ -377,13 +378,10 @@ __global__ __launch_bounds__(P::BS) void ag_step_c16_kernel(RankPtrs x, _Float16
       if (i < nvec) {
         f32x4 lo, hi;
         from_f16x8(h[u], lo, hi);
-        if (FIRST) {
-          vstore<P::NTS>(xs4 + 2 * i, lo);
-          vstore<P::NTS>(xs4 + 2 * i + 1, hi);
-        }
+        vstore<P::NTS>(xs4 + 2 * i, lo);
+        vstore<P::NTS>(xs4 + 2 * i + 1, hi);
         vstore<P::NTS>(xr4 + 2 * i, lo);
         vstore<P::NTS>(xr4 + 2 * i + 1, hi);
-        if (!LAST) vstore<P::NTS>(wr8 + i, h[u]);
       }
     }
   }
@@ -449,9 +447,10 @@ __global__ __launch_bounds__(P::BS) void rs_ag_step_kernel(RankPtrs bufs, RingAr
   }
 }
 
-// Compressed: the owner's wire copy is not read again, so only rank c's is written.
-template <int DIV, bool FIRST, bool LAST, bool VEC_OK, typename P>
-__global__ __launch_bounds__(P::BS) void rs_ag_step_c16_kernel(RankPtrs x, _Float16* wire, RingArgs a) {
+// Compressed: the finished binary16 sum goes, widened, to the owner's and rank c's
+// binary32 buffers; no wire copy is written (the replacing steps forward binary32).
+template <int DIV, bool FIRST, bool VEC_OK, typename P>
+__global__ __launch_bounds__(P::BS) void rs_ag_step_c16_kernel(RankPtrs x, const _Float16* wire, RingArgs a) {
   constexpr int BS = P::BS, U = P::U;
   const int c = blockIdx.y;
   const Chunk ch = chunk_of(c, a);
@@ -462,20 +461,17 @@ __global__ __launch_bounds__(P::BS) void rs_ag_step_c16_kernel(RankPtrs x, _Floa
   float* __restrict__ xo = static_cast<float*>(x.p[own]) + ch.start;
   float* xn = static_cast<float*>(x.p[c]) + ch.start;
   const _Float16* ws = wire + (int64_t)snd * a.wire_stride + ch.start;
-  _Float16* wn = wire + (int64_t)c * a.wire_stride + ch.start;
 
-  const int64_t head = VEC_OK ? head_elems<_Float16>(wn, ch.len) : ch.len;
+  const int64_t head = VEC_OK ? head_elems<_Float16>(ws, ch.len) : ch.len;
   const int64_t nvec = (ch.len - head) / 8;
   const int64_t tail = head + nvec * 8;
   const int64_t gtid = (int64_t)blockIdx.x * BS + threadIdx.x;
   const int64_t gthreads = (int64_t)gridDim.x * BS;
   auto one = [&](int64_t e) {
     const _Float16 sent = FIRST ? (_Float16)xs[e] : ws[e];
-    const _Float16 h = combine1<DIV>((_Float16)xo[e], sent, a);
-    const float f = (float)h;
+    const float f = (float)combine1<DIV>((_Float16)xo[e], sent, a);
     xo[e] = f;
     xn[e] = f;
-    if (!LAST) wn[e] = h;
   };
   for (int64_t e = gtid; e < head; e += gthreads) one(e);
   for (int64_t e = tail + gtid; e < ch.len; e += gthreads) one(e);
@@ -484,7 +480,6 @@ __global__ __launch_bounds__(P::BS) void rs_ag_step_c16_kernel(RankPtrs x, _Floa
   f32x4* __restrict__ xo4 = reinterpret_cast<f32x4*>(xo + head);
   f32x4* xn4 = reinterpret_cast<f32x4*>(xn + head);
   const f16x8* ws8 = reinterpret_cast<const f16x8*>(ws + head);
-  f16x8* wn8 = reinterpret_cast<f16x8*>(wn + head);
   for (int64_t blk = (int64_t)blockIdx.x * BS * U; blk < nvec; blk += gthreads * U) {
     f16x8 sent[U], mine[U];
 #pragma unroll
@@ -507,7 +502,6 @@ __global__ __launch_bounds__(P::BS) void rs_ag_step_c16_kernel(RankPtrs x, _Floa
         vstore<P::NTS>(xo4 + 2 * i + 1, hi);
         vstore<P::NTS>(xn4 + 2 * i, lo);
         vstore<P::NTS>(xn4 + 2 * i + 1, hi);
-        if (!LAST) vstore<P::NTS>(wn8 + i, h);
       }
     }
   }
@@ -695,24 +689,10 @@ void rs_c16_launch(const RankPtrs& x, _Float16* w, const RingArgs& a, int divmod
 }
 
 template <typename P>
-void ag_c16_launch(const RankPtrs& x, _Float16* w, const RingArgs& a, bool vector_ok, hipStream_t stream) {
+void ag_first_c16_launch(const RankPtrs& x, const _Float16* w, const RingArgs& a, bool vector_ok, hipStream_t stream) {
   const dim3 grid = step_grid(a, 8, P::U, P::BS);
-  const bool first = a.step == 0, last = a.step == a.n - 2;
-#define HVDX_AGC(F, L, VOK) \
-  hipLaunchKernelGGL((ag_step_c16_kernel<F, L, VOK, P>), grid, dim3(P::BS), 0, stream, x, w, a)
-#define HVDX_AGC_V(F, L) \
-  if (vector_ok) HVDX_AGC(F, L, true); else HVDX_AGC(F, L, false)
-  if (first && last) {
-    HVDX_AGC_V(true, true);
-  } else if (first) {
-    HVDX_AGC_V(true, false);
-  } else if (last) {
-    HVDX_AGC_V(false, true);
-  } else {
-    HVDX_AGC_V(false, false);
-  }
-#undef HVDX_AGC_V
-#undef HVDX_AGC
+  if (vector_ok) hipLaunchKernelGGL((ag_first_c16_kernel<true, P>), grid, dim3(P::BS), 0, stream, x, w, a);
+  else hipLaunchKernelGGL((ag_first_c16_kernel<false, P>), grid, dim3(P::BS), 0, stream, x, w, a);
 }
 
 }  // namespace
@@ -737,9 +717,10 @@ hipError_t launch_rs_step_c16(const RankPtrs& x, void* wire, const RingArgs& a, 
 }
 
 hipError_t launch_ag_step_c16(const RankPtrs& x, void* wire, const RingArgs& a, bool vector_ok, hipStream_t stream) {
-  _Float16* w = static_cast<_Float16*>(wire);
-  if (streams(a, 4)) ag_c16_launch<C16AgStream>(x, w, a, vector_ok, stream);
-  else ag_c16_launch<C16Cached>(x, w, a, vector_ok, stream);
+  if (a.step > 0) return ag_dispatch<float>(x, a, vector_ok, stream);  // binary16 values held in binary32
+  const _Float16* w = static_cast<const _Float16*>(wire);
+  if (streams(a, 4)) ag_first_c16_launch<C16AgStream>(x, w, a, vector_ok, stream);
+  else ag_first_c16_launch<C16Cached>(x, w, a, vector_ok, stream);
   return hipGetLastError();
 }
 
@@ -779,19 +760,19 @@ template <typename P>
 void rs_ag_c16_launch(const RankPtrs& x, _Float16* w, const RingArgs& a, int divmode, bool vector_ok,
                       hipStream_t stream) {
   const dim3 grid = step_grid(a, 8, P::U, P::BS);
-  const bool first = a.n == 2, last = a.n == 2;  // step N-2 is also the first adding step when N = 2
-#define HVDX_RAC(DIV, F, L, VOK) \
-  hipLaunchKernelGGL((rs_ag_step_c16_kernel<DIV, F, L, VOK, P>), grid, dim3(P::BS), 0, stream, x, w, a)
-#define HVDX_RAC_V(DIV, F, L) \
-  if (vector_ok) HVDX_RAC(DIV, F, L, true); else HVDX_RAC(DIV, F, L, false)
-#define HVDX_RAC_D(F, L) \
-  if (divmode == DIV_NONE) { HVDX_RAC_V(DIV_NONE, F, L); } \
-  else if (divmode == DIV_POW2) { HVDX_RAC_V(DIV_POW2, F, L); } \
-  else { HVDX_RAC_V(DIV_TRUE, F, L); }
-  if (first && last) {
-    HVDX_RAC_D(true, true)
+  const bool first = a.n == 2;  // step N-2 is also the first adding step when N = 2
+#define HVDX_RAC(DIV, F, VOK) \
+  hipLaunchKernelGGL((rs_ag_step_c16_kernel<DIV, F, VOK, P>), grid, dim3(P::BS), 0, stream, x, w, a)
+#define HVDX_RAC_V(DIV, F) \
+  if (vector_ok) HVDX_RAC(DIV, F, true); else HVDX_RAC(DIV, F, false)
+#define HVDX_RAC_D(F) \
+  if (divmode == DIV_NONE) { HVDX_RAC_V(DIV_NONE, F); } \
+  else if (divmode == DIV_POW2) { HVDX_RAC_V(DIV_POW2, F); } \
+  else { HVDX_RAC_V(DIV_TRUE, F); }
+  if (first) {
+    HVDX_RAC_D(true)
   } else {
-    HVDX_RAC_D(false, false)
+    HVDX_RAC_D(false)
   }
 #undef HVDX_RAC_D
 #undef HVDX_RAC_V
