@@ -143,7 +143,15 @@ struct Policy {
 #ifndef HVDX_C16_CACHED
 #define HVDX_C16_CACHED Policy<2, 256, false, false>
 #endif
+#ifndef HVDX_RS16_CACHED  // binary16 buffers (more elements per vector, shorter chunks)
+#define HVDX_RS16_CACHED HVDX_RS_CACHED
+#endif
+#ifndef HVDX_AG16_CACHED
+#define HVDX_AG16_CACHED HVDX_AG_CACHED
+#endif
 using RsCached = HVDX_RS_CACHED;
+using Rs16Cached = HVDX_RS16_CACHED;
+using Ag16Cached = HVDX_AG16_CACHED;
 using RsStream = HVDX_RS_STREAM;
 using AgCached = HVDX_AG_CACHED;
 using AgStream = HVDX_AG_STREAM;
@@ -166,6 +174,18 @@ __device__ __forceinline__ int64_t lane_vec(int64_t blk, int u) {
   if constexpr (P::WAVE) return blk + (int64_t)(threadIdx.x >> 6) * 64 * P::U + u * 64 + (threadIdx.x & 63);
   return blk + (int64_t)u * P::BS + threadIdx.x;
 }
+
+// The cached (working set fits the Infinity Cache) shapes per buffer type.
+template <typename T>
+struct CachedShape {
+  using rs = RsCached;
+  using ag = AgCached;
+};
+template <>
+struct CachedShape<_Float16> {
+  using rs = Rs16Cached;
+  using ag = Ag16Cached;
+};
 
 template <bool NT, typename V>
 __device__ __forceinline__ V vload(const V* p) {
@@ -645,7 +665,7 @@ void rs_launch(const RankPtrs& bufs, const RingArgs& a, int divmode, bool vec_ok
 template <typename T>
 hipError_t rs_dispatch(const RankPtrs& bufs, const RingArgs& a, int divmode, bool vec_ok, hipStream_t st) {
   if (streams(a, sizeof(T))) rs_launch<T, RsStream>(bufs, a, divmode, vec_ok, st);
-  else rs_launch<T, RsCached>(bufs, a, divmode, vec_ok, st);
+  else rs_launch<T, typename CachedShape<T>::rs>(bufs, a, divmode, vec_ok, st);
   return hipGetLastError();
 }
 
@@ -661,7 +681,7 @@ void ag_launch(const RankPtrs& bufs, const RingArgs& a, bool vec_ok, hipStream_t
 template <typename T>
 hipError_t ag_dispatch(const RankPtrs& bufs, const RingArgs& a, bool vec_ok, hipStream_t st) {
   if (streams(a, sizeof(T))) ag_launch<T, AgStream>(bufs, a, vec_ok, st);
-  else ag_launch<T, AgCached>(bufs, a, vec_ok, st);
+  else ag_launch<T, typename CachedShape<T>::ag>(bufs, a, vec_ok, st);
   return hipGetLastError();
 }
 
