@@ -327,17 +327,22 @@ def traffic_for(kernel, workload):
 
 
 def short_kernel_name(full):
-    """rocprofv3 kernel name -> the names bench.py reports."""
+    """rocprofv3 kernel name (demangled, or mangled where it holds binary16 template
+    arguments) -> the names bench.py reports."""
+    import re
+
     base = full.replace("(anonymous namespace)", "anon").split("(")[0]
     for key, short in (("rs_ag_step_c16_kernel", "rs_ag_step_c16"), ("rs_step_c16_kernel", "rs_step_c16"),
-                       ("ag_step_c16_kernel", "ag_step_c16"), ("roundtrip_c16_kernel", "ring"),
+                       ("ag_first_c16_kernel", "ag_first_c16"), ("roundtrip_c16_kernel", "ring"),
                        ("fold_kernel", "fold")):
         if key in base:
             return short
+    half = "<_Float16" in base or "IDF16_" in base
     for key in ("rs_ag_step_kernel", "rs_step_kernel", "ag_step_kernel"):
         if key in base:
-            return key.replace("_kernel", "") + ("_f16" if "<_Float16" in base else "_f32")
-    ring = base.rstrip().endswith(", true>")  # the copy kernels' last template argument: fused with a ring step
+            return key.replace("_kernel", "") + ("_f16" if half else "_f32")
+    # the copy kernels' last template argument: fused with a ring step
+    ring = base.rstrip().endswith(", true>") or re.search(r"Lb1EEEv", base) is not None
     if "unpack_kernel" in base:
         return "ag_unpack" if ring else "unpack"
     if "pack_kernel" in base:
@@ -345,55 +350,87 @@ def short_kernel_name(full):
     return None
 
 
+def shape_of(full):
+    """The launch-shape part of a kernel name (Policy<...> or CopyCfg<...>), for tables."""
+    import re
+
+    m = re.search(r"(Policy|CopyCfg)<[^>]*>", full)
+    if m:
+        return m.group(0).replace(" ", "")
+    m = re.search(r"(Policy|CopyCfg)I((?:L[ib]\d+E)+)E", full)  # mangled: PolicyILi1ELi64ELb1E...E
+    if m:
+        return m.group(1) + "<" + ",".join(x[2:] for x in re.findall(r"L[ib]\d+", m.group(2))) + ">"
+    return ""
+
+
 def summarize_profiles(d):
-    """Per-kernel average duration (kernel trace) and HBM bytes per dispatch (FETCH_SIZE,
-    WRITE_SIZE), each counter scaled by what it reads for a plain 1 GiB device copy."""
+    """Per-kernel durations (kernel trace, prof_<workload>/) and HBM bytes per dispatch
+    (FETCH_SIZE and WRITE_SIZE runs, pmc_fetch_<workload>/ and pmc_write_<workload>/),
+    each counter scaled by what it reads for a plain 1 GiB device copy in the same run.
+    Rows are per instantiation (launch shape); the counted bytes over the traced
+    average duration give the HBM rate each achieved.  Writes profiles/traffic.json
+    (per workload and reported kernel: counted bytes per launch, weighted by launches)."""
     import csv
     import glob
 
-    out_lines, traffic = [], {}
-    stats = sorted(glob.glob(os.path.join(d, "prof_*", "*_kernel_stats.csv")))
-    for f in stats:
+    out_lines, traffic, cal_used = [], {}, {}
+    trace = {}  # (workload, full name) -> (calls, total ns)
+    for f in sorted(glob.glob(os.path.join(d, "prof_*", "*_kernel_stats.csv"))):
         workload = os.path.basename(os.path.dirname(f))[len("prof_"):]
-        rows = list(csv.DictReader(open(f)))
-        out_lines.append(f"## kernel trace: {workload}\n")
-        out_lines.append("| kernel | instantiation | calls | average us | total ms |\n|---|---|---|---|---|")
-        for r in rows:
-            k = short_kernel_name(r["Name"])
-            if k:
-                name = r["Name"].replace("(anonymous namespace)::", "").split("(")[0].replace("void hvdx::", "")
-                out_lines.append(f"| {k} | `{name}` | {r['Calls']} | "
-                                 f"{float(r['AverageNs']) / 1e3:.2f} | {float(r['TotalDurationNs']) / 1e6:.2f} |")
+        for r in csv.DictReader(open(f)):
+            if short_kernel_name(r["Name"]):
+                trace[(workload, r["Name"])] = (int(r["Calls"]), float(r["TotalDurationNs"]))
+    workloads = sorted({w for w, _ in trace} | {os.path.basename(x)[len("pmc_fetch_"):]
+                                               for x in glob.glob(os.path.join(d, "pmc_fetch_*")) if os.path.isdir(x)})
+    for workload in workloads:
+        pmc = {}
+        for counter, sub in (("FETCH_SIZE", "pmc_fetch_"), ("WRITE_SIZE", "pmc_write_")):
+            files = glob.glob(os.path.join(d, sub + workload, "*_counter_collection.csv"))
+            if not files:
+                continue
+            rows = [r for r in csv.DictReader(open(files[0])) if r["Counter_Name"] == counter]
+            cal = [float(r["Counter_Value"]) for r in rows
+                   if "copyBuffer" in r["Kernel_Name"] and int(r["Grid_Size"]) >= (1 << 17)]
+            if not cal:
+                continue
+            factor = (1 << 20) / (sum(cal) / len(cal))  # a 1 GiB copy reads and writes 2^20 KiB
+            per = {}
+            for r in rows:
+                if short_kernel_name(r["Kernel_Name"]):
+                    per.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]) * factor * 1024)
+            pmc[counter] = (factor, {k: sum(v) / len(v) for k, v in per.items()})
+        names = sorted((n for w, n in trace if w == workload), key=lambda n: -trace[(workload, n)][1])
+        counted = len(pmc) == 2
+        if counted:
+            cal_used[workload] = {"FETCH_SIZE": pmc["FETCH_SIZE"][0], "WRITE_SIZE": pmc["WRITE_SIZE"][0]}
+        out_lines.append(f"## {workload}\n")
+        if counted:
+            out_lines.append(f"HBM bytes per dispatch from FETCH_SIZE x {pmc['FETCH_SIZE'][0]:.3f} and WRITE_SIZE x "
+                             f"{pmc['WRITE_SIZE'][0]:.3f} (the factors that make a plain 1 GiB device copy read "
+                             f"and write 1 GiB); counted rate = those bytes / the traced average duration.\n")
+        out_lines.append("| kernel | shape | calls | average us | total ms | fetch MB | write MB | counted GB/s "
+                         "| % of 8 TB/s |\n|---|---|---|---|---|---|---|---|---|")
+        per_short = {}
+        for n in names:
+            calls, tot_ns = trace[(workload, n)]
+            k, avg_us = short_kernel_name(n), tot_ns / calls / 1e3
+            cells = ["-", "-", "-", "-"]
+            if counted and n in pmc["FETCH_SIZE"][1]:
+                fb, wb = pmc["FETCH_SIZE"][1][n], pmc["WRITE_SIZE"][1].get(n, 0.0)
+                rate = (fb + wb) / (avg_us * 1e-6) / 1e9
+                cells = [f"{fb / 1e6:.1f}", f"{wb / 1e6:.1f}", f"{rate:.0f}", f"{rate / HBM_PEAK_GBS * 100:.1f}"]
+                acc = per_short.setdefault(k, [0.0, 0])
+                acc[0] += (fb + wb) * calls
+                acc[1] += calls
+            out_lines.append(f"| {k} | `{shape_of(n)}` | {calls} | {avg_us:.2f} | {tot_ns / 1e6:.2f} | "
+                             + " | ".join(cells) + " |")
         out_lines.append("")
-    pmc = {}
-    for counter, sub in (("FETCH_SIZE", "pmc_fetch"), ("WRITE_SIZE", "pmc_write")):
-        files = glob.glob(os.path.join(d, sub, "*_counter_collection.csv"))
-        if not files:
-            continue
-        rows = [r for r in csv.DictReader(open(files[0])) if r["Counter_Name"] == counter]
-        cal = [float(r["Counter_Value"]) for r in rows
-               if "copyBuffer" in r["Kernel_Name"] and int(r["Grid_Size"]) >= (1 << 17)]
-        if not cal:
-            continue
-        factor = (1 << 20) / (sum(cal) / len(cal))  # a 1 GiB copy reads and writes 2^20 KiB
-        per = {}
-        for r in rows:
-            k = short_kernel_name(r["Kernel_Name"])
-            if k:
-                per.setdefault(k, []).append(float(r["Counter_Value"]) * factor * 1024)
-        pmc[counter] = (factor, {k: sum(v) / len(v) for k, v in per.items()})
-    if len(pmc) == 2:
-        (ff, fetch), (fw, write) = pmc["FETCH_SIZE"], pmc["WRITE_SIZE"]
-        out_lines.append("## HBM traffic per dispatch (resnet50 workload)\n")
-        out_lines.append(f"calibration: a 1 GiB device copy reads FETCH_SIZE x {ff:.3f} and WRITE_SIZE x {fw:.3f}\n")
-        out_lines.append("| kernel | fetch MB | write MB | total MB |\n|---|---|---|---|")
-        for k in sorted(fetch):
-            tot = fetch[k] + write.get(k, 0.0)
-            traffic[f"resnet50/{k}"] = round(tot)
-            out_lines.append(f"| {k} | {fetch[k] / 1e6:.1f} | {write.get(k, 0.0) / 1e6:.1f} | {tot / 1e6:.1f} |")
+        for k, (b, c) in per_short.items():
+            traffic[f"{workload}/{k}"] = round(b / c)
+    if traffic:
         with open(TRAFFIC_FILE, "w") as f:
-            json.dump({"source_hash": kernel_source_hash(), "per_launch_bytes": traffic,
-                       "calibration": {"FETCH_SIZE": ff, "WRITE_SIZE": fw}}, f, indent=1)
+            json.dump({"source_hash": kernel_source_hash(), "per_launch_bytes": traffic, "calibration": cal_used},
+                      f, indent=1)
     return "\n".join(out_lines)
 
 
