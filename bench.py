@@ -307,10 +307,18 @@ def measure_broadcast(name, steps, warmup=2):
 
 
 def kernel_source_hash():
+    """Hash of the kernel sources' code, with // comments and blank lines dropped, so
+    the counter traffic recorded in profiles/traffic.json is tied to the code it was
+    measured on and not to the wording of its comments."""
     h = hashlib.sha256()
-    for f in sorted(os.listdir(os.path.join(ROOT, "paper_1802_05799_amd", "csrc"))):
-        with open(os.path.join(ROOT, "paper_1802_05799_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+    d = os.path.join(ROOT, "paper_1802_05799_amd", "csrc")
+    for f in sorted(os.listdir(d)):
+        h.update(f.encode() + b"\n")
+        with open(os.path.join(d, f)) as fh:
+            for line in fh:
+                code = line.split("//")[0].rstrip()
+                if code:
+                    h.update(code.encode() + b"\n")
     return h.hexdigest()[:16]
 
 

@@ -284,9 +284,9 @@ __global__ __launch_bounds__(P::BS) void ag_step_kernel(RankPtrs bufs, RingArgs 
 // Rank r's binary16 wire copy lives at wire + r * wire_stride.  In adding step s the
 // receiver rounds its own binary32 value to binary16 and adds the sender's binary16
 // partial (at s = 0 the sender's own value, rounded on first touch); the sum goes to
-// the receiver's wire copy.  In replacing step s the receiver takes the sender's wire
-// value and stores it widened into its binary32 buffer (and on its wire, unless
-// nobody forwards it again); at s = 0 the owner also widens its own result.
+// the receiver's wire copy.  Replacing step 0 widens the owner's binary16 result into
+// its own and the receiver's binary32 buffers; every later replacing step forwards a
+// binary16 number already held exactly in binary32, so it is the plain binary32 copy.
 
 __device__ __forceinline__ f16x8 to_f16x8(f32x4 lo, f32x4 hi) {
   f16x8 h;
