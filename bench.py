@@ -55,6 +55,10 @@ def kernel_bytes(ar, kind, bi, step):
     data = sum(ar.numel[t] for t in b.tensors)
     if kind in ("pack", "pack_rs"):  # the fused adding step reuses the values it packs
         return n * (es_t * data + es_b * b.count)
+    if kind in ("cycle_small", "ring_small"):  # every step's messages, as the per-step kernels count them
+        es = es_t if b.direct else es_b
+        ring = (n - 1) * 5 * es * b.count
+        return ring if b.direct else ring + n * (es_t * data + es_b * b.count) + n * (es_b + es_t) * data
     if kind in ("unpack", "ag_unpack"):  # the fused replacing step only changes which buffer is read
         return n * (es_b + es_t) * data
     compressed = b.direct and ar.compress
@@ -74,7 +78,7 @@ def kernel_bytes(ar, kind, bi, step):
 
 
 KIND_OF_CODE = {0: "pack", 1: "rs", 2: "ag", 3: "unpack", 4: "ring", 6: "rs_ag", 7: "fold", 8: "pack_rs",
-                9: "ag_unpack"}
+                9: "ag_unpack", 10: "ring_small", 11: "cycle_small"}
 
 
 def phase_sequence(ar):
@@ -84,6 +88,12 @@ def phase_sequence(ar):
     n = ar.nranks
     for bi, b in enumerate(ar.buckets):
         if b.count == 0:
+            continue
+        if b.small:
+            if not b.direct:
+                out.append((11, bi, -1, 1))
+            elif n > 1:
+                out.append((10, bi, -1, 1))
             continue
         if ar.fuse_boundary and not b.direct and n >= 3:
             out.append((8, bi, 0, 1))
@@ -112,6 +122,8 @@ def phase_sequence(ar):
 
 def kernel_name(ar, kind, bi):
     b = ar.buckets[bi]
+    if kind in ("cycle_small", "ring_small"):
+        return kind
     if kind in ("rs", "ag", "rs_ag"):
         if b.direct and ar.compress:
             return f"{kind}_step_c16"
@@ -346,6 +358,10 @@ def short_kernel_name(full):
         if key in base:
             return short
     half = "<_Float16" in base or "IDF16_" in base
+    if "small_cycle_kernel" in base:
+        return "cycle_small"
+    if "chain_kernel" in base:
+        return "ring_small"
     for key in ("rs_ag_step_kernel", "rs_step_kernel", "ag_step_kernel"):
         if key in base:
             return key.replace("_kernel", "") + ("_f16" if half else "_f32")

@@ -186,6 +186,29 @@ int hvdx_fuse_allreduce(void* const* tensors, const int64_t* numel, const int64_
                         void* stream);
 
 /*
+ * hvdx_fuse_allreduce_small -- hvdx_fuse_allreduce for small fusion buffers: the same
+ * result, bit for bit, in one kernel launch instead of 2N-1.  Each thread takes a
+ * 16-byte stretch of the buffer (element by element where it meets a tensor edge)
+ * through the copy-in for every rank (paper section 7, step 3), all 2(N-1) steps of
+ * the ring of paper section 3 in their order -- each step reading the sender's
+ * buffer and writing the receiver's -- and the copy-out (step 5).  An element's ring
+ * never involves another element, so its steps need not wait for the rest of the
+ * buffer.  Intended for buffers of at most HVDX_SMALL_BUCKET_BYTES per rank, where
+ * the per-step launches cost more than their data; any size works.
+ * Arguments, ownership and errors as hvdx_fuse_allreduce (any nranks >= 1); the
+ * fusion buffers are scratch afterwards (padding is not written).
+ */
+int hvdx_fuse_allreduce_small(void* const* tensors, const int64_t* numel, const int64_t* offset, int ntensors,
+                              int tensor_dtype, void* const* bufs, int64_t buf_count, int buf_dtype, int nranks,
+                              int op, void* stream);
+
+/* Per-rank buffer bytes at or below which a fusion buffer's (or a tensor's) whole ring
+ * costs less in one launch (hvdx_fuse_allreduce_small, hvdx_ring_allreduce_small) than
+ * in one launch per step on MI355X: below it a step's messages take less time than
+ * launching the step.  A recommendation for callers; the library does not switch. */
+#define HVDX_SMALL_BUCKET_BYTES (4 << 20)
+
+/*
  * hvdx_ring_allreduce -- the ring-allreduce of paper section 3: N-1 steps in which
  * every rank adds the chunk received from its left neighbour into its own buffer,
  * then N-1 steps in which the received chunk replaces its own.  In place on all
@@ -218,6 +241,17 @@ int hvdx_fuse_allreduce(void* const* tensors, const int64_t* numel, const int64_
  */
 int hvdx_ring_allreduce(void* const* bufs, int nranks, int64_t count, int dtype, int op, int compress,
                         void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * hvdx_ring_allreduce_small -- hvdx_ring_allreduce without compression, in one
+ * launch: each thread runs all 2(N-1) steps (same schedule, same order of additions,
+ * each step reading the sender's buffer and writing the receiver's) for one 16-byte
+ * vector of every rank buffer, or element by element where a vector crosses a chunk
+ * edge or a buffer is not 16-byte aligned.  Same result, bit for bit.  Intended for
+ * buffers of at most HVDX_SMALL_BUCKET_BYTES; any size works.
+ * Arguments and errors as hvdx_ring_allreduce with compress = HVDX_COMPRESS_NONE.
+ */
+int hvdx_ring_allreduce_small(void* const* bufs, int nranks, int64_t count, int dtype, int op, void* stream);
 
 /*
  * hvdx_ring_reduce_scatter / hvdx_ring_allgather -- the two halves of
@@ -320,6 +354,8 @@ int hvdx_ring_chunk(int64_t count, int nranks, int c, int64_t* start, int64_t* l
 #define HVDX_KERNEL_FOLD 7      /* hvdx_fold_allreduce */
 #define HVDX_KERNEL_PACK_RS 8   /* copy-in with adding step 0 (step = 0) */
 #define HVDX_KERNEL_AG_UNPACK 9 /* replacing step N-2 with copy-out (step = N-2) */
+#define HVDX_KERNEL_RING_SMALL 10  /* hvdx_ring_allreduce_small: every step in one launch */
+#define HVDX_KERNEL_CYCLE_SMALL 11 /* hvdx_fuse_allreduce_small: copy-in, ring, copy-out in one launch */
 
 typedef struct hvdx_trace_record {
   int32_t kind;     /* HVDX_KERNEL_* */

@@ -27,6 +27,7 @@ from ._lib import (  # noqa: F401
     OK,
     PHASE_ALLGATHER,
     PHASE_REDUCE_SCATTER,
+    SMALL_BUCKET_BYTES,
     SUM,
     HvdxError,
     hvdx_broadcast,
@@ -34,6 +35,7 @@ from ._lib import (  # noqa: F401
     hvdx_fold_allreduce,
     hvdx_fuse_ag_unpack,
     hvdx_fuse_allreduce,
+    hvdx_fuse_allreduce_small,
     hvdx_fuse_pack,
     hvdx_fuse_pack_rs,
     hvdx_fuse_plan,
@@ -41,6 +43,7 @@ from ._lib import (  # noqa: F401
     hvdx_last_error,
     hvdx_ring_allgather,
     hvdx_ring_allreduce,
+    hvdx_ring_allreduce_small,
     hvdx_ring_chunk,
     hvdx_ring_reduce_scatter,
     hvdx_ring_step,

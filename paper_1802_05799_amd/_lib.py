@@ -21,6 +21,7 @@ OK, ERR_INVALID, ERR_ALIAS, ERR_WORKSPACE, ERR_HIP, ERR_UNSUPPORTED = 0, -1, -2,
 MAX_RANKS = 128
 DEFAULT_FUSION_THRESHOLD = 64 << 20
 DEFAULT_FUSION_ALIGN = 16
+SMALL_BUCKET_BYTES = 4 << 20  # HVDX_SMALL_BUCKET_BYTES
 
 _p = ctypes.c_void_p
 _i = ctypes.c_int
@@ -37,7 +38,9 @@ _SIGNATURES = {
     "hvdx_fuse_pack_rs": (_i, [_p, _p, _p, _i, _i, _pp, _i64, _i, _i, _p]),
     "hvdx_fuse_ag_unpack": (_i, [_pp, _i64, _i, _p, _p, _p, _i, _i, _i, _p]),
     "hvdx_fuse_allreduce": (_i, [_p, _p, _p, _i, _i, _pp, _i64, _i, _i, _i, _p]),
+    "hvdx_fuse_allreduce_small": (_i, [_p, _p, _p, _i, _i, _pp, _i64, _i, _i, _i, _p]),
     "hvdx_ring_allreduce": (_i, [_pp, _i, _i64, _i, _i, _i, _p, _sz, _p]),
+    "hvdx_ring_allreduce_small": (_i, [_pp, _i, _i64, _i, _i, _p]),
     "hvdx_ring_step": (_i, [_pp, _i, _i64, _i, _i, _i, _i, _i, _p, _sz, _p]),
     "hvdx_ring_reduce_scatter": (_i, [_pp, _i, _i64, _i, _i, _i, _p, _sz, _p]),
     "hvdx_ring_allgather": (_i, [_pp, _i, _i64, _i, _i, _i, _p, _sz, _p]),
@@ -56,6 +59,7 @@ _SIGNATURES = {
 KERNEL_PACK, KERNEL_REDUCE_SCATTER, KERNEL_ALLGATHER, KERNEL_UNPACK, KERNEL_ROUNDTRIP = 0, 1, 2, 3, 4
 KERNEL_BROADCAST, KERNEL_RS_AG, KERNEL_FOLD = 5, 6, 7
 KERNEL_PACK_RS, KERNEL_AG_UNPACK = 8, 9
+KERNEL_RING_SMALL, KERNEL_CYCLE_SMALL = 10, 11
 
 
 class TraceRecord(ctypes.Structure):
@@ -178,6 +182,18 @@ def hvdx_fuse_allreduce(tensors_dev: int, numel_dev: int, offset_dev: int, ntens
     pb, _keep = _ptr_array(bufs)
     _check(lib.hvdx_fuse_allreduce(tensors_dev, numel_dev, offset_dev, ntensors, tensor_dtype, pb, buf_count,
                                    buf_dtype, nranks, op, stream))
+
+
+def hvdx_fuse_allreduce_small(tensors_dev: int, numel_dev: int, offset_dev: int, ntensors: int, tensor_dtype: int,
+                              bufs, buf_count: int, buf_dtype: int, nranks: int, op: int, stream: int = 0) -> None:
+    pb, _keep = _ptr_array(bufs)
+    _check(lib.hvdx_fuse_allreduce_small(tensors_dev, numel_dev, offset_dev, ntensors, tensor_dtype, pb, buf_count,
+                                         buf_dtype, nranks, op, stream))
+
+
+def hvdx_ring_allreduce_small(bufs, nranks: int, count: int, dtype: int, op: int, stream: int = 0) -> None:
+    pb, _keep = _ptr_array(bufs)
+    _check(lib.hvdx_ring_allreduce_small(pb, nranks, count, dtype, op, stream))
 
 
 def hvdx_ring_allreduce(bufs, nranks: int, count: int, dtype: int, op: int, compress: int = COMPRESS_NONE,

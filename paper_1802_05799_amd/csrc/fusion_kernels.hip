@@ -12,7 +12,7 @@
 // per-element path.  Padding is written as zero by the copy-in and skipped by the
 // copy-out.
 
-#include "internal.hpp"
+#include "ring_math.hpp"
 
 namespace hvdx {
 namespace {
@@ -579,6 +579,64 @@ __global__ __launch_bounds__(kBlock) HVDX_COPY_ATTR void unpack_kernel(RankPtrs 
   }
 }
 
+// ---- a small fusion buffer's whole cycle in one launch ------------------------------
+//
+// For buffers so small that launches cost more than their data: each thread takes one
+// 16-byte buffer vector through the copy-in for every rank, all 2(N-1) ring steps
+// (ring_chain: each step reads the sender's buffer and writes the receiver's) and the
+// copy-out for every rank.  Vectors of padding only are skipped (their values never
+// reach a tensor and the buffers are scratch afterwards); edge vectors go element by
+// element.  A block serves one tile of 256 vectors for all ranks.
+using SmallCfg = CopyCfg<1, 1, 0, false, false>;
+
+template <typename TT, typename TB, int DIV>
+__global__ __launch_bounds__(kBlock) void small_cycle_kernel(const void* const* __restrict__ tensors,
+                                                             const int64_t* __restrict__ numel,
+                                                             const int64_t* __restrict__ offset, int ntensors,
+                                                             RankPtrs bufs, RingArgs a, int64_t count) {
+  using Cfg = SmallCfg;
+  using M = Mover<TT, TB>;
+  using VB = typename M::buf_vec;
+  constexpr int V = BufVec<TB>::n;
+  __shared__ int64_t s_off[Cfg::kLdsTensors], s_end[Cfg::kLdsTensors], s_meta[2];
+  __shared__ const void* s_ptr[kLdsPtrs];
+  const int n = a.n;
+  const int64_t p0 = (int64_t)blockIdx.x * Cfg::kTileVecs * V;
+  const int64_t p1 = p0 + (int64_t)Cfg::kTileVecs * V < count ? p0 + (int64_t)Cfg::kTileVecs * V : count;
+  if (p0 >= p1) return;
+  bool pin;
+  const TileTable tt = stage_tile<Cfg::kLdsTensors>(offset, numel, ntensors, p0, p1, tensors, 0, n, 0, n, s_off,
+                                                    s_end, s_meta, s_ptr, &pin);
+  const PtrTable pt{tensors, pin ? s_ptr : nullptr, tt.t0, ntensors, tt.nt, 0, 0, n};
+  const Pos ps = classify<V>(tt, s_off, s_end, offset, numel, p0 + (int64_t)threadIdx.x * V, p1, 0, count);
+  auto buf = [&](int r) { return static_cast<TB*>(bufs.p[r]); };
+  auto ten = [&](int r, int64_t t) { return static_cast<TT*>(const_cast<void*>(pt.get(r, t))); };
+  if (ps.cls == POS_VEC) {
+    for (int r = 0; r < n; ++r)
+      st16<false>(reinterpret_cast<VB*>(buf(r) + ps.p), M::template load<false>(ten(r, ps.t) + ps.li));
+    const int64_t c0 = chunk_index(ps.p, a);
+    if (chunk_index(ps.p + V - 1, a) == c0) {
+      ring_chain<TB, VB, DIV>(bufs, ps.p, (int)c0, a);
+    } else {
+      for (int k = 0; k < V; ++k) ring_chain<TB, TB, DIV>(bufs, ps.p + k, (int)chunk_index(ps.p + k, a), a);
+    }
+    for (int r = 0; r < n; ++r)
+      M::template store<false>(ten(r, ps.t) + ps.li, *reinterpret_cast<const VB*>(buf(r) + ps.p));
+  } else if (ps.cls == POS_EDGE) {
+    for (int k = 0; k < V; ++k) {
+      const int64_t pe = ps.p + k;
+      if (pe >= count) break;
+      const int jk = lookup(tt, s_off, offset, pe);
+      const int64_t tk = tt.t0 + jk;
+      if (tk < 0 || pe >= tensor_end(tt, s_end, offset, numel, jk)) continue;  // padding
+      const int64_t li = pe - tensor_begin(tt, s_off, offset, jk);
+      for (int r = 0; r < n; ++r) buf(r)[pe] = M::cvt_in(ten(r, tk)[li]);
+      ring_chain<TB, TB, DIV>(bufs, pe, (int)chunk_index(pe, a), a);
+      for (int r = 0; r < n; ++r) ten(r, tk)[li] = M::cvt_out(buf(r)[pe]);
+    }
+  }
+}
+
 template <typename Cfg>
 unsigned tiles_for(int64_t count, int buf_dtype) {
   const int64_t v = buf_dtype == HVDX_FLOAT32 ? 4 : 8;
@@ -649,6 +707,29 @@ hipError_t launch_pack(const void* const* srcs, const int64_t* numel, const int6
     else
       pack_with<Pack16Cfg, false>(srcs, numel, offset, ntensors, src_dtype, bufs, count, buf_dtype, nranks, stream);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_small_cycle(const void* const* tensors, const int64_t* numel, const int64_t* offset, int ntensors,
+                              int tensor_dtype, const RankPtrs& bufs, const RingArgs& a, int64_t count, int buf_dtype,
+                              int divmode, hipStream_t stream) {
+  const dim3 grid(tiles_for<SmallCfg>(count, buf_dtype)), block(kBlock);
+#define HVDX_SMALL(TT, TB, DIV) \
+  hipLaunchKernelGGL((small_cycle_kernel<TT, TB, DIV>), grid, block, 0, stream, tensors, numel, offset, ntensors, \
+                     bufs, a, count)
+#define HVDX_SMALL_D(TT, TB) \
+  if (divmode == DIV_NONE) { HVDX_SMALL(TT, TB, DIV_NONE); } \
+  else if (divmode == DIV_POW2) { HVDX_SMALL(TT, TB, DIV_POW2); } \
+  else { HVDX_SMALL(TT, TB, DIV_TRUE); }
+  if (tensor_dtype == HVDX_FLOAT32 && buf_dtype == HVDX_FLOAT32) {
+    HVDX_SMALL_D(float, float)
+  } else if (tensor_dtype == HVDX_FLOAT32) {
+    HVDX_SMALL_D(float, _Float16)
+  } else {
+    HVDX_SMALL_D(_Float16, _Float16)
+  }
+#undef HVDX_SMALL_D
+#undef HVDX_SMALL
   return hipGetLastError();
 }
 

@@ -582,6 +582,38 @@ int hvdx_fuse_allreduce(void* const* tensors, const int64_t* numel, const int64_
   return run_ag_unpack(bufs, buf_count, buf_dtype, tensors, numel, offset, ntensors, tensor_dtype, nranks, st);
 }
 
+int hvdx_fuse_allreduce_small(void* const* tensors, const int64_t* numel, const int64_t* offset, int ntensors,
+                              int tensor_dtype, void* const* bufs, int64_t buf_count, int buf_dtype, int nranks,
+                              int op, void* stream) {
+  int rc = check_fusion(tensors, numel, offset, ntensors, tensor_dtype, bufs, buf_count, buf_dtype, nranks,
+                        "hvdx_fuse_allreduce_small");
+  if (rc) return rc;
+  if (op != HVDX_SUM && op != HVDX_AVERAGE)
+    return fail(HVDX_ERR_INVALID, "hvdx_fuse_allreduce_small: unknown op %d", op);
+  if (buf_count == 0) return HVDX_OK;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  TimedLaunch timed(HVDX_KERNEL_CYCLE_SMALL, -1, nranks, buf_dtype, HVDX_COMPRESS_NONE, buf_count, st);
+  TimedLaunch timed_phase(HVDX_KERNEL_CYCLE_SMALL, -1, nranks, buf_dtype, HVDX_COMPRESS_NONE, buf_count, st, -1,
+                          true);
+  const hipError_t e =
+      hvdx::launch_small_cycle(const_cast<const void* const*>(tensors), numel, offset, ntensors, tensor_dtype,
+                               rank_ptrs(bufs, nranks), ring_args(nranks, buf_count, 0), buf_count, buf_dtype,
+                               div_mode(op, nranks), st);
+  return e == hipSuccess ? HVDX_OK : hip_fail(e, "small cycle launch");
+}
+
+int hvdx_ring_allreduce_small(void* const* bufs, int nranks, int64_t count, int dtype, int op, void* stream) {
+  int rc = check_ring(bufs, nranks, count, dtype, op, HVDX_COMPRESS_NONE, nullptr, 0, "hvdx_ring_allreduce_small");
+  if (rc) return rc;
+  if (count == 0 || nranks == 1) return HVDX_OK;  // no messages; AVERAGE divides by 1
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  TimedLaunch timed(HVDX_KERNEL_RING_SMALL, -1, nranks, dtype, HVDX_COMPRESS_NONE, count, st);
+  TimedLaunch timed_phase(HVDX_KERNEL_RING_SMALL, -1, nranks, dtype, HVDX_COMPRESS_NONE, count, st, -1, true);
+  const hipError_t e = hvdx::launch_chain(rank_ptrs(bufs, nranks), ring_args(nranks, count, 0), count, dtype,
+                                          div_mode(op, nranks), vectors_ok(bufs, nranks, nullptr), st);
+  return e == hipSuccess ? HVDX_OK : hip_fail(e, "small ring launch");
+}
+
 int hvdx_fold_allreduce(void* const* bufs, int nranks, int64_t count, int dtype, int op, int compress,
                         void* stream) {
   int rc = check_ring(bufs, nranks, count, dtype, op, HVDX_COMPRESS_NONE, nullptr, 0, "hvdx_fold_allreduce");

@@ -43,6 +43,13 @@ hipError_t launch_rs_ag_step(const RankPtrs& bufs, const RingArgs& a, int dtype,
                              hipStream_t stream);
 hipError_t launch_rs_ag_step_c16(const RankPtrs& x, void* wire, const RingArgs& a, int divmode, bool vector_ok,
                                  hipStream_t stream);
+// A small ring in one launch: each thread runs every step for its elements.
+hipError_t launch_chain(const RankPtrs& bufs, const RingArgs& a, int64_t count, int dtype, int divmode,
+                        bool vector_ok, hipStream_t stream);
+// A small fusion buffer's copy-in, ring and copy-out in one launch.
+hipError_t launch_small_cycle(const void* const* tensors, const int64_t* numel, const int64_t* offset, int ntensors,
+                              int tensor_dtype, const RankPtrs& bufs, const RingArgs& a, int64_t count, int buf_dtype,
+                              int divmode, hipStream_t stream);
 // The ring's per-element fold in one pass (same bits, no per-step messages).
 hipError_t launch_fold(const RankPtrs& bufs, const RingArgs& a, int64_t count, int dtype, int compress, int divmode,
                        bool vector_ok, hipStream_t stream);

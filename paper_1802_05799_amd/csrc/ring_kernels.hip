@@ -14,95 +14,10 @@
 // finished sum once, by multiplying with 1/N when N is a power of two (exact
 // scaling, same result) and by a correctly rounded division otherwise.
 
-#include "internal.hpp"
+#include "ring_math.hpp"
 
 namespace hvdx {
 namespace {
-
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
-
-template <typename T>
-struct Vec;
-template <>
-struct Vec<float> {
-  using type = f32x4;
-  static constexpr int n = 4;
-};
-template <>
-struct Vec<_Float16> {
-  using type = f16x8;
-  static constexpr int n = 8;
-};
-
-
-template <int DIV>
-__device__ __forceinline__ float finish(float v, const RingArgs& a) {
-  if constexpr (DIV == DIV_POW2) return v * a.inv;
-  if constexpr (DIV == DIV_TRUE) return v / a.nf;
-  return v;
-}
-
-// binary16 finish: scaling by 1/N = 2^-k is done in binary16 itself (one rounding of
-// the exact product, the same bits as through binary32); going through binary32
-// lets the compiler select v_fma_mix with a +0 addend, which turns -0 into +0.
-template <int DIV>
-__device__ __forceinline__ _Float16 finish16(_Float16 v, const RingArgs& a) {
-  if constexpr (DIV == DIV_POW2) return v * (_Float16)a.inv;
-  if constexpr (DIV == DIV_TRUE) return (_Float16)((float)v / a.nf);
-  return v;
-}
-
-// receiver's value + sender's value, and the AVERAGE divide when DIV says so
-template <int DIV>
-__device__ __forceinline__ float combine1(float local, float recv, const RingArgs& a) {
-  return finish<DIV>(local + recv, a);
-}
-template <int DIV>
-__device__ __forceinline__ _Float16 combine1(_Float16 local, _Float16 recv, const RingArgs& a) {
-  return finish16<DIV>(local + recv, a);
-}
-template <int DIV>
-__device__ __forceinline__ f32x4 combine(f32x4 local, f32x4 recv, const RingArgs& a) {
-  f32x4 s = local + recv;
-  if constexpr (DIV != DIV_NONE) {
-#pragma unroll
-    for (int k = 0; k < 4; ++k) s[k] = finish<DIV>(s[k], a);
-  }
-  return s;
-}
-template <int DIV>
-__device__ __forceinline__ f16x8 combine(f16x8 local, f16x8 recv, const RingArgs& a) {
-  f16x8 s = local + recv;
-  if constexpr (DIV == DIV_POW2) s = s * (f16x8)((_Float16)a.inv);
-  if constexpr (DIV == DIV_TRUE) {
-#pragma unroll
-    for (int k = 0; k < 8; ++k) s[k] = finish16<DIV>(s[k], a);
-  }
-  return s;
-}
-
-struct Chunk {
-  int64_t start, len;
-};
-
-__device__ __forceinline__ Chunk chunk_of(int c, const RingArgs& a) {
-  const int64_t cc = c;
-  return {cc * a.q + (cc < a.rem ? cc : a.rem), a.q + (cc < a.rem ? 1 : 0)};
-}
-
-// Sender of chunk c in adding step s and in replacing step s (both mod n); the
-// receiver is the next rank on the ring.
-__device__ __forceinline__ int rs_sender(int c, int s, int n) { return (c + s) % n; }
-__device__ __forceinline__ int ag_sender(int c, int s, int n) { return (c + s + n - 1) % n; }
-
-// Elements [0, head) of a chunk precede its first 16-byte boundary.
-template <typename T>
-__device__ __forceinline__ int64_t head_elems(const void* p, int64_t len) {
-  const uintptr_t mis = reinterpret_cast<uintptr_t>(p) & 15;
-  const int64_t h = mis ? (int64_t)((16 - mis) / sizeof(T)) : 0;
-  return h < len ? h : len;
-}
 
 // ---- launch policies ---------------------------------------------------------------
 //
@@ -536,10 +451,6 @@ __global__ __launch_bounds__(P::BS) void rs_ag_step_c16_kernel(RankPtrs x, const
 // instead of the ring's 5(N-1), with identical bits, but without the per-step
 // messages of a real ring.
 
-__device__ __forceinline__ int64_t chunk_index(int64_t e, const RingArgs& a) {
-  const int64_t big = a.rem * (a.q + 1);  // elements in the first rem (longer) chunks
-  return e < big ? e / (a.q + 1) : a.rem + (e - big) / a.q;
-}
 
 template <typename T, bool COMP>
 struct FoldTypes;
@@ -622,6 +533,29 @@ __global__ __launch_bounds__(kBlock) void fold_kernel(RankPtrs bufs, RingArgs a,
       acc = fold_finish<DIV>(acc, a);
       for (int r = 0; r < n; ++r) static_cast<T*>(bufs.p[r])[e] = F::out(acc);
     }
+  }
+}
+
+// ---- a small ring in one launch ----------------------------------------------------
+//
+// For buffers so small that each step's launch costs more than its messages: one
+// thread runs all 2(N-1) steps for one 16-byte vector (or, where a vector crosses a
+// chunk edge or the buffers are not 16-byte aligned, for each of its elements), each
+// step still reading the sender's buffer and writing the receiver's in memory.
+
+template <typename T, int DIV, bool VEC_OK>
+__global__ __launch_bounds__(kBlock) void chain_kernel(RankPtrs bufs, RingArgs a, int64_t count) {
+  using VT = typename Vec<T>::type;
+  constexpr int V = Vec<T>::n;
+  const int64_t nv = (count + V - 1) / V;
+  for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < nv; i += (int64_t)gridDim.x * kBlock) {
+    const int64_t e0 = i * V;
+    const int64_t c0 = chunk_index(e0, a);
+    if (VEC_OK && e0 + V <= count && chunk_index(e0 + V - 1, a) == c0) {
+      ring_chain<T, VT, DIV>(bufs, e0, (int)c0, a);
+      continue;
+    }
+    for (int64_t e = e0; e < e0 + V && e < count; ++e) ring_chain<T, T, DIV>(bufs, e, (int)chunk_index(e, a), a);
   }
 }
 
@@ -805,6 +739,30 @@ hipError_t launch_rs_ag_step_c16(const RankPtrs& x, void* wire, const RingArgs& 
   _Float16* w = static_cast<_Float16*>(wire);
   if (streams(a, 4)) rs_ag_c16_launch<C16RsStream>(x, w, a, divmode, vector_ok, stream);
   else rs_ag_c16_launch<C16Cached>(x, w, a, divmode, vector_ok, stream);
+  return hipGetLastError();
+}
+
+hipError_t launch_chain(const RankPtrs& bufs, const RingArgs& a, int64_t count, int dtype, int divmode,
+                        bool vector_ok, hipStream_t stream) {
+  const int64_t v = dtype == HVDX_FLOAT32 ? 4 : 8;
+  int64_t blocks = ((count + v - 1) / v + kBlock - 1) / kBlock;
+  if (blocks < 1) blocks = 1;
+  if (blocks > 65536) blocks = 65536;
+  const dim3 grid((unsigned)blocks), block(kBlock);
+#define HVDX_CHAIN(T, DIV) \
+  if (vector_ok) hipLaunchKernelGGL((chain_kernel<T, DIV, true>), grid, block, 0, stream, bufs, a, count); \
+  else hipLaunchKernelGGL((chain_kernel<T, DIV, false>), grid, block, 0, stream, bufs, a, count)
+#define HVDX_CHAIN_D(T) \
+  if (divmode == DIV_NONE) { HVDX_CHAIN(T, DIV_NONE); } \
+  else if (divmode == DIV_POW2) { HVDX_CHAIN(T, DIV_POW2); } \
+  else { HVDX_CHAIN(T, DIV_TRUE); }
+  if (dtype == HVDX_FLOAT32) {
+    HVDX_CHAIN_D(float)
+  } else {
+    HVDX_CHAIN_D(_Float16)
+  }
+#undef HVDX_CHAIN_D
+#undef HVDX_CHAIN
   return hipGetLastError();
 }
 

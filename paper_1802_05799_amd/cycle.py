@@ -12,6 +12,10 @@ The fusion buffers are allocated once, at the size of the largest fused bucket
 paper's step 2 describes.  The descriptor arrays the kernels read (tensor pointers,
 sizes, offsets) are uploaded once at construction, so the tensors must stay
 allocated and in place for the object's lifetime.
+
+Buckets of at most `small_bucket_bytes` per rank (4 MiB by default) run their whole
+cycle in one launch (hvdx_fuse_allreduce_small, hvdx_ring_allreduce_small): there a
+ring step's launch costs more than its messages.  Same bits either way.
 """
 from __future__ import annotations
 
@@ -36,6 +40,7 @@ class Bucket:
     numel_dev: torch.Tensor | None = None
     offset_dev: torch.Tensor | None = None
     ptrs_dev: torch.Tensor | None = None
+    small: bool = False  # the whole cycle in one launch
 
 
 class FusedAllreduce:
@@ -43,13 +48,16 @@ class FusedAllreduce:
 
     def __init__(self, per_rank, op: str = "average", compress: bool = False,
                  threshold_bytes: int = L.DEFAULT_FUSION_THRESHOLD, align_bytes: int = L.DEFAULT_FUSION_ALIGN,
-                 schedule: str = "ring", fuse_boundary: bool = True):
+                 schedule: str = "ring", fuse_boundary: bool = True,
+                 small_bucket_bytes: int = L.SMALL_BUCKET_BYTES):
         """schedule "ring" runs the ring's 2(N-1) steps; "fold" computes the same bits
         with hvdx_fold_allreduce (no per-step messages: a one-GPU bound, not the ring).
         With fuse_boundary (ring schedule, N >= 3) a fusion buffer's copy-in runs with
         the ring's first adding step and its copy-out with the last replacing step
         (hvdx_fuse_allreduce); otherwise copy-in, ring and copy-out are separate calls.
-        Both give the same bits."""
+        With the fused boundary, a bucket of at most small_bucket_bytes per rank (0:
+        none) runs its whole cycle in one launch instead (compressed direct tensors
+        excepted).  All give the same bits."""
         if schedule not in ("ring", "fold"):
             raise ValueError("schedule must be 'ring' or 'fold'")
         self.schedule = schedule
@@ -85,6 +93,10 @@ class FusedAllreduce:
         for t, (b, off) in enumerate(zip(bucket_of, offset)):
             self.buckets[b].tensors.append(t)
             self.buckets[b].offsets.append(off)
+        for b in self.buckets:
+            es = _TORCH_DTYPE[self.dtype if b.direct else self.buf_dtype].itemsize
+            b.small = (self.fuse_boundary and b.count * es <= small_bucket_bytes
+                       and not (b.direct and self.compress))
 
         dev = self.device
         cap = max([b.count for b in self.buckets if not b.direct], default=0)
@@ -123,7 +135,9 @@ class FusedAllreduce:
 
     def ring(self, b: Bucket, stream: int) -> None:
         ptrs, count, dtype, compress, ws, wsb = self.ring_args(b)
-        if self.schedule == "fold":
+        if b.small:
+            L.hvdx_ring_allreduce_small(ptrs, self.nranks, count, dtype, self.op, stream)
+        elif self.schedule == "fold":
             L.hvdx_fold_allreduce(ptrs, self.nranks, count, dtype, self.op, compress, stream)
         else:
             L.hvdx_ring_allreduce(ptrs, self.nranks, count, dtype, self.op, compress, ws, wsb, stream)
@@ -139,19 +153,28 @@ class FusedAllreduce:
         L.hvdx_ring_step(ptrs, self.nranks, count, dtype, self.op, compress, phase, step, ws, wsb, stream)
 
     def fused_cycle(self, b: Bucket, stream: int) -> None:
-        """A fusion buffer's copy-in, ring and copy-out with the boundary steps fused."""
-        L.hvdx_fuse_allreduce(b.ptrs_dev.data_ptr(), b.numel_dev.data_ptr(), b.offset_dev.data_ptr(), len(b.tensors),
-                              self.dtype, self._buf_ptrs, b.count, self.buf_dtype, self.nranks, self.op, stream)
+        """A fusion buffer's copy-in, ring and copy-out with the boundary steps fused
+        (or, for a small bucket, all in one launch)."""
+        fn = L.hvdx_fuse_allreduce_small if b.small else L.hvdx_fuse_allreduce
+        fn(b.ptrs_dev.data_ptr(), b.numel_dev.data_ptr(), b.offset_dev.data_ptr(), len(b.tensors), self.dtype,
+           self._buf_ptrs, b.count, self.buf_dtype, self.nranks, self.op, stream)
 
     def kernel_sequence(self):
         """The kernels one call launches, in order: (kind, bucket index, step) with
         kind "pack", "pack_rs" (copy-in with adding step 0), "rs", "rs_ag" (adding
         step N-2 fused with replacing step 0), "ag", "ag_unpack" (replacing step N-2
-        with copy-out), "unpack", "fold", or "ring" (the one-rank compressed round trip)."""
+        with copy-out), "unpack", "fold", "ring" (the one-rank compressed round trip),
+        "cycle_small" or "ring_small" (a small bucket's whole cycle in one launch)."""
         out = []
         n = self.nranks
         for bi, b in enumerate(self.buckets):
             if b.count == 0:
+                continue
+            if b.small:
+                if not b.direct:
+                    out.append(("cycle_small", bi, -1))
+                elif n > 1:
+                    out.append(("ring_small", bi, -1))
                 continue
             if self.schedule == "fold":
                 if not b.direct:

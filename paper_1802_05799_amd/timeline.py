@@ -34,6 +34,8 @@ KIND_NAMES = {
     L.KERNEL_FOLD: "fold",
     L.KERNEL_PACK_RS: "copy in + reduce-scatter",
     L.KERNEL_AG_UNPACK: "allgather + copy out",
+    L.KERNEL_RING_SMALL: "whole ring (one launch)",
+    L.KERNEL_CYCLE_SMALL: "copy in + whole ring + copy out (one launch)",
 }
 
 
@@ -98,6 +100,9 @@ class Timeline:
                 args = {}
                 if kind == L.KERNEL_BROADCAST:
                     args = broadcast_step_args(step, r, rec["root"], n)
+                if kind in (L.KERNEL_RING_SMALL, L.KERNEL_CYCLE_SMALL):
+                    args = {"steps": f"adding 0-{n - 2}, replacing 0-{n - 2}", "to": (r + 1) % n,
+                            "from": (r - 1) % n}
                 if kind == L.KERNEL_RS_AG:  # adding step N-2, then replacing step 0
                     args = {"send chunks": [(r + 2) % n, (r + 1) % n], "to": (r + 1) % n,
                             "recv chunks": [(r + 1) % n, r], "from": (r - 1) % n,

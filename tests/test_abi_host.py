@@ -198,3 +198,24 @@ def test_fold_argument_errors():
     assert status_of(fo, bufs(2, 8), 2, 8, hv.FLOAT32, hv.SUM, 7) == hv.ERR_INVALID
     assert status_of(fo, [FAKE, FAKE + 16], 2, 8, hv.FLOAT32, hv.SUM) == hv.ERR_ALIAS
     assert status_of(fo, bufs(2, 0), 2, 0, hv.FLOAT32, hv.AVERAGE) == hv.OK
+
+
+def test_small_path_argument_errors():
+    rs, fs = hv.hvdx_ring_allreduce_small, hv.hvdx_fuse_allreduce_small
+    assert status_of(rs, bufs(2, 8), 0, 8, hv.FLOAT32, hv.SUM) == hv.ERR_INVALID  # nranks 0
+    assert status_of(rs, bufs(2, 8), 2, -1, hv.FLOAT32, hv.SUM) == hv.ERR_INVALID
+    assert status_of(rs, bufs(2, 8), 2, 8, 7, hv.SUM) == hv.ERR_INVALID  # dtype
+    assert status_of(rs, bufs(2, 8), 2, 8, hv.FLOAT32, 9) == hv.ERR_INVALID  # op
+    assert status_of(rs, [FAKE, FAKE + 16], 2, 8, hv.FLOAT32, hv.SUM) == hv.ERR_ALIAS
+    assert status_of(rs, [FAKE, FAKE + 2], 2, 8, hv.FLOAT32, hv.SUM) == hv.ERR_INVALID  # misaligned
+    assert status_of(rs, bufs(4, 0), 4, 0, hv.FLOAT32, hv.AVERAGE) == hv.OK  # nothing to do
+    assert status_of(rs, bufs(1, 8), 1, 8, hv.FLOAT32, hv.AVERAGE) == hv.OK  # one rank: no messages
+    b3 = bufs(3, 64)
+    assert status_of(fs, FAKE, FAKE, FAKE, 3, hv.FLOAT32, b3, 64, hv.FLOAT32, 3, 7) == hv.ERR_INVALID  # op
+    assert status_of(fs, 0, FAKE, FAKE, 3, hv.FLOAT32, b3, 64, hv.FLOAT32, 3, hv.SUM) == hv.ERR_INVALID
+    assert status_of(fs, FAKE, FAKE, FAKE, 3, hv.FLOAT16, b3, 64, hv.FLOAT32, 3, hv.SUM) == hv.ERR_UNSUPPORTED
+    assert status_of(fs, FAKE, FAKE, FAKE, 3, hv.FLOAT32, [FAKE, FAKE + 64, FAKE + 4096], 64, hv.FLOAT32, 3,
+                     hv.SUM) == hv.ERR_ALIAS
+    assert status_of(fs, FAKE, FAKE, FAKE, 3, hv.FLOAT32, [FAKE + 4, FAKE + 4096, FAKE + 8192], 64, hv.FLOAT32,
+                     3, hv.SUM) == hv.ERR_INVALID  # fusion buffers must be 16-byte aligned
+    assert status_of(fs, FAKE, FAKE, FAKE, 3, hv.FLOAT32, b3, 0, hv.FLOAT32, 3, hv.AVERAGE) == hv.OK

@@ -115,7 +115,7 @@ CYCLE_CASES = [
 ]
 
 
-@pytest.mark.parametrize("mode", ["ring", "ring-separate", "fold"])
+@pytest.mark.parametrize("mode", ["ring", "ring-one-launch", "ring-separate", "fold"])
 @pytest.mark.parametrize("case", range(len(CYCLE_CASES)))
 def test_fused_allreduce_matches_oracle(case, mode):
     numel, n, threshold, compress, op = CYCLE_CASES[case]
@@ -123,7 +123,9 @@ def test_fused_allreduce_matches_oracle(case, mode):
     host, dev, keep = make_tensors(rng, n, numel, np.float32)
     say(f"cycle case={case} n={n} threshold={threshold} compress={compress} mode={mode}")
     ar = hv.FusedAllreduce(dev, op=op, compress=compress, threshold_bytes=threshold,
-                           schedule="fold" if mode == "fold" else "ring", fuse_boundary=mode == "ring")
+                           schedule="fold" if mode == "fold" else "ring",
+                           fuse_boundary=mode in ("ring", "ring-one-launch"),
+                           small_bucket_bytes=hv.SMALL_BUCKET_BYTES if mode == "ring-one-launch" else 0)
     ar()
     torch.cuda.synchronize()
     want = allreduce.allreduce(host, op, compress=compress, threshold=threshold)

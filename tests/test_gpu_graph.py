@@ -35,12 +35,13 @@ def snapshot(dev):
     return [[x.cpu().numpy() for x in row] for row in dev]
 
 
+@pytest.mark.parametrize("small_bytes", [0, hv.SMALL_BUCKET_BYTES], ids=["per-step", "one-launch"])
 @pytest.mark.parametrize("case", range(len(GRAPH_CASES)))
-def test_graph_replays_match_eager_and_oracle(case):
+def test_graph_replays_match_eager_and_oracle(case, small_bytes):
     numel, n, threshold, compress, op = GRAPH_CASES[case]
     say(f"graph case={case} n={n} threshold={threshold} compress={compress}")
     dev = [[torch.zeros(k, dtype=torch.float32, device="cuda") for k in numel] for _ in range(n)]
-    ar = hv.FusedAllreduce(dev, op=op, compress=compress, threshold_bytes=threshold)
+    ar = hv.FusedAllreduce(dev, op=op, compress=compress, threshold_bytes=threshold, small_bucket_bytes=small_bytes)
     graph = ar.capture()
     torch.cuda.synchronize()
     for rep in range(3):

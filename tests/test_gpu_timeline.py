@@ -24,7 +24,8 @@ def tensors(n, numel, seed=0):
 def test_records_follow_launches(fuse_boundary):
     say(f"timeline records fuse_boundary={fuse_boundary}")
     per_rank = tensors(5, [7, 4000, 100, 30000, 5])
-    ar = hv.FusedAllreduce(per_rank, op="average", threshold_bytes=40000, fuse_boundary=fuse_boundary)
+    ar = hv.FusedAllreduce(per_rank, op="average", threshold_bytes=40000, fuse_boundary=fuse_boundary,
+                           small_bucket_bytes=0)
     sid = torch.cuda.current_stream().cuda_stream
     launches = ar.kernel_sequence()
     with hv.Timeline(capacity=1000) as tl:
@@ -43,9 +44,24 @@ def test_records_follow_launches(fuse_boundary):
     assert ranks == set(range(6))  # GPU track + 5 ranks
 
 
+def test_small_buckets_record_one_launch():
+    """Buckets on the one-launch path: one record each, named for the whole cycle."""
+    say("timeline records small buckets")
+    per_rank = tensors(5, [7, 4000, 100, 30000, 5])
+    ar = hv.FusedAllreduce(per_rank, op="average", threshold_bytes=40000)
+    launches = ar.kernel_sequence()
+    assert {k for k, _, _ in launches} == {"cycle_small", "ring_small"}
+    with hv.Timeline(capacity=100) as tl:
+        ar()
+    code = {"cycle_small": hv._lib.KERNEL_CYCLE_SMALL, "ring_small": hv._lib.KERNEL_RING_SMALL}
+    assert [r["kind"] for r in tl.records] == [code[k] for k, _, _ in launches]
+    names = {e["name"] for e in tl.chrome_trace()["traceEvents"] if e["ph"] == "X" and e["tid"] == 0}
+    assert names == {"copy in + whole ring + copy out (one launch)", "whole ring (one launch)"}
+
+
 def test_capacity_counts_dropped_launches():
     per_rank = tensors(3, [1000, 2000])
-    ar = hv.FusedAllreduce(per_rank)
+    ar = hv.FusedAllreduce(per_rank, small_bucket_bytes=0)  # one launch per ring step
     with hv.Timeline(capacity=2) as tl:
         ar()
     assert len(tl.records) == 2 and tl.dropped == len(ar.kernel_sequence()) - 2
@@ -57,7 +73,7 @@ def test_environment_variable_writes_trace(tmp_path):
         "import sys; sys.path.insert(0, %r)\n"
         "import torch, paper_1802_05799_amd as hv\n"
         "xs = [[torch.ones(1000, device='cuda'), torch.ones(77, device='cuda')] for _ in range(4)]\n"
-        "ar = hv.FusedAllreduce(xs)\n"
+        "ar = hv.FusedAllreduce(xs, small_bucket_bytes=0)\n"
         "ar(); ar(); torch.cuda.synchronize()\n" % ROOT
     )
     say("timeline env subprocess")
@@ -72,7 +88,8 @@ def test_environment_variable_writes_trace(tmp_path):
 @pytest.mark.parametrize("fuse_boundary", [True, False], ids=["fused-boundary", "separate"])
 def test_per_phase_records(fuse_boundary):
     per_rank = tensors(6, [7, 4000, 100, 30000, 5])
-    ar = hv.FusedAllreduce(per_rank, op="average", threshold_bytes=40000, fuse_boundary=fuse_boundary)
+    ar = hv.FusedAllreduce(per_rank, op="average", threshold_bytes=40000, fuse_boundary=fuse_boundary,
+                           small_bucket_bytes=0)
     with hv.Timeline(capacity=100, per_phase=True) as tl:
         ar()
     got = [(r["kind"], r["step"], r["launches"]) for r in tl.records]
