@@ -77,47 +77,8 @@ def kernel_bytes(ar, kind, bi, step):
     return 0
 
 
-KIND_OF_CODE = {0: "pack", 1: "rs", 2: "ag", 3: "unpack", 4: "ring", 6: "rs_ag", 7: "fold", 8: "pack_rs",
-                9: "ag_unpack", 10: "ring_small", 11: "cycle_small"}
-
-
-def phase_sequence(ar):
-    """(timeline kind code, bucket, first step, launches) of each per-phase record one
-    call of `ar` produces."""
-    out = []
-    n = ar.nranks
-    for bi, b in enumerate(ar.buckets):
-        if b.count == 0:
-            continue
-        if b.small:
-            if not b.direct:
-                out.append((11, bi, -1, 1))
-            elif n > 1:
-                out.append((10, bi, -1, 1))
-            continue
-        if ar.fuse_boundary and not b.direct and n >= 3:
-            out.append((8, bi, 0, 1))
-            if n > 3:
-                out.append((1, bi, 1, n - 3))
-            out.append((6, bi, n - 2, 1))
-            if n > 3:
-                out.append((2, bi, 1, n - 3))
-            out.append((9, bi, n - 2, 1))
-            continue
-        if not b.direct:
-            out.append((0, bi, -1, 1))
-        if n == 1:
-            if b.direct and ar.compress:
-                out.append((4, bi, -1, 1))
-        else:
-            if n > 2:
-                out.append((1, bi, 0, n - 2))
-            out.append((6, bi, n - 2, 1))
-            if n > 2:
-                out.append((2, bi, 1, n - 2))
-        if not b.direct:
-            out.append((3, bi, -1, 1))
-    return out
+KIND_CODE = {"pack": 0, "rs": 1, "ag": 2, "unpack": 3, "ring": 4, "rs_ag": 6, "fold": 7, "pack_rs": 8,
+             "ag_unpack": 9, "ring_small": 10, "cycle_small": 11}
 
 
 def kernel_name(ar, kind, bi):
@@ -209,33 +170,30 @@ def measure(name, steps, warmup, threshold=64 << 20, per_kernel_pass=True, sched
         torch.cuda.empty_cache()
         return res
 
-    # the same steps once more under the library's per-phase timeline: HIP events
-    # recorded inside the C library around each run of one kernel (a bucket's
-    # copy-in, its plain adding steps, the fused adding/replacing step, its plain
-    # replacing steps, its copy-out).  Each record's median over the timed steps is
-    # kept: a sample the host stalled is an outlier, not a kernel duration.
-    with hv.Timeline(capacity=64 * (steps + 1) * max(1, len(ar.buckets)), per_phase=True) as tl:
+    # the same steps once more with every launch timed by its own dispatch (the
+    # library hands timeline events to hipExtLaunchKernel, which stamps them with the
+    # kernel's start and end, as a kernel trace does).  Each launch position's median
+    # over the timed steps is kept: a sample the host stalled is an outlier.
+    seq = ar.kernel_sequence()
+    with hv.Timeline(capacity=len(seq) * (steps + 1) + 16) as tl:
         for i in range(steps + 1):
             flush(i)  # not a library launch: no timeline record
             ar(sid)
     recs = tl.records
-    per_step = len(recs) // (steps + 1)
-    if tl.dropped or per_step * (steps + 1) != len(recs):
-        raise RuntimeError(f"timeline recorded {len(recs)} records for {steps + 1} steps")
-    seq = phase_sequence(ar)
-    if [(k, st, la) for k, _bi, st, la in seq] != [(r["kind"], r["step"], r["launches"]) for r in recs[:per_step]]:
+    if tl.dropped or len(recs) != len(seq) * (steps + 1):
+        raise RuntimeError(f"timeline recorded {len(recs)} launches for {steps + 1} steps of {len(seq)}")
+    if [KIND_CODE[k] for k, _bi, _st in seq] != [r["kind"] for r in recs[:len(seq)]]:
         raise RuntimeError("timeline records do not follow the expected launch order")
     per_kernel = {}
     outliers = 0
-    for i, (kcode, bi, st, la) in enumerate(seq):
-        samples = sorted(recs[j * per_step + i]["duration_us"] / 1000.0 for j in range(1, steps + 1))
+    for j, (kind, bi, st) in enumerate(seq):
+        samples = sorted(recs[i * len(seq) + j]["duration_us"] / 1000.0 for i in range(1, steps + 1))
         med = samples[len(samples) // 2]
         outliers += sum(1 for x in samples if x > 1.5 * med)
-        kind = KIND_OF_CODE[kcode]
         d = per_kernel.setdefault(kernel_name(ar, kind, bi), {"launches": 0, "ms": 0.0, "bytes": 0})
-        d["launches"] += la * steps
+        d["launches"] += steps
         d["ms"] += med * steps
-        d["bytes"] += sum(kernel_bytes(ar, kind, bi, s_) for s_ in range(st, st + la)) * steps
+        d["bytes"] += kernel_bytes(ar, kind, bi, st) * steps
     traced_ms = sum(d["ms"] for d in per_kernel.values()) / steps
     for d in per_kernel.values():
         d["avg_us"] = 1000.0 * d["ms"] / d["launches"]
@@ -603,7 +561,8 @@ def main():
         "traffic": traffic_for(dom_name, args.workload),
         "avg_launch_us": round(dom["avg_us"], 2),
         "launches_per_step": dom["launches"] // args.steps,
-        "timing": "median over the timed steps of the library's per-phase timeline events, / launches in the phase",
+        "timing": "median over the timed steps of each launch's kernel time, stamped by its own dispatch "
+                  "(hipExtLaunchKernel events), averaged over the kernel's launches",
         "timing_outlier_samples": head["timing_outliers"],
         "algorithmic_bytes_per_step": dom["bytes"] // args.steps,
     }

@@ -332,9 +332,13 @@ int hvdx_ring_chunk(int64_t count, int nranks, int c, int64_t* start, int64_t* l
  *
  *   hvdx_timeline_begin(capacity, per_phase)  start recording up to `capacity`
  *       (>= 1) records; records past that are counted as dropped.  per_phase = 0
- *       records every launch; per_phase = 1 records each run of launches of one
- *       kernel inside one call (e.g. the N-2 plain adding steps of a ring) as one
- *       record whose `launches` says how many.  Returns HVDX_ERR_INVALID if a
+ *       records every launch, its events stamped by the kernel's own dispatch
+ *       (hipExtLaunchKernel), so a record's duration is the kernel's run time;
+ *       per_phase = 1 records each run of launches of one kernel inside one call
+ *       (e.g. the N-2 plain adding steps of a ring) as one record whose `launches`
+ *       says how many, with event records in the stream around the run.  Either
+ *       way the records cost GPU time (a few microseconds per launch or per run).
+ *       Returns HVDX_ERR_INVALID if a
  *       timeline is already recording or capacity < 1, HVDX_ERR_HIP if the events
  *       cannot be created.
  *   hvdx_timeline_end(out, capacity, nrecords, ndropped)  wait for the recorded

@@ -50,9 +50,9 @@ hipError_t launch_bcast_step(const RankPtrs& bufs, const BcastArgs& a, bool vect
   if (bx > (1 << 20)) bx = 1 << 20;
   const dim3 grid((unsigned)bx, (unsigned)(a.n - 1));
   if (vector_ok)
-    hipLaunchKernelGGL((bcast_step_kernel<true>), grid, dim3(kBlock), 0, stream, bufs, a);
+    HVDX_LAUNCH((bcast_step_kernel<true>), grid, dim3(kBlock), 0, stream, bufs, a);
   else
-    hipLaunchKernelGGL((bcast_step_kernel<false>), grid, dim3(kBlock), 0, stream, bufs, a);
+    HVDX_LAUNCH((bcast_step_kernel<false>), grid, dim3(kBlock), 0, stream, bufs, a);
   return hipGetLastError();
 }
 

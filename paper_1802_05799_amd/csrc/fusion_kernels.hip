@@ -666,13 +666,13 @@ void pack_with(const void* const* srcs, const int64_t* numel, const int64_t* off
   const dim3 grid = copy_grid<Cfg, RING>(count, buf_dtype, nranks);
   const int64_t q = count / nranks, rem = count % nranks;
   if (src_dtype == HVDX_FLOAT32 && buf_dtype == HVDX_FLOAT32)
-    hipLaunchKernelGGL((pack_kernel<float, float, Cfg, RING>), grid, dim3(kBlock), 0, stream, srcs, numel, offset,
+    HVDX_LAUNCH((pack_kernel<float, float, Cfg, RING>), grid, dim3(kBlock), 0, stream, srcs, numel, offset,
                        ntensors, bufs, count, nranks, rpb, q, rem);
   else if (src_dtype == HVDX_FLOAT32 && buf_dtype == HVDX_FLOAT16)
-    hipLaunchKernelGGL((pack_kernel<float, _Float16, Cfg, RING>), grid, dim3(kBlock), 0, stream, srcs, numel,
+    HVDX_LAUNCH((pack_kernel<float, _Float16, Cfg, RING>), grid, dim3(kBlock), 0, stream, srcs, numel,
                        offset, ntensors, bufs, count, nranks, rpb, q, rem);
   else
-    hipLaunchKernelGGL((pack_kernel<_Float16, _Float16, Cfg, RING>), grid, dim3(kBlock), 0, stream, srcs, numel,
+    HVDX_LAUNCH((pack_kernel<_Float16, _Float16, Cfg, RING>), grid, dim3(kBlock), 0, stream, srcs, numel,
                        offset, ntensors, bufs, count, nranks, rpb, q, rem);
 }
 
@@ -683,13 +683,13 @@ void unpack_with(const RankPtrs& bufs, int64_t count, int buf_dtype, void* const
   const dim3 grid = copy_grid<Cfg, RING>(count, buf_dtype, nranks);
   const int64_t q = count / nranks, rem = count % nranks;
   if (dst_dtype == HVDX_FLOAT32 && buf_dtype == HVDX_FLOAT32)
-    hipLaunchKernelGGL((unpack_kernel<float, float, Cfg, RING>), grid, dim3(kBlock), 0, stream, bufs, count, dsts,
+    HVDX_LAUNCH((unpack_kernel<float, float, Cfg, RING>), grid, dim3(kBlock), 0, stream, bufs, count, dsts,
                        numel, offset, ntensors, nranks, rpb, q, rem);
   else if (dst_dtype == HVDX_FLOAT32 && buf_dtype == HVDX_FLOAT16)
-    hipLaunchKernelGGL((unpack_kernel<float, _Float16, Cfg, RING>), grid, dim3(kBlock), 0, stream, bufs, count,
+    HVDX_LAUNCH((unpack_kernel<float, _Float16, Cfg, RING>), grid, dim3(kBlock), 0, stream, bufs, count,
                        dsts, numel, offset, ntensors, nranks, rpb, q, rem);
   else
-    hipLaunchKernelGGL((unpack_kernel<_Float16, _Float16, Cfg, RING>), grid, dim3(kBlock), 0, stream, bufs, count,
+    HVDX_LAUNCH((unpack_kernel<_Float16, _Float16, Cfg, RING>), grid, dim3(kBlock), 0, stream, bufs, count,
                        dsts, numel, offset, ntensors, nranks, rpb, q, rem);
 }
 
@@ -715,7 +715,7 @@ hipError_t launch_small_cycle(const void* const* tensors, const int64_t* numel, 
                               int divmode, hipStream_t stream) {
   const dim3 grid(tiles_for<SmallCfg>(count, buf_dtype)), block(kBlock);
 #define HVDX_SMALL(TT, TB, DIV) \
-  hipLaunchKernelGGL((small_cycle_kernel<TT, TB, DIV>), grid, block, 0, stream, tensors, numel, offset, ntensors, \
+  HVDX_LAUNCH((small_cycle_kernel<TT, TB, DIV>), grid, block, 0, stream, tensors, numel, offset, ntensors, \
                      bufs, a, count)
 #define HVDX_SMALL_D(TT, TB) \
   if (divmode == DIV_NONE) { HVDX_SMALL(TT, TB, DIV_NONE); } \

@@ -37,9 +37,19 @@ Timeline& timeline() {
   return t;
 }
 
-// Brackets kernel launches with timeline events when a timeline is recording at
-// this granularity: a phase record (phase = true) covers several launches and is
-// taken only in per-phase mode, a launch record only in per-launch mode.
+}  // namespace
+
+hvdx::LaunchEvents& hvdx::pending_launch_events() {
+  thread_local LaunchEvents ev;
+  return ev;
+}
+
+namespace {
+
+// Times kernel launches for the timeline when it records at this granularity.  A
+// launch record (per-launch mode) hands its events to the one launch in its scope,
+// which stamps them with the kernel's own start and end; a phase record (per-phase
+// mode) covers several launches with event records in the stream before and after.
 class TimedLaunch {
  public:
   TimedLaunch(int kind, int step, int nranks, int dtype, int compress, int64_t count, hipStream_t st, int root = -1,
@@ -65,20 +75,34 @@ class TimedLaunch {
     e.rec.count = count;
     e.start = t.pool[2 * t.entries.size()];
     e.end = t.pool[2 * t.entries.size() + 1];
-    if (hipEventRecord(e.start, st_) == hipSuccess) {
+    if (!phase) {
+      t.entries.push_back(e);
+      hvdx::pending_launch_events() = {e.start, e.end};
+      start_ = e.start;
+      end_ = e.end;
+    } else if (hipEventRecord(e.start, st_) == hipSuccess) {
       t.entries.push_back(e);
       end_ = e.end;
     }
   }
   // The lock is still held here: no other thread's launch lands inside the record.
   ~TimedLaunch() {
+    if (start_) {
+      hvdx::LaunchEvents& ev = hvdx::pending_launch_events();
+      if (ev.start == start_) {  // nothing was launched (an error): a zero-length record
+        ev = hvdx::LaunchEvents{};
+        (void)hipEventRecord(start_, st_);
+        (void)hipEventRecord(end_, st_);
+      }
+      return;
+    }
     if (end_) (void)hipEventRecord(end_, st_);
   }
 
  private:
   hipStream_t st_;
   std::unique_lock<std::recursive_mutex> lock_;
-  hipEvent_t end_ = nullptr;
+  hipEvent_t start_ = nullptr, end_ = nullptr;
 };
 
 int fail(int code, const char* fmt, ...) {

@@ -1,6 +1,7 @@
 // Internal declarations shared by the library's translation units (not installed).
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
@@ -8,6 +9,14 @@
 #include "hvdx.h"
 
 namespace hvdx {
+
+// Events that a timeline record hands to this thread's next kernel launch, which then
+// runs through hipExtLaunchKernel: the dispatch itself stamps them with the kernel's
+// start and end, with no extra commands in the stream.  Empty when nothing waits.
+struct LaunchEvents {
+  hipEvent_t start = nullptr, stop = nullptr;
+};
+LaunchEvents& pending_launch_events();
 
 // Every rank's base pointer travels in the kernel arguments (1 KiB).
 struct RankPtrs {
@@ -72,3 +81,17 @@ hipError_t launch_unpack(const RankPtrs& bufs, int64_t count, int buf_dtype, voi
                          bool ring, hipStream_t stream);
 
 }  // namespace hvdx
+
+// Every kernel launch of the library goes through this.
+#define HVDX_LAUNCH(kernel, grid, block, shmem, stream, ...)                                                \
+  do {                                                                                                      \
+    ::hvdx::LaunchEvents& hvdx_ev_ = ::hvdx::pending_launch_events();                                       \
+    if (hvdx_ev_.start) {                                                                                   \
+      const ::hvdx::LaunchEvents hvdx_take_ = hvdx_ev_;                                                     \
+      hvdx_ev_ = ::hvdx::LaunchEvents{};                                                                    \
+      hipExtLaunchKernelGGL(kernel, grid, block, shmem, stream, hvdx_take_.start, hvdx_take_.stop, 0,       \
+                            __VA_ARGS__);                                                                   \
+    } else {                                                                                                \
+      hipLaunchKernelGGL(kernel, grid, block, shmem, stream, __VA_ARGS__);                                  \
+    }                                                                                                       \
+  } while (0)

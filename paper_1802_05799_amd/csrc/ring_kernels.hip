@@ -583,7 +583,7 @@ bool streams(const RingArgs& a, int esize) { return (a.q + 1) * a.n * (int64_t)e
 template <typename T, typename P>
 void rs_launch(const RankPtrs& bufs, const RingArgs& a, int divmode, bool vec_ok, hipStream_t st) {
   const dim3 grid = step_grid(a, Vec<T>::n, P::U, P::BS);
-#define HVDX_RS(DIV, VOK) hipLaunchKernelGGL((rs_step_kernel<T, DIV, VOK, P>), grid, dim3(P::BS), 0, st, bufs, a)
+#define HVDX_RS(DIV, VOK) HVDX_LAUNCH((rs_step_kernel<T, DIV, VOK, P>), grid, dim3(P::BS), 0, st, bufs, a)
   if (vec_ok) {
     if (divmode == DIV_NONE) HVDX_RS(DIV_NONE, true);
     else if (divmode == DIV_POW2) HVDX_RS(DIV_POW2, true);
@@ -607,9 +607,9 @@ template <typename T, typename P>
 void ag_launch(const RankPtrs& bufs, const RingArgs& a, bool vec_ok, hipStream_t st) {
   const dim3 grid = step_grid(a, Vec<T>::n, P::U, P::BS);
   if (vec_ok)
-    hipLaunchKernelGGL((ag_step_kernel<T, true, P>), grid, dim3(P::BS), 0, st, bufs, a);
+    HVDX_LAUNCH((ag_step_kernel<T, true, P>), grid, dim3(P::BS), 0, st, bufs, a);
   else
-    hipLaunchKernelGGL((ag_step_kernel<T, false, P>), grid, dim3(P::BS), 0, st, bufs, a);
+    HVDX_LAUNCH((ag_step_kernel<T, false, P>), grid, dim3(P::BS), 0, st, bufs, a);
 }
 
 template <typename T>
@@ -625,7 +625,7 @@ void rs_c16_launch(const RankPtrs& x, _Float16* w, const RingArgs& a, int divmod
   const dim3 grid = step_grid(a, 8, P::U, P::BS);
   const bool first = a.step == 0;
 #define HVDX_RSC(DIV, F, VOK) \
-  hipLaunchKernelGGL((rs_step_c16_kernel<DIV, F, VOK, P>), grid, dim3(P::BS), 0, stream, x, w, a)
+  HVDX_LAUNCH((rs_step_c16_kernel<DIV, F, VOK, P>), grid, dim3(P::BS), 0, stream, x, w, a)
 #define HVDX_RSC_V(DIV, F) \
   if (vector_ok) HVDX_RSC(DIV, F, true); else HVDX_RSC(DIV, F, false)
 #define HVDX_RSC_F(DIV) \
@@ -645,8 +645,8 @@ void rs_c16_launch(const RankPtrs& x, _Float16* w, const RingArgs& a, int divmod
 template <typename P>
 void ag_first_c16_launch(const RankPtrs& x, const _Float16* w, const RingArgs& a, bool vector_ok, hipStream_t stream) {
   const dim3 grid = step_grid(a, 8, P::U, P::BS);
-  if (vector_ok) hipLaunchKernelGGL((ag_first_c16_kernel<true, P>), grid, dim3(P::BS), 0, stream, x, w, a);
-  else hipLaunchKernelGGL((ag_first_c16_kernel<false, P>), grid, dim3(P::BS), 0, stream, x, w, a);
+  if (vector_ok) HVDX_LAUNCH((ag_first_c16_kernel<true, P>), grid, dim3(P::BS), 0, stream, x, w, a);
+  else HVDX_LAUNCH((ag_first_c16_kernel<false, P>), grid, dim3(P::BS), 0, stream, x, w, a);
 }
 
 }  // namespace
@@ -682,7 +682,7 @@ hipError_t launch_roundtrip_c16(void* x, int64_t count, hipStream_t stream) {
   int64_t blocks = (count + kBlock * 4 - 1) / (kBlock * 4);
   if (blocks < 1) blocks = 1;
   if (blocks > 65536) blocks = 65536;
-  hipLaunchKernelGGL(roundtrip_c16_kernel, dim3((unsigned)blocks), dim3(kBlock), 0, stream, static_cast<float*>(x),
+  HVDX_LAUNCH(roundtrip_c16_kernel, dim3((unsigned)blocks), dim3(kBlock), 0, stream, static_cast<float*>(x),
                      count);
   return hipGetLastError();
 }
@@ -690,7 +690,7 @@ hipError_t launch_roundtrip_c16(void* x, int64_t count, hipStream_t stream) {
 hipError_t launch_rs_ag_step(const RankPtrs& bufs, const RingArgs& a, int dtype, int divmode, bool vector_ok,
                              hipStream_t stream) {
 #define HVDX_RSAG(T, P, DIV, VOK) \
-  hipLaunchKernelGGL((rs_ag_step_kernel<T, DIV, VOK, P>), step_grid(a, Vec<T>::n, P::U, P::BS), dim3(P::BS), 0, \
+  HVDX_LAUNCH((rs_ag_step_kernel<T, DIV, VOK, P>), step_grid(a, Vec<T>::n, P::U, P::BS), dim3(P::BS), 0, \
                      stream, bufs, a)
 #define HVDX_RSAG_V(T, P, DIV) \
   if (vector_ok) HVDX_RSAG(T, P, DIV, true); else HVDX_RSAG(T, P, DIV, false)
@@ -716,7 +716,7 @@ void rs_ag_c16_launch(const RankPtrs& x, _Float16* w, const RingArgs& a, int div
   const dim3 grid = step_grid(a, 8, P::U, P::BS);
   const bool first = a.n == 2;  // step N-2 is also the first adding step when N = 2
 #define HVDX_RAC(DIV, F, VOK) \
-  hipLaunchKernelGGL((rs_ag_step_c16_kernel<DIV, F, VOK, P>), grid, dim3(P::BS), 0, stream, x, w, a)
+  HVDX_LAUNCH((rs_ag_step_c16_kernel<DIV, F, VOK, P>), grid, dim3(P::BS), 0, stream, x, w, a)
 #define HVDX_RAC_V(DIV, F) \
   if (vector_ok) HVDX_RAC(DIV, F, true); else HVDX_RAC(DIV, F, false)
 #define HVDX_RAC_D(F) \
@@ -750,8 +750,8 @@ hipError_t launch_chain(const RankPtrs& bufs, const RingArgs& a, int64_t count, 
   if (blocks > 65536) blocks = 65536;
   const dim3 grid((unsigned)blocks), block(kBlock);
 #define HVDX_CHAIN(T, DIV) \
-  if (vector_ok) hipLaunchKernelGGL((chain_kernel<T, DIV, true>), grid, block, 0, stream, bufs, a, count); \
-  else hipLaunchKernelGGL((chain_kernel<T, DIV, false>), grid, block, 0, stream, bufs, a, count)
+  if (vector_ok) HVDX_LAUNCH((chain_kernel<T, DIV, true>), grid, block, 0, stream, bufs, a, count); \
+  else HVDX_LAUNCH((chain_kernel<T, DIV, false>), grid, block, 0, stream, bufs, a, count)
 #define HVDX_CHAIN_D(T) \
   if (divmode == DIV_NONE) { HVDX_CHAIN(T, DIV_NONE); } \
   else if (divmode == DIV_POW2) { HVDX_CHAIN(T, DIV_POW2); } \
@@ -773,8 +773,8 @@ hipError_t launch_fold(const RankPtrs& bufs, const RingArgs& a, int64_t count, i
   if (blocks > (1 << 20)) blocks = 1 << 20;
   const dim3 grid((unsigned)blocks), block(kBlock);
 #define HVDX_FOLD(T, C, DIV) \
-  if (vector_ok) hipLaunchKernelGGL((fold_kernel<T, DIV, C, true>), grid, block, 0, stream, bufs, a, count); \
-  else hipLaunchKernelGGL((fold_kernel<T, DIV, C, false>), grid, block, 0, stream, bufs, a, count)
+  if (vector_ok) HVDX_LAUNCH((fold_kernel<T, DIV, C, true>), grid, block, 0, stream, bufs, a, count); \
+  else HVDX_LAUNCH((fold_kernel<T, DIV, C, false>), grid, block, 0, stream, bufs, a, count)
 #define HVDX_FOLD_D(T, C) \
   if (divmode == DIV_NONE) { HVDX_FOLD(T, C, DIV_NONE); } \
   else if (divmode == DIV_POW2) { HVDX_FOLD(T, C, DIV_POW2); } \
