@@ -53,8 +53,10 @@ def kernel_bytes(ar, kind, bi, step):
     es_t = 4 if ar.dtype == 0 else 2  # tensor element size
     es_b = 4 if ar.buf_dtype == 0 else 2  # buffer element size
     data = sum(ar.numel[t] for t in b.tensors)
-    if kind in ("pack", "pack_rs"):  # the fused adding step reuses the values it packs
+    if kind == "pack":
         return n * (es_t * data + es_b * b.count)
+    if kind == "pack_rs":  # the adding step reuses the values it packs; no rank stores its own sent chunk
+        return n * es_t * data + (n - 1) * es_b * b.count
     if kind in ("cycle_small", "ring_small"):  # every step's messages, as the per-step kernels count them
         es = es_t if b.direct else es_b
         ring = (n - 1) * 5 * es * b.count

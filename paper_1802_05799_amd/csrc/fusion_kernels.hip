@@ -411,7 +411,7 @@ __global__ __launch_bounds__(kBlock) HVDX_COPY_ATTR void pack_kernel(const void*
                                                                     const int64_t* __restrict__ numel,
                                                                     const int64_t* __restrict__ offset, int ntensors,
                                                                     RankPtrs bufs, int64_t count, int nranks, int rpb,
-                                                                    int64_t q, int64_t rem) {
+                                                                    int64_t q, int64_t rem, int skip_sender) {
   static_assert(!RING || (Cfg::RB >= 2 && (Cfg::RPB == 0 || Cfg::RPB >= 2)),
                 "the fused copy-in needs the sender and receiver in one load batch");
   constexpr int V = BufVec<TB>::n;
@@ -455,6 +455,7 @@ __global__ __launch_bounds__(kBlock) HVDX_COPY_ATTR void pack_kernel(const void*
       for (int rr = 0; rr < kRankBatch; ++rr) {
         const int slot = v0 + rr;
         if (slot >= bs.rend) break;
+        if (RING && skip_sender && slot == 0) continue;  // the sender's copy of its own chunk is never read
         TB* __restrict__ buf = static_cast<TB*>(bufs.p[pt.rank(slot)]);
 #pragma unroll
         for (int u = 0; u < kPosPerLane; ++u) {
@@ -471,6 +472,7 @@ __global__ __launch_bounds__(kBlock) HVDX_COPY_ATTR void pack_kernel(const void*
 
     if (!edges) continue;
     for (int slot = bs.rbeg; slot < bs.rend; ++slot) {
+      if (RING && skip_sender && slot == 0) continue;
       const int r = pt.rank(slot);
       TB* __restrict__ buf = static_cast<TB*>(bufs.p[r]);
       for (int u = 0; u < kPosPerLane; ++u) {
@@ -661,19 +663,19 @@ dim3 copy_grid(int64_t count, int buf_dtype, int nranks) {
 
 template <typename Cfg, bool RING>
 void pack_with(const void* const* srcs, const int64_t* numel, const int64_t* offset, int ntensors, int src_dtype,
-               const RankPtrs& bufs, int64_t count, int buf_dtype, int nranks, hipStream_t stream) {
+               const RankPtrs& bufs, int64_t count, int buf_dtype, int nranks, int skip_sender, hipStream_t stream) {
   const int rpb = ranks_per_block<Cfg>(nranks);
   const dim3 grid = copy_grid<Cfg, RING>(count, buf_dtype, nranks);
   const int64_t q = count / nranks, rem = count % nranks;
   if (src_dtype == HVDX_FLOAT32 && buf_dtype == HVDX_FLOAT32)
     HVDX_LAUNCH((pack_kernel<float, float, Cfg, RING>), grid, dim3(kBlock), 0, stream, srcs, numel, offset,
-                       ntensors, bufs, count, nranks, rpb, q, rem);
+                       ntensors, bufs, count, nranks, rpb, q, rem, skip_sender);
   else if (src_dtype == HVDX_FLOAT32 && buf_dtype == HVDX_FLOAT16)
     HVDX_LAUNCH((pack_kernel<float, _Float16, Cfg, RING>), grid, dim3(kBlock), 0, stream, srcs, numel,
-                       offset, ntensors, bufs, count, nranks, rpb, q, rem);
+                       offset, ntensors, bufs, count, nranks, rpb, q, rem, skip_sender);
   else
     HVDX_LAUNCH((pack_kernel<_Float16, _Float16, Cfg, RING>), grid, dim3(kBlock), 0, stream, srcs, numel,
-                       offset, ntensors, bufs, count, nranks, rpb, q, rem);
+                       offset, ntensors, bufs, count, nranks, rpb, q, rem, skip_sender);
 }
 
 template <typename Cfg, bool RING>
@@ -697,15 +699,19 @@ void unpack_with(const RankPtrs& bufs, int64_t count, int buf_dtype, void* const
 
 hipError_t launch_pack(const void* const* srcs, const int64_t* numel, const int64_t* offset, int ntensors,
                        int src_dtype, const RankPtrs& bufs, int64_t count, int buf_dtype, int nranks, bool ring,
-                       hipStream_t stream) {
+                       bool skip_sender, hipStream_t stream) {
+  const int skip = ring && skip_sender ? 1 : 0;
   if (buf_dtype == HVDX_FLOAT32) {
-    if (ring) pack_with<PackCfg, true>(srcs, numel, offset, ntensors, src_dtype, bufs, count, buf_dtype, nranks, stream);
-    else pack_with<PackCfg, false>(srcs, numel, offset, ntensors, src_dtype, bufs, count, buf_dtype, nranks, stream);
+    if (ring)
+      pack_with<PackCfg, true>(srcs, numel, offset, ntensors, src_dtype, bufs, count, buf_dtype, nranks, skip, stream);
+    else
+      pack_with<PackCfg, false>(srcs, numel, offset, ntensors, src_dtype, bufs, count, buf_dtype, nranks, 0, stream);
   } else {
     if (ring)
-      pack_with<Pack16Cfg, true>(srcs, numel, offset, ntensors, src_dtype, bufs, count, buf_dtype, nranks, stream);
+      pack_with<Pack16Cfg, true>(srcs, numel, offset, ntensors, src_dtype, bufs, count, buf_dtype, nranks, skip,
+                                 stream);
     else
-      pack_with<Pack16Cfg, false>(srcs, numel, offset, ntensors, src_dtype, bufs, count, buf_dtype, nranks, stream);
+      pack_with<Pack16Cfg, false>(srcs, numel, offset, ntensors, src_dtype, bufs, count, buf_dtype, nranks, 0, stream);
   }
   return hipGetLastError();
 }

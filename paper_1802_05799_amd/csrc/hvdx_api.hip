@@ -436,19 +436,23 @@ int hvdx_fuse_pack(const void* const* srcs, const int64_t* numel, const int64_t*
   TimedLaunch timed_phase(HVDX_KERNEL_PACK, -1, nranks, buf_dtype, HVDX_COMPRESS_NONE, buf_count,
                           static_cast<hipStream_t>(stream), -1, true);
   const hipError_t e = hvdx::launch_pack(srcs, numel, offset, ntensors, src_dtype, rank_ptrs(bufs, nranks),
-                                         buf_count, buf_dtype, nranks, false, static_cast<hipStream_t>(stream));
+                                         buf_count, buf_dtype, nranks, false, false,
+                                         static_cast<hipStream_t>(stream));
   return e == hipSuccess ? HVDX_OK : hip_fail(e, "pack launch");
 }
 
 // The copy-in fused with adding step 0, or the copy-out fused with replacing step N-2
-// (arguments already checked, nranks >= 3, buf_count > 0).
+// (arguments already checked, nranks >= 3, buf_count > 0).  Inside a whole cycle the
+// copy-in leaves out each chunk's sender's copy of its own chunk: the sender's value
+// goes straight from its tensor into the receiver's sum, and replacing step 0
+// overwrites that copy before anything reads it.
 static int run_pack_rs(const void* const* srcs, const int64_t* numel, const int64_t* offset, int ntensors,
                        int src_dtype, void* const* bufs, int64_t buf_count, int buf_dtype, int nranks,
-                       hipStream_t st) {
+                       bool in_cycle, hipStream_t st) {
   TimedLaunch timed(HVDX_KERNEL_PACK_RS, 0, nranks, buf_dtype, HVDX_COMPRESS_NONE, buf_count, st);
   TimedLaunch timed_phase(HVDX_KERNEL_PACK_RS, 0, nranks, buf_dtype, HVDX_COMPRESS_NONE, buf_count, st, -1, true);
   const hipError_t e = hvdx::launch_pack(srcs, numel, offset, ntensors, src_dtype, rank_ptrs(bufs, nranks), buf_count,
-                                         buf_dtype, nranks, true, st);
+                                         buf_dtype, nranks, true, in_cycle, st);
   return e == hipSuccess ? HVDX_OK : hip_fail(e, "fused copy-in launch");
 }
 
@@ -471,7 +475,7 @@ int hvdx_fuse_pack_rs(const void* const* srcs, const int64_t* numel, const int64
   if (nranks < 3)
     return fail(HVDX_ERR_UNSUPPORTED, "hvdx_fuse_pack_rs: needs 3 or more ranks (adding step 0 is the last one)");
   if (buf_count == 0) return HVDX_OK;
-  return run_pack_rs(srcs, numel, offset, ntensors, src_dtype, bufs, buf_count, buf_dtype, nranks,
+  return run_pack_rs(srcs, numel, offset, ntensors, src_dtype, bufs, buf_count, buf_dtype, nranks, false,
                      static_cast<hipStream_t>(stream));
 }
 
@@ -589,7 +593,7 @@ int hvdx_fuse_allreduce(void* const* tensors, const int64_t* numel, const int64_
                             stream);
   }
   const int last = nranks - 2;
-  rc = run_pack_rs(srcs, numel, offset, ntensors, tensor_dtype, bufs, buf_count, buf_dtype, nranks, st);
+  rc = run_pack_rs(srcs, numel, offset, ntensors, tensor_dtype, bufs, buf_count, buf_dtype, nranks, true, st);
   if (!rc)
     rc = run_steps(bufs, nranks, buf_count, buf_dtype, op, HVDX_COMPRESS_NONE, HVDX_PHASE_REDUCE_SCATTER, 1, last,
                    nullptr, st);

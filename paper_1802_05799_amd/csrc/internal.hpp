@@ -72,10 +72,11 @@ struct BcastArgs {
 hipError_t launch_bcast_step(const RankPtrs& bufs, const BcastArgs& a, bool vector_ok, hipStream_t stream);
 
 // Launchers (fusion_kernels.hip).  With `ring` (nranks >= 3), the copy-in also does
-// the ring's adding step 0 and the copy-out its replacing step N-2.
+// the ring's adding step 0 (and with `skip_sender` leaves out each chunk's sender's
+// own copy, which the fused cycle never reads) and the copy-out its replacing step N-2.
 hipError_t launch_pack(const void* const* srcs, const int64_t* numel, const int64_t* offset, int ntensors,
                        int src_dtype, const RankPtrs& bufs, int64_t count, int buf_dtype, int nranks, bool ring,
-                       hipStream_t stream);
+                       bool skip_sender, hipStream_t stream);
 hipError_t launch_unpack(const RankPtrs& bufs, int64_t count, int buf_dtype, void* const* dsts,
                          const int64_t* numel, const int64_t* offset, int ntensors, int dst_dtype, int nranks,
                          bool ring, hipStream_t stream);
