@@ -10,8 +10,8 @@ The metric is algorithm bandwidth: one rank's fp32 gradient bytes / step time.
 Prints one JSON line.  Besides the headline workload it reports, per workload,
 the step time and the per-kernel time split measured with HIP events; the roofline
 object is for the kernel with the largest share of the step (HBM-bound: achieved
-algorithmic bytes / time against the 8 TB/s peak).  `cpu_baseline` times the CPU
-oracle on a bounded sample of the same workload on this host.
+algorithmic bytes / time against the 8 TB/s peak).  `cpu_baseline` times the C
+oracle on the same whole workload on this host's cores.
 """
 from __future__ import annotations
 
@@ -37,7 +37,7 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-ablation", action="store_true", help="skip the fusion-threshold sweep")
     p.add_argument("--no-broadcast", action="store_true", help="skip the broadcast measurement")
-    p.add_argument("--cpu-seconds", type=float, default=12.0, help="target oracle time for the CPU baseline")
+    p.add_argument("--cpu-seconds", type=float, default=10.0, help="target oracle time for the CPU baseline")
     p.add_argument("--calibration-copy-mib", type=int, default=0,
                    help="first run 3 plain device copies of this many MiB (a known-traffic kernel for counters)")
     p.add_argument("--summarize-profiles", metavar="DIR",
@@ -419,39 +419,49 @@ def summarize_profiles(d):
 
 
 def cpu_baseline(name, target_s):
-    """The oracle (plan, copy-in, ring, copy-out) on a bounded sample of the workload:
-    all N ranks, the last tensors of the ready list (the network's first layers, many
-    small tensors) up to 1.5M elements per rank, repeated until about target_s seconds."""
+    """The C oracle (oracle/csrc/oracle.c: plan, copy-in, ring, copy-out) on the whole
+    workload: every rank's tensors from the workload's seeded generator, copied to host
+    memory; the fusion buffers allocated once, as the paper's step 2 allocates the
+    fusion buffer once.  Timed with every thread OpenMP is given (OMP_NUM_THREADS),
+    repeated until about target_s seconds, and once with a single thread."""
     import numpy as np
+    import torch
 
-    from oracle import allreduce as oall
-    from workloads import configs, rng
+    from oracle import native
+    from workloads import configs
+    from workloads import gpu as wgpu
 
     w = configs.get(name)
-    numel, prefix = w.numel(), w.prefix()
-    pick, total = [], 0
-    for t in range(len(numel) - 1, -1, -1):
-        if total >= 1_500_000:
-            break
-        pick.append(t)
-        total += numel[t]
-    pick.reverse()
-    inputs = [[rng.values(w.dist, w.key(r), np.arange(prefix[t], prefix[t] + numel[t]), w.sigma) for t in pick]
-              for r in range(w.nranks)]
-    reps, t_oracle = 0, 0.0
-    while t_oracle < target_s:
+    numel = w.numel()
+    per_rank_dev, storage, starts = wgpu.make_rank_tensors(w, device="cuda:0")
+    torch.cuda.synchronize()
+    flats = [f.cpu().numpy() for f in storage]
+    del per_rank_dev, storage
+    torch.cuda.empty_cache()
+    inputs = [[flat[s : s + n] for s, n in zip(starts, numel)] for flat in flats]
+    out = [[np.ones(n, dtype=np.float32) for n in numel] for _ in range(w.nranks)]  # touched before timing
+    ws = np.ones(native.workspace_bytes(numel, w.nranks, compress=w.compress), dtype=np.uint8)
+    threads = native.max_threads()
+    native.allreduce(inputs, w.op, compress=w.compress, threads=threads, out=out, workspace=ws)  # warm-up
+    reps, t_threads = 0, 0.0
+    while t_threads < target_s:
         t0 = time.perf_counter()
-        oall.allreduce(inputs, w.op, compress=w.compress)
-        t_oracle += time.perf_counter() - t0
+        native.allreduce(inputs, w.op, compress=w.compress, threads=threads, out=out, workspace=ws)
+        t_threads += time.perf_counter() - t0
         reps += 1
-    rank_bytes = 4 * total
+    t0 = time.perf_counter()
+    native.allreduce(inputs, w.op, compress=w.compress, threads=1, out=out, workspace=ws)
+    t_one = time.perf_counter() - t0
+    rank_bytes = 4 * sum(numel)
     return {
-        "value": rank_bytes * reps / t_oracle / 1e9,
+        "value": rank_bytes * reps / t_threads / 1e9,
         "unit": "GB/s",
-        "cores": 1,
+        "cores": threads,
         "kind": "oracle",
-        "sample": f"{name}: {len(pick)} tensors ({total} elements per rank, the first layers), "
-        f"{w.nranks} ranks, {reps} runs in {t_oracle:.1f} s, numpy single thread",
+        "sample": f"{name} whole: {len(numel)} tensors, {sum(numel)} elements per rank, {w.nranks} ranks; "
+        f"C oracle, {threads} OpenMP threads, {reps} allreduces in {t_threads:.1f} s",
+        "ms_per_allreduce": 1e3 * t_threads / reps,
+        "single_thread": {"value": rank_bytes / t_one / 1e9, "ms_per_allreduce": 1e3 * t_one},
         "host_cpus": os.cpu_count(),
     }
 

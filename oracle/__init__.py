@@ -17,6 +17,9 @@ Plain, slow, written to be checked against the paper by eye:
                    that averages gradients).
 * ``broadcast`` -- the root's variables copied to every rank (paper sections 4
                    and 5), as a pipelined chain along the ring.
+* ``native``    -- the same allreduce as plain C (``csrc/oracle.c``, built by
+                   ``build.py``), bit-identical to the numpy modules, fast enough to
+                   run whole workloads on the host's cores.
 
 Arithmetic is in the buffer's precision (binary32, or binary16 when compressed),
 because the result of the method is defined by that arithmetic in ring order; an
