@@ -463,7 +463,19 @@ def cpu_baseline(name, target_s):
         "ms_per_allreduce": 1e3 * t_threads / reps,
         "single_thread": {"value": rank_bytes / t_one / 1e9, "ms_per_allreduce": 1e3 * t_one},
         "host_cpus": os.cpu_count(),
+        "host_cpu_model": host_cpu_model(),
     }
+
+
+def host_cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
 
 
 def main():
