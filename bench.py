@@ -40,6 +40,8 @@ def parse():
     p.add_argument("--cpu-seconds", type=float, default=10.0, help="target oracle time for the CPU baseline")
     p.add_argument("--calibration-copy-mib", type=int, default=0,
                    help="first run 3 plain device copies of this many MiB (a known-traffic kernel for counters)")
+    p.add_argument("--oracle-configs", metavar="NAMES",
+                   help="time only the C oracle on these workloads (comma-separated, whole, host cores) and exit")
     p.add_argument("--summarize-profiles", metavar="DIR",
                    help="no GPU: summarize rocprofv3 output under DIR (prof_*/ kernel stats, pmc_fetch/, pmc_write/) "
                         "into profiles/")
@@ -418,12 +420,10 @@ def summarize_profiles(d):
     return "\n".join(out_lines)
 
 
-def cpu_baseline(name, target_s):
-    """The C oracle (oracle/csrc/oracle.c: plan, copy-in, ring, copy-out) on the whole
-    workload: every rank's tensors from the workload's seeded generator, copied to host
-    memory; the fusion buffers allocated once, as the paper's step 2 allocates the
-    fusion buffer once.  Timed with every thread OpenMP is given (OMP_NUM_THREADS),
-    repeated until about target_s seconds, and once with a single thread."""
+def _oracle_inputs(name):
+    """Every rank's tensors of workload `name` in host memory, from the workload's seeded
+    generator (run on the GPU, then copied), with preallocated, touched outputs and a
+    fusion-buffer workspace for the C oracle."""
     import numpy as np
     import torch
 
@@ -441,17 +441,36 @@ def cpu_baseline(name, target_s):
     inputs = [[flat[s : s + n] for s, n in zip(starts, numel)] for flat in flats]
     out = [[np.ones(n, dtype=np.float32) for n in numel] for _ in range(w.nranks)]  # touched before timing
     ws = np.ones(native.workspace_bytes(numel, w.nranks, compress=w.compress), dtype=np.uint8)
-    threads = native.max_threads()
-    native.allreduce(inputs, w.op, compress=w.compress, threads=threads, out=out, workspace=ws)  # warm-up
-    reps, t_threads = 0, 0.0
-    while t_threads < target_s:
+    return w, inputs, out, ws
+
+
+def _time_oracle(w, inputs, out, ws, threads, target_s):
+    """(allreduces, seconds): the C oracle repeated until about target_s seconds."""
+    from oracle import native
+
+    reps, spent = 0, 0.0
+    while reps == 0 or spent < target_s:
         t0 = time.perf_counter()
         native.allreduce(inputs, w.op, compress=w.compress, threads=threads, out=out, workspace=ws)
-        t_threads += time.perf_counter() - t0
+        spent += time.perf_counter() - t0
         reps += 1
-    t0 = time.perf_counter()
-    native.allreduce(inputs, w.op, compress=w.compress, threads=1, out=out, workspace=ws)
-    t_one = time.perf_counter() - t0
+    return reps, spent
+
+
+def cpu_baseline(name, target_s):
+    """The C oracle (oracle/csrc/oracle.c: plan, copy-in, ring, copy-out) on the whole
+    workload: every rank's tensors from the workload's seeded generator, copied to host
+    memory; the fusion buffers allocated once, as the paper's step 2 allocates the
+    fusion buffer once.  Timed with every thread OpenMP is given (OMP_NUM_THREADS),
+    repeated until about target_s seconds, and once with a single thread."""
+    from oracle import native
+
+    w, inputs, out, ws = _oracle_inputs(name)
+    numel = w.numel()
+    threads = native.max_threads()
+    _time_oracle(w, inputs, out, ws, threads, 0.0)  # warm-up
+    reps, t_threads = _time_oracle(w, inputs, out, ws, threads, target_s)
+    _, t_one = _time_oracle(w, inputs, out, ws, 1, 0.0)
     rank_bytes = 4 * sum(numel)
     return {
         "value": rank_bytes * reps / t_threads / 1e9,
@@ -465,6 +484,42 @@ def cpu_baseline(name, target_s):
         "host_cpus": os.cpu_count(),
         "host_cpu_model": host_cpu_model(),
     }
+
+
+def oracle_per_config(names, target_s):
+    """The C oracle on every named workload, whole: one warm-up allreduce, then all
+    OpenMP threads until about target_s seconds, then one allreduce on one thread."""
+    import gc
+
+    from oracle import native
+
+    res = {}
+    threads = native.max_threads()
+    for name in names:
+        print(f"oracle {name}: inputs", file=sys.stderr, flush=True)
+        w, inputs, out, ws = _oracle_inputs(name)
+        print(f"oracle {name}: warm-up", file=sys.stderr, flush=True)
+        _time_oracle(w, inputs, out, ws, threads, 0.0)
+        print(f"oracle {name}: {threads} threads", file=sys.stderr, flush=True)
+        reps, t_threads = _time_oracle(w, inputs, out, ws, threads, target_s)
+        rank_bytes = 4 * sum(w.numel())
+        res[name] = {
+            "nranks": w.nranks,
+            "threads": threads,
+            "ms_threads": round(1e3 * t_threads / reps, 3),
+            "algbw_threads_GBps": round(rank_bytes * reps / t_threads / 1e9, 4),
+            "allreduces": reps,
+        }
+        # one thread takes up to `threads` times as long; left out where that could pass two minutes
+        if t_threads / reps * threads <= 120.0:
+            print(f"oracle {name}: one thread", file=sys.stderr, flush=True)
+            _, t_one = _time_oracle(w, inputs, out, ws, 1, 0.0)
+            res[name]["ms_one_thread"] = round(1e3 * t_one, 3)
+            res[name]["algbw_one_thread_GBps"] = round(rank_bytes / t_one / 1e9, 4)
+        print(f"oracle {name}: {res[name]}", file=sys.stderr, flush=True)
+        del inputs, out, ws
+        gc.collect()
+    return {"oracle_per_config": res, "host_cpus": os.cpu_count(), "host_cpu_model": host_cpu_model()}
 
 
 def host_cpu_model():
@@ -482,6 +537,9 @@ def main():
     args = parse()
     if args.summarize_profiles:
         print(summarize_profiles(args.summarize_profiles))
+        return
+    if args.oracle_configs:
+        print(json.dumps(oracle_per_config(args.oracle_configs.split(","), args.cpu_seconds)), flush=True)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print(
