@@ -47,6 +47,7 @@ PACK_CASES = [
     ([33, 31, 1, 2, 3, 4, 5, 6, 7, 8, 9, 100000], 5, 4, 64),
     ([257] * 40 + [70000, 3, 9000], 7, 2, 16),  # binary16 buffer
     ([257] * 40 + [70000, 3, 9000], 7, 2, 2),
+    ([5000, 3, 70000], 128, 4, 16),  # the most ranks a call takes
 ]
 
 
@@ -112,6 +113,8 @@ CYCLE_CASES = [
     ([3000, 1, 2, 50000, 64, 64, 64, 128 * 1024, 9], 6, 40000, True, "average"),
     ([3000, 1, 2, 50000, 64, 64, 64, 128 * 1024, 9], 5, 40000, False, "average"),
     ([1], 1, 64, True, "average"),
+    ([5000, 300, 70000, 9], 128, 40000, False, "average"),  # the most ranks a call takes
+    ([5000, 300, 70000, 9], 128, 40000, True, "average"),
 ]
 
 
@@ -143,6 +146,8 @@ FUSED_CASES = [
     ([257] * 40 + [70000, 3, 9000], 6, np.float16, 16),  # binary16 buffer
     ([1, 0, 2], 8, np.float32, 16),  # fewer buffer elements than ranks: empty chunks
     ([3000, 1, 2, 50000, 64, 64, 64, 128 * 1024, 9], 13, np.float16, 2),
+    ([5000, 300, 70000], 128, np.float32, 16),  # the most ranks a call takes
+    ([5000, 300, 70001], 128, np.float16, 2),
 ]
 
 

@@ -65,6 +65,7 @@ SMALL_CASES = [
     ([1, 0, 2], 8, np.float32, 16, "sum"),  # fewer buffer elements than ranks
     ([3000, 1, 2, 50000, 64, 64, 64, 128 * 1024, 9], 13, np.float16, 2, "average"),
     ([5000, 300, 70000], 32, np.float32, 16, "average"),
+    ([5000, 300, 70001], 128, np.float16, 2, "average"),  # the most ranks a call takes
 ]
 
 
