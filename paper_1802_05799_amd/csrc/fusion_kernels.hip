@@ -17,8 +17,6 @@
 namespace hvdx {
 namespace {
 
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 
 // Shape of a copy kernel: POS 16-byte buffer vectors per lane in a row (a row is
 // kBlock*POS vectors), SUB rows per block (one tensor lookup serves them all), RB
@@ -56,8 +54,8 @@ struct CopyCfg {
 #ifndef HVDX_PACK16_CFG
 #define HVDX_PACK16_CFG HVDX_PACK_CFG
 #endif
-#ifndef HVDX_UNPACK16_CFG  // binary16 -> binary32 writes twice what it reads: cached stores win
-#define HVDX_UNPACK16_CFG CopyCfg<2, 2, 2, false, false>
+#ifndef HVDX_UNPACK16_CFG
+#define HVDX_UNPACK16_CFG HVDX_UNPACK_CFG
 #endif
 using PackCfg = HVDX_PACK_CFG;      // binary32 buffers
 using UnpackCfg = HVDX_UNPACK_CFG;
@@ -78,13 +76,21 @@ __device__ __forceinline__ int tile_vec(int u) {
   return u * kBlock + threadIdx.x;
 }
 
-template <typename TB>
+// Elements a lane moves as one vector: 16 bytes on the wider side, so that every load
+// and store instruction of a wavefront covers one contiguous run of memory (binary32
+// tensors with a binary16 buffer: 16-byte tensor vectors, 8-byte buffer vectors).
+template <typename TT, typename TB>
 struct BufVec {
-  static constexpr int n = 16 / sizeof(TB);  // buffer elements per 16 bytes
+  static constexpr int n = 16 / (sizeof(TT) > sizeof(TB) ? sizeof(TT) : sizeof(TB));
 };
 
-// Convert and move VEC = 16/sizeof(TB) elements between a tensor of type TT and
-// the buffer of type TB (TT == TB, or TT = float and TB = _Float16).
+// Host side: the same count from the data types.
+inline int64_t vec_elems(int tensor_dtype, int buf_dtype) {
+  return tensor_dtype == HVDX_FLOAT32 || buf_dtype == HVDX_FLOAT32 ? 4 : 8;
+}
+
+// Convert and move BufVec<TT, TB>::n elements between a tensor of type TT and the
+// buffer of type TB (TT == TB, or TT = float and TB = _Float16).
 template <typename TT, typename TB>
 struct Mover;
 
@@ -149,52 +155,37 @@ struct Mover<_Float16, _Float16> {
 };
 
 template <>
-struct Mover<float, _Float16> {  // tensor binary32, buffer binary16
-  using buf_vec = f16x8;
+struct Mover<float, _Float16> {  // tensor binary32 (16-byte vectors), buffer binary16 (8-byte vectors)
+  using buf_vec = f16x4;
   template <bool NT>
-  __device__ static f16x8 load(const float* src) {
-    f32x4 lo, hi;
-    if (aligned16(src)) {
-      lo = ld16<NT>(reinterpret_cast<const f32x4*>(src));
-      hi = ld16<NT>(reinterpret_cast<const f32x4*>(src) + 1);
-    } else {
-      lo = f32x4{src[0], src[1], src[2], src[3]};
-      hi = f32x4{src[4], src[5], src[6], src[7]};
-    }
-    f16x8 h;
+  __device__ static f16x4 load(const float* src) {
+    const f32x4 x = aligned16(src) ? ld16<NT>(reinterpret_cast<const f32x4*>(src))
+                                   : f32x4{src[0], src[1], src[2], src[3]};
+    f16x4 h;
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      h[k] = (_Float16)lo[k];
-      h[k + 4] = (_Float16)hi[k];
-    }
+    for (int k = 0; k < 4; ++k) h[k] = (_Float16)x[k];
     return h;
   }
   template <bool NT>
-  __device__ static void store(float* dst, f16x8 h) {
-    f32x4 lo, hi;
+  __device__ static void store(float* dst, f16x4 h) {
+    f32x4 x;
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      lo[k] = (float)h[k];
-      hi[k] = (float)h[k + 4];
-    }
+    for (int k = 0; k < 4; ++k) x[k] = (float)h[k];
     if (aligned16(dst)) {
-      st16<NT>(reinterpret_cast<f32x4*>(dst), lo);
-      st16<NT>(reinterpret_cast<f32x4*>(dst) + 1, hi);
+      st16<NT>(reinterpret_cast<f32x4*>(dst), x);
       return;
     }
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      dst[k] = lo[k];
-      dst[k + 4] = hi[k];
-    }
+    for (int k = 0; k < 4; ++k) dst[k] = x[k];
   }
   __device__ static _Float16 cvt_in(float v) { return (_Float16)v; }
   __device__ static float cvt_out(_Float16 v) { return (float)v; }
 };
 
-__device__ __forceinline__ void store_zero(float* p) { *reinterpret_cast<f32x4*>(p) = (f32x4)(0.0f); }
-__device__ __forceinline__ void store_zero(_Float16* p) {
-  *reinterpret_cast<f16x8*>(p) = (f16x8)((_Float16)0.0f);
+// Zero one buffer vector (padding).
+template <typename VB, typename TB>
+__device__ __forceinline__ void store_zero(TB* p) {
+  *reinterpret_cast<VB*>(p) = (VB)((TB)0);
 }
 
 // Last tensor t in [lo, hi) whose offset is <= p, or lo - 1 if none (global memory).
@@ -414,7 +405,7 @@ __global__ __launch_bounds__(kBlock) HVDX_COPY_ATTR void pack_kernel(const void*
                                                                     int64_t q, int64_t rem, int skip_sender) {
   static_assert(!RING || (Cfg::RB >= 2 && (Cfg::RPB == 0 || Cfg::RPB >= 2)),
                 "the fused copy-in needs the sender and receiver in one load batch");
-  constexpr int V = BufVec<TB>::n;
+  constexpr int V = BufVec<TT, TB>::n;
   using VB = typename Mover<TT, TB>::buf_vec;
   constexpr int kPosPerLane = Cfg::POS, kRankBatch = Cfg::RB, kTileVecs = Cfg::kTileVecs;
   __shared__ int64_t s_off[Cfg::kLdsTensors], s_end[Cfg::kLdsTensors], s_meta[2];
@@ -464,7 +455,7 @@ __global__ __launch_bounds__(kBlock) HVDX_COPY_ATTR void pack_kernel(const void*
             if (RING && rr > 0 && slot == 1) x = x + v[rr > 0 ? rr - 1 : 0][u];  // receiver: own + sender's
             st16<Cfg::NTS>(reinterpret_cast<VB*>(buf + pos[u].p), x);
           } else if (pos[u].cls == POS_ZERO) {
-            store_zero(buf + pos[u].p);  // padding: zero, and zero + zero for a receiver
+            store_zero<VB>(buf + pos[u].p);  // padding: zero, and zero + zero for a receiver
           }
         }
       }
@@ -508,7 +499,7 @@ __global__ __launch_bounds__(kBlock) HVDX_COPY_ATTR void unpack_kernel(RankPtrs 
                                                                       const int64_t* __restrict__ numel,
                                                                       const int64_t* __restrict__ offset, int ntensors,
                                                                       int nranks, int rpb, int64_t q, int64_t rem) {
-  constexpr int V = BufVec<TB>::n;
+  constexpr int V = BufVec<TT, TB>::n;
   using VB = typename Mover<TT, TB>::buf_vec;
   constexpr int kPosPerLane = Cfg::POS, kRankBatch = Cfg::RB, kTileVecs = Cfg::kTileVecs;
   __shared__ int64_t s_off[Cfg::kLdsTensors], s_end[Cfg::kLdsTensors], s_meta[2];
@@ -599,7 +590,7 @@ __global__ __launch_bounds__(kBlock) void small_cycle_kernel(const void* const* 
   using Cfg = SmallCfg;
   using M = Mover<TT, TB>;
   using VB = typename M::buf_vec;
-  constexpr int V = BufVec<TB>::n;
+  constexpr int V = BufVec<TT, TB>::n;
   __shared__ int64_t s_off[Cfg::kLdsTensors], s_end[Cfg::kLdsTensors], s_meta[2];
   __shared__ const void* s_ptr[kLdsPtrs];
   const int n = a.n;
@@ -640,9 +631,8 @@ __global__ __launch_bounds__(kBlock) void small_cycle_kernel(const void* const* 
 }
 
 template <typename Cfg>
-unsigned tiles_for(int64_t count, int buf_dtype) {
-  const int64_t v = buf_dtype == HVDX_FLOAT32 ? 4 : 8;
-  const int64_t per = (int64_t)Cfg::kTileVecs * v;
+unsigned tiles_for(int64_t count, int64_t vec) {
+  const int64_t per = (int64_t)Cfg::kTileVecs * vec;
   return (unsigned)((count + per - 1) / per);
 }
 
@@ -652,20 +642,20 @@ int ranks_per_block(int nranks) { return Cfg::RPB > 0 && Cfg::RPB < nranks ? Cfg
 // Plain: (tiles, rank groups).  Fused with a ring step: (tiles a chunk can meet --
 // its length plus up to a tile of slack before its start -- chunks, rank groups).
 template <typename Cfg, bool RING>
-dim3 copy_grid(int64_t count, int buf_dtype, int nranks) {
+dim3 copy_grid(int64_t count, int64_t vec, int nranks) {
   const int rpb = ranks_per_block<Cfg>(nranks);
   const unsigned groups = (unsigned)((nranks + rpb - 1) / rpb);
-  if (!RING) return dim3(tiles_for<Cfg>(count, buf_dtype), groups);
-  const int64_t tile = (int64_t)Cfg::kTileVecs * (buf_dtype == HVDX_FLOAT32 ? 4 : 8);
+  if (!RING) return dim3(tiles_for<Cfg>(count, vec), groups);
+  const int64_t tile = (int64_t)Cfg::kTileVecs * vec;
   const int64_t longest = count / nranks + (count % nranks ? 1 : 0);
-  return dim3(tiles_for<Cfg>(longest + tile - 1, buf_dtype), (unsigned)nranks, groups);
+  return dim3(tiles_for<Cfg>(longest + tile - 1, vec), (unsigned)nranks, groups);
 }
 
 template <typename Cfg, bool RING>
 void pack_with(const void* const* srcs, const int64_t* numel, const int64_t* offset, int ntensors, int src_dtype,
                const RankPtrs& bufs, int64_t count, int buf_dtype, int nranks, int skip_sender, hipStream_t stream) {
   const int rpb = ranks_per_block<Cfg>(nranks);
-  const dim3 grid = copy_grid<Cfg, RING>(count, buf_dtype, nranks);
+  const dim3 grid = copy_grid<Cfg, RING>(count, vec_elems(src_dtype, buf_dtype), nranks);
   const int64_t q = count / nranks, rem = count % nranks;
   if (src_dtype == HVDX_FLOAT32 && buf_dtype == HVDX_FLOAT32)
     HVDX_LAUNCH((pack_kernel<float, float, Cfg, RING>), grid, dim3(kBlock), 0, stream, srcs, numel, offset,
@@ -682,7 +672,7 @@ template <typename Cfg, bool RING>
 void unpack_with(const RankPtrs& bufs, int64_t count, int buf_dtype, void* const* dsts, const int64_t* numel,
                  const int64_t* offset, int ntensors, int dst_dtype, int nranks, hipStream_t stream) {
   const int rpb = ranks_per_block<Cfg>(nranks);
-  const dim3 grid = copy_grid<Cfg, RING>(count, buf_dtype, nranks);
+  const dim3 grid = copy_grid<Cfg, RING>(count, vec_elems(dst_dtype, buf_dtype), nranks);
   const int64_t q = count / nranks, rem = count % nranks;
   if (dst_dtype == HVDX_FLOAT32 && buf_dtype == HVDX_FLOAT32)
     HVDX_LAUNCH((unpack_kernel<float, float, Cfg, RING>), grid, dim3(kBlock), 0, stream, bufs, count, dsts,
@@ -719,7 +709,7 @@ hipError_t launch_pack(const void* const* srcs, const int64_t* numel, const int6
 hipError_t launch_small_cycle(const void* const* tensors, const int64_t* numel, const int64_t* offset, int ntensors,
                               int tensor_dtype, const RankPtrs& bufs, const RingArgs& a, int64_t count, int buf_dtype,
                               int divmode, hipStream_t stream) {
-  const dim3 grid(tiles_for<SmallCfg>(count, buf_dtype)), block(kBlock);
+  const dim3 grid(tiles_for<SmallCfg>(count, vec_elems(tensor_dtype, buf_dtype))), block(kBlock);
 #define HVDX_SMALL(TT, TB, DIV) \
   HVDX_LAUNCH((small_cycle_kernel<TT, TB, DIV>), grid, block, 0, stream, tensors, numel, offset, ntensors, \
                      bufs, a, count)

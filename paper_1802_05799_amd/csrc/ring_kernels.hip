@@ -213,12 +213,18 @@ __device__ __forceinline__ f16x8 to_f16x8(f32x4 lo, f32x4 hi) {
   return h;
 }
 
-__device__ __forceinline__ void from_f16x8(f16x8 h, f32x4& lo, f32x4& hi) {
+__device__ __forceinline__ f16x4 narrow4(f32x4 x) {
+  f16x4 h;
 #pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    lo[k] = (float)h[k];
-    hi[k] = (float)h[k + 4];
-  }
+  for (int k = 0; k < 4; ++k) h[k] = (_Float16)x[k];
+  return h;
+}
+
+__device__ __forceinline__ f32x4 widen4(f16x4 h) {
+  f32x4 x;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) x[k] = (float)h[k];
+  return x;
 }
 
 template <int DIV, bool FIRST, bool VEC_OK, typename P>
@@ -284,9 +290,11 @@ __global__ __launch_bounds__(P::BS) void ag_first_c16_kernel(RankPtrs x, const _
   float* __restrict__ xr = static_cast<float*>(x.p[rcv]) + ch.start;
   const _Float16* __restrict__ ws = wire + (int64_t)snd * a.wire_stride + ch.start;
 
-  const int64_t head = VEC_OK ? head_elems<_Float16>(ws, ch.len) : ch.len;
-  const int64_t nvec = (ch.len - head) / 8;
-  const int64_t tail = head + nvec * 8;
+  // four elements per lane: 16-byte binary32 stores, 8-byte binary16 loads, each
+  // contiguous across the wavefront (the binary32 side fixes the alignment)
+  const int64_t head = VEC_OK ? head_elems<float>(xs, ch.len) : ch.len;
+  const int64_t nvec = (ch.len - head) / 4;
+  const int64_t tail = head + nvec * 4;
   const int64_t gtid = (int64_t)blockIdx.x * BS + threadIdx.x;
   const int64_t gthreads = (int64_t)gridDim.x * BS;
   auto one = [&](int64_t e) {
@@ -299,24 +307,21 @@ __global__ __launch_bounds__(P::BS) void ag_first_c16_kernel(RankPtrs x, const _
 
   f32x4* __restrict__ xs4 = reinterpret_cast<f32x4*>(xs + head);
   f32x4* __restrict__ xr4 = reinterpret_cast<f32x4*>(xr + head);
-  const f16x8* __restrict__ ws8 = reinterpret_cast<const f16x8*>(ws + head);
+  const f16x4* __restrict__ ws4 = reinterpret_cast<const f16x4*>(ws + head);
   for (int64_t blk = (int64_t)blockIdx.x * BS * U; blk < nvec; blk += gthreads * U) {
-    f16x8 h[U];
+    f16x4 h[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int64_t i = lane_vec<P>(blk, u);
-      if (i < nvec) h[u] = vload<P::NTL>(ws8 + i);
+      if (i < nvec) h[u] = vload<P::NTL>(ws4 + i);
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int64_t i = lane_vec<P>(blk, u);
       if (i < nvec) {
-        f32x4 lo, hi;
-        from_f16x8(h[u], lo, hi);
-        vstore<P::NTS>(xs4 + 2 * i, lo);
-        vstore<P::NTS>(xs4 + 2 * i + 1, hi);
-        vstore<P::NTS>(xr4 + 2 * i, lo);
-        vstore<P::NTS>(xr4 + 2 * i + 1, hi);
+        const f32x4 f = widen4(h[u]);
+        vstore<P::NTS>(xs4 + i, f);
+        vstore<P::NTS>(xr4 + i, f);
       }
     }
   }
@@ -397,9 +402,11 @@ __global__ __launch_bounds__(P::BS) void rs_ag_step_c16_kernel(RankPtrs x, const
   float* xn = static_cast<float*>(x.p[c]) + ch.start;
   const _Float16* ws = wire + (int64_t)snd * a.wire_stride + ch.start;
 
-  const int64_t head = VEC_OK ? head_elems<_Float16>(ws, ch.len) : ch.len;
-  const int64_t nvec = (ch.len - head) / 8;
-  const int64_t tail = head + nvec * 8;
+  // four elements per lane, so that the binary32 loads and both binary32 stores are
+  // 16 bytes per lane and contiguous across the wavefront
+  const int64_t head = VEC_OK ? head_elems<float>(xo, ch.len) : ch.len;
+  const int64_t nvec = (ch.len - head) / 4;
+  const int64_t tail = head + nvec * 4;
   const int64_t gtid = (int64_t)blockIdx.x * BS + threadIdx.x;
   const int64_t gthreads = (int64_t)gridDim.x * BS;
   auto one = [&](int64_t e) {
@@ -414,29 +421,24 @@ __global__ __launch_bounds__(P::BS) void rs_ag_step_c16_kernel(RankPtrs x, const
   const f32x4* xs4 = reinterpret_cast<const f32x4*>(xs + head);
   f32x4* __restrict__ xo4 = reinterpret_cast<f32x4*>(xo + head);
   f32x4* xn4 = reinterpret_cast<f32x4*>(xn + head);
-  const f16x8* ws8 = reinterpret_cast<const f16x8*>(ws + head);
+  const f16x4* ws4 = reinterpret_cast<const f16x4*>(ws + head);
   for (int64_t blk = (int64_t)blockIdx.x * BS * U; blk < nvec; blk += gthreads * U) {
-    f16x8 sent[U], mine[U];
+    f16x4 sent[U], mine[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int64_t i = lane_vec<P>(blk, u);
       if (i < nvec) {
-        mine[u] = to_f16x8(vload<P::NTL>(xo4 + 2 * i), vload<P::NTL>(xo4 + 2 * i + 1));
-        sent[u] = FIRST ? to_f16x8(vload<P::NTL>(xs4 + 2 * i), vload<P::NTL>(xs4 + 2 * i + 1))
-                        : vload<P::NTL>(ws8 + i);
+        mine[u] = narrow4(vload<P::NTL>(xo4 + i));
+        sent[u] = FIRST ? narrow4(vload<P::NTL>(xs4 + i)) : vload<P::NTL>(ws4 + i);
       }
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int64_t i = lane_vec<P>(blk, u);
       if (i < nvec) {
-        const f16x8 h = combine<DIV>(mine[u], sent[u], a);
-        f32x4 lo, hi;
-        from_f16x8(h, lo, hi);
-        vstore<P::NTS>(xo4 + 2 * i, lo);
-        vstore<P::NTS>(xo4 + 2 * i + 1, hi);
-        vstore<P::NTS>(xn4 + 2 * i, lo);
-        vstore<P::NTS>(xn4 + 2 * i + 1, hi);
+        const f32x4 f = widen4(combine<DIV>(mine[u], sent[u], a));
+        vstore<P::NTS>(xo4 + i, f);
+        vstore<P::NTS>(xn4 + i, f);
       }
     }
   }
@@ -644,7 +646,7 @@ void rs_c16_launch(const RankPtrs& x, _Float16* w, const RingArgs& a, int divmod
 
 template <typename P>
 void ag_first_c16_launch(const RankPtrs& x, const _Float16* w, const RingArgs& a, bool vector_ok, hipStream_t stream) {
-  const dim3 grid = step_grid(a, 8, P::U, P::BS);
+  const dim3 grid = step_grid(a, 4, P::U, P::BS);
   if (vector_ok) HVDX_LAUNCH((ag_first_c16_kernel<true, P>), grid, dim3(P::BS), 0, stream, x, w, a);
   else HVDX_LAUNCH((ag_first_c16_kernel<false, P>), grid, dim3(P::BS), 0, stream, x, w, a);
 }
@@ -713,7 +715,7 @@ namespace {
 template <typename P>
 void rs_ag_c16_launch(const RankPtrs& x, _Float16* w, const RingArgs& a, int divmode, bool vector_ok,
                       hipStream_t stream) {
-  const dim3 grid = step_grid(a, 8, P::U, P::BS);
+  const dim3 grid = step_grid(a, 4, P::U, P::BS);
   const bool first = a.n == 2;  // step N-2 is also the first adding step when N = 2
 #define HVDX_RAC(DIV, F, VOK) \
   HVDX_LAUNCH((rs_ag_step_c16_kernel<DIV, F, VOK, P>), grid, dim3(P::BS), 0, stream, x, w, a)

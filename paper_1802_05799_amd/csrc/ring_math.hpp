@@ -10,6 +10,7 @@ namespace {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
 
 template <typename T>
 struct Vec;
@@ -71,6 +72,17 @@ __device__ __forceinline__ f16x8 combine(f16x8 local, f16x8 recv, const RingArgs
   return s;
 }
 
+template <int DIV>
+__device__ __forceinline__ f16x4 combine(f16x4 local, f16x4 recv, const RingArgs& a) {
+  f16x4 s = local + recv;
+  if constexpr (DIV == DIV_POW2) s = s * (f16x4)((_Float16)a.inv);
+  if constexpr (DIV == DIV_TRUE) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) s[k] = finish16<DIV>(s[k], a);
+  }
+  return s;
+}
+
 struct Chunk {
   int64_t start, len;
 };
@@ -114,6 +126,10 @@ __device__ __forceinline__ f32x4 add_step(f32x4 local, f32x4 recv, const RingArg
 }
 template <int DIV>
 __device__ __forceinline__ f16x8 add_step(f16x8 local, f16x8 recv, const RingArgs& a) {
+  return combine<DIV>(local, recv, a);
+}
+template <int DIV>
+__device__ __forceinline__ f16x4 add_step(f16x4 local, f16x4 recv, const RingArgs& a) {
   return combine<DIV>(local, recv, a);
 }
 
