@@ -38,7 +38,7 @@ struct Policy {
   static constexpr bool WAVE = WAVE_;  // a wavefront's U vectors are contiguous (else block-strided)
 };
 #ifndef HVDX_RS_CACHED
-#define HVDX_RS_CACHED Policy<4, 256, false, true>
+#define HVDX_RS_CACHED Policy<2, 256, false, true>
 #endif
 #ifndef HVDX_RS_STREAM
 #define HVDX_RS_STREAM Policy<1, 256, true, true>
