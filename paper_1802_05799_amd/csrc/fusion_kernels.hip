@@ -18,17 +18,19 @@ namespace hvdx {
 namespace {
 
 
-// Shape of a copy kernel: POS 16-byte buffer vectors per lane in a row (a row is
-// kBlock*POS vectors), SUB rows per block (one tensor lookup serves them all), RB
-// ranks whose loads are in flight together, RPB ranks per block (0 = all),
-// non-temporal loads/stores, and the lane layout.  Measured on MI355X with the
-// workloads' buckets: a block's prologue (two rounds of dependent loads to find its
-// tensors) has to be amortized over enough data in flight.  Two ranks per block with
-// two block-strided vectors per lane and one row (four loads in flight per lane,
-// 16 KiB read and written per block, 3 KiB of LDS) was best in both directions.
-// One rank per block with one vector per lane (the best pattern for a plain copy
-// between many buffers, tried with the receiver's block loading the sender's values
-// too) lost to the prologue even with 8 rows; more rows, more ranks per batch or
+// Shape of a copy kernel: POS buffer vectors per lane in a row (a row is kBlock*POS
+// vectors), SUB rows per block (one tensor lookup serves them all), RB ranks whose
+// loads are in flight together, RPB ranks per block (0 = all), non-temporal
+// loads/stores, and the lane layout.  Measured on MI355X with the workloads' buckets:
+// a block's prologue (two rounds of dependent loads to find its tensors) has to be
+// amortized over enough data.  The copy-out is best with two ranks per block and two
+// block-strided vectors per lane (four loads in flight per lane, one row); the
+// binary32 copy-in with four ranks per block in two load batches of two and one
+// vector per lane (the same tensor lookup serves twice the ranks; 0.6-0.9% off the
+// whole ResNet-50, Inception-V3 and VGG-16 allreduces against the copy-out's shape,
+// while its own rate drops 3 points and the following kernels gain more).  One rank
+// per block with one vector per lane (the best pattern for a plain copy between many
+// buffers) lost to the prologue even with 8 rows; more rows, four ranks per batch or
 // wavefront-contiguous lanes did not help either.
 #ifndef HVDX_LDS_TENSORS
 #define HVDX_LDS_TENSORS 64
@@ -46,13 +48,13 @@ struct CopyCfg {
   static constexpr int kLdsTensors = kTileVecs + 8 < HVDX_LDS_TENSORS ? kTileVecs + 8 : HVDX_LDS_TENSORS;
 };
 #ifndef HVDX_PACK_CFG
-#define HVDX_PACK_CFG CopyCfg<2, 2, 2, true, true>
+#define HVDX_PACK_CFG CopyCfg<1, 2, 4, true, true>
 #endif
 #ifndef HVDX_UNPACK_CFG
 #define HVDX_UNPACK_CFG CopyCfg<2, 2, 2, true, true>
 #endif
-#ifndef HVDX_PACK16_CFG
-#define HVDX_PACK16_CFG HVDX_PACK_CFG
+#ifndef HVDX_PACK16_CFG  // binary16 buffers: the copy-out's shape measured 2 points faster here
+#define HVDX_PACK16_CFG CopyCfg<2, 2, 2, true, true>
 #endif
 #ifndef HVDX_UNPACK16_CFG
 #define HVDX_UNPACK16_CFG HVDX_UNPACK_CFG
