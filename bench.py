@@ -78,6 +78,8 @@ def kernel_bytes(ar, kind, bi, step):
         if compressed:  # step 0 widens the owner's binary16 into two buffers; later steps copy binary32
             return (10 if step == 0 else 8) * b.count
         return 2 * es_b * b.count if not b.direct else 2 * es_t * b.count
+    if kind == "fold":  # every rank's value read once and the result written to every rank
+        return 2 * n * (es_t if b.direct else es_b) * b.count
     return 0
 
 

@@ -477,6 +477,18 @@ struct FoldTypes<float, true> {  // binary32 data, binary16 arithmetic
 
 constexpr int kFoldBatch = 8;  // ranks whose loads are in flight together
 
+// Four elements as one access: 16 bytes of binary32, 8 of binary16.
+template <typename T>
+struct Four;
+template <>
+struct Four<float> {
+  using type = f32x4;
+};
+template <>
+struct Four<_Float16> {
+  using type = f16x4;
+};
+
 template <int DIV>
 __device__ __forceinline__ float fold_finish(float v, const RingArgs& a) {
   return finish<DIV>(v, a);
@@ -497,18 +509,16 @@ __global__ __launch_bounds__(kBlock) void fold_kernel(RankPtrs bufs, RingArgs a,
     const int64_t e0 = i * V;
     const int64_t c0 = chunk_index(e0, a);
     const bool whole = VEC_OK && e0 + V <= count && chunk_index(e0 + V - 1, a) == c0;
-    if (whole) {
+    if (whole) {  // one aligned 4-element access per rank, contiguous across the wavefront
+      using VT = typename Four<T>::type;
       A acc[V];
-      T v[kFoldBatch][V];
+      VT v[kFoldBatch];
       for (int k0 = 0; k0 < n; k0 += kFoldBatch) {
 #pragma unroll
         for (int kk = 0; kk < kFoldBatch; ++kk) {
           const int k = k0 + kk;
-          if (k < n) {
-            const T* p = static_cast<const T*>(bufs.p[(c0 + k) % n]) + e0;
-#pragma unroll
-            for (int j = 0; j < V; ++j) v[kk][j] = p[j];
-          }
+          if (k < n)
+            v[kk] = *reinterpret_cast<const VT*>(static_cast<const T*>(bufs.p[(c0 + k) % n]) + e0);
         }
 #pragma unroll
         for (int kk = 0; kk < kFoldBatch; ++kk) {
@@ -519,13 +529,11 @@ __global__ __launch_bounds__(kBlock) void fold_kernel(RankPtrs bufs, RingArgs a,
           }
         }
       }
+      VT out;
 #pragma unroll
-      for (int j = 0; j < V; ++j) acc[j] = fold_finish<DIV>(acc[j], a);
-      for (int r = 0; r < n; ++r) {
-        T* p = static_cast<T*>(bufs.p[r]) + e0;
-#pragma unroll
-        for (int j = 0; j < V; ++j) p[j] = F::out(acc[j]);
-      }
+      for (int j = 0; j < V; ++j) out[j] = F::out(fold_finish<DIV>(acc[j], a));
+      for (int r = 0; r < n; ++r)
+        *reinterpret_cast<VT*>(static_cast<T*>(bufs.p[r]) + e0) = out;
       continue;
     }
     for (int64_t e = e0; e < e0 + V && e < count; ++e) {  // vectors that cross a chunk edge
