@@ -168,11 +168,13 @@ int hvdx_fuse_ag_unpack(const void* const* bufs, int64_t buf_count, int buf_dtyp
  * to 5, around the ring-allreduce of section 3), in place on the tensors: their
  * values end exactly as hvdx_fuse_pack, hvdx_ring_allreduce (buf_dtype, no
  * compression) and hvdx_fuse_unpack would leave them.  For nranks >= 3 it launches
- * hvdx_fuse_pack_rs, adding steps 1..N-3, the fused adding step N-2 / replacing
- * step 0, replacing steps 1..N-3, and hvdx_fuse_ag_unpack: 2N-3 launches and five
- * buffer passes fewer than the separate calls.  For nranks <= 2 it makes the
- * separate calls.  The fusion buffers are scratch: their contents afterwards are
- * unspecified.
+ * the copy-in fused with adding step 0 (as hvdx_fuse_pack_rs, except that no rank
+ * stores its copy of the chunk it sends in that step: nothing reads it before
+ * replacing step 0 overwrites it), adding steps 1..N-3, the fused adding step N-2 /
+ * replacing step 0, replacing steps 1..N-3, and hvdx_fuse_ag_unpack: 2N-3 launches
+ * and five buffer passes fewer than the separate calls.  For nranks <= 2 it makes
+ * the separate calls.  The fusion buffers are scratch: their contents afterwards
+ * are unspecified.
  *
  *   tensors[nranks*ntensors]  DEVICE array of device pointers, rank-major, read
  *                             and then written at [0, numel[t]), tensor_dtype
