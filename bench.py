@@ -607,15 +607,17 @@ def main():
                                 "share": round(v["share"], 4)} for k, v in r["kernels"].items()},
             }
 
-    # fusion ablation (paper section 7): the same workload with other buffer sizes;
-    # threshold 0 reduces every tensor with its own ring (no fusion)
+    # fusion ablation (paper section 7): ResNet-50 and Inception-V3 with other buffer
+    # sizes; threshold 0 reduces every tensor with its own ring (no fusion)
     ablation = {}
     if not args.no_ablation:
-        for thr in (0, 1 << 20, 4 << 20, 16 << 20, 64 << 20, 256 << 20):
-            r = measure(args.workload, max(3, args.steps // 4), 2, threshold=thr, per_kernel_pass=False)
-            ablation[str(thr)] = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in r.items()}
-            print(f"# fusion threshold {thr}: {r['ms_per_step']:.3f} ms/step, graph {r['graph_ms_per_step']:.3f}",
-                  file=sys.stderr, flush=True)
+        for name in dict.fromkeys([args.workload] + ([] if args.no_per_config else ["resnet50", "inceptionv3"])):
+            ablation[name] = {}
+            for thr in (0, 1 << 20, 4 << 20, 16 << 20, 64 << 20, 256 << 20):
+                r = measure(name, max(3, args.steps // 4), 2, threshold=thr, per_kernel_pass=False)
+                ablation[name][str(thr)] = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in r.items()}
+                print(f"# {name} fusion threshold {thr}: {r['ms_per_step']:.3f} ms/step, "
+                      f"graph {r['graph_ms_per_step']:.3f}", file=sys.stderr, flush=True)
 
     # the ring's fold computed directly (same bits, no per-step messages): a bound for
     # one GPU, reported beside the ring, never as the headline value
@@ -673,7 +675,7 @@ def main():
         "busbw_GBps": round(head["busbw_GBps"], 2),
         "roofline": roofline,
         "per_config": per_config,
-        "fusion_ablation": {"workload": args.workload, "by_threshold_bytes": ablation},
+        "fusion_ablation": {"by_workload_and_threshold_bytes": ablation},
         "broadcast": bcast,
         "fold_schedule": fold,
     }
