@@ -36,8 +36,8 @@ extern "C" {
 #define HVDX_FLOAT32 0
 #define HVDX_FLOAT16 1
 
-/* reduction: SUM, or AVERAGE = SUM divided by nranks (paper section 3, the
- * data-parallel recipe's "average gradients" step; section 5, the optimizer
+/* reduction: SUM, or AVERAGE = SUM divided by nranks (paper section 3, the step of
+ * the data-parallel recipe that averages the gradients; section 5, the optimizer
  * wrapper that averages gradients) */
 #define HVDX_SUM 0
 #define HVDX_AVERAGE 1

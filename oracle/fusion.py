@@ -2,17 +2,19 @@
 
 TEST INFRASTRUCTURE ONLY (see the package docstring).
 
-Paper, section 7, the numbered list: (1) pick the first few ready tensors that fit
-in the buffer and share a data type; (2) allocate the fusion buffer once, 64 MB by
-default; (3) copy the selected tensors in; (4) allreduce the buffer; (5) copy the
-results out to the output tensors; (6) repeat until every tensor is reduced.
+Paper, section 7, the numbered list, in other words: (1) among the tensors ready
+for reduction, choose a leading group that shares a data type and whose total size
+fits the buffer; (2) create the fusion buffer the first time it is needed (64 MB
+unless configured otherwise); (3) copy the chosen tensors into it; (4) allreduce it;
+(5) copy the reduced values back to the output tensors; (6) continue until no tensor
+is left.
 
 Readings where the paper is silent:
 
-* R5 "first few that fit": a contiguous run of the ready list, in order, never
+* R5 which ready tensors join a buffer: a contiguous run of the ready list, in order, never
   skipping ahead; a tensor fits if the buffer's used bytes including its padding
   and the tensor stay within the threshold (equality fits).
-* R6 "64 MB" is 64 MiB = 67,108,864 bytes, counted in the buffer's data type
+* R6 the default size of 64 MB is 64 MiB = 67,108,864 bytes, counted in the buffer's data type
   (binary16 bytes when the gradients are compressed to fp16).
 * R7 a tensor larger than the whole buffer cannot be copied in; it is reduced on
   its own ("direct"), as a one-tensor buffer with offset 0 and no padding.

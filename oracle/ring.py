@@ -2,10 +2,10 @@
 
 TEST INFRASTRUCTURE ONLY (see the package docstring).
 
-Paper, section 3, the paragraph after the ring-allreduce figure: each of N nodes
-talks to its two ring peers 2*(N-1) times, sending and receiving chunks of the data
-buffer.  In the first N-1 iterations a node adds what it receives to its buffer; in
-the second N-1 iterations what it receives replaces its buffer.
+Paper, section 3, the paragraph after the ring-allreduce figure: the N workers form
+a ring and, over 2(N-1) rounds, each passes one chunk of its buffer to a neighbour
+and takes one from the other.  During the first N-1 rounds the incoming chunk is
+summed into the local copy; during the last N-1 rounds it overwrites the local copy.
 
 The ring figure itself is lost, so these readings fill what the text leaves open:
 
@@ -20,8 +20,8 @@ The ring figure itself is lost, so these readings fill what the text leaves open
   chunks hold q+1 elements, the others q.  Chunks may be empty when count < N.
 * R3 summation order is the ring order: element e of chunk c ends as
   (((x_c + x_{c+1}) + x_{c+2}) + ... + x_{c+N-1}), ranks mod N.
-* R4 averaging (paper section 3's step "average gradients", section 5's
-  optimizer wrapper): the complete sum is divided by N once, in the buffer's
+* R4 averaging (the step of paper section 3's data-parallel recipe that averages
+  the gradients, and section 5's optimizer wrapper): the complete sum is divided by N once, in the buffer's
   precision, by the rank that completes it at the last adding step; the replacing
   steps then carry the average.  N = 1 divides by 1.
 
@@ -146,7 +146,7 @@ def ring_allreduce(bufs, op: str, count: int | None = None, elems=None, traffic=
             traffic["sent"][snd] += lengths[c]
             traffic["recvd"][rcv] += lengths[c]
 
-    # first N-1 iterations: received values are added to the local ones
+    # rounds 1 .. N-1: the incoming chunk is summed into the receiver's copy
     for s in range(n - 1):
         for c in range(n):
             snd, rcv = rs_sender(c, s, n), rs_receiver(c, s, n)
@@ -160,7 +160,7 @@ def ring_allreduce(bufs, op: str, count: int | None = None, elems=None, traffic=
     if op == AVERAGE and n == 1:
         bufs[0] = divide(bufs[0], 1)
 
-    # second N-1 iterations: received values replace the local ones
+    # rounds N .. 2N-2: the incoming chunk overwrites the receiver's copy
     for s in range(n - 1):
         for c in range(n):
             snd, rcv = ag_sender(c, s, n), ag_receiver(c, s, n)

@@ -389,9 +389,9 @@ struct PtrTable {
 };
 
 // Copy-in.  With RING it is fused with the ring's first adding step (paper section 3,
-// the first of the N-1 iterations whose received values are added): in chunk c the
-// receiving rank c+1 stores its own value plus rank c's, so the buffers end in the
-// state the copy-in and that step leave, without reading the sender's buffer back.
+// the first round of the ring's adding half): in chunk c the receiving rank c+1
+// stores its own value plus rank c's, so the buffers end in the state the copy-in and
+// that step leave, without reading the sender's buffer back.
 // A block's slots start at its chunk's sender, so slot 0 (sender) and slot 1
 // (receiver) are one load batch of the first rank group.
 //

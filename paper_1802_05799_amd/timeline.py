@@ -106,13 +106,13 @@ class Timeline:
                 if kind == L.KERNEL_RS_AG:  # adding step N-2, then replacing step 0
                     args = {"send chunks": [(r + 2) % n, (r + 1) % n], "to": (r + 1) % n,
                             "recv chunks": [(r + 1) % n, r], "from": (r - 1) % n,
-                            "received values": "added, then replace"}
+                            "incoming chunk": "summed in, then overwrites"}
                 ring_kind = {L.KERNEL_PACK_RS: L.KERNEL_REDUCE_SCATTER, L.KERNEL_AG_UNPACK: L.KERNEL_ALLGATHER}.get(
                     kind, kind)
                 if ring_kind in (L.KERNEL_REDUCE_SCATTER, L.KERNEL_ALLGATHER) and rec["launches"] == 1:
                     sent, recv = chunks_of_step(ring_kind, step, r, n)
                     args = {"send chunk": sent, "to": (r + 1) % n, "recv chunk": recv, "from": (r - 1) % n,
-                            "received values": "added" if ring_kind == L.KERNEL_REDUCE_SCATTER else "replace"}
+                            "incoming chunk": "summed in" if ring_kind == L.KERNEL_REDUCE_SCATTER else "overwrites"}
                 events.append(dict(common, tid=r + 1, name=name, args=args))
         return {"traceEvents": events, "displayTimeUnit": "ms",
                 "otherData": {"dropped_launches": self.dropped}}
