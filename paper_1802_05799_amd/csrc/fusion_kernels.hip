@@ -18,13 +18,14 @@ namespace hvdx {
 namespace {
 
 
-// Shape of a copy kernel: POS buffer vectors per lane in a row (a row is kBlock*POS
-// vectors), SUB rows per block (one tensor lookup serves them all), RB ranks whose
+// Shape of a copy kernel: POS buffer vectors per lane in a row (a row is BS*POS
+// vectors for BS threads per block), SUB rows per block (one tensor lookup serves them all), RB ranks whose
 // loads are in flight together, RPB ranks per block (0 = all), non-temporal
 // loads/stores, and the lane layout.  Measured on MI355X with the workloads' buckets:
 // a block's prologue (two rounds of dependent loads to find its tensors) has to be
 // amortized over enough data.  The copy-out is best with two ranks per block and two
-// block-strided vectors per lane (four loads in flight per lane, one row); the
+// block-strided vectors per lane (four loads in flight per lane, one row) in
+// 512-thread blocks (1.5 points over 256 on ResNet-50's buffers; 128 lost); the
 // binary32 copy-in with four ranks per block in two load batches of two and one
 // vector per lane (the same tensor lookup serves twice the ranks; 0.6-0.9% off the
 // whole ResNet-50, Inception-V3 and VGG-16 allreduces against the copy-out's shape,
@@ -35,13 +36,15 @@ namespace {
 #ifndef HVDX_LDS_TENSORS
 #define HVDX_LDS_TENSORS 64
 #endif
-template <int POS_, int RB_, int RPB_, bool NTL_, bool NTS_, bool WAVE_ = false, int SUB_ = 1>
+template <int POS_, int RB_, int RPB_, bool NTL_, bool NTS_, bool WAVE_ = false, int SUB_ = 1, int BS_ = kBlock>
 struct CopyCfg {
+  static_assert(BS_ >= 128 && BS_ % 64 == 0, "the tile lookup takes two wavefronts");
+  static constexpr int BS = BS_;  // threads per block
   static constexpr int POS = POS_, RB = RB_, RPB = RPB_;
   static constexpr bool NTL = NTL_, NTS = NTS_;
   static constexpr bool WAVE = WAVE_;  // a wavefront's POS vectors are contiguous (else block-strided)
-  static constexpr int SUB = SUB_;     // rows of kBlock*POS vectors a block moves one after another
-  static constexpr int kRowVecs = kBlock * POS_;
+  static constexpr int SUB = SUB_;     // rows of BS*POS vectors a block moves one after another
+  static constexpr int kRowVecs = BS_ * POS_;
   static constexpr int kTileVecs = kRowVecs * SUB_;  // a block's tile: one tensor lookup serves all its rows
   // A tile's tensors staged in LDS; a tile that spans more looks its tensors up in
   // global memory instead.
@@ -51,7 +54,7 @@ struct CopyCfg {
 #define HVDX_PACK_CFG CopyCfg<1, 2, 4, true, true>
 #endif
 #ifndef HVDX_UNPACK_CFG
-#define HVDX_UNPACK_CFG CopyCfg<2, 2, 2, true, true>
+#define HVDX_UNPACK_CFG CopyCfg<2, 2, 2, true, true, false, 1, 512>
 #endif
 #ifndef HVDX_PACK16_CFG  // binary16 buffers: the copy-out's shape measured 2 points faster here
 #define HVDX_PACK16_CFG CopyCfg<2, 2, 2, true, true>
@@ -75,7 +78,7 @@ constexpr int kLdsPtrs = HVDX_LDS_PTRS;  // (rank, tensor) pointers a tile can s
 template <typename Cfg>
 __device__ __forceinline__ int tile_vec(int u) {
   if constexpr (Cfg::WAVE) return (threadIdx.x >> 6) * 64 * Cfg::POS + u * 64 + (threadIdx.x & 63);
-  return u * kBlock + threadIdx.x;
+  return u * Cfg::BS + threadIdx.x;
 }
 
 // Elements a lane moves as one vector: 16 bytes on the wider side, so that every load
@@ -249,7 +252,7 @@ __device__ TileTable stage_tile(const int64_t* offset, const int64_t* numel, int
   const int nr = r1 - r0;
   const bool pin = tt.in_lds && (int64_t)tt.nt * nr <= kLdsPtrs;
   const int work = pin ? tt.nt * nr : (tt.in_lds ? tt.nt : 0);
-  for (int idx = threadIdx.x; idx < work; idx += kBlock) {
+  for (int idx = threadIdx.x; idx < work; idx += blockDim.x) {
     if (idx < tt.nt) {
       const int64_t t = tt.t0 + idx;
       s_off[idx] = t >= 0 ? offset[t] : INT64_MIN;  // positions before the first tensor are padding
@@ -400,7 +403,7 @@ struct PtrTable {
 // element path out of the vector pass keeps the vector pass's registers low enough
 // for full occupancy.
 template <typename TT, typename TB, typename Cfg, bool RING>
-__global__ __launch_bounds__(kBlock) HVDX_COPY_ATTR void pack_kernel(const void* const* __restrict__ srcs,
+__global__ __launch_bounds__(Cfg::BS) HVDX_COPY_ATTR void pack_kernel(const void* const* __restrict__ srcs,
                                                                     const int64_t* __restrict__ numel,
                                                                     const int64_t* __restrict__ offset, int ntensors,
                                                                     RankPtrs bufs, int64_t count, int nranks, int rpb,
@@ -496,7 +499,7 @@ __global__ __launch_bounds__(kBlock) HVDX_COPY_ATTR void pack_kernel(const void*
 // from rank c-3's buffer (mod N) and its own buffer keeps the chunk's older values.
 // Two passes per row, as in the copy-in.
 template <typename TT, typename TB, typename Cfg, bool RING>
-__global__ __launch_bounds__(kBlock) HVDX_COPY_ATTR void unpack_kernel(RankPtrs bufs, int64_t count,
+__global__ __launch_bounds__(Cfg::BS) HVDX_COPY_ATTR void unpack_kernel(RankPtrs bufs, int64_t count,
                                                                       void* const* __restrict__ dsts,
                                                                       const int64_t* __restrict__ numel,
                                                                       const int64_t* __restrict__ offset, int ntensors,
@@ -660,13 +663,13 @@ void pack_with(const void* const* srcs, const int64_t* numel, const int64_t* off
   const dim3 grid = copy_grid<Cfg, RING>(count, vec_elems(src_dtype, buf_dtype), nranks);
   const int64_t q = count / nranks, rem = count % nranks;
   if (src_dtype == HVDX_FLOAT32 && buf_dtype == HVDX_FLOAT32)
-    HVDX_LAUNCH((pack_kernel<float, float, Cfg, RING>), grid, dim3(kBlock), 0, stream, srcs, numel, offset,
+    HVDX_LAUNCH((pack_kernel<float, float, Cfg, RING>), grid, dim3(Cfg::BS), 0, stream, srcs, numel, offset,
                        ntensors, bufs, count, nranks, rpb, q, rem, skip_sender);
   else if (src_dtype == HVDX_FLOAT32 && buf_dtype == HVDX_FLOAT16)
-    HVDX_LAUNCH((pack_kernel<float, _Float16, Cfg, RING>), grid, dim3(kBlock), 0, stream, srcs, numel,
+    HVDX_LAUNCH((pack_kernel<float, _Float16, Cfg, RING>), grid, dim3(Cfg::BS), 0, stream, srcs, numel,
                        offset, ntensors, bufs, count, nranks, rpb, q, rem, skip_sender);
   else
-    HVDX_LAUNCH((pack_kernel<_Float16, _Float16, Cfg, RING>), grid, dim3(kBlock), 0, stream, srcs, numel,
+    HVDX_LAUNCH((pack_kernel<_Float16, _Float16, Cfg, RING>), grid, dim3(Cfg::BS), 0, stream, srcs, numel,
                        offset, ntensors, bufs, count, nranks, rpb, q, rem, skip_sender);
 }
 
@@ -677,13 +680,13 @@ void unpack_with(const RankPtrs& bufs, int64_t count, int buf_dtype, void* const
   const dim3 grid = copy_grid<Cfg, RING>(count, vec_elems(dst_dtype, buf_dtype), nranks);
   const int64_t q = count / nranks, rem = count % nranks;
   if (dst_dtype == HVDX_FLOAT32 && buf_dtype == HVDX_FLOAT32)
-    HVDX_LAUNCH((unpack_kernel<float, float, Cfg, RING>), grid, dim3(kBlock), 0, stream, bufs, count, dsts,
+    HVDX_LAUNCH((unpack_kernel<float, float, Cfg, RING>), grid, dim3(Cfg::BS), 0, stream, bufs, count, dsts,
                        numel, offset, ntensors, nranks, rpb, q, rem);
   else if (dst_dtype == HVDX_FLOAT32 && buf_dtype == HVDX_FLOAT16)
-    HVDX_LAUNCH((unpack_kernel<float, _Float16, Cfg, RING>), grid, dim3(kBlock), 0, stream, bufs, count,
+    HVDX_LAUNCH((unpack_kernel<float, _Float16, Cfg, RING>), grid, dim3(Cfg::BS), 0, stream, bufs, count,
                        dsts, numel, offset, ntensors, nranks, rpb, q, rem);
   else
-    HVDX_LAUNCH((unpack_kernel<_Float16, _Float16, Cfg, RING>), grid, dim3(kBlock), 0, stream, bufs, count,
+    HVDX_LAUNCH((unpack_kernel<_Float16, _Float16, Cfg, RING>), grid, dim3(Cfg::BS), 0, stream, bufs, count,
                        dsts, numel, offset, ntensors, nranks, rpb, q, rem);
 }
 
