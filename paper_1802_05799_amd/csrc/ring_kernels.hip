@@ -26,7 +26,8 @@ namespace {
 // best reduce-scatter keeps loads cached and streams its stores non-temporally
 // (the next step re-reads what this one wrote from the cache), and the best
 // all-gather is plain with two vectors per lane; when it does not fit, one vector
-// per lane with every access non-temporal streams closest to the HBM limit.  The
+// per lane with every access non-temporal, in 64-thread blocks, streams closest to
+// the HBM limit.  The
 // fused step N-2/0 (two reads, two writes) does best with one vector per lane in
 // both regimes.  Each shape can be replaced at build time (-DHVDX_RS_CACHED=...).
 template <int U_, int BS_, bool NTL_, bool NTS_, bool WAVE_ = false>
