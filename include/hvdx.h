@@ -64,8 +64,9 @@ extern "C" {
 
 /*
  * hvdx_fuse_plan -- group tensors into fusion buffers (paper section 7, steps 1,
- * 2 and 6: take the first ready tensors that fit in the buffer, repeat until all
- * are reduced).  Host only; touches no GPU state.
+ * 2 and 6: a leading run of the ready tensors whose total fits the buffer forms
+ * one buffer, and so on until every tensor has one).  Host only; touches no GPU
+ * state.
  *
  *   numel[ntensors]        host, elements of each tensor in ready order (>= 0)
  *   buf_dtype              HVDX_FLOAT32 or HVDX_FLOAT16: element type of the
