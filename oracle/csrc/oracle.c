@@ -10,9 +10,9 @@
  * thread or with OpenMP threads over the elements of each chunk.
  *
  * What it follows:
- *   - section 7, the six-step list (Tensor Fusion): pick the first ready tensors
- *     that fit in the fusion buffer, copy them in, allreduce the buffer, copy the
- *     results out, repeat;
+ *   - section 7, the six-step list (Tensor Fusion): a leading run of the ready
+ *     tensors whose total fits the fusion buffer is copied in, the buffer is
+ *     allreduced, the results are copied out, and so on until none is left;
  *   - section 3, the paragraph after the ring-allreduce figure: N-1 iterations in
  *     which a received chunk is added to the local one, then N-1 in which it
  *     replaces it;
