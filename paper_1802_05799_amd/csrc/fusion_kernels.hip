@@ -377,6 +377,17 @@ __device__ __forceinline__ BlockSpan block_span(int64_t tile_elems, int64_t coun
   return b;
 }
 
+// A tile wholly inside one tensor and, fused with a ring step, one chunk: every
+// lane's vectors are whole vectors of that tensor (the common case for large
+// tensors), so the copy needs no per-vector classification.  Block-uniform.
+template <typename Cfg, int V>
+__device__ __forceinline__ bool whole_tile(const TileTable& tt, const BlockSpan& bs, const int64_t* s_off,
+                                           const int64_t* s_end, const int64_t* offset, const int64_t* numel) {
+  const int64_t end = bs.p0 + (int64_t)Cfg::kTileVecs * V;
+  if (Cfg::SUB != 1 || tt.nt != 1 || tt.t0 < 0 || bs.p0 < bs.cs || end > bs.ce) return false;
+  return tensor_begin(tt, s_off, offset, 0) <= bs.p0 && end <= tensor_end(tt, s_end, offset, numel, 0);
+}
+
 // The tile's (rank, tensor) pointers, staged in LDS when they fit so that the data
 // loads do not wait behind dependent pointer loads.  A block serves "slots" [r0, r0+nr);
 // slot v is rank (v + rot) mod n (rot = 0 except in the copy-in fused with a ring step).
@@ -424,6 +435,36 @@ __global__ __launch_bounds__(Cfg::BS) HVDX_COPY_ATTR void pack_kernel(const void
                                                     rot, nranks, s_off, s_end, s_meta, s_ptr, &pin);
   const PtrTable pt{srcs, pin ? s_ptr : nullptr, tt.t0, ntensors, tt.nt, bs.rbeg, rot, nranks};
   const int receiver = bs.c + 1 == nranks ? 0 : bs.c + 1;  // of chunk c in adding step 0
+
+  if (whole_tile<Cfg, V>(tt, bs, s_off, s_end, offset, numel)) {  // no per-vector classification needed
+    const int64_t li0 = bs.p0 - tensor_begin(tt, s_off, offset, 0);
+    for (int v0 = bs.rbeg; v0 < bs.rend; v0 += kRankBatch) {
+      VB v[kRankBatch][kPosPerLane];
+#pragma unroll
+      for (int rr = 0; rr < kRankBatch; ++rr) {
+        const int slot = v0 + rr;
+        if (slot >= bs.rend) continue;
+        const TT* src = static_cast<const TT*>(pt.get(slot, tt.t0)) + li0;
+#pragma unroll
+        for (int u = 0; u < kPosPerLane; ++u)
+          v[rr][u] = Mover<TT, TB>::template load<Cfg::NTL>(src + tile_vec<Cfg>(u) * V);
+      }
+#pragma unroll
+      for (int rr = 0; rr < kRankBatch; ++rr) {
+        const int slot = v0 + rr;
+        if (slot >= bs.rend) break;
+        if (RING && skip_sender && slot == 0) continue;  // the sender's copy of its own chunk is never read
+        TB* __restrict__ buf = static_cast<TB*>(bufs.p[pt.rank(slot)]) + bs.p0;
+#pragma unroll
+        for (int u = 0; u < kPosPerLane; ++u) {
+          VB x = v[rr][u];
+          if (RING && rr > 0 && slot == 1) x = x + v[rr > 0 ? rr - 1 : 0][u];  // receiver: own + sender's
+          st16<Cfg::NTS>(reinterpret_cast<VB*>(buf + tile_vec<Cfg>(u) * V), x);
+        }
+      }
+    }
+    return;
+  }
 
   for (int row = 0; row < Cfg::SUB; ++row) {
     const int64_t r0 = bs.p0 + (int64_t)row * Cfg::kRowVecs * V;
@@ -518,6 +559,32 @@ __global__ __launch_bounds__(Cfg::BS) HVDX_COPY_ATTR void unpack_kernel(RankPtrs
   const TileTable tt = stage_tile<Cfg::kLdsTensors>(offset, numel, ntensors, bs.p0, bs.p1, dsts, bs.rbeg, bs.rend, 0,
                                                     nranks, s_off, s_end, s_meta, s_ptr, &pin);
   const PtrTable pt{dsts, pin ? s_ptr : nullptr, tt.t0, ntensors, tt.nt, bs.rbeg, 0, nranks};
+
+  if (whole_tile<Cfg, V>(tt, bs, s_off, s_end, offset, numel)) {  // no per-vector classification needed
+    const int64_t li0 = bs.p0 - tensor_begin(tt, s_off, offset, 0);
+    for (int rb = bs.rbeg; rb < bs.rend; rb += kRankBatch) {
+      VB v[kRankBatch][kPosPerLane];
+#pragma unroll
+      for (int rr = 0; rr < kRankBatch; ++rr) {
+        const int r = rb + rr;
+        const int from = r == receiver ? (r == 0 ? nranks - 1 : r - 1) : r;
+        const TB* __restrict__ buf = static_cast<const TB*>(bufs.p[r < bs.rend ? from : bs.rbeg]) + bs.p0;
+#pragma unroll
+        for (int u = 0; u < kPosPerLane; ++u)
+          if (r < bs.rend) v[rr][u] = ld16<Cfg::NTL>(reinterpret_cast<const VB*>(buf + tile_vec<Cfg>(u) * V));
+      }
+#pragma unroll
+      for (int rr = 0; rr < kRankBatch; ++rr) {
+        const int r = rb + rr;
+        if (r >= bs.rend) break;
+        TT* dst = static_cast<TT*>(const_cast<void*>(pt.get(r, tt.t0))) + li0;
+#pragma unroll
+        for (int u = 0; u < kPosPerLane; ++u)
+          Mover<TT, TB>::template store<Cfg::NTS>(dst + tile_vec<Cfg>(u) * V, v[rr][u]);
+      }
+    }
+    return;
+  }
 
   for (int row = 0; row < Cfg::SUB; ++row) {
     const int64_t r0 = bs.p0 + (int64_t)row * Cfg::kRowVecs * V;
