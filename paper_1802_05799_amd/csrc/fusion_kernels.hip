@@ -59,8 +59,8 @@ struct CopyCfg {
 #ifndef HVDX_PACK16_CFG  // binary16 buffers: the copy-out's shape measured 2 points faster here
 #define HVDX_PACK16_CFG CopyCfg<2, 2, 2, true, true>
 #endif
-#ifndef HVDX_UNPACK16_CFG
-#define HVDX_UNPACK16_CFG HVDX_UNPACK_CFG
+#ifndef HVDX_UNPACK16_CFG  // binary16 buffers: 256-thread blocks, 2 points over 512 here
+#define HVDX_UNPACK16_CFG CopyCfg<2, 2, 2, true, true>
 #endif
 using PackCfg = HVDX_PACK_CFG;      // binary32 buffers
 using UnpackCfg = HVDX_UNPACK_CFG;
