@@ -26,12 +26,12 @@ namespace {
 // amortized over enough data.  The copy-out is best with two ranks per block and two
 // block-strided vectors per lane (four loads in flight per lane, one row) in
 // 512-thread blocks (1.5 points over 256 on ResNet-50's buffers; 128 lost); the
-// binary32 copy-in with four ranks per block in two load batches of two and one
-// vector per lane (the same tensor lookup serves twice the ranks; 0.6-0.9% off the
-// whole ResNet-50, Inception-V3 and VGG-16 allreduces against the copy-out's shape,
-// while its own rate drops 3 points and the following kernels gain more).  One rank
-// per block with one vector per lane (the best pattern for a plain copy between many
-// buffers) lost to the prologue even with 8 rows; more rows, four ranks per batch or
+// copy-in the same shape in 256-thread blocks.  Once tiles inside one tensor skip the
+// per-vector classification, this copy-in beat four ranks per block with one vector
+// per lane (0.8% off the whole ResNet-50 allreduce, 0.6% off Inception-V3, in three
+// alternating pairs of runs), which had been ahead before.  One rank per block with
+// one vector per lane (the best pattern for a plain copy between many buffers) lost
+// to the prologue even with 8 rows; more rows, four ranks per batch or
 // wavefront-contiguous lanes did not help either.
 #ifndef HVDX_LDS_TENSORS
 #define HVDX_LDS_TENSORS 64
@@ -51,12 +51,12 @@ struct CopyCfg {
   static constexpr int kLdsTensors = kTileVecs + 8 < HVDX_LDS_TENSORS ? kTileVecs + 8 : HVDX_LDS_TENSORS;
 };
 #ifndef HVDX_PACK_CFG
-#define HVDX_PACK_CFG CopyCfg<1, 2, 4, true, true>
+#define HVDX_PACK_CFG CopyCfg<2, 2, 2, true, true>
 #endif
 #ifndef HVDX_UNPACK_CFG
 #define HVDX_UNPACK_CFG CopyCfg<2, 2, 2, true, true, false, 1, 512>
 #endif
-#ifndef HVDX_PACK16_CFG  // binary16 buffers: the copy-out's shape measured 2 points faster here
+#ifndef HVDX_PACK16_CFG
 #define HVDX_PACK16_CFG CopyCfg<2, 2, 2, true, true>
 #endif
 #ifndef HVDX_UNPACK16_CFG  // binary16 buffers: 256-thread blocks, 2 points over 512 here
