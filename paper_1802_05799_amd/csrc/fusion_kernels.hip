@@ -23,16 +23,20 @@ namespace {
 // loads are in flight together, RPB ranks per block (0 = all), non-temporal
 // loads/stores, and the lane layout.  Measured on MI355X with the workloads' buckets:
 // a block's prologue (two rounds of dependent loads to find its tensors) has to be
-// amortized over enough data.  The copy-out is best with two ranks per block and two
-// block-strided vectors per lane (four loads in flight per lane, one row) in
-// 512-thread blocks (1.5 points over 256 on ResNet-50's buffers; 128 lost); the
-// copy-in the same shape in 256-thread blocks.  Once tiles inside one tensor skip the
-// per-vector classification, this copy-in beat four ranks per block with one vector
-// per lane (0.8% off the whole ResNet-50 allreduce, 0.6% off Inception-V3, in three
-// alternating pairs of runs), which had been ahead before.  One rank per block with
+// amortized over enough data, yet a plain copy streams fastest with only one or two
+// 16-byte loads in flight per lane (83% of peak against 78% with four).  The
+// copy-out serves two ranks per block one after the other, two block-strided
+// vectors per lane, in 256-thread blocks, and loads the first rank's vectors before
+// the tensor lookup: against both ranks' four loads at once in 512-thread blocks it
+// went from 75% to 78% of peak on ResNet-50's buffers (71% to 75% on Inception-V3's,
+// 68% to 74% on VGG-16's; each step 1% faster); without the early loads this shape
+// was no better.  The copy-in's loads need the lookup first; it is best with both
+// ranks' two vectors per lane in flight at once (one vector per lane lost 8 points;
+// four ranks per block in two batches lost 0.8% of the ResNet-50 step once tiles
+// inside one tensor skip the per-vector classification).  One rank per block with
 // one vector per lane (the best pattern for a plain copy between many buffers) lost
-// to the prologue even with 8 rows; more rows, four ranks per batch or
-// wavefront-contiguous lanes did not help either.
+// to the prologue even with 8 rows; more rows or wavefront-contiguous lanes did not
+// help either.
 #ifndef HVDX_LDS_TENSORS
 #define HVDX_LDS_TENSORS 64
 #endif
@@ -54,18 +58,21 @@ struct CopyCfg {
 #define HVDX_PACK_CFG CopyCfg<2, 2, 2, true, true>
 #endif
 #ifndef HVDX_UNPACK_CFG
-#define HVDX_UNPACK_CFG CopyCfg<2, 2, 2, true, true, false, 1, 512>
+#define HVDX_UNPACK_CFG CopyCfg<2, 1, 2, true, true>
 #endif
 #ifndef HVDX_PACK16_CFG
 #define HVDX_PACK16_CFG CopyCfg<2, 2, 2, true, true>
 #endif
-#ifndef HVDX_UNPACK16_CFG  // binary16 buffers: 256-thread blocks, 2 points over 512 here
-#define HVDX_UNPACK16_CFG CopyCfg<2, 2, 2, true, true>
+#ifndef HVDX_UNPACK16_CFG
+#define HVDX_UNPACK16_CFG CopyCfg<2, 1, 2, true, true>
 #endif
 using PackCfg = HVDX_PACK_CFG;      // binary32 buffers
 using UnpackCfg = HVDX_UNPACK_CFG;
 using Pack16Cfg = HVDX_PACK16_CFG;  // binary16 buffers
 using Unpack16Cfg = HVDX_UNPACK16_CFG;
+#ifndef HVDX_UNPACK_EARLY  // copy-out: buffer loads issued before the tensor lookup
+#define HVDX_UNPACK_EARLY 1
+#endif
 #ifndef HVDX_COPY_ATTR
 #define HVDX_COPY_ATTR
 #endif
@@ -555,6 +562,25 @@ __global__ __launch_bounds__(Cfg::BS) HVDX_COPY_ATTR void unpack_kernel(RankPtrs
   if (bs.p0 >= bs.p1) return;  // past the end of a shorter chunk: the whole block leaves
   // the rank that receives chunk c in the last replacing step, which reads its sender's buffer
   const int receiver = RING ? (bs.c + nranks - 2) % nranks : -1;
+  // Rank batch rb's buffer vectors at the tile's whole-row positions (the positions
+  // every lane serves in row 0).
+  auto load_batch = [&](VB (&v)[kRankBatch][kPosPerLane], int rb) {
+#pragma unroll
+    for (int rr = 0; rr < kRankBatch; ++rr) {
+      const int r = rb + rr;
+      const int from = r == receiver ? (r == 0 ? nranks - 1 : r - 1) : r;
+      const TB* __restrict__ buf = static_cast<const TB*>(bufs.p[r < bs.rend ? from : bs.rbeg]) + bs.p0;
+#pragma unroll
+      for (int u = 0; u < kPosPerLane; ++u)
+        if (r < bs.rend) v[rr][u] = ld16<Cfg::NTL>(reinterpret_cast<const VB*>(buf + tile_vec<Cfg>(u) * V));
+    }
+  };
+  // Where the buffer is read does not depend on the tensors: when the whole tile lies
+  // inside the buffer, the first rank batch is loaded before the tensor lookup, whose
+  // dependent loads and barriers then overlap those loads' latency.
+  const bool early = HVDX_UNPACK_EARLY && Cfg::SUB == 1 && bs.p0 + (int64_t)kTileVecs * V <= count;
+  VB pre[kRankBatch][kPosPerLane];
+  if (early) load_batch(pre, bs.rbeg);
   bool pin;
   const TileTable tt = stage_tile<Cfg::kLdsTensors>(offset, numel, ntensors, bs.p0, bs.p1, dsts, bs.rbeg, bs.rend, 0,
                                                     nranks, s_off, s_end, s_meta, s_ptr, &pin);
@@ -564,14 +590,13 @@ __global__ __launch_bounds__(Cfg::BS) HVDX_COPY_ATTR void unpack_kernel(RankPtrs
     const int64_t li0 = bs.p0 - tensor_begin(tt, s_off, offset, 0);
     for (int rb = bs.rbeg; rb < bs.rend; rb += kRankBatch) {
       VB v[kRankBatch][kPosPerLane];
+      if (early && rb == bs.rbeg) {
 #pragma unroll
-      for (int rr = 0; rr < kRankBatch; ++rr) {
-        const int r = rb + rr;
-        const int from = r == receiver ? (r == 0 ? nranks - 1 : r - 1) : r;
-        const TB* __restrict__ buf = static_cast<const TB*>(bufs.p[r < bs.rend ? from : bs.rbeg]) + bs.p0;
+        for (int rr = 0; rr < kRankBatch; ++rr)
 #pragma unroll
-        for (int u = 0; u < kPosPerLane; ++u)
-          if (r < bs.rend) v[rr][u] = ld16<Cfg::NTL>(reinterpret_cast<const VB*>(buf + tile_vec<Cfg>(u) * V));
+          for (int u = 0; u < kPosPerLane; ++u) v[rr][u] = pre[rr][u];
+      } else {
+        load_batch(v, rb);
       }
 #pragma unroll
       for (int rr = 0; rr < kRankBatch; ++rr) {
@@ -605,9 +630,12 @@ __global__ __launch_bounds__(Cfg::BS) HVDX_COPY_ATTR void unpack_kernel(RankPtrs
         const int from = r == receiver ? (r == 0 ? nranks - 1 : r - 1) : r;
         const TB* __restrict__ buf = static_cast<const TB*>(bufs.p[r < bs.rend ? from : bs.rbeg]);
 #pragma unroll
-        for (int u = 0; u < kPosPerLane; ++u)
-          if (r < bs.rend && pos[u].cls == POS_VEC)
-            v[rr][u] = ld16<Cfg::NTL>(reinterpret_cast<const VB*>(buf + pos[u].p));
+        for (int u = 0; u < kPosPerLane; ++u) {
+          if (r >= bs.rend || pos[u].cls != POS_VEC) continue;
+          // row 0's positions are the ones loaded early
+          v[rr][u] = early && row == 0 && rb == bs.rbeg ? pre[rr][u]
+                                                        : ld16<Cfg::NTL>(reinterpret_cast<const VB*>(buf + pos[u].p));
+        }
       }
 #pragma unroll
       for (int rr = 0; rr < kRankBatch; ++rr) {
