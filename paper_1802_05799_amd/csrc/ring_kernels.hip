@@ -50,6 +50,15 @@ struct Policy {
 #ifndef HVDX_AG_STREAM  // 64-thread blocks: 76.5% -> 77.7% (binary32), 78% -> 80% (compressed ring)
 #define HVDX_AG_STREAM Policy<1, 64, true, true>
 #endif
+// Replacing step N-3 is the last one launched on its own before the fused copy-out,
+// which reads what it writes.  With cached stores its dirty lines were written back
+// while the copy-out streamed (77.5% of peak for the copy-out against 79% with this
+// step's stores streamed): streaming them took 0.5-0.7% off the ResNet-50 step, the
+// other workloads unchanged.  On the earlier replacing steps streamed stores lose
+// more than that, since the next step re-reads their output from the caches.
+#ifndef HVDX_AG_LAST_CACHED
+#define HVDX_AG_LAST_CACHED Policy<2, 512, false, true>
+#endif
 #ifndef HVDX_RSAG_CACHED  // two reads and two writes per vector: one vector per lane measured best
 #define HVDX_RSAG_CACHED Policy<1, 256, false, true>
 #endif
@@ -71,6 +80,7 @@ using Ag16Cached = HVDX_AG16_CACHED;
 using RsStream = HVDX_RS_STREAM;
 using AgCached = HVDX_AG_CACHED;
 using AgStream = HVDX_AG_STREAM;
+using AgLastCached = HVDX_AG_LAST_CACHED;
 using RsAgCached = HVDX_RSAG_CACHED;
 using RsAgStream = HVDX_RSAG_STREAM;
 using C16Cached = HVDX_C16_CACHED;
@@ -626,6 +636,7 @@ void ag_launch(const RankPtrs& bufs, const RingArgs& a, bool vec_ok, hipStream_t
 template <typename T>
 hipError_t ag_dispatch(const RankPtrs& bufs, const RingArgs& a, bool vec_ok, hipStream_t st) {
   if (streams(a, sizeof(T))) ag_launch<T, AgStream>(bufs, a, vec_ok, st);
+  else if (a.step == a.n - 3) ag_launch<T, AgLastCached>(bufs, a, vec_ok, st);
   else ag_launch<T, typename CachedShape<T>::ag>(bufs, a, vec_ok, st);
   return hipGetLastError();
 }
