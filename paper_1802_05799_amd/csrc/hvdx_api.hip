@@ -140,6 +140,8 @@ int check_rank_buffers(void* const* bufs, int nranks, int64_t count, int esize, 
   if (nranks < 1 || nranks > HVDX_MAX_RANKS)
     return fail(HVDX_ERR_INVALID, "%s: nranks=%d outside 1..%d", what, nranks, HVDX_MAX_RANKS);
   if (count < 0) return fail(HVDX_ERR_INVALID, "%s: negative element count %lld", what, (long long)count);
+  if (count > (INT64_MAX >> 4))  // byte extents below must not overflow
+    return fail(HVDX_ERR_INVALID, "%s: element count %lld too large", what, (long long)count);
   for (int r = 0; r < nranks; ++r) {
     if (!bufs[r] && count > 0) return fail(HVDX_ERR_INVALID, "%s: buffer of rank %d is NULL", what, r);
     if (reinterpret_cast<uintptr_t>(bufs[r]) % esize)

@@ -103,6 +103,7 @@ def test_ring_argument_errors():
     assert status_of(ar, bufs(2, 8), 0, 8, hv.FLOAT32, hv.SUM) == hv.ERR_INVALID  # nranks 0
     assert status_of(ar, bufs(129, 8), 129, 8, hv.FLOAT32, hv.SUM) == hv.ERR_INVALID  # too many ranks
     assert status_of(ar, bufs(2, 8), 2, -1, hv.FLOAT32, hv.SUM) == hv.ERR_INVALID  # negative count
+    assert status_of(ar, bufs(2, 8), 2, 1 << 62, hv.FLOAT32, hv.SUM) == hv.ERR_INVALID  # byte extents overflow
     assert status_of(ar, bufs(2, 8), 2, 8, 7, hv.SUM) == hv.ERR_INVALID  # dtype
     assert status_of(ar, bufs(2, 8), 2, 8, hv.FLOAT32, 9) == hv.ERR_INVALID  # op
     assert status_of(ar, bufs(2, 8), 2, 8, hv.FLOAT32, hv.SUM, 5) == hv.ERR_INVALID  # compression
