@@ -49,7 +49,10 @@ def parse():
 
 
 def kernel_bytes(ar, kind, bi, step):
-    """Algorithmic HBM bytes one launch must move (reads + writes)."""
+    """Algorithmic HBM bytes one launch must move (reads + writes); a launch that serves
+    two buckets' rings (bi a pair of indices) moves the sum of both."""
+    if isinstance(bi, tuple):
+        return sum(kernel_bytes(ar, kind, x, step) for x in bi)
     b = ar.buckets[bi]
     n = ar.nranks
     es_t = 4 if ar.dtype == 0 else 2  # tensor element size
@@ -88,7 +91,7 @@ KIND_CODE = {"pack": 0, "rs": 1, "ag": 2, "unpack": 3, "ring": 4, "rs_ag": 6, "f
 
 
 def kernel_name(ar, kind, bi):
-    b = ar.buckets[bi]
+    b = ar.buckets[bi[0] if isinstance(bi, tuple) else bi]
     if kind in ("cycle_small", "ring_small"):
         return kind
     if kind in ("rs", "ag", "rs_ag"):

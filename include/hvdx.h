@@ -189,6 +189,41 @@ int hvdx_fuse_allreduce(void* const* tensors, const int64_t* numel, const int64_
                         void* stream);
 
 /*
+ * hvdx_fuse_allreduce_pair -- two fusion buffers' whole cycles (paper section 7,
+ * steps 3 to 5, for two buffers of one call) with each ring step of both buffers in
+ * one launch: the copy-in of b0 and of b1 (each fused with adding step 0), then
+ * adding steps 1..N-3, the fused adding step N-2 / replacing step 0 and replacing
+ * steps 1..N-3, each launched once for both rings, then the copy-outs of b0 and b1:
+ * 2N-1 launches instead of 2(2N-3).  The tensors end exactly as after
+ * hvdx_fuse_allreduce on b0 and then on b1 (the two rings share no data, and each
+ * element's additions keep its own ring's order).  For callers with several fusion
+ * buffers ready at once; each buffer keeps its own plan and its own fusion buffers.
+ *
+ *   b0, b1         host pointers to bucket descriptors (fields as the arguments of
+ *                  hvdx_fuse_allreduce: tensors, numel, offset, ntensors, bufs,
+ *                  buf_count)
+ *   tensor_dtype, buf_dtype, nranks, op   shared by both buckets
+ * All 2*nranks fusion buffers must be pairwise disjoint (checked); the buckets'
+ * tensors must be disjoint from each other and from every fusion buffer (not
+ * checked: device data).
+ * Errors: as hvdx_fuse_allreduce for each bucket; HVDX_ERR_INVALID for a NULL
+ * descriptor, HVDX_ERR_ALIAS when fusion buffers of the two buckets overlap,
+ * HVDX_ERR_UNSUPPORTED for nranks < 3.  A bucket with buf_count 0 is skipped (the
+ * other runs as hvdx_fuse_allreduce).
+ */
+typedef struct hvdx_bucket {
+  void* const* tensors;   /* DEVICE array [nranks*ntensors] of device pointers */
+  const int64_t* numel;   /* DEVICE array [ntensors] */
+  const int64_t* offset;  /* DEVICE array [ntensors] */
+  int ntensors;
+  void* const* bufs;      /* host array [nranks] of device pointers, buf_count elements each */
+  int64_t buf_count;
+} hvdx_bucket;
+
+int hvdx_fuse_allreduce_pair(const hvdx_bucket* b0, const hvdx_bucket* b1, int tensor_dtype, int buf_dtype,
+                             int nranks, int op, void* stream);
+
+/*
  * hvdx_fuse_allreduce_small -- hvdx_fuse_allreduce for small fusion buffers: the same
  * result, bit for bit, in one kernel launch instead of 2N-1.  Each thread takes a
  * 16-byte stretch of the buffer (element by element where it meets a tensor edge)

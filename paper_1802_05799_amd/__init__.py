@@ -35,6 +35,7 @@ from ._lib import (  # noqa: F401
     hvdx_fold_allreduce,
     hvdx_fuse_ag_unpack,
     hvdx_fuse_allreduce,
+    hvdx_fuse_allreduce_pair,
     hvdx_fuse_allreduce_small,
     hvdx_fuse_pack,
     hvdx_fuse_pack_rs,

@@ -39,6 +39,7 @@ _SIGNATURES = {
     "hvdx_fuse_ag_unpack": (_i, [_pp, _i64, _i, _p, _p, _p, _i, _i, _i, _p]),
     "hvdx_fuse_allreduce": (_i, [_p, _p, _p, _i, _i, _pp, _i64, _i, _i, _i, _p]),
     "hvdx_fuse_allreduce_small": (_i, [_p, _p, _p, _i, _i, _pp, _i64, _i, _i, _i, _p]),
+    "hvdx_fuse_allreduce_pair": (_i, [_p, _p, _i, _i, _i, _i, _p]),
     "hvdx_ring_allreduce": (_i, [_pp, _i, _i64, _i, _i, _i, _p, _sz, _p]),
     "hvdx_ring_allreduce_small": (_i, [_pp, _i, _i64, _i, _i, _p]),
     "hvdx_ring_step": (_i, [_pp, _i, _i64, _i, _i, _i, _i, _i, _p, _sz, _p]),
@@ -60,6 +61,19 @@ KERNEL_PACK, KERNEL_REDUCE_SCATTER, KERNEL_ALLGATHER, KERNEL_UNPACK, KERNEL_ROUN
 KERNEL_BROADCAST, KERNEL_RS_AG, KERNEL_FOLD = 5, 6, 7
 KERNEL_PACK_RS, KERNEL_AG_UNPACK = 8, 9
 KERNEL_RING_SMALL, KERNEL_CYCLE_SMALL = 10, 11
+
+
+class Bucket(ctypes.Structure):
+    """hvdx_bucket: one fusion buffer's descriptors (device tables, host rank pointers)."""
+
+    _fields_ = [
+        ("tensors", ctypes.c_void_p),
+        ("numel", ctypes.c_void_p),
+        ("offset", ctypes.c_void_p),
+        ("ntensors", ctypes.c_int),
+        ("bufs", _pp),
+        ("buf_count", ctypes.c_int64),
+    ]
 
 
 class TraceRecord(ctypes.Structure):
@@ -182,6 +196,22 @@ def hvdx_fuse_allreduce(tensors_dev: int, numel_dev: int, offset_dev: int, ntens
     pb, _keep = _ptr_array(bufs)
     _check(lib.hvdx_fuse_allreduce(tensors_dev, numel_dev, offset_dev, ntensors, tensor_dtype, pb, buf_count,
                                    buf_dtype, nranks, op, stream))
+
+
+def hvdx_fuse_allreduce_pair(b0, b1, tensor_dtype: int, buf_dtype: int, nranks: int, op: int,
+                             stream: int = 0) -> None:
+    """b0, b1: (tensors_dev, numel_dev, offset_dev, ntensors, bufs, buf_count) each."""
+    keep = []
+
+    def desc(b):
+        tensors_dev, numel_dev, offset_dev, ntensors, bufs, buf_count = b
+        pb, arr = _ptr_array(bufs)
+        keep.append(arr)
+        return Bucket(tensors_dev, numel_dev, offset_dev, ntensors, pb, buf_count)
+
+    d0, d1 = desc(b0), desc(b1)
+    _check(lib.hvdx_fuse_allreduce_pair(ctypes.addressof(d0), ctypes.addressof(d1), tensor_dtype, buf_dtype, nranks,
+                                        op, stream))
 
 
 def hvdx_fuse_allreduce_small(tensors_dev: int, numel_dev: int, offset_dev: int, ntensors: int, tensor_dtype: int,

@@ -6,6 +6,7 @@
 #include <stdio.h>
 
 #include <algorithm>
+#include <initializer_list>
 #include <mutex>
 #include <utility>
 #include <vector>
@@ -610,6 +611,87 @@ int hvdx_fuse_allreduce(void* const* tensors, const int64_t* numel, const int64_
                  st);
   if (rc) return rc;
   return run_ag_unpack(bufs, buf_count, buf_dtype, tensors, numel, offset, ntensors, tensor_dtype, nranks, st);
+}
+
+// One step of two rings in one launch (arguments already checked, nranks >= 3).
+static int run_pair_step(const hvdx_bucket* b0, const hvdx_bucket* b1, int dtype, int op, int kind, int step,
+                         int nranks, hipStream_t st) {
+  hvdx::RingPair m{};
+  m.bufs[0] = rank_ptrs(b0->bufs, nranks);
+  m.bufs[1] = rank_ptrs(b1->bufs, nranks);
+  m.a[0] = ring_args(nranks, b0->buf_count, step);
+  m.a[1] = ring_args(nranks, b1->buf_count, step);
+  TimedLaunch timed(kind, step, nranks, dtype, HVDX_COMPRESS_NONE, b0->buf_count + b1->buf_count, st);
+  hipError_t e;
+  if (kind == HVDX_KERNEL_RS_AG) e = hvdx::launch_rs_ag_step_pair(m, dtype, div_mode(op, nranks), st);
+  else if (kind == HVDX_KERNEL_REDUCE_SCATTER) e = hvdx::launch_rs_step_pair(m, dtype, hvdx::DIV_NONE, st);
+  else e = hvdx::launch_ag_step_pair(m, dtype, st);
+  return e == hipSuccess ? HVDX_OK : hip_fail(e, "two-ring step launch");
+}
+
+// Steps [s0, s1) of one phase for two rings, as one timeline phase record.
+static int run_pair_steps(const hvdx_bucket* b0, const hvdx_bucket* b1, int dtype, int op, int kind, int s0, int s1,
+                          int nranks, hipStream_t st) {
+  if (s1 <= s0) return HVDX_OK;
+  TimedLaunch timed(kind, s0, nranks, dtype, HVDX_COMPRESS_NONE, b0->buf_count + b1->buf_count, st, -1, true,
+                    s1 - s0);
+  for (int s = s0; s < s1; ++s) {
+    const int rc = run_pair_step(b0, b1, dtype, op, kind, s, nranks, st);
+    if (rc) return rc;
+  }
+  return HVDX_OK;
+}
+
+int hvdx_fuse_allreduce_pair(const hvdx_bucket* b0, const hvdx_bucket* b1, int tensor_dtype, int buf_dtype,
+                             int nranks, int op, void* stream) {
+  static const char* what = "hvdx_fuse_allreduce_pair";
+  if (!b0 || !b1) return fail(HVDX_ERR_INVALID, "%s: a bucket descriptor is NULL", what);
+  for (const hvdx_bucket* b : {b0, b1}) {
+    const int rc = check_fusion(b->tensors, b->numel, b->offset, b->ntensors, tensor_dtype, b->bufs, b->buf_count,
+                                buf_dtype, nranks, what);
+    if (rc) return rc;
+  }
+  if (op != HVDX_SUM && op != HVDX_AVERAGE) return fail(HVDX_ERR_INVALID, "%s: unknown op %d", what, op);
+  if (nranks < 3) return fail(HVDX_ERR_UNSUPPORTED, "%s: needs 3 or more ranks", what);
+  const int es = elem_size(buf_dtype);
+  if (b0->buf_count > 0 && b1->buf_count > 0) {  // both rings run at once: all 2N buffers disjoint
+    std::vector<std::pair<uintptr_t, uintptr_t>> rg;
+    for (const hvdx_bucket* b : {b0, b1})
+      for (int r = 0; r < nranks; ++r) {
+        const uintptr_t x = reinterpret_cast<uintptr_t>(b->bufs[r]);
+        rg.emplace_back(x, x + (uintptr_t)b->buf_count * es);
+      }
+    if (overlapping(rg)) return fail(HVDX_ERR_ALIAS, "%s: fusion buffers of the two buckets overlap", what);
+  }
+  if (b0->buf_count == 0 || b1->buf_count == 0) {
+    const hvdx_bucket* b = b0->buf_count ? b0 : b1;
+    return hvdx_fuse_allreduce(b->tensors, b->numel, b->offset, b->ntensors, tensor_dtype, b->bufs, b->buf_count,
+                               buf_dtype, nranks, op, stream);
+  }
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int last = nranks - 2;
+  int rc = HVDX_OK;
+  for (const hvdx_bucket* b : {b0, b1}) {
+    rc = run_pack_rs(const_cast<const void* const*>(b->tensors), b->numel, b->offset, b->ntensors, tensor_dtype,
+                     b->bufs, b->buf_count, buf_dtype, nranks, true, st);
+    if (rc) return rc;
+  }
+  rc = run_pair_steps(b0, b1, buf_dtype, op, HVDX_KERNEL_REDUCE_SCATTER, 1, last, nranks, st);
+  if (rc) return rc;
+  {
+    TimedLaunch timed_phase(HVDX_KERNEL_RS_AG, last, nranks, buf_dtype, HVDX_COMPRESS_NONE,
+                            b0->buf_count + b1->buf_count, st, -1, true);
+    rc = run_pair_step(b0, b1, buf_dtype, op, HVDX_KERNEL_RS_AG, last, nranks, st);
+    if (rc) return rc;
+  }
+  rc = run_pair_steps(b0, b1, buf_dtype, op, HVDX_KERNEL_ALLGATHER, 1, last, nranks, st);
+  if (rc) return rc;
+  for (const hvdx_bucket* b : {b0, b1}) {
+    rc = run_ag_unpack(b->bufs, b->buf_count, buf_dtype, b->tensors, b->numel, b->offset, b->ntensors, tensor_dtype,
+                       nranks, st);
+    if (rc) return rc;
+  }
+  return HVDX_OK;
 }
 
 int hvdx_fuse_allreduce_small(void* const* tensors, const int64_t* numel, const int64_t* offset, int ntensors,

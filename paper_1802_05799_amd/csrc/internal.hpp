@@ -34,6 +34,12 @@ struct RingArgs {
   int64_t wire_stride;  // elements per rank in the fp16 wire workspace
 };
 
+// The same step of two rings (two fusion buffers of one call) in one launch.
+struct RingPair {
+  RankPtrs bufs[2];
+  RingArgs a[2];  // same n and step, each ring its own count
+};
+
 // How the last adding step finishes an AVERAGE.
 enum DivMode { DIV_NONE = 0, DIV_POW2 = 1, DIV_TRUE = 2 };
 
@@ -52,6 +58,11 @@ hipError_t launch_rs_ag_step(const RankPtrs& bufs, const RingArgs& a, int dtype,
                              hipStream_t stream);
 hipError_t launch_rs_ag_step_c16(const RankPtrs& x, void* wire, const RingArgs& a, int divmode, bool vector_ok,
                                  hipStream_t stream);
+// One step of two rings at once (binary32 or binary16 buffers, both 16-byte aligned):
+// an adding step, adding step N-2 fused with replacing step 0, a replacing step.
+hipError_t launch_rs_step_pair(const RingPair& m, int dtype, int divmode, hipStream_t stream);
+hipError_t launch_rs_ag_step_pair(const RingPair& m, int dtype, int divmode, hipStream_t stream);
+hipError_t launch_ag_step_pair(const RingPair& m, int dtype, hipStream_t stream);
 // A small ring in one launch: each thread runs every step for its elements.
 hipError_t launch_chain(const RankPtrs& bufs, const RingArgs& a, int64_t count, int dtype, int divmode,
                         bool vector_ok, hipStream_t stream);

@@ -127,7 +127,7 @@ __device__ __forceinline__ void vstore(V* p, V v) {
 // ---- plain ring (buffers of type T) ---------------------------------------------------
 
 template <typename T, int DIV, bool VEC_OK, typename P>
-__global__ __launch_bounds__(P::BS) void rs_step_kernel(RankPtrs bufs, RingArgs a) {
+__device__ __forceinline__ void rs_step_body(const RankPtrs& bufs, const RingArgs& a) {
   using VT = typename Vec<T>::type;
   constexpr int V = Vec<T>::n;
   constexpr int BS = P::BS, U = P::U;
@@ -167,8 +167,19 @@ __global__ __launch_bounds__(P::BS) void rs_step_kernel(RankPtrs bufs, RingArgs 
   }
 }
 
+template <typename T, int DIV, bool VEC_OK, typename P>
+__global__ __launch_bounds__(P::BS) void rs_step_kernel(RankPtrs bufs, RingArgs a) {
+  rs_step_body<T, DIV, VEC_OK, P>(bufs, a);
+}
+
+// The same step of two rings (two fusion buffers) in one launch: block z serves ring z.
+template <typename T, int DIV, bool VEC_OK, typename P>
+__global__ __launch_bounds__(P::BS) void rs_step_pair_kernel(RingPair m) {
+  rs_step_body<T, DIV, VEC_OK, P>(m.bufs[blockIdx.z], m.a[blockIdx.z]);
+}
+
 template <typename T, bool VEC_OK, typename P>
-__global__ __launch_bounds__(P::BS) void ag_step_kernel(RankPtrs bufs, RingArgs a) {
+__device__ __forceinline__ void ag_step_body(const RankPtrs& bufs, const RingArgs& a) {
   using VT = typename Vec<T>::type;
   constexpr int V = Vec<T>::n;
   constexpr int BS = P::BS, U = P::U;
@@ -203,6 +214,17 @@ __global__ __launch_bounds__(P::BS) void ag_step_kernel(RankPtrs bufs, RingArgs 
       if (i < nvec) d4[i] = s4[i];
     }
   }
+}
+
+template <typename T, bool VEC_OK, typename P>
+__global__ __launch_bounds__(P::BS) void ag_step_kernel(RankPtrs bufs, RingArgs a) {
+  ag_step_body<T, VEC_OK, P>(bufs, a);
+}
+
+// The same step of two rings (two fusion buffers) in one launch: block z serves ring z.
+template <typename T, bool VEC_OK, typename P>
+__global__ __launch_bounds__(P::BS) void ag_step_pair_kernel(RingPair m) {
+  ag_step_body<T, VEC_OK, P>(m.bufs[blockIdx.z], m.a[blockIdx.z]);
 }
 
 // ---- compressed ring: binary32 buffers, binary16 on the wire ------------------------
@@ -346,7 +368,7 @@ __global__ __launch_bounds__(P::BS) void ag_first_c16_kernel(RankPtrs x, const _
 // reading it back.  The buffers end exactly as after the two steps.
 
 template <typename T, int DIV, bool VEC_OK, typename P>
-__global__ __launch_bounds__(P::BS) void rs_ag_step_kernel(RankPtrs bufs, RingArgs a) {
+__device__ __forceinline__ void rs_ag_step_body(const RankPtrs& bufs, const RingArgs& a) {
   using VT = typename Vec<T>::type;
   constexpr int V = Vec<T>::n;
   constexpr int BS = P::BS, U = P::U;
@@ -396,6 +418,17 @@ __global__ __launch_bounds__(P::BS) void rs_ag_step_kernel(RankPtrs bufs, RingAr
       }
     }
   }
+}
+
+template <typename T, int DIV, bool VEC_OK, typename P>
+__global__ __launch_bounds__(P::BS) void rs_ag_step_kernel(RankPtrs bufs, RingArgs a) {
+  rs_ag_step_body<T, DIV, VEC_OK, P>(bufs, a);
+}
+
+// The same step of two rings (two fusion buffers) in one launch: block z serves ring z.
+template <typename T, int DIV, bool VEC_OK, typename P>
+__global__ __launch_bounds__(P::BS) void rs_ag_step_pair_kernel(RingPair m) {
+  rs_ag_step_body<T, DIV, VEC_OK, P>(m.bufs[blockIdx.z], m.a[blockIdx.z]);
 }
 
 // Compressed: the finished binary16 sum goes, widened, to the owner's and rank c's
@@ -682,6 +715,78 @@ hipError_t launch_rs_step(const RankPtrs& bufs, const RingArgs& a, int dtype, in
 hipError_t launch_ag_step(const RankPtrs& bufs, const RingArgs& a, int dtype, bool vector_ok, hipStream_t stream) {
   return dtype == HVDX_FLOAT32 ? ag_dispatch<float>(bufs, a, vector_ok, stream)
                                : ag_dispatch<_Float16>(bufs, a, vector_ok, stream);
+}
+
+namespace {
+
+// Two rings in one launch: a grid as wide as the longer ring's step needs, one row
+// per chunk, one layer per ring; the shorter ring's surplus blocks find no work.
+dim3 pair_grid(const RingPair& m, int elems_per_vec, int unroll, int bs) {
+  const dim3 g0 = step_grid(m.a[0], elems_per_vec, unroll, bs), g1 = step_grid(m.a[1], elems_per_vec, unroll, bs);
+  return dim3(g0.x > g1.x ? g0.x : g1.x, (unsigned)m.a[0].n, 2);
+}
+
+// Both rings take the launch shape of the longer one.
+bool pair_streams(const RingPair& m, int esize) { return streams(m.a[0].q >= m.a[1].q ? m.a[0] : m.a[1], esize); }
+
+template <typename T, typename P>
+void rs_pair_launch(const RingPair& m, int divmode, hipStream_t st) {
+  const dim3 grid = pair_grid(m, Vec<T>::n, P::U, P::BS);
+  if (divmode == DIV_NONE) HVDX_LAUNCH((rs_step_pair_kernel<T, DIV_NONE, true, P>), grid, dim3(P::BS), 0, st, m);
+  else if (divmode == DIV_POW2) HVDX_LAUNCH((rs_step_pair_kernel<T, DIV_POW2, true, P>), grid, dim3(P::BS), 0, st, m);
+  else HVDX_LAUNCH((rs_step_pair_kernel<T, DIV_TRUE, true, P>), grid, dim3(P::BS), 0, st, m);
+}
+
+template <typename T, typename P>
+void rs_ag_pair_launch(const RingPair& m, int divmode, hipStream_t st) {
+  const dim3 grid = pair_grid(m, Vec<T>::n, P::U, P::BS);
+  if (divmode == DIV_NONE) HVDX_LAUNCH((rs_ag_step_pair_kernel<T, DIV_NONE, true, P>), grid, dim3(P::BS), 0, st, m);
+  else if (divmode == DIV_POW2)
+    HVDX_LAUNCH((rs_ag_step_pair_kernel<T, DIV_POW2, true, P>), grid, dim3(P::BS), 0, st, m);
+  else HVDX_LAUNCH((rs_ag_step_pair_kernel<T, DIV_TRUE, true, P>), grid, dim3(P::BS), 0, st, m);
+}
+
+template <typename T, typename P>
+void ag_pair_launch(const RingPair& m, hipStream_t st) {
+  HVDX_LAUNCH((ag_step_pair_kernel<T, true, P>), pair_grid(m, Vec<T>::n, P::U, P::BS), dim3(P::BS), 0, st, m);
+}
+
+template <typename T>
+hipError_t rs_pair_dispatch(const RingPair& m, int divmode, hipStream_t st) {
+  if (pair_streams(m, sizeof(T))) rs_pair_launch<T, RsStream>(m, divmode, st);
+  else rs_pair_launch<T, typename CachedShape<T>::rs>(m, divmode, st);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t rs_ag_pair_dispatch(const RingPair& m, int divmode, hipStream_t st) {
+  if (pair_streams(m, sizeof(T))) rs_ag_pair_launch<T, RsAgStream>(m, divmode, st);
+  else rs_ag_pair_launch<T, RsAgCached>(m, divmode, st);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t ag_pair_dispatch(const RingPair& m, hipStream_t st) {
+  if (pair_streams(m, sizeof(T))) ag_pair_launch<T, AgStream>(m, st);
+  else if (m.a[0].step == m.a[0].n - 3) ag_pair_launch<T, AgLastCached>(m, st);
+  else ag_pair_launch<T, typename CachedShape<T>::ag>(m, st);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_rs_step_pair(const RingPair& m, int dtype, int divmode, hipStream_t stream) {
+  return dtype == HVDX_FLOAT32 ? rs_pair_dispatch<float>(m, divmode, stream)
+                               : rs_pair_dispatch<_Float16>(m, divmode, stream);
+}
+
+hipError_t launch_rs_ag_step_pair(const RingPair& m, int dtype, int divmode, hipStream_t stream) {
+  return dtype == HVDX_FLOAT32 ? rs_ag_pair_dispatch<float>(m, divmode, stream)
+                               : rs_ag_pair_dispatch<_Float16>(m, divmode, stream);
+}
+
+hipError_t launch_ag_step_pair(const RingPair& m, int dtype, hipStream_t stream) {
+  return dtype == HVDX_FLOAT32 ? ag_pair_dispatch<float>(m, stream) : ag_pair_dispatch<_Float16>(m, stream);
 }
 
 hipError_t launch_rs_step_c16(const RankPtrs& x, void* wire, const RingArgs& a, int divmode, bool vector_ok,

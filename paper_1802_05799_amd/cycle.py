@@ -15,7 +15,9 @@ allocated and in place for the object's lifetime.
 
 Buckets of at most `small_bucket_bytes` per rank (4 MiB by default) run their whole
 cycle in one launch (hvdx_fuse_allreduce_small, hvdx_ring_allreduce_small): there a
-ring step's launch costs more than its messages.  Same bits either way.
+ring step's launch costs more than its messages.  Two consecutive fused buckets on
+the per-step path run together (hvdx_fuse_allreduce_pair: each ring step of both in
+one launch), the second with fusion buffers of its own.  Same bits either way.
 """
 from __future__ import annotations
 
@@ -41,6 +43,7 @@ class Bucket:
     offset_dev: torch.Tensor | None = None
     ptrs_dev: torch.Tensor | None = None
     small: bool = False  # the whole cycle in one launch
+    pair: int = 0  # 1: runs with the next bucket, 2: with the previous one (its own fusion buffers)
 
 
 class FusedAllreduce:
@@ -49,7 +52,7 @@ class FusedAllreduce:
     def __init__(self, per_rank, op: str = "average", compress: bool = False,
                  threshold_bytes: int = L.DEFAULT_FUSION_THRESHOLD, align_bytes: int = L.DEFAULT_FUSION_ALIGN,
                  schedule: str = "ring", fuse_boundary: bool = True,
-                 small_bucket_bytes: int = L.SMALL_BUCKET_BYTES):
+                 small_bucket_bytes: int = L.SMALL_BUCKET_BYTES, pair_buckets: bool = True):
         """schedule "ring" runs the ring's 2(N-1) steps; "fold" computes the same bits
         with hvdx_fold_allreduce (no per-step messages: a one-GPU bound, not the ring).
         With fuse_boundary (ring schedule, N >= 3) a fusion buffer's copy-in runs with
@@ -57,7 +60,8 @@ class FusedAllreduce:
         (hvdx_fuse_allreduce); otherwise copy-in, ring and copy-out are separate calls.
         With the fused boundary, a bucket of at most small_bucket_bytes per rank (0:
         none) runs its whole cycle in one launch instead (compressed direct tensors
-        excepted).  All give the same bits."""
+        excepted).  With pair_buckets (fused boundary) two consecutive fused buckets
+        on the per-step path share each ring step's launch.  All give the same bits."""
         if schedule not in ("ring", "fold"):
             raise ValueError("schedule must be 'ring' or 'fold'")
         self.schedule = schedule
@@ -98,10 +102,23 @@ class FusedAllreduce:
             b.small = (self.fuse_boundary and b.count * es <= small_bucket_bytes
                        and not (b.direct and self.compress))
 
+        if pair_buckets and self.fuse_boundary and n >= 3:
+            i = 0
+            while i + 1 < len(self.buckets):
+                a, b = self.buckets[i], self.buckets[i + 1]
+                if all(not x.direct and not x.small and x.count > 0 for x in (a, b)):
+                    a.pair, b.pair = 1, 2
+                    i += 2
+                else:
+                    i += 1
+
         dev = self.device
-        cap = max([b.count for b in self.buckets if not b.direct], default=0)
-        # one fusion buffer per rank, allocated once and reused for every bucket
+        cap = max([b.count for b in self.buckets if not b.direct and b.pair != 2], default=0)
+        cap2 = max([b.count for b in self.buckets if b.pair == 2], default=0)
+        # one fusion buffer per rank, allocated once and reused for every bucket; the
+        # second bucket of a pair runs at the same time as the first and has its own
         self.bufs = [torch.empty(max(cap, 1), dtype=_TORCH_DTYPE[self.buf_dtype], device=dev) for _ in range(n)]
+        self.bufs2 = [torch.empty(cap2, dtype=_TORCH_DTYPE[self.buf_dtype], device=dev) for _ in range(n if cap2 else 0)]
         ws = max([L.hvdx_ring_workspace_bytes(n, b.count, self.dtype, self.compress)
                   for b in self.buckets if b.direct], default=0)
         self.workspace = torch.empty(max(ws, 1), dtype=torch.uint8, device=dev)
@@ -114,6 +131,7 @@ class FusedAllreduce:
             b.ptrs_dev = torch.tensor([self.tensors[r][t].data_ptr() for r in range(n) for t in b.tensors],
                                       dtype=torch.int64, device=dev)
         self._buf_ptrs = [x.data_ptr() for x in self.bufs]
+        self._buf2_ptrs = [x.data_ptr() for x in self.bufs2]
         _timeline.start_from_env()
 
     # ---- the steps, exposed separately for tracing ------------------------------------
@@ -159,16 +177,31 @@ class FusedAllreduce:
         fn(b.ptrs_dev.data_ptr(), b.numel_dev.data_ptr(), b.offset_dev.data_ptr(), len(b.tensors), self.dtype,
            self._buf_ptrs, b.count, self.buf_dtype, self.nranks, self.op, stream)
 
+    def fused_pair(self, a: Bucket, b: Bucket, stream: int) -> None:
+        """Two fusion buffers' cycles with each ring step of both in one launch."""
+        desc = [(x.ptrs_dev.data_ptr(), x.numel_dev.data_ptr(), x.offset_dev.data_ptr(), len(x.tensors), bufs,
+                 x.count) for x, bufs in ((a, self._buf_ptrs), (b, self._buf2_ptrs))]
+        L.hvdx_fuse_allreduce_pair(desc[0], desc[1], self.dtype, self.buf_dtype, self.nranks, self.op, stream)
+
     def kernel_sequence(self):
         """The kernels one call launches, in order: (kind, bucket index, step) with
         kind "pack", "pack_rs" (copy-in with adding step 0), "rs", "rs_ag" (adding
         step N-2 fused with replacing step 0), "ag", "ag_unpack" (replacing step N-2
         with copy-out), "unpack", "fold", "ring" (the one-rank compressed round trip),
-        "cycle_small" or "ring_small" (a small bucket's whole cycle in one launch)."""
+        "cycle_small" or "ring_small" (a small bucket's whole cycle in one launch).
+        A launch that serves a pair of buckets names both: (kind, (i, i + 1), step)."""
         out = []
         n = self.nranks
         for bi, b in enumerate(self.buckets):
-            if b.count == 0:
+            if b.count == 0 or b.pair == 2:
+                continue
+            if b.pair == 1:
+                both = (bi, bi + 1)
+                out += [("pack_rs", bi, 0), ("pack_rs", bi + 1, 0)]
+                out += [("rs", both, s) for s in range(1, n - 2)]
+                out.append(("rs_ag", both, n - 2))
+                out += [("ag", both, s) for s in range(1, n - 2)]
+                out += [("ag_unpack", bi, n - 2), ("ag_unpack", bi + 1, n - 2)]
                 continue
             if b.small:
                 if not b.direct:
@@ -223,8 +256,12 @@ class FusedAllreduce:
     def __call__(self, stream: int | None = None) -> None:
         if stream is None:
             stream = torch.cuda.current_stream(self.device).cuda_stream
-        for b in self.buckets:
-            if b.direct:
+        for i, b in enumerate(self.buckets):
+            if b.pair == 1:
+                self.fused_pair(b, self.buckets[i + 1], stream)
+            elif b.pair == 2:
+                continue
+            elif b.direct:
                 self.ring(b, stream)
             elif self.fuse_boundary:
                 self.fused_cycle(b, stream)

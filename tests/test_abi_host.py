@@ -220,3 +220,23 @@ def test_small_path_argument_errors():
     assert status_of(fs, FAKE, FAKE, FAKE, 3, hv.FLOAT32, [FAKE + 4, FAKE + 4096, FAKE + 8192], 64, hv.FLOAT32,
                      3, hv.SUM) == hv.ERR_INVALID  # fusion buffers must be 16-byte aligned
     assert status_of(fs, FAKE, FAKE, FAKE, 3, hv.FLOAT32, b3, 0, hv.FLOAT32, 3, hv.AVERAGE) == hv.OK
+
+
+def test_pair_argument_errors():
+    """hvdx_fuse_allreduce_pair refuses bad descriptors before any launch."""
+    fp = hv.hvdx_fuse_allreduce_pair
+    b3 = bufs(3, 64)
+    c3 = [x + (1 << 24) for x in b3]  # the second bucket's fusion buffers, disjoint from the first's
+    d0, d1 = (FAKE, FAKE, FAKE, 3, b3, 64), (FAKE, FAKE, FAKE, 2, c3, 40)
+    assert status_of(fp, d0, d1, hv.FLOAT32, hv.FLOAT32, 3, 7) == hv.ERR_INVALID  # op
+    assert status_of(fp, (FAKE, FAKE, FAKE, 3, b3[:2], 64), (FAKE, FAKE, FAKE, 2, c3[:2], 40), hv.FLOAT32,
+                     hv.FLOAT32, 2, hv.SUM) == hv.ERR_UNSUPPORTED  # two ranks: no adding step before the last
+    assert status_of(fp, (0, FAKE, FAKE, 3, b3, 64), d1, hv.FLOAT32, hv.FLOAT32, 3, hv.SUM) == hv.ERR_INVALID
+    assert status_of(fp, d0, (FAKE, FAKE, FAKE, 2, c3, 40), hv.FLOAT16, hv.FLOAT32, 3,
+                     hv.SUM) == hv.ERR_UNSUPPORTED  # binary16 tensors, binary32 buffers
+    overlap = (FAKE, FAKE, FAKE, 2, [b3[1] + 64, c3[1], c3[2]], 40)  # inside rank 1's first buffer
+    assert status_of(fp, d0, overlap, hv.FLOAT32, hv.FLOAT32, 3, hv.SUM) == hv.ERR_ALIAS
+    assert status_of(fp, d0, (FAKE, FAKE, FAKE, 2, [c3[0], c3[1] + 8, c3[2]], 40), hv.FLOAT32, hv.FLOAT32, 3,
+                     hv.SUM) == hv.ERR_INVALID  # fusion buffers must be 16-byte aligned
+    lib = hv._lib.lib
+    assert lib.hvdx_fuse_allreduce_pair(None, None, hv.FLOAT32, hv.FLOAT32, 3, hv.SUM, None) == hv.ERR_INVALID

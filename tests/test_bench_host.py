@@ -54,6 +54,16 @@ def test_whole_cycle_bytes_match_the_step_count():
     assert total == separate - (3 + 1 + 1 + 2) * 4 * count
 
 
+def test_a_launch_serving_two_buckets_counts_both():
+    """The same ring step of two fusion buffers in one launch moves both rings' bytes."""
+    ar = fake_allreduce(5, [300, 200, 77], [([0], 300, False), ([1, 2], 280, False)])
+    for kind in ("rs", "rs_ag", "ag"):
+        assert bench.kernel_bytes(ar, kind, (0, 1), 1) == bench.kernel_bytes(ar, kind, 0, 1) + \
+            bench.kernel_bytes(ar, kind, 1, 1)
+        assert bench.kernel_name(ar, kind, (0, 1)) == bench.kernel_name(ar, kind, 0)
+    assert bench.kernel_bytes(ar, "rs", (0, 1), 1) == 3 * 4 * (300 + 280)
+
+
 REAL_NAMES = {
     "void hvdx::(anonymous namespace)::unpack_kernel<float, float, hvdx::(anonymous namespace)::CopyCfg<2, 2, 2, "
     "true, true, false, 1>, true>(hvdx::RankPtrs, long, void* const*, long const*, long const*, int, int, int, "

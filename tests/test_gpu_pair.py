@@ -1,0 +1,95 @@
+"""Two fusion buffers' cycles with each ring step of both in one launch
+(hvdx_fuse_allreduce_pair, used by FusedAllreduce for consecutive fused buckets):
+bit for bit the oracle's result, and the same as running the buckets one by one."""
+import numpy as np
+import pytest
+import torch
+
+import paper_1802_05799_amd as hv
+from _gpu import assert_bits_equal, say
+from oracle import allreduce
+
+pytestmark = pytest.mark.gpu
+
+CASES = [
+    # (numel, nranks, threshold bytes, compress, op)
+    ([6000, 3000, 7001, 2500, 9000, 40, 12000, 333], 5, 40000, False, "average"),  # pair, one alone, a direct
+    ([6000, 3000, 7001, 2500, 9000, 40, 12000, 333], 8, 40000, True, "sum"),  # binary16 buffers
+    ([3, 5], 8, 32, False, "average"),  # both rings shorter than the rank count
+    ([1000, 1, 1500, 70000, 513, 700], 3, 8192, False, "sum"),  # three ranks: no plain ring step
+    ([2048] * 5 + [100], 13, 16384, False, "average"),  # two pairs' worth, the last bucket alone
+    ([100003, 31, 64000, 7], 4, 256 << 10, True, "average"),  # rings of very different lengths
+]
+
+
+@pytest.mark.parametrize("case", range(len(CASES)))
+def test_pairs_match_oracle_and_single_cycles(case):
+    numel, n, threshold, compress, op = CASES[case]
+    say(f"pair case {case}: N={n} numel={numel[:4]}... threshold={threshold} compress={compress} {op}")
+    rng = np.random.default_rng(4200 + case)
+    host = [[(rng.standard_normal(k) * 0.01).astype(np.float32) for k in numel] for _ in range(n)]
+    want1 = allreduce.allreduce(host, op, compress=compress, threshold=threshold)
+    want2 = allreduce.allreduce(want1, op, compress=compress, threshold=threshold)
+    for pair in (True, False):
+        dev = [[torch.from_numpy(x).cuda() for x in row] for row in host]
+        ar = hv.FusedAllreduce(dev, op=op, compress=compress, threshold_bytes=threshold, small_bucket_bytes=0,
+                               pair_buckets=pair)
+        assert any(b.pair == 1 for b in ar.buckets) == pair
+        for rep, want in enumerate((want1, want2)):  # the second call reduces the first's result again
+            ar()
+            torch.cuda.synchronize()
+            for r in range(n):
+                for t in range(len(numel)):
+                    assert_bits_equal(dev[r][t].cpu().numpy(), want[r][t], f"pair={pair} call {rep} rank {r} t {t}")
+
+
+def test_pair_entry_point_directly():
+    """The C entry point on two hand-built buckets of one rank set, against the
+    oracle, with a bucket of count 0 as the degenerate partner."""
+    n = 6
+    say("pair entry point: two buckets and an empty partner")
+    rng = np.random.default_rng(77)
+    numel = [[4001, 17], [2999]]
+    per_rank = [[(rng.standard_normal(k) * 0.01).astype(np.float32) for ks in numel for k in ks] for _ in range(n)]
+    dev = [[torch.from_numpy(x).cuda() for x in row] for row in per_rank]
+    descs, keep = [], []
+    t0 = 0
+    for ks in numel:
+        offs, count = [], 0
+        for k in ks:
+            start = (count + 3) // 4 * 4
+            offs.append(start)
+            count = start + k
+        idx = list(range(t0, t0 + len(ks)))
+        t0 += len(ks)
+        bufs = [torch.full((count,), float("nan"), device="cuda") for _ in range(n)]
+        ptrs = torch.tensor([dev[r][t].data_ptr() for r in range(n) for t in idx], dtype=torch.int64, device="cuda")
+        nm = torch.tensor(ks, dtype=torch.int64, device="cuda")
+        off = torch.tensor(offs, dtype=torch.int64, device="cuda")
+        keep += [bufs, ptrs, nm, off]
+        descs.append((ptrs.data_ptr(), nm.data_ptr(), off.data_ptr(), len(ks), [b.data_ptr() for b in bufs], count))
+    stream = torch.cuda.current_stream().cuda_stream
+    hv.hvdx_fuse_allreduce_pair(descs[0], descs[1], hv.FLOAT32, hv.FLOAT32, n, hv.AVERAGE, stream)
+    torch.cuda.synchronize()
+    # each bucket alone, as the oracle's plan would form it (threshold large enough for one bucket each)
+    want = [[None] * 3 for _ in range(n)]
+    for ids in ([0, 1], [2]):
+        sub = [[per_rank[r][t] for t in ids] for r in range(n)]
+        got = allreduce.allreduce(sub, "average", threshold=1 << 30)
+        for r in range(n):
+            for j, t in enumerate(ids):
+                want[r][t] = got[r][j]
+    for r in range(n):
+        for t in range(3):
+            assert_bits_equal(dev[r][t].cpu().numpy(), want[r][t], f"rank {r} t {t}")
+    # a partner with nothing to reduce: the other bucket runs alone
+    empty = (descs[1][0], descs[1][1], descs[1][2], 1, descs[1][4], 0)
+    before = [[x.cpu().numpy().copy() for x in row] for row in dev]
+    hv.hvdx_fuse_allreduce_pair(descs[0], empty, hv.FLOAT32, hv.FLOAT32, n, hv.SUM, stream)
+    torch.cuda.synchronize()
+    sub = [[before[r][t] for t in (0, 1)] for r in range(n)]
+    got = allreduce.allreduce(sub, "sum", threshold=1 << 30)
+    for r in range(n):
+        for t in (0, 1):
+            assert_bits_equal(dev[r][t].cpu().numpy(), got[r][t], f"empty partner: rank {r} t {t}")
+        assert_bits_equal(dev[r][2].cpu().numpy(), before[r][2], f"empty partner untouched: rank {r}")
