@@ -329,9 +329,11 @@ def short_kernel_name(full):
         return "cycle_small"
     if "chain_kernel" in base:
         return "ring_small"
-    for key in ("rs_ag_step_kernel", "rs_step_kernel", "ag_step_kernel"):
+    # a launch serving two fusion buffers' rings reports as the one-ring kernel of its step
+    for key in ("rs_ag_step_pair_kernel", "rs_step_pair_kernel", "ag_step_pair_kernel", "rs_ag_step_kernel",
+                "rs_step_kernel", "ag_step_kernel"):
         if key in base:
-            return key.replace("_kernel", "") + ("_f16" if half else "_f32")
+            return key.replace("_pair", "").replace("_kernel", "") + ("_f16" if half else "_f32")
     # the copy kernels' last template argument: fused with a ring step
     ring = base.rstrip().endswith(", true>") or re.search(r"Lb1EEEv", base) is not None
     if "unpack_kernel" in base:
@@ -342,15 +344,17 @@ def short_kernel_name(full):
 
 
 def shape_of(full):
-    """The launch-shape part of a kernel name (Policy<...> or CopyCfg<...>), for tables."""
+    """The launch-shape part of a kernel name (Policy<...> or CopyCfg<...>), for tables;
+    " x2" marks a launch that serves two fusion buffers' rings."""
     import re
 
+    two = " x2" if "pair_kernel" in full else ""
     m = re.search(r"(Policy|CopyCfg)<[^>]*>", full)
     if m:
-        return m.group(0).replace(" ", "")
+        return m.group(0).replace(" ", "") + two
     m = re.search(r"(Policy|CopyCfg)I((?:L[ib]\d+E)+)E", full)  # mangled: PolicyILi1ELi64ELb1E...E
     if m:
-        return m.group(1) + "<" + ",".join(x[2:] for x in re.findall(r"L[ib]\d+", m.group(2))) + ">"
+        return m.group(1) + "<" + ",".join(x[2:] for x in re.findall(r"L[ib]\d+", m.group(2))) + ">" + two
     return ""
 
 

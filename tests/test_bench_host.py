@@ -83,6 +83,10 @@ REAL_NAMES = {
     "EPKDF16_NS_8RingArgsE": ("rs_ag_step_c16", "Policy<1,64,1,1,0>"),
     "void hvdx::(anonymous namespace)::small_cycle_kernel<float, float, 1>(void const* const*, long const*, long "
     "const*, int, hvdx::RankPtrs, hvdx::RingArgs, long)": ("cycle_small", ""),
+    "void hvdx::(anonymous namespace)::rs_ag_step_pair_kernel<float, 1, true, hvdx::(anonymous namespace)::Policy<1, "
+    "256, false, true, false> >(hvdx::RingPair)": ("rs_ag_step_f32", "Policy<1,256,false,true,false> x2"),
+    "void hvdx::(anonymous namespace)::ag_step_pair_kernel<float, true, hvdx::(anonymous namespace)::Policy<2, 512, "
+    "false, true, false> >(hvdx::RingPair)": ("ag_step_f32", "Policy<2,512,false,true,false> x2"),
     "__amd_rocclr_copyBuffer": (None, ""),
 }
 
