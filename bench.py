@@ -334,6 +334,10 @@ def short_kernel_name(full):
                 "rs_step_kernel", "ag_step_kernel"):
         if key in base:
             return key.replace("_pair", "").replace("_kernel", "") + ("_f16" if half else "_f32")
+    if "unpack_pair_kernel" in base:  # two fusion buffers per launch, always fused with a ring step
+        return "ag_unpack"
+    if "pack_pair_kernel" in base:
+        return "pack_rs"
     # the copy kernels' last template argument: fused with a ring step
     ring = base.rstrip().endswith(", true>") or re.search(r"Lb1EEEv", base) is not None
     if "unpack_kernel" in base:

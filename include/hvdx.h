@@ -190,11 +190,10 @@ int hvdx_fuse_allreduce(void* const* tensors, const int64_t* numel, const int64_
 
 /*
  * hvdx_fuse_allreduce_pair -- two fusion buffers' whole cycles (paper section 7,
- * steps 3 to 5, for two buffers of one call) with each ring step of both buffers in
- * one launch: the copy-in of b0 and of b1 (each fused with adding step 0), then
- * adding steps 1..N-3, the fused adding step N-2 / replacing step 0 and replacing
- * steps 1..N-3, each launched once for both rings, then the copy-outs of b0 and b1:
- * 2N-1 launches instead of 2(2N-3).  The tensors end exactly as after
+ * steps 3 to 5, for two buffers of one call) with each launch serving both buffers:
+ * the copy-ins fused with adding step 0, adding steps 1..N-3, the fused adding step
+ * N-2 / replacing step 0, replacing steps 1..N-3, and replacing step N-2 fused with
+ * the copy-outs: 2N-3 launches instead of 2(2N-3).  The tensors end exactly as after
  * hvdx_fuse_allreduce on b0 and then on b1 (the two rings share no data, and each
  * element's additions keep its own ring's order).  For callers with several fusion
  * buffers ready at once; each buffer keeps its own plan and its own fusion buffers.

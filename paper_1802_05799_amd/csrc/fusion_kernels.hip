@@ -361,23 +361,20 @@ struct BlockSpan {
 
 template <bool RING>
 __device__ __forceinline__ BlockSpan block_span(int64_t tile_elems, int64_t count, int nranks, int rpb, int64_t q,
-                                                int64_t rem) {
+                                                int64_t rem, int group, int64_t bx) {
   BlockSpan b;
-  int group;
   if constexpr (RING) {
     b.c = blockIdx.y;
     b.cs = chunk_start(b.c, q, rem);
     b.ce = b.cs + q + (b.c < rem ? 1 : 0);
-    b.p0 = (b.cs & ~(tile_elems - 1)) + (int64_t)blockIdx.x * tile_elems;  // tile_elems is a power of two
+    b.p0 = (b.cs & ~(tile_elems - 1)) + bx * tile_elems;  // tile_elems is a power of two
     b.p1 = b.p0 + tile_elems < b.ce ? b.p0 + tile_elems : b.ce;
-    group = blockIdx.z;
   } else {
     b.c = 0;
     b.cs = 0;
     b.ce = count;
-    b.p0 = (int64_t)blockIdx.x * tile_elems;
+    b.p0 = bx * tile_elems;
     b.p1 = b.p0 + tile_elems < count ? b.p0 + tile_elems : count;
-    group = blockIdx.y;
   }
   b.rbeg = group * rpb;
   b.rend = b.rbeg + rpb < nranks ? b.rbeg + rpb : nranks;
@@ -421,11 +418,10 @@ struct PtrTable {
 // element path out of the vector pass keeps the vector pass's registers low enough
 // for full occupancy.
 template <typename TT, typename TB, typename Cfg, bool RING>
-__global__ __launch_bounds__(Cfg::BS) HVDX_COPY_ATTR void pack_kernel(const void* const* __restrict__ srcs,
-                                                                    const int64_t* __restrict__ numel,
-                                                                    const int64_t* __restrict__ offset, int ntensors,
-                                                                    RankPtrs bufs, int64_t count, int nranks, int rpb,
-                                                                    int64_t q, int64_t rem, int skip_sender) {
+__device__ __forceinline__ void pack_body(const void* const* __restrict__ srcs, const int64_t* __restrict__ numel,
+                                          const int64_t* __restrict__ offset, int ntensors, const RankPtrs& bufs,
+                                          int64_t count, int nranks, int rpb, int64_t q, int64_t rem, int skip_sender,
+                                          int group, int64_t bx) {
   static_assert(!RING || (Cfg::RB >= 2 && (Cfg::RPB == 0 || Cfg::RPB >= 2)),
                 "the fused copy-in needs the sender and receiver in one load batch");
   constexpr int V = BufVec<TT, TB>::n;
@@ -434,7 +430,7 @@ __global__ __launch_bounds__(Cfg::BS) HVDX_COPY_ATTR void pack_kernel(const void
   __shared__ int64_t s_off[Cfg::kLdsTensors], s_end[Cfg::kLdsTensors], s_meta[2];
   __shared__ const void* s_ptr[kLdsPtrs];
   static_assert((kTileVecs & (kTileVecs - 1)) == 0, "tiles are a power of two vectors");
-  const BlockSpan bs = block_span<RING>((int64_t)kTileVecs * V, count, nranks, rpb, q, rem);
+  const BlockSpan bs = block_span<RING>((int64_t)kTileVecs * V, count, nranks, rpb, q, rem, group, bx);
   if (bs.p0 >= bs.p1) return;  // past the end of a shorter chunk: the whole block leaves
   const int rot = bs.c;
   bool pin;
@@ -542,23 +538,43 @@ __global__ __launch_bounds__(Cfg::BS) HVDX_COPY_ATTR void pack_kernel(const void
   }
 }
 
+template <typename TT, typename TB, typename Cfg, bool RING>
+__global__ __launch_bounds__(Cfg::BS) HVDX_COPY_ATTR void pack_kernel(const void* const* __restrict__ srcs,
+                                                                    const int64_t* __restrict__ numel,
+                                                                    const int64_t* __restrict__ offset, int ntensors,
+                                                                    RankPtrs bufs, int64_t count, int nranks, int rpb,
+                                                                    int64_t q, int64_t rem, int skip_sender) {
+  pack_body<TT, TB, Cfg, RING>(srcs, numel, offset, ntensors, bufs, count, nranks, rpb, q, rem, skip_sender,
+                               RING ? (int)blockIdx.z : (int)blockIdx.y, blockIdx.x);
+}
+
+// The fused copy-in of two fusion buffers in one launch: block columns [0, x0) serve
+// buffer 0's chunk tiles, [x0, gridDim.x) buffer 1's, so neither has idle blocks.
+template <typename TT, typename TB, typename Cfg>
+__global__ __launch_bounds__(Cfg::BS) HVDX_COPY_ATTR void pack_pair_kernel(CopyPair m, int nranks, int rpb,
+                                                                         int x0) {
+  const int b = (int)blockIdx.x >= x0 ? 1 : 0;
+  pack_body<TT, TB, Cfg, true>(static_cast<const void* const*>(m.t[b]), m.numel[b], m.offset[b], m.ntensors[b],
+                               m.bufs[b], m.count[b], nranks, rpb, m.q[b], m.rem[b], 1, blockIdx.z,
+                               (int64_t)blockIdx.x - b * x0);
+}
+
 // Copy-out.  With RING it is fused with the ring's last replacing step: in chunk c
 // that step hands rank c-3's final values to rank c-2, so rank c-2 copies them out
 // from rank c-3's buffer (mod N) and its own buffer keeps the chunk's older values.
 // Two passes per row, as in the copy-in.
 template <typename TT, typename TB, typename Cfg, bool RING>
-__global__ __launch_bounds__(Cfg::BS) HVDX_COPY_ATTR void unpack_kernel(RankPtrs bufs, int64_t count,
-                                                                      void* const* __restrict__ dsts,
-                                                                      const int64_t* __restrict__ numel,
-                                                                      const int64_t* __restrict__ offset, int ntensors,
-                                                                      int nranks, int rpb, int64_t q, int64_t rem) {
+__device__ __forceinline__ void unpack_body(const RankPtrs& bufs, int64_t count, void* const* __restrict__ dsts,
+                                            const int64_t* __restrict__ numel, const int64_t* __restrict__ offset,
+                                            int ntensors, int nranks, int rpb, int64_t q, int64_t rem, int group,
+                                            int64_t bx) {
   constexpr int V = BufVec<TT, TB>::n;
   using VB = typename Mover<TT, TB>::buf_vec;
   constexpr int kPosPerLane = Cfg::POS, kRankBatch = Cfg::RB, kTileVecs = Cfg::kTileVecs;
   __shared__ int64_t s_off[Cfg::kLdsTensors], s_end[Cfg::kLdsTensors], s_meta[2];
   __shared__ const void* s_ptr[kLdsPtrs];
   static_assert((kTileVecs & (kTileVecs - 1)) == 0, "tiles are a power of two vectors");
-  const BlockSpan bs = block_span<RING>((int64_t)kTileVecs * V, count, nranks, rpb, q, rem);
+  const BlockSpan bs = block_span<RING>((int64_t)kTileVecs * V, count, nranks, rpb, q, rem, group, bx);
   if (bs.p0 >= bs.p1) return;  // past the end of a shorter chunk: the whole block leaves
   // the rank that receives chunk c in the last replacing step, which reads its sender's buffer
   const int receiver = RING ? (bs.c + nranks - 2) % nranks : -1;
@@ -670,6 +686,25 @@ __global__ __launch_bounds__(Cfg::BS) HVDX_COPY_ATTR void unpack_kernel(RankPtrs
       }
     }
   }
+}
+
+template <typename TT, typename TB, typename Cfg, bool RING>
+__global__ __launch_bounds__(Cfg::BS) HVDX_COPY_ATTR void unpack_kernel(RankPtrs bufs, int64_t count,
+                                                                      void* const* __restrict__ dsts,
+                                                                      const int64_t* __restrict__ numel,
+                                                                      const int64_t* __restrict__ offset, int ntensors,
+                                                                      int nranks, int rpb, int64_t q, int64_t rem) {
+  unpack_body<TT, TB, Cfg, RING>(bufs, count, dsts, numel, offset, ntensors, nranks, rpb, q, rem,
+                                 RING ? (int)blockIdx.z : (int)blockIdx.y, blockIdx.x);
+}
+
+// The fused copy-out of two fusion buffers in one launch (columns as pack_pair_kernel).
+template <typename TT, typename TB, typename Cfg>
+__global__ __launch_bounds__(Cfg::BS) HVDX_COPY_ATTR void unpack_pair_kernel(CopyPair m, int nranks, int rpb,
+                                                                           int x0) {
+  const int b = (int)blockIdx.x >= x0 ? 1 : 0;
+  unpack_body<TT, TB, Cfg, true>(m.bufs[b], m.count[b], m.t[b], m.numel[b], m.offset[b], m.ntensors[b], nranks, rpb,
+                                 m.q[b], m.rem[b], blockIdx.z, (int64_t)blockIdx.x - b * x0);
 }
 
 // ---- a small fusion buffer's whole cycle in one launch ------------------------------
@@ -785,6 +820,45 @@ void unpack_with(const RankPtrs& bufs, int64_t count, int buf_dtype, void* const
                        dsts, numel, offset, ntensors, nranks, rpb, q, rem);
 }
 
+// Two buffers in one launch: buffer 0's chunk-tile columns (x0 of them), then buffer 1's.
+template <typename Cfg>
+dim3 pair_grid(const CopyPair& m, int64_t vec, int nranks, unsigned* x0) {
+  const dim3 g0 = copy_grid<Cfg, true>(m.count[0], vec, nranks), g1 = copy_grid<Cfg, true>(m.count[1], vec, nranks);
+  *x0 = g0.x;
+  return dim3(g0.x + g1.x, (unsigned)nranks, g0.z);
+}
+
+template <typename Cfg>
+void pack_pair_with(const CopyPair& m, int src_dtype, int buf_dtype, int nranks, hipStream_t stream) {
+  const int rpb = ranks_per_block<Cfg>(nranks);
+  unsigned x0;
+  const dim3 grid = pair_grid<Cfg>(m, vec_elems(src_dtype, buf_dtype), nranks, &x0);
+  if (src_dtype == HVDX_FLOAT32 && buf_dtype == HVDX_FLOAT32)
+    HVDX_LAUNCH((pack_pair_kernel<float, float, Cfg>), grid, dim3(Cfg::BS), 0, stream, m, nranks, rpb, (int)x0);
+  else if (src_dtype == HVDX_FLOAT32 && buf_dtype == HVDX_FLOAT16)
+    HVDX_LAUNCH((pack_pair_kernel<float, _Float16, Cfg>), grid, dim3(Cfg::BS), 0, stream, m, nranks, rpb,
+                (int)x0);
+  else
+    HVDX_LAUNCH((pack_pair_kernel<_Float16, _Float16, Cfg>), grid, dim3(Cfg::BS), 0, stream, m, nranks, rpb,
+                (int)x0);
+}
+
+template <typename Cfg>
+void unpack_pair_with(const CopyPair& m, int buf_dtype, int dst_dtype, int nranks, hipStream_t stream) {
+  const int rpb = ranks_per_block<Cfg>(nranks);
+  unsigned x0;
+  const dim3 grid = pair_grid<Cfg>(m, vec_elems(dst_dtype, buf_dtype), nranks, &x0);
+  if (dst_dtype == HVDX_FLOAT32 && buf_dtype == HVDX_FLOAT32)
+    HVDX_LAUNCH((unpack_pair_kernel<float, float, Cfg>), grid, dim3(Cfg::BS), 0, stream, m, nranks, rpb,
+                (int)x0);
+  else if (dst_dtype == HVDX_FLOAT32 && buf_dtype == HVDX_FLOAT16)
+    HVDX_LAUNCH((unpack_pair_kernel<float, _Float16, Cfg>), grid, dim3(Cfg::BS), 0, stream, m, nranks, rpb,
+                (int)x0);
+  else
+    HVDX_LAUNCH((unpack_pair_kernel<_Float16, _Float16, Cfg>), grid, dim3(Cfg::BS), 0, stream, m, nranks, rpb,
+                (int)x0);
+}
+
 }  // namespace
 
 hipError_t launch_pack(const void* const* srcs, const int64_t* numel, const int64_t* offset, int ntensors,
@@ -803,6 +877,18 @@ hipError_t launch_pack(const void* const* srcs, const int64_t* numel, const int6
     else
       pack_with<Pack16Cfg, false>(srcs, numel, offset, ntensors, src_dtype, bufs, count, buf_dtype, nranks, 0, stream);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_pack_pair(const CopyPair& m, int src_dtype, int buf_dtype, int nranks, hipStream_t stream) {
+  if (buf_dtype == HVDX_FLOAT32) pack_pair_with<PackCfg>(m, src_dtype, buf_dtype, nranks, stream);
+  else pack_pair_with<Pack16Cfg>(m, src_dtype, buf_dtype, nranks, stream);
+  return hipGetLastError();
+}
+
+hipError_t launch_unpack_pair(const CopyPair& m, int buf_dtype, int dst_dtype, int nranks, hipStream_t stream) {
+  if (buf_dtype == HVDX_FLOAT32) unpack_pair_with<UnpackCfg>(m, buf_dtype, dst_dtype, nranks, stream);
+  else unpack_pair_with<Unpack16Cfg>(m, buf_dtype, dst_dtype, nranks, stream);
   return hipGetLastError();
 }
 

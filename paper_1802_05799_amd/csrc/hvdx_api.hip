@@ -670,11 +670,25 @@ int hvdx_fuse_allreduce_pair(const hvdx_bucket* b0, const hvdx_bucket* b1, int t
   }
   hipStream_t st = static_cast<hipStream_t>(stream);
   const int last = nranks - 2;
+  const int64_t both = b0->buf_count + b1->buf_count;
+  hvdx::CopyPair cp{};
+  const hvdx_bucket* bk[2] = {b0, b1};
+  for (int i = 0; i < 2; ++i) {
+    cp.t[i] = bk[i]->tensors;
+    cp.numel[i] = bk[i]->numel;
+    cp.offset[i] = bk[i]->offset;
+    cp.ntensors[i] = bk[i]->ntensors;
+    cp.bufs[i] = rank_ptrs(bk[i]->bufs, nranks);
+    cp.count[i] = bk[i]->buf_count;
+    cp.q[i] = bk[i]->buf_count / nranks;
+    cp.rem[i] = bk[i]->buf_count % nranks;
+  }
   int rc = HVDX_OK;
-  for (const hvdx_bucket* b : {b0, b1}) {
-    rc = run_pack_rs(const_cast<const void* const*>(b->tensors), b->numel, b->offset, b->ntensors, tensor_dtype,
-                     b->bufs, b->buf_count, buf_dtype, nranks, true, st);
-    if (rc) return rc;
+  {
+    TimedLaunch timed(HVDX_KERNEL_PACK_RS, 0, nranks, buf_dtype, HVDX_COMPRESS_NONE, both, st);
+    TimedLaunch timed_phase(HVDX_KERNEL_PACK_RS, 0, nranks, buf_dtype, HVDX_COMPRESS_NONE, both, st, -1, true);
+    const hipError_t e = hvdx::launch_pack_pair(cp, tensor_dtype, buf_dtype, nranks, st);
+    if (e != hipSuccess) return hip_fail(e, "two-buffer copy-in launch");
   }
   rc = run_pair_steps(b0, b1, buf_dtype, op, HVDX_KERNEL_REDUCE_SCATTER, 1, last, nranks, st);
   if (rc) return rc;
@@ -686,12 +700,10 @@ int hvdx_fuse_allreduce_pair(const hvdx_bucket* b0, const hvdx_bucket* b1, int t
   }
   rc = run_pair_steps(b0, b1, buf_dtype, op, HVDX_KERNEL_ALLGATHER, 1, last, nranks, st);
   if (rc) return rc;
-  for (const hvdx_bucket* b : {b0, b1}) {
-    rc = run_ag_unpack(b->bufs, b->buf_count, buf_dtype, b->tensors, b->numel, b->offset, b->ntensors, tensor_dtype,
-                       nranks, st);
-    if (rc) return rc;
-  }
-  return HVDX_OK;
+  TimedLaunch timed(HVDX_KERNEL_AG_UNPACK, last, nranks, buf_dtype, HVDX_COMPRESS_NONE, both, st);
+  TimedLaunch timed_phase(HVDX_KERNEL_AG_UNPACK, last, nranks, buf_dtype, HVDX_COMPRESS_NONE, both, st, -1, true);
+  const hipError_t e = hvdx::launch_unpack_pair(cp, buf_dtype, tensor_dtype, nranks, st);
+  return e == hipSuccess ? HVDX_OK : hip_fail(e, "two-buffer copy-out launch");
 }
 
 int hvdx_fuse_allreduce_small(void* const* tensors, const int64_t* numel, const int64_t* offset, int ntensors,

@@ -40,6 +40,16 @@ struct RingPair {
   RingArgs a[2];  // same n and step, each ring its own count
 };
 
+// The fused copy-in or copy-out of two fusion buffers in one launch.
+struct CopyPair {
+  void* const* t[2];  // DEVICE tables of tensor pointers, rank-major
+  const int64_t* numel[2];
+  const int64_t* offset[2];
+  int ntensors[2];
+  RankPtrs bufs[2];
+  int64_t count[2], q[2], rem[2];  // buffer elements and their ring partition
+};
+
 // How the last adding step finishes an AVERAGE.
 enum DivMode { DIV_NONE = 0, DIV_POW2 = 1, DIV_TRUE = 2 };
 
@@ -63,6 +73,10 @@ hipError_t launch_rs_ag_step_c16(const RankPtrs& x, void* wire, const RingArgs& 
 hipError_t launch_rs_step_pair(const RingPair& m, int dtype, int divmode, hipStream_t stream);
 hipError_t launch_rs_ag_step_pair(const RingPair& m, int dtype, int divmode, hipStream_t stream);
 hipError_t launch_ag_step_pair(const RingPair& m, int dtype, hipStream_t stream);
+// The copy-in fused with adding step 0 (no sender storing its own sent chunk), and
+// replacing step N-2 fused with the copy-out, for two fusion buffers at once.
+hipError_t launch_pack_pair(const CopyPair& m, int src_dtype, int buf_dtype, int nranks, hipStream_t stream);
+hipError_t launch_unpack_pair(const CopyPair& m, int buf_dtype, int dst_dtype, int nranks, hipStream_t stream);
 // A small ring in one launch: each thread runs every step for its elements.
 hipError_t launch_chain(const RankPtrs& bufs, const RingArgs& a, int64_t count, int dtype, int divmode,
                         bool vector_ok, hipStream_t stream);

@@ -16,8 +16,8 @@ allocated and in place for the object's lifetime.
 Buckets of at most `small_bucket_bytes` per rank (4 MiB by default) run their whole
 cycle in one launch (hvdx_fuse_allreduce_small, hvdx_ring_allreduce_small): there a
 ring step's launch costs more than its messages.  Two consecutive fused buckets on
-the per-step path run together (hvdx_fuse_allreduce_pair: each ring step of both in
-one launch), the second with fusion buffers of its own.  Same bits either way.
+the per-step path run together (hvdx_fuse_allreduce_pair: each launch serves both),
+the second with fusion buffers of its own.  Same bits either way.
 """
 from __future__ import annotations
 
@@ -61,7 +61,7 @@ class FusedAllreduce:
         With the fused boundary, a bucket of at most small_bucket_bytes per rank (0:
         none) runs its whole cycle in one launch instead (compressed direct tensors
         excepted).  With pair_buckets (fused boundary) two consecutive fused buckets
-        on the per-step path share each ring step's launch.  All give the same bits."""
+        on the per-step path share every launch.  All give the same bits."""
         if schedule not in ("ring", "fold"):
             raise ValueError("schedule must be 'ring' or 'fold'")
         self.schedule = schedule
@@ -178,7 +178,7 @@ class FusedAllreduce:
            self._buf_ptrs, b.count, self.buf_dtype, self.nranks, self.op, stream)
 
     def fused_pair(self, a: Bucket, b: Bucket, stream: int) -> None:
-        """Two fusion buffers' cycles with each ring step of both in one launch."""
+        """Two fusion buffers' cycles with every launch serving both."""
         desc = [(x.ptrs_dev.data_ptr(), x.numel_dev.data_ptr(), x.offset_dev.data_ptr(), len(x.tensors), bufs,
                  x.count) for x, bufs in ((a, self._buf_ptrs), (b, self._buf2_ptrs))]
         L.hvdx_fuse_allreduce_pair(desc[0], desc[1], self.dtype, self.buf_dtype, self.nranks, self.op, stream)
@@ -197,11 +197,11 @@ class FusedAllreduce:
                 continue
             if b.pair == 1:
                 both = (bi, bi + 1)
-                out += [("pack_rs", bi, 0), ("pack_rs", bi + 1, 0)]
+                out.append(("pack_rs", both, 0))
                 out += [("rs", both, s) for s in range(1, n - 2)]
                 out.append(("rs_ag", both, n - 2))
                 out += [("ag", both, s) for s in range(1, n - 2)]
-                out += [("ag_unpack", bi, n - 2), ("ag_unpack", bi + 1, n - 2)]
+                out.append(("ag_unpack", both, n - 2))
                 continue
             if b.small:
                 if not b.direct:

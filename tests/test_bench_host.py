@@ -87,6 +87,10 @@ REAL_NAMES = {
     "256, false, true, false> >(hvdx::RingPair)": ("rs_ag_step_f32", "Policy<1,256,false,true,false> x2"),
     "void hvdx::(anonymous namespace)::ag_step_pair_kernel<float, true, hvdx::(anonymous namespace)::Policy<2, 512, "
     "false, true, false> >(hvdx::RingPair)": ("ag_step_f32", "Policy<2,512,false,true,false> x2"),
+    "void hvdx::(anonymous namespace)::unpack_pair_kernel<float, float, hvdx::(anonymous namespace)::CopyCfg<2, 1, 2, "
+    "true, true, false, 1, 256> >(hvdx::CopyPair, int, int, int)": ("ag_unpack", "CopyCfg<2,1,2,true,true,false,1,256> x2"),
+    "_ZN4hvdx12_GLOBAL__N_116pack_pair_kernelIfDF16_NS0_7CopyCfgILi2ELi2ELi2ELb1ELb1ELb0ELi1ELi256EEEEEvNS_8CopyPairEiii":
+        ("pack_rs", "CopyCfg<2,2,2,1,1,0,1,256> x2"),
     "__amd_rocclr_copyBuffer": (None, ""),
 }
 
