@@ -15,9 +15,9 @@ allocated and in place for the object's lifetime.
 
 Buckets of at most `small_bucket_bytes` per rank (4 MiB by default) run their whole
 cycle in one launch (hvdx_fuse_allreduce_small, hvdx_ring_allreduce_small): there a
-ring step's launch costs more than its messages.  Two consecutive fused buckets on
-the per-step path run together (hvdx_fuse_allreduce_pair: each launch serves both),
-the second with fusion buffers of its own.  Same bits either way.
+ring step's launch costs more than its messages.  Fused buckets on the per-step path
+run two at a time, paired in plan order (hvdx_fuse_allreduce_pair: each launch serves
+both), the second of a pair with fusion buffers of its own.  Same bits either way.
 """
 from __future__ import annotations
 
@@ -43,7 +43,8 @@ class Bucket:
     offset_dev: torch.Tensor | None = None
     ptrs_dev: torch.Tensor | None = None
     small: bool = False  # the whole cycle in one launch
-    pair: int = 0  # 1: runs with the next bucket, 2: with the previous one (its own fusion buffers)
+    pair: int = 0  # 1: runs together with the later bucket `partner`; 2: with an earlier one
+    partner: int = -1  # (the second of a pair has fusion buffers of its own)
 
 
 class FusedAllreduce:
@@ -60,8 +61,8 @@ class FusedAllreduce:
         (hvdx_fuse_allreduce); otherwise copy-in, ring and copy-out are separate calls.
         With the fused boundary, a bucket of at most small_bucket_bytes per rank (0:
         none) runs its whole cycle in one launch instead (compressed direct tensors
-        excepted).  With pair_buckets (fused boundary) two consecutive fused buckets
-        on the per-step path share every launch.  All give the same bits."""
+        excepted).  With pair_buckets (fused boundary) the fused buckets on the per-step
+        path run two at a time, every launch serving both.  All give the same bits."""
         if schedule not in ("ring", "fold"):
             raise ValueError("schedule must be 'ring' or 'fold'")
         self.schedule = schedule
@@ -103,14 +104,13 @@ class FusedAllreduce:
                        and not (b.direct and self.compress))
 
         if pair_buckets and self.fuse_boundary and n >= 3:
-            i = 0
-            while i + 1 < len(self.buckets):
-                a, b = self.buckets[i], self.buckets[i + 1]
-                if all(not x.direct and not x.small and x.count > 0 for x in (a, b)):
-                    a.pair, b.pair = 1, 2
-                    i += 2
-                else:
-                    i += 1
+            # fused buckets on the per-step path, paired in plan order; a pair runs at its first
+            # member's place, so a direct tensor or small bucket between the two runs after both
+            # (the buckets share no data: the bits do not depend on the order)
+            ok = [i for i, x in enumerate(self.buckets) if not x.direct and not x.small and x.count > 0]
+            for i, j in zip(ok[0::2], ok[1::2]):
+                self.buckets[i].pair, self.buckets[i].partner = 1, j
+                self.buckets[j].pair, self.buckets[j].partner = 2, i
 
         dev = self.device
         cap = max([b.count for b in self.buckets if not b.direct and b.pair != 2], default=0)
@@ -189,14 +189,14 @@ class FusedAllreduce:
         step N-2 fused with replacing step 0), "ag", "ag_unpack" (replacing step N-2
         with copy-out), "unpack", "fold", "ring" (the one-rank compressed round trip),
         "cycle_small" or "ring_small" (a small bucket's whole cycle in one launch).
-        A launch that serves a pair of buckets names both: (kind, (i, i + 1), step)."""
+        A launch that serves a pair of buckets names both: (kind, (i, j), step)."""
         out = []
         n = self.nranks
         for bi, b in enumerate(self.buckets):
             if b.count == 0 or b.pair == 2:
                 continue
             if b.pair == 1:
-                both = (bi, bi + 1)
+                both = (bi, b.partner)
                 out.append(("pack_rs", both, 0))
                 out += [("rs", both, s) for s in range(1, n - 2)]
                 out.append(("rs_ag", both, n - 2))
@@ -258,7 +258,7 @@ class FusedAllreduce:
             stream = torch.cuda.current_stream(self.device).cuda_stream
         for i, b in enumerate(self.buckets):
             if b.pair == 1:
-                self.fused_pair(b, self.buckets[i + 1], stream)
+                self.fused_pair(b, self.buckets[b.partner], stream)
             elif b.pair == 2:
                 continue
             elif b.direct:

@@ -96,6 +96,8 @@ def test_per_phase_records(fuse_boundary):
     got = [(r["kind"], r["step"], r["launches"]) for r in tl.records]
     want = []
     for bi, b in enumerate(ar.buckets):
+        if b.pair == 2:  # ran together with an earlier bucket: that pair's records cover it
+            continue
         if fuse_boundary and not b.direct:  # copy-in + step 0, steps 1-3, 4 + 0, steps 1-3, 4 + copy-out
             want += [(8, 0, 1), (1, 1, 3), (6, 4, 1), (2, 1, 3), (9, 4, 1)]
             continue
