@@ -10,8 +10,7 @@ import ctypes
 import os
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-# HVDX_LIBRARY may name another build of the same library (e.g. a tuning variant)
-LIB_PATH = os.environ.get("HVDX_LIBRARY") or os.path.join(HERE, "libhvdx.so")
+LIB_PATH = os.path.join(HERE, "libhvdx.so")  # the library build() makes, next to this file
 
 FLOAT32, FLOAT16 = 0, 1
 SUM, AVERAGE = 0, 1

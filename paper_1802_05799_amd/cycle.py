@@ -47,6 +47,19 @@ class Bucket:
     partner: int = -1  # (the second of a pair has fusion buffers of its own)
 
 
+def _check_disjoint(tensors) -> None:
+    """Raise ValueError when two of the tensors (any ranks) share memory.  The kernels
+    read and write every rank's tensors in one launch (both buckets' in a paired
+    launch), so a tensor listed twice, or two views of one storage, would make the
+    result depend on the order of blocks; the device pointers cannot be checked on the
+    C side."""
+    spans = sorted((x.data_ptr(), x.data_ptr() + x.numel() * x.element_size(), r, t)
+                   for r, ts in enumerate(tensors) for t, x in enumerate(ts) if x.numel() > 0)
+    for (a0, a1, ra, ta), (b0, b1, rb, tb) in zip(spans, spans[1:]):
+        if b0 < a1:
+            raise ValueError(f"tensors overlap in memory: rank {ra} tensor {ta} and rank {rb} tensor {tb}")
+
+
 class FusedAllreduce:
     """In-place allreduce of N ranks' gradient lists (SUM or AVERAGE)."""
 
@@ -83,6 +96,7 @@ class FusedAllreduce:
                     raise ValueError("tensors must match across ranks in shape, dtype and device")
                 if not x.is_contiguous() or x.device.type != "cuda":
                     raise ValueError("tensors must be contiguous GPU tensors")
+        _check_disjoint(self.tensors)
         self.device = t0[0].device if ntensors else torch.device("cuda", torch.cuda.current_device())
         self.dtype = _HVDX_DTYPE[t0[0].dtype] if ntensors else L.FLOAT32
         if compress and self.dtype != L.FLOAT32:

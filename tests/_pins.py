@@ -287,3 +287,37 @@ def pin_columns(ring_mod, seed=3):
 
 
 RING_PINS = [pin_bruteforce, pin_golden_states, pin_exact_integers, pin_one_hot, pin_rank_bits, pin_order, pin_traffic, pin_columns]
+
+
+# ---- check (2): the bound on the distance to the binary64 sum -------------------------
+def check2_coefficients(n, op, buffer, cast_in):
+    """(c, eta) such that check (2) holds as |result - ref| <= c * A + eta per element.
+
+    ref is the binary64 sum of the rank inputs x_r (the uncast binary32 values), divided
+    by N for AVERAGE; A = sum_r |x_r| divided by D (D = N for AVERAGE, 1 for SUM).
+    buffer: "f32" or "f16", the type the ring adds in; cast_in: the inputs are rounded to
+    binary16 on the way in (fp16 compression of binary32 gradients).
+
+    Derivation (reading R13: Higham's recursive-summation bound).  u is the buffer
+    type's unit roundoff (2^-24 or 2^-11) and g = (N-1)u / (1 - (N-1)u) bounds the
+    relative error of N-1 additions done one after the other: |s - S'| <= g * T' for
+    the computed sum s, the exact sum S' and T' = sum |x'_r| of the values the ring
+    adds.  Addition keeps fl(a+b) = (a+b)(1+d) with |d| <= u also under gradual
+    underflow (a sum of subnormals is exact), so no absolute term enters there.
+      * Rounding the inputs to binary16: x' = x(1+d) + e with |d| <= u and
+        |e| <= 2^-25 (half the subnormal spacing), so |S' - S| <= u T + N 2^-25 and
+        T' <= (1+u) T + N 2^-25.  Without the cast x' = x: u_c = 0, e = 0.
+      * SUM: |s - S| <= g T' + |S' - S| <= T (u_c + g(1+u_c)) + N e (1 + g).
+      * AVERAGE: the one division by N rounds once, |fl(s/N) - s/N| <= u |s|/N + h, with
+        h = half the smallest subnormal of the buffer type (2^-150, 2^-25), and
+        |s| <= (1+g) T'.  So |fl(s/N) - S/N| <= (T/N)(u_c + (g + u(1+g))(1+u_c))
+        + e (1 + g + u(1+g)) + h.
+    """
+    u = 2.0 ** -24 if buffer == "f32" else 2.0 ** -11
+    g = (n - 1) * u / (1 - (n - 1) * u)
+    uc = 2.0 ** -11 if cast_in else 0.0
+    e = 2.0 ** -25 if cast_in else 0.0
+    if op == "sum":
+        return uc + g * (1 + uc), n * e * (1 + g)
+    h = 2.0 ** -150 if buffer == "f32" else 2.0 ** -25
+    return uc + (g + u * (1 + g)) * (1 + uc), e * (1 + g + u * (1 + g)) + h

@@ -240,3 +240,23 @@ def test_pair_argument_errors():
                      hv.SUM) == hv.ERR_INVALID  # fusion buffers must be 16-byte aligned
     lib = hv._lib.lib
     assert lib.hvdx_fuse_allreduce_pair(None, None, hv.FLOAT32, hv.FLOAT32, 3, hv.SUM, None) == hv.ERR_INVALID
+
+
+def test_fused_allreduce_rejects_overlapping_tensors():
+    """Paired launches read and write two buckets' tensors at once, so the cycle refuses
+    tensors that share memory (checked on the host, before any device work)."""
+    import torch
+
+    from paper_1802_05799_amd import cycle
+
+    base = torch.zeros(1000)
+    a, b, c = base[0:100], base[100:300], base[300:400]
+    cycle._check_disjoint([[a, b], [c, base[400:600]]])  # disjoint: no error
+    cycle._check_disjoint([[a, base[0:0]], [c, base[0:0]]])  # empty views take no memory
+    with pytest.raises(ValueError, match="overlap"):
+        cycle._check_disjoint([[a, b], [a, c]])  # one tensor on two ranks
+    with pytest.raises(ValueError, match="overlap"):
+        cycle._check_disjoint([[a, base[50:60]]])  # a view inside another
+    with pytest.raises(ValueError, match="overlap"):
+        cycle._check_disjoint([[base[0:101], b], [c, base[500:600]]])  # one element shared
+

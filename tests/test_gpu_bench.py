@@ -16,7 +16,8 @@ def test_bench_prints_one_complete_json_line(monkeypatch, capsys):
         sys.path.insert(0, ROOT)
     import bench
 
-    monkeypatch.setattr(sys, "argv", ["bench.py", "--steps", "3", "--warmup", "1", "--no-per-config",
+    monkeypatch.setattr(sys, "argv", ["bench.py", "--workload", "resnet50", "--steps", "3", "--warmup", "1",
+                                      "--no-per-config",
                                       "--no-ablation", "--no-broadcast", "--cpu-seconds", "0.5"])
     capsys.readouterr()
     bench.main()
@@ -37,6 +38,11 @@ def test_bench_prints_one_complete_json_line(monkeypatch, capsys):
     assert roof["traffic"] is None or roof["traffic"] > 0
     per_launch = roof["algorithmic_bytes_per_step"] / roof["launches_per_step"]
     assert roof["achieved"] == pytest.approx(per_launch / (roof["avg_launch_us"] * 1e-6) / 1e9, rel=2e-3)
+    ring = out["ring_roofline"]
+    assert ring["bound"] == "hbm" and ring["peak"] == 8000.0 and 0 < ring["achieved"] < ring["peak"]
+    assert set(ring["kernels"]) == {"rs_step_f32", "rs_ag_step_f32", "ag_step_f32"}
+    assert ring["achieved"] == pytest.approx(
+        ring["algorithmic_bytes_per_step"] / (ring["kernel_ms_per_step"] * 1e-3) / 1e9, rel=2e-3)
     cpu = out["cpu_baseline"]
     assert cpu["kind"] == "oracle" and cpu["unit"] == "GB/s" and cpu["value"] > 0 and cpu["cores"] >= 1
     assert cpu["sample"]

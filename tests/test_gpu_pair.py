@@ -1,5 +1,6 @@
 """Two fusion buffers' cycles with each ring step of both in one launch
-(hvdx_fuse_allreduce_pair, used by FusedAllreduce for consecutive fused buckets):
+(hvdx_fuse_allreduce_pair, used by FusedAllreduce for fused buckets paired in plan
+order, also across a direct tensor between them):
 bit for bit the oracle's result, and the same as running the buckets one by one."""
 import numpy as np
 import pytest
@@ -12,19 +13,26 @@ from oracle import allreduce
 pytestmark = pytest.mark.gpu
 
 CASES = [
-    # (numel, nranks, threshold bytes, compress, op)
-    ([6000, 3000, 7001, 2500, 9000, 40, 12000, 333], 5, 40000, False, "average"),  # pair, one alone, a direct
-    ([6000, 3000, 7001, 2500, 9000, 40, 12000, 333], 8, 40000, True, "sum"),  # binary16 buffers
-    ([3, 5], 8, 32, False, "average"),  # both rings shorter than the rank count
-    ([1000, 1, 1500, 70000, 513, 700], 3, 8192, False, "sum"),  # three ranks: no plain ring step
-    ([2048] * 5 + [100], 13, 16384, False, "average"),  # two pairs' worth, the last bucket alone
-    ([100003, 31, 64000, 7], 4, 256 << 10, True, "average"),  # rings of very different lengths
+    # (numel, nranks, threshold bytes, compress, op, the pairs FusedAllreduce forms)
+    # buckets [0,1] [2,3] [4,5] fused, [6] direct, [7] fused: the second pair spans the direct tensor
+    ([6000, 3000, 7001, 2500, 9000, 40, 12000, 333], 5, 40000, False, "average", [(0, 1), (2, 4)]),
+    # binary16 buffers: three fused buckets, the last alone
+    ([6000, 3000, 7001, 2500, 9000, 40, 12000, 333], 8, 40000, True, "sum", [(0, 1)]),
+    ([3, 5], 8, 32, False, "average", [(0, 1)]),  # both rings shorter than the rank count
+    # three ranks (no plain ring step): fused, fused, direct, fused (alone)
+    ([1000, 1, 1500, 70000, 513, 700], 3, 8192, False, "sum", [(0, 1)]),
+    ([2048] * 5 + [100], 13, 16384, False, "average", [(0, 1)]),  # a pair, the last bucket alone
+    ([100003, 31, 64000, 7], 4, 256 << 10, True, "average", [(0, 1)]),  # rings of very different lengths
+    # the most ranks a call takes (full rank-pointer tables in the kernel argument):
+    # fused [0,1,2] and [3] paired, [4] direct, [5] alone; binary32 and binary16 buffers
+    ([3000, 5000, 257, 9000, 70000, 4100], 128, 40000, False, "average", [(0, 1)]),
+    ([3000, 5000, 257, 9000, 70000, 4100], 128, 20000, True, "average", [(0, 1)]),
 ]
 
 
 @pytest.mark.parametrize("case", range(len(CASES)))
 def test_pairs_match_oracle_and_single_cycles(case):
-    numel, n, threshold, compress, op = CASES[case]
+    numel, n, threshold, compress, op, pairs = CASES[case]
     say(f"pair case {case}: N={n} numel={numel[:4]}... threshold={threshold} compress={compress} {op}")
     rng = np.random.default_rng(4200 + case)
     host = [[(rng.standard_normal(k) * 0.01).astype(np.float32) for k in numel] for _ in range(n)]
@@ -34,7 +42,8 @@ def test_pairs_match_oracle_and_single_cycles(case):
         dev = [[torch.from_numpy(x).cuda() for x in row] for row in host]
         ar = hv.FusedAllreduce(dev, op=op, compress=compress, threshold_bytes=threshold, small_bucket_bytes=0,
                                pair_buckets=pair)
-        assert any(b.pair == 1 for b in ar.buckets) == pair
+        got_pairs = [(i, b.partner) for i, b in enumerate(ar.buckets) if b.pair == 1]
+        assert got_pairs == (pairs if pair else [])
         for rep, want in enumerate((want1, want2)):  # the second call reduces the first's result again
             ar()
             torch.cuda.synchronize()

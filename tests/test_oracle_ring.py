@@ -55,9 +55,9 @@ def test_owner_after_reduce_scatter():
 
 def test_check1_every_rank_identical_and_check2_fp64_bound():
     """Checks (1) and (2): identical ranks; |got - fp64 sum| within the recursive-summation
-    bound gamma_{N-1} * sum|x| (+ one rounding for the divide), and within rel 1e-6*N."""
+    bound gamma_{N-1} * sum|x| plus one rounding for the divide (derived in
+    _pins.check2_coefficients), and within rel 1e-6*N."""
     rng = np.random.default_rng(6)
-    u = 2.0 ** -24
     for n in (1, 2, 3, 4, 7, 8, 16, 33):
         count = 3 * n + 101
         x = (rng.standard_normal((n, count)) * 0.01).astype(np.float32)
@@ -67,30 +67,30 @@ def test_check1_every_rank_identical_and_check2_fp64_bound():
             d = n if op == "average" else 1
             ref = x.astype(np.float64).sum(axis=0) / d
             absum = np.abs(x.astype(np.float64)).sum(axis=0) / d
-            k = n - 1
-            gamma = k * u / (1 - k * u)
-            bound = (gamma + u) * absum
+            c, eta = _pins.check2_coefficients(n, op, "f32", cast_in=False)
             err = np.abs(got[0].astype(np.float64) - ref)
-            assert np.all(err <= bound), (n, op)
+            assert np.all(err <= c * absum + eta), (n, op)
             assert np.all(err <= 1e-6 * n * absum)
 
 
 def test_fp16_buffers_fp64_bound():
-    """Check (2) for binary16 buffers: rel (N+1)*2^-11 of sum|x| plus half a subnormal
-    quantum per rounding."""
+    """Check (2) for binary16 buffers fed with binary32 values rounded on the way in: the
+    bound of _pins.check2_coefficients (the cast's rounding, N-1 binary16 additions, the
+    divide, half a subnormal spacing per rounding in the subnormal range)."""
     rng = np.random.default_rng(7)
-    for n in (2, 4, 5, 16, 64):
+    for n in (1, 2, 4, 5, 16, 64):
         count = 2 * n + 257
         x32 = (rng.standard_normal((n, count)) * 0.01).astype(np.float32)
+        x32[:, :4] *= 2.0 ** -12  # some inputs and sums in binary16's subnormal range
         x16 = x32.astype(np.float16)
         for op in ("sum", "average"):
             got = ring.ring_allreduce(x16.copy(), op)
             d = n if op == "average" else 1
             ref = x32.astype(np.float64).sum(axis=0) / d
             absum = np.abs(x32.astype(np.float64)).sum(axis=0) / d
-            eta = 2 * n * 2.0 ** -25
+            c, eta = _pins.check2_coefficients(n, op, "f16", cast_in=True)
             err = np.abs(got[0].astype(np.float64) - ref)
-            assert np.all(err <= 1.01 * (n + 1) * 2.0 ** -11 * absum + eta), (n, op)
+            assert np.all(err <= c * absum + eta), (n, op)
 
 
 def test_empty_and_single_rank():
