@@ -291,6 +291,34 @@ int hvdx_ring_allreduce(void* const* bufs, int nranks, int64_t count, int dtype,
 int hvdx_ring_allreduce_small(void* const* bufs, int nranks, int64_t count, int dtype, int op, void* stream);
 
 /*
+ * hvdx_ring_allreduce_noalloc -- hvdx_ring_allreduce for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc): the same kernels, the same result bit for bit, but the
+ * compression workspace is a static array inside the library instead of an argument.
+ * The call allocates nothing (no hipMalloc, hipFree or allocating library routine).
+ *
+ *   bufs, nranks, count, dtype, op, compress, stream   as hvdx_ring_allreduce
+ *
+ * Limit: hvdx_ring_workspace_bytes(nranks, count, dtype, compress) must not exceed
+ * hvdx_ring_noalloc_max_bytes() (64 MiB: e.g. 8 ranks of up to 4,194,304 binary32
+ * elements compressed); larger requests return HVDX_ERR_WORKSPACE before any HIP
+ * call.  Without compression no workspace is used and any size works.
+ * The static array is held by every GPU the library runs on until the process ends;
+ * its device address is looked up on the first call per device (the stream's device,
+ * or the current device for the null stream).  Nothing in it needs to start at zero
+ * (every wire element a step reads was written by an earlier step of the same call),
+ * and it keeps the last call's contents.  All calls on one GPU share the array:
+ * calls that overlap in time on one GPU (on different streams, or from different
+ * threads) race; serialize them on one stream.
+ * Errors: as hvdx_ring_allreduce; HVDX_ERR_WORKSPACE beyond the limit;
+ * HVDX_ERR_UNSUPPORTED on a device index of 64 or more.
+ */
+int hvdx_ring_allreduce_noalloc(void* const* bufs, int nranks, int64_t count, int dtype, int op, int compress,
+                                void* stream);
+/* Bytes of the static compression workspace behind hvdx_ring_allreduce_noalloc. */
+size_t hvdx_ring_noalloc_max_bytes(void);
+
+/*
  * hvdx_ring_reduce_scatter / hvdx_ring_allgather -- the two halves of
  * hvdx_ring_allreduce (paper section 3: the N-1 adding iterations, then the N-1
  * replacing iterations), each one call.  Running the first and then the second

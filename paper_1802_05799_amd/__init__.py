@@ -45,6 +45,8 @@ from ._lib import (  # noqa: F401
     hvdx_ring_allgather,
     hvdx_ring_allreduce,
     hvdx_ring_allreduce_small,
+    hvdx_ring_allreduce_noalloc,
+    hvdx_ring_noalloc_max_bytes,
     hvdx_ring_chunk,
     hvdx_ring_reduce_scatter,
     hvdx_ring_step,

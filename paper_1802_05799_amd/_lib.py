@@ -41,6 +41,8 @@ _SIGNATURES = {
     "hvdx_fuse_allreduce_pair": (_i, [_p, _p, _i, _i, _i, _i, _p]),
     "hvdx_ring_allreduce": (_i, [_pp, _i, _i64, _i, _i, _i, _p, _sz, _p]),
     "hvdx_ring_allreduce_small": (_i, [_pp, _i, _i64, _i, _i, _p]),
+    "hvdx_ring_allreduce_noalloc": (_i, [_pp, _i, _i64, _i, _i, _i, _p]),
+    "hvdx_ring_noalloc_max_bytes": (_sz, []),
     "hvdx_ring_step": (_i, [_pp, _i, _i64, _i, _i, _i, _i, _i, _p, _sz, _p]),
     "hvdx_ring_reduce_scatter": (_i, [_pp, _i, _i64, _i, _i, _i, _p, _sz, _p]),
     "hvdx_ring_allgather": (_i, [_pp, _i, _i64, _i, _i, _i, _p, _sz, _p]),
@@ -229,6 +231,16 @@ def hvdx_ring_allreduce(bufs, nranks: int, count: int, dtype: int, op: int, comp
                         workspace: int = 0, workspace_bytes: int = 0, stream: int = 0) -> None:
     pb, _keep = _ptr_array(bufs)
     _check(lib.hvdx_ring_allreduce(pb, nranks, count, dtype, op, compress, workspace, workspace_bytes, stream))
+
+
+def hvdx_ring_allreduce_noalloc(bufs, nranks: int, count: int, dtype: int, op: int, compress: int = COMPRESS_NONE,
+                                stream: int = 0) -> None:
+    pb, _keep = _ptr_array(bufs)
+    _check(lib.hvdx_ring_allreduce_noalloc(pb, nranks, count, dtype, op, compress, stream))
+
+
+def hvdx_ring_noalloc_max_bytes() -> int:
+    return lib.hvdx_ring_noalloc_max_bytes()
 
 
 def hvdx_ring_reduce_scatter(bufs, nranks: int, count: int, dtype: int, op: int, compress: int = COMPRESS_NONE,

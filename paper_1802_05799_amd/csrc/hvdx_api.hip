@@ -284,6 +284,45 @@ int check_fusion(const void* const* tensors, const int64_t* numel, const int64_t
 
 }  // namespace
 
+// ---- the ring without a caller-provided workspace --------------------------------------
+//
+// The compressed ring's binary16 wire copies live in `scratch`, a static device array
+// that the code object carries (one copy per GPU the library runs on, held until the
+// process ends).  Its device address is looked up once per device, with that device
+// current, and kept; host code never passes the array's own name to a kernel (on the
+// host that name is only a stand-in for the device symbol).
+namespace {
+constexpr size_t kScratchBytes = (size_t)64 << 20;
+__attribute__((used)) static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+constexpr int kScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kScratchDevices] = {};
+
+int scratch_for(hipStream_t st, void** out, const char* what) {
+  int dev = -1;
+  hipError_t e = st ? hipStreamGetDevice(st, &dev) : hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "static workspace: the stream's device");
+  if (dev < 0 || dev >= kScratchDevices)
+    return fail(HVDX_ERR_UNSUPPORTED, "%s: device %d beyond the %d this build serves", what, dev, kScratchDevices);
+  std::lock_guard<std::mutex> g(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    int cur = -1;
+    e = hipGetDevice(&cur);
+    if (e != hipSuccess) return hip_fail(e, "static workspace: hipGetDevice");
+    if (cur != dev && (e = hipSetDevice(dev)) != hipSuccess) return hip_fail(e, "static workspace: hipSetDevice");
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (cur != dev) (void)hipSetDevice(cur);
+    if (e != hipSuccess) return hip_fail(e, "static workspace: hipGetSymbolAddress");
+    if (!p || (reinterpret_cast<uintptr_t>(p) & 255))
+      return fail(HVDX_ERR_HIP, "%s: static workspace address %p is not 256-byte aligned", what, p);
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return HVDX_OK;
+}
+}  // namespace
+
 extern "C" {
 
 int hvdx_version(void) { return HVDX_VERSION; }
@@ -754,6 +793,31 @@ int hvdx_fold_allreduce(void* const* bufs, int nranks, int64_t count, int dtype,
   const hipError_t e = hvdx::launch_fold(rank_ptrs(bufs, nranks), a, count, dtype, compress, div_mode(op, nranks),
                                          vectors_ok(bufs, nranks, nullptr), st);
   return e == hipSuccess ? HVDX_OK : hip_fail(e, "fold launch");
+}
+
+size_t hvdx_ring_noalloc_max_bytes(void) { return kScratchBytes; }
+
+int hvdx_ring_allreduce_noalloc(void* const* bufs, int nranks, int64_t count, int dtype, int op, int compress,
+                                void* stream) {
+  static const char* what = "hvdx_ring_allreduce_noalloc";
+  // every argument check first (no HIP call before them), the workspace's size included
+  int rc = check_ring(bufs, nranks, count, dtype, op, HVDX_COMPRESS_NONE, nullptr, 0, what);
+  if (rc) return rc;
+  if (compress != HVDX_COMPRESS_NONE && compress != HVDX_COMPRESS_FP16)
+    return fail(HVDX_ERR_INVALID, "%s: unknown compression %d", what, compress);
+  if (compress == HVDX_COMPRESS_FP16 && dtype != HVDX_FLOAT32)
+    return fail(HVDX_ERR_INVALID, "%s: fp16 compression needs float32 buffers", what);
+  const size_t need = hvdx_ring_workspace_bytes(nranks, count, dtype, compress);
+  if (need > kScratchBytes)
+    return fail(HVDX_ERR_WORKSPACE, "%s: %d ranks of %lld elements need %zu bytes of wire workspace; the static one "
+                "holds %zu (use hvdx_ring_allreduce with a workspace)", what, nranks, (long long)count, need,
+                kScratchBytes);
+  if (need == 0)  // nothing compressed: no workspace at all
+    return hvdx_ring_allreduce(bufs, nranks, count, dtype, op, compress, nullptr, 0, stream);
+  void* ws = nullptr;
+  rc = scratch_for(static_cast<hipStream_t>(stream), &ws, what);
+  if (rc) return rc;
+  return hvdx_ring_allreduce(bufs, nranks, count, dtype, op, compress, ws, kScratchBytes, stream);
 }
 
 static int check_bcast(void* const* bufs, int nranks, int64_t nbytes, int root, const char* what) {

@@ -260,3 +260,28 @@ def test_fused_allreduce_rejects_overlapping_tensors():
     with pytest.raises(ValueError, match="overlap"):
         cycle._check_disjoint([[base[0:101], b], [c, base[500:600]]])  # one element shared
 
+
+def test_noalloc_ring_argument_checks():
+    """The allocation-free ring checks its arguments and the static workspace's size
+    before any HIP call (so these run without a GPU)."""
+    lib = ctypes.CDLL(hv.LIB_PATH)
+    lib.hvdx_ring_allreduce_noalloc.restype = ctypes.c_int
+    lib.hvdx_ring_allreduce_noalloc.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_int,
+                                                ctypes.c_int, ctypes.c_int, ctypes.c_void_p]
+    cap = hv.hvdx_ring_noalloc_max_bytes()
+    assert cap == 64 << 20
+
+    def status(n, count, dtype=hv.FLOAT32, op=hv.AVERAGE, compress=hv.COMPRESS_FP16, ptrs=None):
+        ptrs = ptrs or [FAKE + r * (1 << 32) for r in range(n)]
+        arr = (ctypes.c_void_p * len(ptrs))(*ptrs)
+        return lib.hvdx_ring_allreduce_noalloc(arr, n, count, dtype, op, compress, None)
+
+    assert status(8, 4_194_304 + 1) == hv.ERR_WORKSPACE  # 8 x 4,194,432 binary16 elements > 64 MiB
+    assert "static" in hv.hvdx_last_error()
+    assert status(128, 262_145) == hv.ERR_WORKSPACE
+    assert status(2, 10, dtype=hv.FLOAT16) == hv.ERR_INVALID  # compression needs binary32
+    assert status(2, 10, compress=7) == hv.ERR_INVALID
+    assert status(2, 10, op=9) == hv.ERR_INVALID
+    assert status(0, 10) == hv.ERR_INVALID
+    assert status(2, 10, ptrs=[FAKE, FAKE + 8]) == hv.ERR_ALIAS
+    assert status(3, 0) == hv.OK  # nothing to do, no HIP call
