@@ -370,6 +370,36 @@ int hvdx_broadcast(void* const* bufs, int nranks, int64_t nbytes, int root, void
 int hvdx_broadcast_step(void* const* bufs, int nranks, int64_t nbytes, int root, int step, void* stream);
 
 /*
+ * hvdx_broadcast_tensors -- hvdx_broadcast for many tensors in one call (paper
+ * sections 4 and 5: every variable broadcast from the root at start-up), 2N-2 launches
+ * in all instead of 2N-2 per tensor.  The tensors are laid end to end in a virtual
+ * byte space, tensor t at [voffset[t], voffset[t] + nbytes[t]), and the chain of
+ * hvdx_broadcast runs over that space as over one buffer of total_bytes bytes: chunk j
+ * is the j-th run of whole 16-byte units, and in step s rank root+k forwards chunk s-k
+ * to rank root+k+1.  Bytes of the space that belong to no tensor are not moved.  Every
+ * rank ends with the root's bytes of every tensor.
+ *
+ *   ptrs[nranks*ntensors]  DEVICE array of tensor pointers, rank-major (rank r's tensor t
+ *                          at r*ntensors + t); the tensors must not overlap (not
+ *                          checked: the table is in device memory); 16-byte aligned
+ *                          copies move as vectors, others byte by byte
+ *   nbytes[ntensors]       DEVICE array, bytes of each tensor (>= 0)
+ *   voffset[ntensors]      DEVICE array, ascending multiples of 16 with
+ *                          voffset[t] >= voffset[t-1] + nbytes[t-1]
+ *   total_bytes            >= voffset[T-1] + nbytes[T-1]; 0 (or ntensors 0) is a no-op
+ *   root                   0..nranks-1
+ * hvdx_broadcast_layout (host) computes the densest layout: each tensor at the first
+ * multiple of 16 at or after the previous one's end; total_bytes = the last one's end.
+ * hvdx_broadcast_tensors_step runs step `step` (0 <= step < 2*nranks-2) alone.
+ * Errors: HVDX_ERR_INVALID (host-side arguments), HVDX_ERR_HIP.
+ */
+int hvdx_broadcast_layout(const int64_t* nbytes, int ntensors, int64_t* voffset, int64_t* total_bytes);
+int hvdx_broadcast_tensors(const void* const* ptrs, const int64_t* nbytes, const int64_t* voffset, int ntensors,
+                           int64_t total_bytes, int nranks, int root, void* stream);
+int hvdx_broadcast_tensors_step(const void* const* ptrs, const int64_t* nbytes, const int64_t* voffset, int ntensors,
+                                int64_t total_bytes, int nranks, int root, int step, void* stream);
+
+/*
  * hvdx_fold_allreduce -- the same result as hvdx_ring_allreduce, bit for bit,
  * computed without the ring's messages: each element's N values are read once and
  * added in the ring's order (starting at the rank whose chunk holds the element,

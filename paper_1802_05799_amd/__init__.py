@@ -32,6 +32,9 @@ from ._lib import (  # noqa: F401
     HvdxError,
     hvdx_broadcast,
     hvdx_broadcast_step,
+    hvdx_broadcast_layout,
+    hvdx_broadcast_tensors,
+    hvdx_broadcast_tensors_step,
     hvdx_fold_allreduce,
     hvdx_fuse_ag_unpack,
     hvdx_fuse_allreduce,
@@ -60,18 +63,73 @@ from .cycle import FusedAllreduce  # noqa: F401
 from .timeline import Timeline  # noqa: F401
 
 
+class TensorBroadcast:
+    """Rank `root`'s tensors copied into every other rank's (paper sections 4 and 5:
+    consistent initial variables), every tensor of the list in one chain:
+    hvdx_broadcast_tensors runs the 2N-2 chain steps once for the whole list, over the
+    tensors laid end to end at 16-byte aligned starts.  Bytes are copied, not
+    interpreted: tensor t must have the same byte count on every rank (any dtype), be
+    contiguous, on one GPU, and share memory with no other tensor.  The descriptor
+    tables are uploaded once (asynchronously, from pinned memory); the tensors must stay
+    allocated and in place."""
+
+    def __init__(self, per_rank):
+        import numpy as np
+
+        if not per_rank or len(per_rank) > MAX_RANKS:
+            raise ValueError(f"need 1..{MAX_RANKS} ranks")
+        self.nranks = n = len(per_rank)
+        self.ntensors = nt = len(per_rank[0])
+        if any(len(ts) != nt for ts in per_rank):
+            raise ValueError("every rank needs the same number of tensors")
+        flat = [x for ts in per_rank for x in ts]
+        if not all(x.is_cuda and x.is_contiguous() for x in flat):
+            raise ValueError("broadcast needs contiguous GPU tensors")
+        if len({x.get_device() for x in flat}) > 1:
+            raise ValueError("broadcast needs every tensor on one GPU")
+        ptr = np.fromiter((x.data_ptr() for x in flat), dtype=np.int64, count=len(flat))
+        nbytes = np.fromiter((x.nbytes for x in flat), dtype=np.int64, count=len(flat)).reshape(n, nt)
+        if (nbytes != nbytes[:1]).any():
+            raise ValueError("tensor t must have the same byte count on every rank")
+        live = nbytes.reshape(-1) > 0
+        starts = ptr[live]
+        order = np.argsort(starts, kind="stable")
+        ends = starts[order] + nbytes.reshape(-1)[live][order]
+        if (ends[:-1] > starts[order][1:]).any():
+            raise ValueError("tensors overlap in memory")
+        self.device = flat[0].device if flat else torch.device("cuda", torch.cuda.current_device())
+        voff, self.total = hvdx_broadcast_layout(nbytes[0].tolist() if nt else [])
+        # one upload: the rank-major pointer table, then the byte counts, then the starts
+        host = torch.from_numpy(np.concatenate([ptr, nbytes[0], np.asarray(voff, dtype=np.int64), [0]]))
+        self.tables = host.pin_memory().to(self.device, non_blocking=True)
+        self._ready = torch.cuda.Event()  # a call on another stream waits for the upload
+        self._ready.record(torch.cuda.current_stream(self.device))
+        self._waited = set()
+        k = n * nt
+        self._args = (self.tables.data_ptr(), self.tables.data_ptr() + 8 * k, self.tables.data_ptr() + 8 * (k + nt),
+                      nt, self.total, n)
+        self.tensors = per_rank  # keeps the tensors alive as long as the tables point at them
+
+    def _stream(self, stream):
+        if stream is None:
+            stream = torch.cuda.current_stream(self.device).cuda_stream
+        if stream not in self._waited:  # once per stream: the tables' upload precedes the first launch
+            torch.cuda.ExternalStream(stream, device=self.device).wait_event(self._ready)
+            self._waited.add(stream)
+        return stream
+
+    def __call__(self, root: int = 0, stream: int | None = None) -> None:
+        hvdx_broadcast_tensors(*self._args, root, self._stream(stream))
+
+    def step(self, root: int, step: int, stream: int | None = None) -> None:
+        """One chain step alone (hvdx_broadcast_tensors_step)."""
+        hvdx_broadcast_tensors_step(*self._args, root, step, self._stream(stream))
+
+
 def broadcast_(per_rank, root: int = 0) -> None:
-    """Copy rank `root`'s tensors into every other rank's, tensor by tensor (paper
-    sections 4 and 5: consistent initial variables).  Tensors must be contiguous GPU
-    tensors of matching shapes and dtypes across ranks."""
-    n = len(per_rank)
-    for ts in zip(*per_rank):
-        ref = ts[0]
-        for x in ts:
-            if x.shape != ref.shape or x.dtype != ref.dtype or not x.is_contiguous() or x.device.type != "cuda":
-                raise ValueError("broadcast needs contiguous GPU tensors matching across ranks")
-        stream = torch.cuda.current_stream(ref.device).cuda_stream
-        hvdx_broadcast([x.data_ptr() for x in ts], n, ref.numel() * ref.element_size(), root, stream)
+    """Copy rank `root`'s tensors into every other rank's, all of them in one chain
+    (TensorBroadcast)."""
+    TensorBroadcast(per_rank)(root)
 
 
 def allreduce_(per_rank, op: str = "average", compress: bool = False,

@@ -53,6 +53,9 @@ _SIGNATURES = {
     "hvdx_version": (_i, []),
     "hvdx_broadcast": (_i, [_pp, _i, _i64, _i, _p]),
     "hvdx_broadcast_step": (_i, [_pp, _i, _i64, _i, _i, _p]),
+    "hvdx_broadcast_layout": (_i, [_pi64, _i, _pi64, _pi64]),
+    "hvdx_broadcast_tensors": (_i, [_p, _p, _p, _i, _i64, _i, _i, _p]),
+    "hvdx_broadcast_tensors_step": (_i, [_p, _p, _p, _i, _i64, _i, _i, _i, _p]),
     "hvdx_fold_allreduce": (_i, [_pp, _i, _i64, _i, _i, _i, _p]),
     "hvdx_timeline_begin": (_i, [_i, _i]),
     "hvdx_timeline_end": (_i, [_p, _i, ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_int)]),
@@ -289,3 +292,24 @@ def hvdx_fold_allreduce(bufs, nranks: int, count: int, dtype: int, op: int, comp
                         stream: int = 0) -> None:
     pb, _keep = _ptr_array(bufs)
     _check(lib.hvdx_fold_allreduce(pb, nranks, count, dtype, op, compress, stream))
+
+
+def hvdx_broadcast_layout(nbytes):
+    """(virtual start of each tensor, length of the space) for hvdx_broadcast_tensors."""
+    n = len(nbytes)
+    a = (ctypes.c_int64 * max(1, n))(*nbytes)
+    off = (ctypes.c_int64 * max(1, n))()
+    total = ctypes.c_int64()
+    _check(lib.hvdx_broadcast_layout(a, n, off, ctypes.byref(total)))
+    return list(off[:n]), total.value
+
+
+def hvdx_broadcast_tensors(ptrs_dev: int, nbytes_dev: int, voffset_dev: int, ntensors: int, total_bytes: int,
+                           nranks: int, root: int, stream: int = 0) -> None:
+    _check(lib.hvdx_broadcast_tensors(ptrs_dev, nbytes_dev, voffset_dev, ntensors, total_bytes, nranks, root, stream))
+
+
+def hvdx_broadcast_tensors_step(ptrs_dev: int, nbytes_dev: int, voffset_dev: int, ntensors: int, total_bytes: int,
+                                nranks: int, root: int, step: int, stream: int = 0) -> None:
+    _check(lib.hvdx_broadcast_tensors_step(ptrs_dev, nbytes_dev, voffset_dev, ntensors, total_bytes, nranks, root,
+                                           step, stream))

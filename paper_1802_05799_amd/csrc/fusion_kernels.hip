@@ -765,6 +765,79 @@ __global__ __launch_bounds__(kBlock) void small_cycle_kernel(const void* const* 
   }
 }
 
+// ---- the broadcast chain over many tensors ------------------------------------------
+//
+// One chain step (paper sections 4 and 5; reading B2): block row y is link k, from rank
+// root+k to rank root+k+1, carrying chunk step-k of the virtual byte space in which the
+// call's tensors lie end to end, each starting on a 16-byte boundary.  A block copies
+// one tile of its chunk.  It finds the tile's tensors as the copy kernels do (positions
+// are bytes here, and the two ranks of the link are the tile's two pointer slots); a
+// tile inside one tensor whose two copies are 16-byte aligned there is moved as whole
+// vectors, otherwise each lane takes its 16-byte units one by one: a unit inside one
+// tensor with both copies aligned as a vector, a tensor's short last unit or an
+// unaligned copy byte by byte.  Bytes between tensors belong to none and are skipped.
+using BcastCfg = CopyCfg<2, 1, 2, true, true>;
+typedef unsigned int b32x4 __attribute__((ext_vector_type(4)));
+
+__global__ __launch_bounds__(BcastCfg::BS) void bcast_tensors_step_kernel(BcastTensorsArgs a) {
+  using Cfg = BcastCfg;
+  constexpr int V = 16;  // bytes per unit
+  constexpr int64_t kTileBytes = (int64_t)Cfg::kTileVecs * V;
+  __shared__ int64_t s_off[Cfg::kLdsTensors], s_end[Cfg::kLdsTensors], s_meta[2];
+  __shared__ const void* s_ptr[kLdsPtrs];
+  const int k = blockIdx.y;
+  const int64_t j = (int64_t)a.step - k;
+  if (j < 0 || j >= a.n) return;  // this link carries nothing in this step
+  const int src = (a.root + k) % a.n;
+  const int64_t u0 = j * a.q + (j < a.rem ? j : a.rem);
+  const int64_t units = a.q + (j < a.rem ? 1 : 0);
+  const int64_t lo = u0 * V < a.total ? u0 * V : a.total;
+  const int64_t hi = (u0 + units) * V < a.total ? (u0 + units) * V : a.total;
+  const int64_t p0 = lo + (int64_t)blockIdx.x * kTileBytes;
+  if (p0 >= hi) return;  // past the end of a shorter chunk: the whole block leaves
+  const int64_t p1 = p0 + kTileBytes < hi ? p0 + kTileBytes : hi;
+  bool pin;
+  // slot 0 is the sending rank, slot 1 the receiving one
+  const TileTable tt = stage_tile<Cfg::kLdsTensors>(a.voff, a.nbytes, a.ntensors, p0, p1, a.ptrs, 0, 2, src, a.n,
+                                                    s_off, s_end, s_meta, s_ptr, &pin);
+  const PtrTable pt{a.ptrs, pin ? s_ptr : nullptr, tt.t0, a.ntensors, tt.nt, 0, src, a.n};
+
+  if (tt.nt == 1 && tt.t0 >= 0 && p1 - p0 == kTileBytes) {  // block-uniform
+    const int64_t beg = tensor_begin(tt, s_off, a.voff, 0);
+    const int64_t end = tensor_end(tt, s_end, a.voff, a.nbytes, 0);
+    const unsigned char* s = static_cast<const unsigned char*>(pt.get(0, tt.t0)) + (p0 - beg);
+    unsigned char* d = static_cast<unsigned char*>(const_cast<void*>(pt.get(1, tt.t0))) + (p0 - beg);
+    if (beg <= p0 && p1 <= end && aligned16(s) && aligned16(d)) {
+      b32x4 v[Cfg::POS];
+#pragma unroll
+      for (int u = 0; u < Cfg::POS; ++u) v[u] = ld16<Cfg::NTL>(reinterpret_cast<const b32x4*>(s + tile_vec<Cfg>(u) * V));
+#pragma unroll
+      for (int u = 0; u < Cfg::POS; ++u) st16<Cfg::NTS>(reinterpret_cast<b32x4*>(d + tile_vec<Cfg>(u) * V), v[u]);
+      return;
+    }
+  }
+
+  for (int u = 0; u < Cfg::POS; ++u) {
+    const int64_t p = p0 + (int64_t)tile_vec<Cfg>(u) * V;
+    if (p >= p1) continue;
+    const int jt = lookup(tt, s_off, a.voff, p);
+    const int64_t t = tt.t0 + jt;
+    if (t < 0) continue;  // before the first tensor
+    const int64_t beg = tensor_begin(tt, s_off, a.voff, jt);
+    const int64_t end = tensor_end(tt, s_end, a.voff, a.nbytes, jt);
+    if (p >= end) continue;  // between two tensors
+    // tensor t starts at or before p (lookup), so bytes [p, stop) are its own
+    const int64_t stop = p + V < end ? (p + V < p1 ? p + V : p1) : (end < p1 ? end : p1);
+    const unsigned char* s = static_cast<const unsigned char*>(pt.get(0, t)) + (p - beg);
+    unsigned char* d = static_cast<unsigned char*>(const_cast<void*>(pt.get(1, t))) + (p - beg);
+    if (stop - p == V && aligned16(s) && aligned16(d)) {
+      st16<Cfg::NTS>(reinterpret_cast<b32x4*>(d), ld16<Cfg::NTL>(reinterpret_cast<const b32x4*>(s)));
+    } else {
+      for (int64_t e = 0; e < stop - p; ++e) d[e] = s[e];
+    }
+  }
+}
+
 template <typename Cfg>
 unsigned tiles_for(int64_t count, int64_t vec) {
   const int64_t per = (int64_t)Cfg::kTileVecs * vec;
@@ -912,6 +985,16 @@ hipError_t launch_small_cycle(const void* const* tensors, const int64_t* numel, 
   }
 #undef HVDX_SMALL_D
 #undef HVDX_SMALL
+  return hipGetLastError();
+}
+
+hipError_t launch_bcast_tensors_step(const BcastTensorsArgs& a, hipStream_t stream) {
+  const int64_t tile = (int64_t)BcastCfg::kTileVecs * 16;
+  const int64_t longest = (a.q + (a.rem ? 1 : 0)) * 16;  // bytes of the longest chunk
+  int64_t bx = (longest + tile - 1) / tile;
+  if (bx < 1) bx = 1;
+  if (bx > 0x7fffffff) return hipErrorInvalidValue;  // one tile per block: no block may be dropped
+  HVDX_LAUNCH(bcast_tensors_step_kernel, dim3((unsigned)bx, (unsigned)(a.n - 1)), dim3(BcastCfg::BS), 0, stream, a);
   return hipGetLastError();
 }
 

@@ -853,6 +853,78 @@ int hvdx_broadcast_step(void* const* bufs, int nranks, int64_t nbytes, int root,
   return bcast_step(bufs, nranks, nbytes, root, step, static_cast<hipStream_t>(stream));
 }
 
+int hvdx_broadcast_layout(const int64_t* nbytes, int ntensors, int64_t* voffset, int64_t* total_bytes) {
+  if (ntensors < 0 || !total_bytes || (ntensors > 0 && (!nbytes || !voffset)))
+    return fail(HVDX_ERR_INVALID, "hvdx_broadcast_layout: bad arguments");
+  int64_t end = 0;
+  for (int t = 0; t < ntensors; ++t) {
+    if (nbytes[t] < 0 || nbytes[t] > (INT64_MAX >> 2) - end)
+      return fail(HVDX_ERR_INVALID, "hvdx_broadcast_layout: bad byte count for tensor %d", t);
+    voffset[t] = (end + 15) / 16 * 16;
+    end = voffset[t] + nbytes[t];
+  }
+  *total_bytes = end;
+  return HVDX_OK;
+}
+
+static int check_bcast_tensors(const void* const* ptrs, const int64_t* nbytes, const int64_t* voffset, int ntensors,
+                               int64_t total_bytes, int nranks, int root, const char* what) {
+  if (ntensors < 0) return fail(HVDX_ERR_INVALID, "%s: negative tensor count", what);
+  if (ntensors > 0 && (!ptrs || !nbytes || !voffset))
+    return fail(HVDX_ERR_INVALID, "%s: a descriptor array is NULL", what);
+  if (nranks < 1 || nranks > HVDX_MAX_RANKS)
+    return fail(HVDX_ERR_INVALID, "%s: nranks=%d outside 1..%d", what, nranks, HVDX_MAX_RANKS);
+  if (root < 0 || root >= nranks) return fail(HVDX_ERR_INVALID, "%s: root %d outside 0..%d", what, root, nranks - 1);
+  if (total_bytes < 0 || total_bytes > (INT64_MAX >> 2))
+    return fail(HVDX_ERR_INVALID, "%s: bad virtual length %lld", what, (long long)total_bytes);
+  return HVDX_OK;
+}
+
+static int bcast_tensors_step(const void* const* ptrs, const int64_t* nbytes, const int64_t* voffset, int ntensors,
+                              int64_t total_bytes, int nranks, int root, int step, hipStream_t st) {
+  hvdx::BcastTensorsArgs a{};
+  a.ptrs = ptrs;
+  a.nbytes = nbytes;
+  a.voff = voffset;
+  a.ntensors = ntensors;
+  a.n = nranks;
+  a.root = root;
+  a.step = step;
+  a.total = total_bytes;
+  const int64_t units = (total_bytes + 15) / 16;
+  a.q = units / nranks;
+  a.rem = units % nranks;
+  TimedLaunch timed(HVDX_KERNEL_BROADCAST, step, nranks, -1, HVDX_COMPRESS_NONE, total_bytes, st, root);
+  TimedLaunch timed_phase(HVDX_KERNEL_BROADCAST, step, nranks, -1, HVDX_COMPRESS_NONE, total_bytes, st, root, true);
+  const hipError_t e = hvdx::launch_bcast_tensors_step(a, st);
+  return e == hipSuccess ? HVDX_OK : hip_fail(e, "tensor broadcast step launch");
+}
+
+int hvdx_broadcast_tensors_step(const void* const* ptrs, const int64_t* nbytes, const int64_t* voffset, int ntensors,
+                                int64_t total_bytes, int nranks, int root, int step, void* stream) {
+  int rc = check_bcast_tensors(ptrs, nbytes, voffset, ntensors, total_bytes, nranks, root,
+                               "hvdx_broadcast_tensors_step");
+  if (rc) return rc;
+  if (step < 0 || step > 2 * nranks - 3)
+    return fail(HVDX_ERR_INVALID, "hvdx_broadcast_tensors_step: step %d outside 0..%d", step, 2 * nranks - 3);
+  if (total_bytes == 0 || ntensors == 0) return HVDX_OK;
+  return bcast_tensors_step(ptrs, nbytes, voffset, ntensors, total_bytes, nranks, root, step,
+                            static_cast<hipStream_t>(stream));
+}
+
+int hvdx_broadcast_tensors(const void* const* ptrs, const int64_t* nbytes, const int64_t* voffset, int ntensors,
+                           int64_t total_bytes, int nranks, int root, void* stream) {
+  int rc = check_bcast_tensors(ptrs, nbytes, voffset, ntensors, total_bytes, nranks, root, "hvdx_broadcast_tensors");
+  if (rc) return rc;
+  if (total_bytes == 0 || ntensors == 0) return HVDX_OK;
+  for (int s = 0; s < 2 * nranks - 2; ++s) {
+    rc = bcast_tensors_step(ptrs, nbytes, voffset, ntensors, total_bytes, nranks, root, s,
+                            static_cast<hipStream_t>(stream));
+    if (rc) return rc;
+  }
+  return HVDX_OK;
+}
+
 int hvdx_broadcast(void* const* bufs, int nranks, int64_t nbytes, int root, void* stream) {
   int rc = check_bcast(bufs, nranks, nbytes, root, "hvdx_broadcast");
   if (rc) return rc;

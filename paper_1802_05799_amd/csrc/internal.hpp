@@ -96,6 +96,19 @@ struct BcastArgs {
 };
 hipError_t launch_bcast_step(const RankPtrs& bufs, const BcastArgs& a, bool vector_ok, hipStream_t stream);
 
+// One chain step of a broadcast of many tensors (fusion_kernels.hip): the chain runs over
+// a virtual byte space in which tensor t occupies [voff[t], voff[t] + nbytes[t]).
+struct BcastTensorsArgs {
+  const void* const* ptrs;  // DEVICE table of tensor pointers, rank-major [n * ntensors]
+  const int64_t* nbytes;    // DEVICE [ntensors]
+  const int64_t* voff;      // DEVICE [ntensors], ascending multiples of 16, disjoint extents
+  int ntensors;
+  int n, root, step;
+  int64_t total;            // bytes of the virtual space
+  int64_t q, rem;           // 16-byte units per chunk: q, the first rem chunks one more
+};
+hipError_t launch_bcast_tensors_step(const BcastTensorsArgs& a, hipStream_t stream);
+
 // Launchers (fusion_kernels.hip).  With `ring` (nranks >= 3), the copy-in also does
 // the ring's adding step 0 (and with `skip_sender` leaves out each chunk's sender's
 // own copy, which the fused cycle never reads) and the copy-out its replacing step N-2.

@@ -285,3 +285,37 @@ def test_noalloc_ring_argument_checks():
     assert status(0, 10) == hv.ERR_INVALID
     assert status(2, 10, ptrs=[FAKE, FAKE + 8]) == hv.ERR_ALIAS
     assert status(3, 0) == hv.OK  # nothing to do, no HIP call
+
+
+def test_broadcast_layout_matches_oracle():
+    from oracle import broadcast
+
+    g = np.random.default_rng(12)
+    for _ in range(200):
+        sizes = [int(s) for s in g.integers(0, 100, size=g.integers(0, 12))]
+        assert tuple(hv.hvdx_broadcast_layout(sizes)) == broadcast.tensor_layout(sizes)
+    with pytest.raises(hv.HvdxError):
+        hv.hvdx_broadcast_layout([5, -1])
+
+
+def test_broadcast_tensors_argument_checks():
+    lib = ctypes.CDLL(hv.LIB_PATH)
+    f = lib.hvdx_broadcast_tensors
+    f.restype = ctypes.c_int
+    f.argtypes = [ctypes.c_void_p] * 3 + [ctypes.c_int, ctypes.c_int64, ctypes.c_int, ctypes.c_int, ctypes.c_void_p]
+    fs = lib.hvdx_broadcast_tensors_step
+    fs.restype = ctypes.c_int
+    fs.argtypes = [ctypes.c_void_p] * 3 + [ctypes.c_int, ctypes.c_int64, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                           ctypes.c_void_p]
+    assert f(FAKE, FAKE, FAKE, 3, 100, 0, 0, None) == hv.ERR_INVALID  # no ranks
+    assert f(FAKE, FAKE, FAKE, 3, 100, 129, 0, None) == hv.ERR_INVALID
+    assert f(FAKE, FAKE, FAKE, 3, 100, 4, 4, None) == hv.ERR_INVALID  # root out of range
+    assert f(FAKE, FAKE, FAKE, -1, 100, 4, 0, None) == hv.ERR_INVALID
+    assert f(None, FAKE, FAKE, 3, 100, 4, 0, None) == hv.ERR_INVALID
+    assert f(FAKE, FAKE, None, 3, 100, 4, 0, None) == hv.ERR_INVALID
+    assert f(FAKE, FAKE, FAKE, 3, -5, 4, 0, None) == hv.ERR_INVALID
+    assert f(FAKE, FAKE, FAKE, 3, 0, 4, 0, None) == hv.OK  # empty space: nothing launched
+    assert f(None, None, None, 0, 0, 4, 0, None) == hv.OK
+    assert fs(FAKE, FAKE, FAKE, 3, 100, 4, 0, 6, None) == hv.ERR_INVALID  # steps 0..5 for 4 ranks
+    assert fs(FAKE, FAKE, FAKE, 3, 100, 4, 0, -1, None) == hv.ERR_INVALID
+    assert fs(FAKE, FAKE, FAKE, 3, 0, 4, 0, 5, None) == hv.OK

@@ -168,6 +168,22 @@ def broadcast_pins_fail(bmod):
         want_step0[2, 0:16] = x[1, 0:16]  # step 0: only chunk 0 leaves the root
         if not np.array_equal(seen[0], want_step0):
             return "schedule"
+        # many tensors per call (reading B2): layout and the hand-worked two-tensor chain
+        if bmod.tensor_layout([5, 16, 0, 33, 1]) != ([0, 16, 32, 32, 80], 81):
+            return "layout"
+        xs = [[(np.arange(s, dtype=np.int64) * 7 + 31 * r + 1).astype(np.uint8) for s in (10, 20)] for r in range(3)]
+        seen = {}
+        bmod.chain_broadcast_tensors([[a.copy() for a in row] for row in xs], 1,
+                                     observe=lambda s, pr: seen.__setitem__(s, [[a.copy() for a in row] for row in pr]))
+        # after step 0 only chunk 0 (tensor 0) has reached rank 2
+        if not (np.array_equal(seen[0][2][0], xs[1][0]) and np.array_equal(seen[0][2][1], xs[2][1])
+                and np.array_equal(seen[0][0][0], xs[0][0])):
+            return "tensor schedule"
+        for n in (2, 4):
+            ys = [[(np.arange(s) + 13 * r).astype(np.uint8) for s in (3, 40, 0, 17)] for r in range(n)]
+            got = bmod.chain_broadcast_tensors([[a.copy() for a in row] for row in ys], n - 1)
+            if not all(np.array_equal(a, b) for row in got for a, b in zip(row, ys[n - 1])):
+                return "tensor result"
     except Exception as exc:
         return type(exc).__name__
     return None
@@ -182,6 +198,9 @@ BROADCAST_MUTANTS = [
     ("root ignored", "src, dst = (root + k) % n, (root + k + 1) % n", "src, dst = k % n, (k + 1) % n"),
     ("copy reversed", "bufs[dst, lo:hi] = bufs[src, lo:hi]", "bufs[src, lo:hi] = bufs[dst, lo:hi]"),
     ("traffic counts sender as receiver", 'traffic["recvd"][dst] += hi - lo', 'traffic["recvd"][src] += hi - lo'),
+    ("tensors packed without alignment", "start = -(-end // UNIT) * UNIT", "start = end"),
+    ("tensor gaps rounded down", "start = -(-end // UNIT) * UNIT", "start = end // UNIT * UNIT"),
+    ("tensor copied back from rank 0", "a[:] = bufs[r, s : s + a.size]", "a[:] = bufs[0, s : s + a.size]"),
 ]
 
 
