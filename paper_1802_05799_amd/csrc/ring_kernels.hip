@@ -127,7 +127,7 @@ __device__ __forceinline__ void vstore(V* p, V v) {
 // ---- plain ring (buffers of type T) ---------------------------------------------------
 
 template <typename T, int DIV, bool VEC_OK, typename P>
-__device__ __forceinline__ void rs_step_body(const RankPtrs& bufs, const RingArgs& a) {
+__device__ __forceinline__ void rs_step_body(const RankPtrs& bufs, const RingArgs& a, int64_t bx, int64_t gx) {
   using VT = typename Vec<T>::type;
   constexpr int V = Vec<T>::n;
   constexpr int BS = P::BS, U = P::U;
@@ -141,14 +141,14 @@ __device__ __forceinline__ void rs_step_body(const RankPtrs& bufs, const RingArg
   const int64_t head = VEC_OK ? head_elems<T>(dst, ch.len) : ch.len;
   const int64_t nvec = (ch.len - head) / V;
   const int64_t tail = head + nvec * V;
-  const int64_t gtid = (int64_t)blockIdx.x * BS + threadIdx.x;
-  const int64_t gthreads = (int64_t)gridDim.x * BS;
+  const int64_t gtid = bx * BS + threadIdx.x;
+  const int64_t gthreads = gx * BS;
   for (int64_t e = gtid; e < head; e += gthreads) dst[e] = combine1<DIV>(dst[e], src[e], a);
   for (int64_t e = tail + gtid; e < ch.len; e += gthreads) dst[e] = combine1<DIV>(dst[e], src[e], a);
 
   const VT* __restrict__ s4 = reinterpret_cast<const VT*>(src + head);
   VT* __restrict__ d4 = reinterpret_cast<VT*>(dst + head);
-  for (int64_t blk = (int64_t)blockIdx.x * BS * U; blk < nvec; blk += gthreads * U) {
+  for (int64_t blk = bx * BS * U; blk < nvec; blk += gthreads * U) {
     VT x[U], y[U];
     if (blk + BS * U <= nvec) {  // whole tile: all loads in flight at once
 #pragma unroll
@@ -169,17 +169,20 @@ __device__ __forceinline__ void rs_step_body(const RankPtrs& bufs, const RingArg
 
 template <typename T, int DIV, bool VEC_OK, typename P>
 __global__ __launch_bounds__(P::BS) void rs_step_kernel(RankPtrs bufs, RingArgs a) {
-  rs_step_body<T, DIV, VEC_OK, P>(bufs, a);
+  rs_step_body<T, DIV, VEC_OK, P>(bufs, a, blockIdx.x, gridDim.x);
 }
 
-// The same step of two rings (two fusion buffers) in one launch: block z serves ring z.
+// The same step of two rings (two fusion buffers) in one launch: block columns
+// [0, x0) serve ring 0 as its own grid would, columns [x0, gridDim.x) ring 1.
 template <typename T, int DIV, bool VEC_OK, typename P>
-__global__ __launch_bounds__(P::BS) void rs_step_pair_kernel(RingPair m) {
-  rs_step_body<T, DIV, VEC_OK, P>(m.bufs[blockIdx.z], m.a[blockIdx.z]);
+__global__ __launch_bounds__(P::BS) void rs_step_pair_kernel(RingPair m, int x0) {
+  const int z = (int)blockIdx.x >= x0 ? 1 : 0;
+  rs_step_body<T, DIV, VEC_OK, P>(m.bufs[z], m.a[z], z ? (int64_t)blockIdx.x - x0 : (int64_t)blockIdx.x,
+      z ? (int64_t)gridDim.x - x0 : (int64_t)x0);
 }
 
 template <typename T, bool VEC_OK, typename P>
-__device__ __forceinline__ void ag_step_body(const RankPtrs& bufs, const RingArgs& a) {
+__device__ __forceinline__ void ag_step_body(const RankPtrs& bufs, const RingArgs& a, int64_t bx, int64_t gx) {
   using VT = typename Vec<T>::type;
   constexpr int V = Vec<T>::n;
   constexpr int BS = P::BS, U = P::U;
@@ -193,14 +196,14 @@ __device__ __forceinline__ void ag_step_body(const RankPtrs& bufs, const RingArg
   const int64_t head = VEC_OK ? head_elems<T>(dst, ch.len) : ch.len;
   const int64_t nvec = (ch.len - head) / V;
   const int64_t tail = head + nvec * V;
-  const int64_t gtid = (int64_t)blockIdx.x * BS + threadIdx.x;
-  const int64_t gthreads = (int64_t)gridDim.x * BS;
+  const int64_t gtid = bx * BS + threadIdx.x;
+  const int64_t gthreads = gx * BS;
   for (int64_t e = gtid; e < head; e += gthreads) dst[e] = src[e];
   for (int64_t e = tail + gtid; e < ch.len; e += gthreads) dst[e] = src[e];
 
   const VT* __restrict__ s4 = reinterpret_cast<const VT*>(src + head);
   VT* __restrict__ d4 = reinterpret_cast<VT*>(dst + head);
-  for (int64_t blk = (int64_t)blockIdx.x * BS * U; blk < nvec; blk += gthreads * U) {
+  for (int64_t blk = bx * BS * U; blk < nvec; blk += gthreads * U) {
     VT x[U];
     if (blk + BS * U <= nvec) {
 #pragma unroll
@@ -218,13 +221,16 @@ __device__ __forceinline__ void ag_step_body(const RankPtrs& bufs, const RingArg
 
 template <typename T, bool VEC_OK, typename P>
 __global__ __launch_bounds__(P::BS) void ag_step_kernel(RankPtrs bufs, RingArgs a) {
-  ag_step_body<T, VEC_OK, P>(bufs, a);
+  ag_step_body<T, VEC_OK, P>(bufs, a, blockIdx.x, gridDim.x);
 }
 
-// The same step of two rings (two fusion buffers) in one launch: block z serves ring z.
+// The same step of two rings (two fusion buffers) in one launch: block columns
+// [0, x0) serve ring 0 as its own grid would, columns [x0, gridDim.x) ring 1.
 template <typename T, bool VEC_OK, typename P>
-__global__ __launch_bounds__(P::BS) void ag_step_pair_kernel(RingPair m) {
-  ag_step_body<T, VEC_OK, P>(m.bufs[blockIdx.z], m.a[blockIdx.z]);
+__global__ __launch_bounds__(P::BS) void ag_step_pair_kernel(RingPair m, int x0) {
+  const int z = (int)blockIdx.x >= x0 ? 1 : 0;
+  ag_step_body<T, VEC_OK, P>(m.bufs[z], m.a[z], z ? (int64_t)blockIdx.x - x0 : (int64_t)blockIdx.x,
+      z ? (int64_t)gridDim.x - x0 : (int64_t)x0);
 }
 
 // ---- compressed ring: binary32 buffers, binary16 on the wire ------------------------
@@ -368,7 +374,7 @@ __global__ __launch_bounds__(P::BS) void ag_first_c16_kernel(RankPtrs x, const _
 // reading it back.  The buffers end exactly as after the two steps.
 
 template <typename T, int DIV, bool VEC_OK, typename P>
-__device__ __forceinline__ void rs_ag_step_body(const RankPtrs& bufs, const RingArgs& a) {
+__device__ __forceinline__ void rs_ag_step_body(const RankPtrs& bufs, const RingArgs& a, int64_t bx, int64_t gx) {
   using VT = typename Vec<T>::type;
   constexpr int V = Vec<T>::n;
   constexpr int BS = P::BS, U = P::U;
@@ -385,8 +391,8 @@ __device__ __forceinline__ void rs_ag_step_body(const RankPtrs& bufs, const Ring
   const int64_t head = VEC_OK ? head_elems<T>(dst, ch.len) : ch.len;
   const int64_t nvec = (ch.len - head) / V;
   const int64_t tail = head + nvec * V;
-  const int64_t gtid = (int64_t)blockIdx.x * BS + threadIdx.x;
-  const int64_t gthreads = (int64_t)gridDim.x * BS;
+  const int64_t gtid = bx * BS + threadIdx.x;
+  const int64_t gthreads = gx * BS;
   auto one = [&](int64_t e) {
     const T v = combine1<DIV>(dst[e], src[e], a);
     dst[e] = v;
@@ -398,7 +404,7 @@ __device__ __forceinline__ void rs_ag_step_body(const RankPtrs& bufs, const Ring
   const VT* s4 = reinterpret_cast<const VT*>(src + head);
   VT* __restrict__ d4 = reinterpret_cast<VT*>(dst + head);
   VT* n4 = reinterpret_cast<VT*>(nxt + head);
-  for (int64_t blk = (int64_t)blockIdx.x * BS * U; blk < nvec; blk += gthreads * U) {
+  for (int64_t blk = bx * BS * U; blk < nvec; blk += gthreads * U) {
     VT x[U], y[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -422,13 +428,16 @@ __device__ __forceinline__ void rs_ag_step_body(const RankPtrs& bufs, const Ring
 
 template <typename T, int DIV, bool VEC_OK, typename P>
 __global__ __launch_bounds__(P::BS) void rs_ag_step_kernel(RankPtrs bufs, RingArgs a) {
-  rs_ag_step_body<T, DIV, VEC_OK, P>(bufs, a);
+  rs_ag_step_body<T, DIV, VEC_OK, P>(bufs, a, blockIdx.x, gridDim.x);
 }
 
-// The same step of two rings (two fusion buffers) in one launch: block z serves ring z.
+// The same step of two rings (two fusion buffers) in one launch: block columns
+// [0, x0) serve ring 0 as its own grid would, columns [x0, gridDim.x) ring 1.
 template <typename T, int DIV, bool VEC_OK, typename P>
-__global__ __launch_bounds__(P::BS) void rs_ag_step_pair_kernel(RingPair m) {
-  rs_ag_step_body<T, DIV, VEC_OK, P>(m.bufs[blockIdx.z], m.a[blockIdx.z]);
+__global__ __launch_bounds__(P::BS) void rs_ag_step_pair_kernel(RingPair m, int x0) {
+  const int z = (int)blockIdx.x >= x0 ? 1 : 0;
+  rs_ag_step_body<T, DIV, VEC_OK, P>(m.bufs[z], m.a[z], z ? (int64_t)blockIdx.x - x0 : (int64_t)blockIdx.x,
+      z ? (int64_t)gridDim.x - x0 : (int64_t)x0);
 }
 
 // Compressed: the finished binary16 sum goes, widened, to the owner's and rank c's
@@ -719,11 +728,13 @@ hipError_t launch_ag_step(const RankPtrs& bufs, const RingArgs& a, int dtype, bo
 
 namespace {
 
-// Two rings in one launch: a grid as wide as the longer ring's step needs, one row
-// per chunk, one layer per ring; the shorter ring's surplus blocks find no work.
-dim3 pair_grid(const RingPair& m, int elems_per_vec, int unroll, int bs) {
+// Two rings in one launch: ring 0's columns of blocks (each column one row per chunk),
+// then ring 1's, each ring with as many columns as its own step needs, so no block is
+// launched without work; *x0 is the first column of ring 1.
+dim3 pair_grid(const RingPair& m, int elems_per_vec, int unroll, int bs, int* x0) {
   const dim3 g0 = step_grid(m.a[0], elems_per_vec, unroll, bs), g1 = step_grid(m.a[1], elems_per_vec, unroll, bs);
-  return dim3(g0.x > g1.x ? g0.x : g1.x, (unsigned)m.a[0].n, 2);
+  *x0 = (int)g0.x;
+  return dim3(g0.x + g1.x, (unsigned)m.a[0].n, 1);
 }
 
 // Both rings take the launch shape of the longer one.
@@ -731,24 +742,31 @@ bool pair_streams(const RingPair& m, int esize) { return streams(m.a[0].q >= m.a
 
 template <typename T, typename P>
 void rs_pair_launch(const RingPair& m, int divmode, hipStream_t st) {
-  const dim3 grid = pair_grid(m, Vec<T>::n, P::U, P::BS);
-  if (divmode == DIV_NONE) HVDX_LAUNCH((rs_step_pair_kernel<T, DIV_NONE, true, P>), grid, dim3(P::BS), 0, st, m);
-  else if (divmode == DIV_POW2) HVDX_LAUNCH((rs_step_pair_kernel<T, DIV_POW2, true, P>), grid, dim3(P::BS), 0, st, m);
-  else HVDX_LAUNCH((rs_step_pair_kernel<T, DIV_TRUE, true, P>), grid, dim3(P::BS), 0, st, m);
+  int x0;
+  const dim3 grid = pair_grid(m, Vec<T>::n, P::U, P::BS, &x0);
+  if (divmode == DIV_NONE)
+    HVDX_LAUNCH((rs_step_pair_kernel<T, DIV_NONE, true, P>), grid, dim3(P::BS), 0, st, m, x0);
+  else if (divmode == DIV_POW2)
+    HVDX_LAUNCH((rs_step_pair_kernel<T, DIV_POW2, true, P>), grid, dim3(P::BS), 0, st, m, x0);
+  else HVDX_LAUNCH((rs_step_pair_kernel<T, DIV_TRUE, true, P>), grid, dim3(P::BS), 0, st, m, x0);
 }
 
 template <typename T, typename P>
 void rs_ag_pair_launch(const RingPair& m, int divmode, hipStream_t st) {
-  const dim3 grid = pair_grid(m, Vec<T>::n, P::U, P::BS);
-  if (divmode == DIV_NONE) HVDX_LAUNCH((rs_ag_step_pair_kernel<T, DIV_NONE, true, P>), grid, dim3(P::BS), 0, st, m);
+  int x0;
+  const dim3 grid = pair_grid(m, Vec<T>::n, P::U, P::BS, &x0);
+  if (divmode == DIV_NONE)
+    HVDX_LAUNCH((rs_ag_step_pair_kernel<T, DIV_NONE, true, P>), grid, dim3(P::BS), 0, st, m, x0);
   else if (divmode == DIV_POW2)
-    HVDX_LAUNCH((rs_ag_step_pair_kernel<T, DIV_POW2, true, P>), grid, dim3(P::BS), 0, st, m);
-  else HVDX_LAUNCH((rs_ag_step_pair_kernel<T, DIV_TRUE, true, P>), grid, dim3(P::BS), 0, st, m);
+    HVDX_LAUNCH((rs_ag_step_pair_kernel<T, DIV_POW2, true, P>), grid, dim3(P::BS), 0, st, m, x0);
+  else HVDX_LAUNCH((rs_ag_step_pair_kernel<T, DIV_TRUE, true, P>), grid, dim3(P::BS), 0, st, m, x0);
 }
 
 template <typename T, typename P>
 void ag_pair_launch(const RingPair& m, hipStream_t st) {
-  HVDX_LAUNCH((ag_step_pair_kernel<T, true, P>), pair_grid(m, Vec<T>::n, P::U, P::BS), dim3(P::BS), 0, st, m);
+  int x0;
+  const dim3 grid = pair_grid(m, Vec<T>::n, P::U, P::BS, &x0);
+  HVDX_LAUNCH((ag_step_pair_kernel<T, true, P>), grid, dim3(P::BS), 0, st, m, x0);
 }
 
 template <typename T>
