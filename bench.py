@@ -416,6 +416,14 @@ def summarize_profiles(d):
                     per.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]) * factor * 1024)
             pmc[counter] = (factor, {k: sum(v) / len(v) for k, v in per.items()})
         names = sorted((n for w, n in trace if w == workload), key=lambda n: -trace[(workload, n)][1])
+        # with fp16 compression the binary32 replacing-step kernel runs only as the
+        # compressed ring's later replacing steps, which bench.py reports as ag_step_c16
+        compressed = any(short_kernel_name(n) == "rs_step_c16" for n in names)
+
+        def short(n):
+            k = short_kernel_name(n)
+            return "ag_step_c16" if compressed and k == "ag_step_f32" else k
+
         counted = len(pmc) == 2
         if counted:
             cal_used[workload] = {"FETCH_SIZE": pmc["FETCH_SIZE"][0], "WRITE_SIZE": pmc["WRITE_SIZE"][0]}
@@ -429,7 +437,7 @@ def summarize_profiles(d):
         per_short = {}
         for n in names:
             calls, tot_ns = trace[(workload, n)]
-            k, avg_us = short_kernel_name(n), tot_ns / calls / 1e3
+            k, avg_us = short(n), tot_ns / calls / 1e3
             cells = ["-", "-", "-", "-"]
             if counted and n in pmc["FETCH_SIZE"][1]:
                 fb, wb = pmc["FETCH_SIZE"][1][n], pmc["WRITE_SIZE"][1].get(n, 0.0)
@@ -440,6 +448,20 @@ def summarize_profiles(d):
                 acc[1] += calls
             out_lines.append(f"| {k} | `{shape_of(n)}` | {calls} | {avg_us:.2f} | {tot_ns / 1e6:.2f} | "
                              + " | ".join(cells) + " |")
+        out_lines.append("")
+        # the same rows gathered under the names bench.py reports (all launch shapes of a
+        # kernel together, weighted by calls), as its per-kernel figures are
+        out_lines.append("Per reported kernel (all its launch shapes, weighted by calls):\n")
+        out_lines.append("| kernel | calls | average us | total ms | counted MB per launch |\n|---|---|---|---|---|")
+        agg = {}
+        for n in names:
+            calls, tot_ns = trace[(workload, n)]
+            a = agg.setdefault(short(n), [0, 0.0])
+            a[0] += calls
+            a[1] += tot_ns
+        for k, (calls, tot_ns) in sorted(agg.items(), key=lambda kv: -kv[1][1]):
+            mb = f"{per_short[k][0] / per_short[k][1] / 1e6:.1f}" if k in per_short else "-"
+            out_lines.append(f"| {k} | {calls} | {tot_ns / calls / 1e3:.2f} | {tot_ns / 1e6:.2f} | {mb} |")
         out_lines.append("")
         for k, (b, c) in per_short.items():
             traffic[f"{workload}/{k}"] = round(b / c)

@@ -129,7 +129,8 @@ def test_summarize_profiles_scales_counters_by_the_copy(tmp_path, monkeypatch):
     text = bench.summarize_profiles(str(d))
     assert "FETCH_SIZE x 2.000 and WRITE_SIZE x 1.000" in text
     row = [line for line in text.splitlines() if line.startswith("| rs_step_f32")]
-    assert row == ["| rs_step_f32 | `Policy<2,256,false,true,false>` | 10 | 1.00 | 0.01 | 0.2 | 0.1 | 256 | 3.2 |"]
+    assert row == ["| rs_step_f32 | `Policy<2,256,false,true,false>` | 10 | 1.00 | 0.01 | 0.2 | 0.1 | 256 | 3.2 |",
+                   "| rs_step_f32 | 10 | 1.00 | 0.01 | 0.3 |"]  # the per-reported-kernel table
     rec = json.load(open(tmp_path / "traffic.json"))
     assert rec["per_launch_bytes"] == {"w/rs_step_f32": 256000}
     assert rec["calibration"] == {"w": {"FETCH_SIZE": 2.0, "WRITE_SIZE": 1.0}}
