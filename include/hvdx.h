@@ -223,6 +223,66 @@ int hvdx_fuse_allreduce_pair(const hvdx_bucket* b0, const hvdx_bucket* b1, int t
                              int nranks, int op, void* stream);
 
 /*
+ * Tile tables for the fused copies (paper section 7, steps 3 and 5, fused with the
+ * ring's first and last step as in hvdx_fuse_allreduce).  A fusion buffer's copy can be
+ * cut, once, into tiles that each lie inside one tensor (or one run of padding) and one
+ * ring chunk; a kernel then needs no search for the tensors of its stretch of the buffer:
+ * each block reads its tile and moves it for one rank, one 16-byte vector per lane.
+ *
+ * hvdx_fuse_copy_tiles -- host only, pure: the tiles of one direction for a buffer
+ * described as for hvdx_fuse_allreduce (numel, offset: HOST arrays here).
+ *   direction  HVDX_COPY_IN: every buffer position, padding included, cut at tensor
+ *              ends, chunk ends and multiples of the tile length in buffer positions (the
+ *              copy-in writes the buffer: its stores start on the buffer's tile bounds);
+ *              HVDX_COPY_OUT: every tensor element, cut at tensor ends, chunk ends and
+ *              multiples of the tile length inside each tensor (the copy-out writes the
+ *              tensors: its stores start on the tensors' own tile bounds).  After a chunk
+ *              boundary that is not on a vector boundary, a short tile reaches the next one.
+ *   tiles      host array of `capacity` entries, or NULL to count them
+ * Returns the number of tiles (written when tiles is not NULL and capacity suffices),
+ * or a negative HVDX_ERR_* (HVDX_ERR_WORKSPACE when capacity is too small).  A tile holds
+ * at most hvdx_fuse_tile_elems(tensor_dtype, buf_dtype) elements: what one 256-thread
+ * block moves (1024 for binary32 buffers, 2048 for binary16 buffers).
+ */
+#define HVDX_COPY_IN 0
+#define HVDX_COPY_OUT 1
+typedef struct hvdx_copy_tile {
+  int64_t pos;     /* buffer position of the tile's first element */
+  int64_t li;      /* that element's index in its tensor (0 for padding) */
+  int32_t tensor;  /* tensor index, -1 for a run of padding (HVDX_COPY_IN only) */
+  int32_t len;     /* elements in the tile, 1 .. hvdx_fuse_tile_elems(...) */
+  int32_t chunk;   /* ring chunk holding every element of the tile */
+  int32_t reserved;
+} hvdx_copy_tile;
+int64_t hvdx_fuse_copy_tiles(const int64_t* numel, const int64_t* offset, int ntensors, int64_t buf_count,
+                             int tensor_dtype, int buf_dtype, int nranks, int direction, hvdx_copy_tile* tiles,
+                             int64_t capacity);
+/* The most elements a tile holds for these types (0 for an unsupported pair). */
+int64_t hvdx_fuse_tile_elems(int tensor_dtype, int buf_dtype);
+
+/*
+ * hvdx_fuse_allreduce_tiled -- hvdx_fuse_allreduce (b1 NULL) or hvdx_fuse_allreduce_pair
+ * (b0 and b1) with the fused copies driven by tile tables: the same result, bit for bit,
+ * the same launches, the same scratch contents of the fusion buffers afterwards.
+ *   b*->b              the bucket, as for hvdx_fuse_allreduce_pair
+ *   b*->in_tiles       DEVICE array of n_in tiles from hvdx_fuse_copy_tiles(HVDX_COPY_IN)
+ *   b*->out_tiles      DEVICE array of n_out tiles from hvdx_fuse_copy_tiles(HVDX_COPY_OUT)
+ * for exactly this bucket (numel, offset, buf_count, both types and nranks): the tables
+ * are device memory and are not checked; other tables make the kernels read or write
+ * outside the buffers and tensors.  Errors as hvdx_fuse_allreduce_pair, and
+ * HVDX_ERR_INVALID for a missing table or a negative tile count.
+ */
+typedef struct hvdx_tiled_bucket {
+  hvdx_bucket b;
+  const hvdx_copy_tile* in_tiles;
+  int64_t n_in;
+  const hvdx_copy_tile* out_tiles;
+  int64_t n_out;
+} hvdx_tiled_bucket;
+int hvdx_fuse_allreduce_tiled(const hvdx_tiled_bucket* b0, const hvdx_tiled_bucket* b1, int tensor_dtype,
+                              int buf_dtype, int nranks, int op, void* stream);
+
+/*
  * hvdx_fuse_allreduce_small -- hvdx_fuse_allreduce for small fusion buffers: the same
  * result, bit for bit, in one kernel launch instead of 2N-1.  Each thread takes a
  * 16-byte stretch of the buffer (element by element where it meets a tensor edge)

@@ -39,6 +39,11 @@ from ._lib import (  # noqa: F401
     hvdx_fuse_ag_unpack,
     hvdx_fuse_allreduce,
     hvdx_fuse_allreduce_pair,
+    hvdx_fuse_allreduce_tiled,
+    hvdx_fuse_copy_tiles,
+    hvdx_fuse_tile_elems,
+    COPY_IN,
+    COPY_OUT,
     hvdx_fuse_allreduce_small,
     hvdx_fuse_pack,
     hvdx_fuse_pack_rs,

@@ -16,6 +16,7 @@ FLOAT32, FLOAT16 = 0, 1
 SUM, AVERAGE = 0, 1
 COMPRESS_NONE, COMPRESS_FP16 = 0, 1
 PHASE_REDUCE_SCATTER, PHASE_ALLGATHER = 0, 1
+COPY_IN, COPY_OUT = 0, 1
 OK, ERR_INVALID, ERR_ALIAS, ERR_WORKSPACE, ERR_HIP, ERR_UNSUPPORTED = 0, -1, -2, -3, -4, -5
 MAX_RANKS = 128
 DEFAULT_FUSION_THRESHOLD = 64 << 20
@@ -39,6 +40,9 @@ _SIGNATURES = {
     "hvdx_fuse_allreduce": (_i, [_p, _p, _p, _i, _i, _pp, _i64, _i, _i, _i, _p]),
     "hvdx_fuse_allreduce_small": (_i, [_p, _p, _p, _i, _i, _pp, _i64, _i, _i, _i, _p]),
     "hvdx_fuse_allreduce_pair": (_i, [_p, _p, _i, _i, _i, _i, _p]),
+    "hvdx_fuse_copy_tiles": (_i64, [_pi64, _p, _i, _i64, _i, _i, _i, _i, _p, _i64]),
+    "hvdx_fuse_allreduce_tiled": (_i, [_p, _p, _i, _i, _i, _i, _p]),
+    "hvdx_fuse_tile_elems": (_i64, [_i, _i]),
     "hvdx_ring_allreduce": (_i, [_pp, _i, _i64, _i, _i, _i, _p, _sz, _p]),
     "hvdx_ring_allreduce_small": (_i, [_pp, _i, _i64, _i, _i, _p]),
     "hvdx_ring_allreduce_noalloc": (_i, [_pp, _i, _i64, _i, _i, _i, _p]),
@@ -77,6 +81,32 @@ class Bucket(ctypes.Structure):
         ("ntensors", ctypes.c_int),
         ("bufs", _pp),
         ("buf_count", ctypes.c_int64),
+    ]
+
+
+class CopyTile(ctypes.Structure):
+    """hvdx_copy_tile: one tile of a fused copy (a stretch of one tensor or of padding,
+    inside one ring chunk)."""
+
+    _fields_ = [
+        ("pos", ctypes.c_int64),
+        ("li", ctypes.c_int64),
+        ("tensor", ctypes.c_int32),
+        ("len", ctypes.c_int32),
+        ("chunk", ctypes.c_int32),
+        ("reserved", ctypes.c_int32),
+    ]
+
+
+class TiledBucket(ctypes.Structure):
+    """hvdx_tiled_bucket: a bucket and the device tile tables of its two fused copies."""
+
+    _fields_ = [
+        ("b", Bucket),
+        ("in_tiles", ctypes.c_void_p),
+        ("n_in", ctypes.c_int64),
+        ("out_tiles", ctypes.c_void_p),
+        ("n_out", ctypes.c_int64),
     ]
 
 
@@ -216,6 +246,47 @@ def hvdx_fuse_allreduce_pair(b0, b1, tensor_dtype: int, buf_dtype: int, nranks: 
     d0, d1 = desc(b0), desc(b1)
     _check(lib.hvdx_fuse_allreduce_pair(ctypes.addressof(d0), ctypes.addressof(d1), tensor_dtype, buf_dtype, nranks,
                                         op, stream))
+
+
+def hvdx_fuse_copy_tiles(numel, offset, buf_count: int, tensor_dtype: int, buf_dtype: int, nranks: int,
+                         direction: int):
+    """The tile table of one fused copy of a buffer (host arrays in, a ctypes array of
+    CopyTile out)."""
+    n = len(numel)
+    a_numel = (ctypes.c_int64 * max(1, n))(*numel)
+    a_off = (ctypes.c_int64 * max(1, n))(*offset)
+    args = (a_numel, a_off, n, buf_count, tensor_dtype, buf_dtype, nranks, direction)
+    k = lib.hvdx_fuse_copy_tiles(*args, None, 0)
+    if k < 0:
+        _check(int(k))
+    tiles = (CopyTile * max(1, k))()
+    got = lib.hvdx_fuse_copy_tiles(*args, ctypes.cast(tiles, ctypes.c_void_p), k)
+    if got < 0:
+        _check(int(got))
+    return tiles, k
+
+
+def hvdx_fuse_tile_elems(tensor_dtype: int, buf_dtype: int) -> int:
+    return lib.hvdx_fuse_tile_elems(tensor_dtype, buf_dtype)
+
+
+def hvdx_fuse_allreduce_tiled(t0, t1, tensor_dtype: int, buf_dtype: int, nranks: int, op: int,
+                              stream: int = 0) -> None:
+    """t0, t1 (t1 may be None): (tensors_dev, numel_dev, offset_dev, ntensors, bufs, buf_count,
+    in_tiles_dev, n_in, out_tiles_dev, n_out) each."""
+    keep = []
+
+    def desc(t):
+        tensors_dev, numel_dev, offset_dev, ntensors, bufs, buf_count, in_dev, n_in, out_dev, n_out = t
+        pb, arr = _ptr_array(bufs)
+        keep.append(arr)
+        return TiledBucket(Bucket(tensors_dev, numel_dev, offset_dev, ntensors, pb, buf_count), in_dev, n_in, out_dev,
+                           n_out)
+
+    d0 = desc(t0)
+    d1 = desc(t1) if t1 is not None else None
+    _check(lib.hvdx_fuse_allreduce_tiled(ctypes.addressof(d0), ctypes.addressof(d1) if d1 is not None else None,
+                                         tensor_dtype, buf_dtype, nranks, op, stream))
 
 
 def hvdx_fuse_allreduce_small(tensors_dev: int, numel_dev: int, offset_dev: int, ntensors: int, tensor_dtype: int,

@@ -745,6 +745,169 @@ int hvdx_fuse_allreduce_pair(const hvdx_bucket* b0, const hvdx_bucket* b1, int t
   return e == hipSuccess ? HVDX_OK : hip_fail(e, "two-buffer copy-out launch");
 }
 
+int64_t hvdx_fuse_tile_elems(int tensor_dtype, int buf_dtype) {
+  if (!elem_size(tensor_dtype) || !elem_size(buf_dtype) || (tensor_dtype == HVDX_FLOAT16 && buf_dtype == HVDX_FLOAT32))
+    return 0;
+  return (int64_t)hvdx::kTileLanes * hvdx::tile_vectors(tensor_dtype, buf_dtype) *
+         hvdx::tile_vec_elems(tensor_dtype, buf_dtype);
+}
+
+int64_t hvdx_fuse_copy_tiles(const int64_t* numel, const int64_t* offset, int ntensors, int64_t buf_count,
+                             int tensor_dtype, int buf_dtype, int nranks, int direction, hvdx_copy_tile* tiles,
+                             int64_t capacity) {
+  static const char* what = "hvdx_fuse_copy_tiles";
+  if (ntensors < 0 || (ntensors > 0 && (!numel || !offset)))
+    return fail(HVDX_ERR_INVALID, "%s: bad tensor table", what);
+  if (!elem_size(tensor_dtype) || !elem_size(buf_dtype)) return fail(HVDX_ERR_INVALID, "%s: unknown dtype", what);
+  if (tensor_dtype == HVDX_FLOAT16 && buf_dtype == HVDX_FLOAT32)
+    return fail(HVDX_ERR_UNSUPPORTED, "%s: float16 tensors with a float32 buffer", what);
+  if (nranks < 1 || nranks > HVDX_MAX_RANKS)
+    return fail(HVDX_ERR_INVALID, "%s: nranks=%d outside 1..%d", what, nranks, HVDX_MAX_RANKS);
+  if (buf_count < 0 || buf_count > (INT64_MAX >> 4)) return fail(HVDX_ERR_INVALID, "%s: bad buffer length", what);
+  if (direction != HVDX_COPY_IN && direction != HVDX_COPY_OUT)
+    return fail(HVDX_ERR_INVALID, "%s: unknown direction %d", what, direction);
+  if (capacity < 0 || (capacity > 0 && !tiles)) return fail(HVDX_ERR_INVALID, "%s: bad capacity", what);
+  int64_t prev_end = 0;
+  for (int t = 0; t < ntensors; ++t) {  // tensors in order, disjoint, inside the buffer
+    if (numel[t] < 0 || offset[t] < prev_end || offset[t] > buf_count || numel[t] > buf_count - offset[t])
+      return fail(HVDX_ERR_INVALID, "%s: tensor %d does not fit the buffer after the previous one", what, t);
+    if (numel[t] > 0) prev_end = offset[t] + numel[t];
+  }
+  const int64_t vec = hvdx::tile_vec_elems(tensor_dtype, buf_dtype);
+  const int64_t tile = hvdx_fuse_tile_elems(tensor_dtype, buf_dtype);
+  const int64_t q = buf_count / nranks, rem = buf_count % nranks, big = rem * (q + 1);
+  auto chunk_of = [&](int64_t p) { return p < big ? p / (q + 1) : rem + (p - big) / q; };
+  auto chunk_end = [&](int64_t c) { return (c + 1) * q + std::min<int64_t>(c + 1, rem); };
+  int64_t n = 0;
+  // Cut [a, b) (tensor t, or padding for t < 0) at chunk ends and at the tile grid that starts
+  // at `base`; a piece that starts off the vector grid ends at the next vector boundary.
+  auto cut = [&](int64_t a, int64_t b, int t, int64_t base) {
+    for (int64_t p = a; p < b;) {
+      const int64_t c = chunk_of(p);
+      int64_t stop = std::min(b, chunk_end(c));
+      stop = std::min(stop, base + ((p - base) / tile + 1) * tile);
+      if ((p - base) % vec) stop = std::min(stop, base + ((p - base) / vec + 1) * vec);
+      if (tiles && n < capacity) {
+        hvdx_copy_tile& x = tiles[n];
+        x.pos = p;
+        x.li = t >= 0 ? p - offset[t] : 0;
+        x.tensor = t;
+        x.len = (int32_t)(stop - p);
+        x.chunk = (int32_t)c;
+        x.reserved = 0;
+      }
+      ++n;
+      p = stop;
+    }
+  };
+  if (direction == HVDX_COPY_IN) {  // every buffer position, on the buffer's tile grid
+    int64_t at = 0;
+    for (int t = 0; t < ntensors; ++t) {
+      if (numel[t] == 0) continue;
+      cut(at, offset[t], -1, 0);
+      cut(offset[t], offset[t] + numel[t], t, 0);
+      at = offset[t] + numel[t];
+    }
+    cut(at, buf_count, -1, 0);
+  } else {  // every tensor element, on each tensor's own tile grid
+    for (int t = 0; t < ntensors; ++t)
+      if (numel[t] > 0) cut(offset[t], offset[t] + numel[t], t, offset[t]);
+  }
+  if (tiles && n > capacity)
+    return fail(HVDX_ERR_WORKSPACE, "%s: %lld tiles, room for %lld", what, (long long)n, (long long)capacity);
+  return n;
+}
+
+int hvdx_fuse_allreduce_tiled(const hvdx_tiled_bucket* t0, const hvdx_tiled_bucket* t1, int tensor_dtype,
+                              int buf_dtype, int nranks, int op, void* stream) {
+  static const char* what = "hvdx_fuse_allreduce_tiled";
+  if (!t0) return fail(HVDX_ERR_INVALID, "%s: the first bucket is NULL", what);
+  for (const hvdx_tiled_bucket* t : {t0, t1}) {
+    if (!t) continue;
+    const int rc = check_fusion(t->b.tensors, t->b.numel, t->b.offset, t->b.ntensors, tensor_dtype, t->b.bufs,
+                                t->b.buf_count, buf_dtype, nranks, what);
+    if (rc) return rc;
+    if (t->n_in < 0 || t->n_out < 0 || (t->n_in > 0 && !t->in_tiles) || (t->n_out > 0 && !t->out_tiles) ||
+        (t->b.buf_count > 0 && t->n_in == 0))
+      return fail(HVDX_ERR_INVALID, "%s: a tile table is missing", what);
+  }
+  if (op != HVDX_SUM && op != HVDX_AVERAGE) return fail(HVDX_ERR_INVALID, "%s: unknown op %d", what, op);
+  if (nranks < 3) return fail(HVDX_ERR_UNSUPPORTED, "%s: needs 3 or more ranks", what);
+  const int es = elem_size(buf_dtype);
+  if (t1 && t0->b.buf_count > 0 && t1->b.buf_count > 0) {  // both run at once: all 2N buffers disjoint
+    std::vector<std::pair<uintptr_t, uintptr_t>> rg;
+    for (const hvdx_tiled_bucket* t : {t0, t1})
+      for (int r = 0; r < nranks; ++r) {
+        const uintptr_t x = reinterpret_cast<uintptr_t>(t->b.bufs[r]);
+        rg.emplace_back(x, x + (uintptr_t)t->b.buf_count * es);
+      }
+    if (overlapping(rg)) return fail(HVDX_ERR_ALIAS, "%s: fusion buffers of the two buckets overlap", what);
+  }
+  // the buckets with something to reduce, one or two
+  const hvdx_tiled_bucket* run[2] = {nullptr, nullptr};
+  int nrun = 0;
+  for (const hvdx_tiled_bucket* t : {t0, t1})
+    if (t && t->b.buf_count > 0) run[nrun++] = t;
+  if (nrun == 0) return HVDX_OK;
+  const int64_t n_in = run[0]->n_in + (nrun > 1 ? run[1]->n_in : 0);
+  const int64_t n_out = run[0]->n_out + (nrun > 1 ? run[1]->n_out : 0);
+  if (n_in > 0x7fffffff || n_out > 0x7fffffff) return fail(HVDX_ERR_UNSUPPORTED, "%s: too many tiles", what);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int last = nranks - 2;
+  const int64_t both = run[0]->b.buf_count + (nrun > 1 ? run[1]->b.buf_count : 0);
+  hvdx::TiledCopy k{};
+  for (int i = 0; i < nrun; ++i) {
+    k.m.t[i] = run[i]->b.tensors;
+    k.m.numel[i] = run[i]->b.numel;
+    k.m.offset[i] = run[i]->b.offset;
+    k.m.ntensors[i] = run[i]->b.ntensors;
+    k.m.bufs[i] = rank_ptrs(run[i]->b.bufs, nranks);
+    k.m.count[i] = run[i]->b.buf_count;
+  }
+  {
+    TimedLaunch timed(HVDX_KERNEL_PACK_RS, 0, nranks, buf_dtype, HVDX_COMPRESS_NONE, both, st);
+    TimedLaunch timed_phase(HVDX_KERNEL_PACK_RS, 0, nranks, buf_dtype, HVDX_COMPRESS_NONE, both, st, -1, true);
+    k.tiles[0] = run[0]->in_tiles;
+    k.tiles[1] = nrun > 1 ? run[1]->in_tiles : nullptr;
+    k.x0 = run[0]->n_in;
+    const hipError_t e = hvdx::launch_pack_tiles(k, tensor_dtype, buf_dtype, nranks, n_in, st);
+    if (e != hipSuccess) return hip_fail(e, "tiled copy-in launch");
+  }
+  int rc;
+  if (nrun == 2) {
+    rc = run_pair_steps(&run[0]->b, &run[1]->b, buf_dtype, op, HVDX_KERNEL_REDUCE_SCATTER, 1, last, nranks, st);
+    if (rc) return rc;
+    {
+      TimedLaunch timed_phase(HVDX_KERNEL_RS_AG, last, nranks, buf_dtype, HVDX_COMPRESS_NONE, both, st, -1, true);
+      rc = run_pair_step(&run[0]->b, &run[1]->b, buf_dtype, op, HVDX_KERNEL_RS_AG, last, nranks, st);
+      if (rc) return rc;
+    }
+    rc = run_pair_steps(&run[0]->b, &run[1]->b, buf_dtype, op, HVDX_KERNEL_ALLGATHER, 1, last, nranks, st);
+  } else {
+    void* const* bufs = run[0]->b.bufs;
+    const int64_t count = run[0]->b.buf_count;
+    rc = run_steps(bufs, nranks, count, buf_dtype, op, HVDX_COMPRESS_NONE, HVDX_PHASE_REDUCE_SCATTER, 1, last, nullptr,
+                   st);
+    if (rc) return rc;
+    {
+      TimedLaunch timed_phase(HVDX_KERNEL_RS_AG, last, nranks, buf_dtype, HVDX_COMPRESS_NONE, count, st, -1, true);
+      rc = run_step(bufs, nranks, count, buf_dtype, op, HVDX_COMPRESS_NONE, HVDX_PHASE_REDUCE_SCATTER, last, nullptr,
+                    st, true);
+      if (rc) return rc;
+    }
+    rc = run_steps(bufs, nranks, count, buf_dtype, op, HVDX_COMPRESS_NONE, HVDX_PHASE_ALLGATHER, 1, last, nullptr, st);
+  }
+  if (rc) return rc;
+  if (n_out == 0) return HVDX_OK;  // every tensor empty: nothing to copy out
+  TimedLaunch timed(HVDX_KERNEL_AG_UNPACK, last, nranks, buf_dtype, HVDX_COMPRESS_NONE, both, st);
+  TimedLaunch timed_phase(HVDX_KERNEL_AG_UNPACK, last, nranks, buf_dtype, HVDX_COMPRESS_NONE, both, st, -1, true);
+  k.tiles[0] = run[0]->out_tiles;
+  k.tiles[1] = nrun > 1 ? run[1]->out_tiles : nullptr;
+  k.x0 = run[0]->n_out;
+  const hipError_t e = hvdx::launch_unpack_tiles(k, buf_dtype, tensor_dtype, nranks, n_out, st);
+  return e == hipSuccess ? HVDX_OK : hip_fail(e, "tiled copy-out launch");
+}
+
 int hvdx_fuse_allreduce_small(void* const* tensors, const int64_t* numel, const int64_t* offset, int ntensors,
                               int tensor_dtype, void* const* bufs, int64_t buf_count, int buf_dtype, int nranks,
                               int op, void* stream) {

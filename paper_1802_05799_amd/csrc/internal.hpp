@@ -50,6 +50,34 @@ struct CopyPair {
   int64_t count[2], q[2], rem[2];  // buffer elements and their ring partition
 };
 
+// The fused copies of one or two fusion buffers driven by tile tables (hvdx_copy_tile):
+// blocks [0, x0) take bucket 0's tiles, the rest bucket 1's.  A tile is at most
+// kTileLanes * tile_vectors(...) vectors of tile_vec_elems(...) elements: the host cuts
+// the tables and the kernels move them with the same constants.
+constexpr int kTileLanes = 256;
+#ifndef HVDX_TILE_U32
+#define HVDX_TILE_U32 1  // binary32 tensors and buffers
+#endif
+#ifndef HVDX_TILE_U16
+#define HVDX_TILE_U16 2  // binary32 tensors, binary16 buffers: two vectors per lane (+3 points against one)
+#endif
+#ifndef HVDX_TILE_UH
+#define HVDX_TILE_UH 1  // binary16 tensors and buffers
+#endif
+inline int tile_vec_elems(int tensor_dtype, int buf_dtype) {
+  return tensor_dtype == HVDX_FLOAT32 || buf_dtype == HVDX_FLOAT32 ? 4 : 8;
+}
+inline int tile_vectors(int tensor_dtype, int buf_dtype) {
+  if (tensor_dtype == HVDX_FLOAT32 && buf_dtype == HVDX_FLOAT32) return HVDX_TILE_U32;
+  if (tensor_dtype == HVDX_FLOAT32) return HVDX_TILE_U16;
+  return HVDX_TILE_UH;
+}
+struct TiledCopy {
+  CopyPair m;  // tensors and buffers of the buckets (the partition fields are not used)
+  const hvdx_copy_tile* tiles[2];
+  int64_t x0;
+};
+
 // How the last adding step finishes an AVERAGE.
 enum DivMode { DIV_NONE = 0, DIV_POW2 = 1, DIV_TRUE = 2 };
 
@@ -77,6 +105,12 @@ hipError_t launch_ag_step_pair(const RingPair& m, int dtype, hipStream_t stream)
 // replacing step N-2 fused with the copy-out, for two fusion buffers at once.
 hipError_t launch_pack_pair(const CopyPair& m, int src_dtype, int buf_dtype, int nranks, hipStream_t stream);
 hipError_t launch_unpack_pair(const CopyPair& m, int buf_dtype, int dst_dtype, int nranks, hipStream_t stream);
+// The same two fused copies driven by tile tables, for one or two buckets: `blocks` tiles in
+// all, each block one tile and one rank.
+hipError_t launch_pack_tiles(const TiledCopy& k, int src_dtype, int buf_dtype, int nranks, int64_t blocks,
+                             hipStream_t stream);
+hipError_t launch_unpack_tiles(const TiledCopy& k, int buf_dtype, int dst_dtype, int nranks, int64_t blocks,
+                               hipStream_t stream);
 // A small ring in one launch: each thread runs every step for its elements.
 hipError_t launch_chain(const RankPtrs& bufs, const RingArgs& a, int64_t count, int dtype, int divmode,
                         bool vector_ok, hipStream_t stream);

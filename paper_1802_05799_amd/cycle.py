@@ -43,6 +43,7 @@ class Bucket:
     offset_dev: torch.Tensor | None = None
     ptrs_dev: torch.Tensor | None = None
     small: bool = False  # the whole cycle in one launch
+    tiles: tuple | None = None  # (device copy-in table, tiles, device copy-out table, tiles)
     pair: int = 0  # 1: runs together with the later bucket `partner`; 2: with an earlier one
     partner: int = -1  # (the second of a pair has fusion buffers of its own)
 
@@ -66,7 +67,7 @@ class FusedAllreduce:
     def __init__(self, per_rank, op: str = "average", compress: bool = False,
                  threshold_bytes: int = L.DEFAULT_FUSION_THRESHOLD, align_bytes: int = L.DEFAULT_FUSION_ALIGN,
                  schedule: str = "ring", fuse_boundary: bool = True,
-                 small_bucket_bytes: int = L.SMALL_BUCKET_BYTES, pair_buckets: bool = True):
+                 small_bucket_bytes: int = L.SMALL_BUCKET_BYTES, pair_buckets: bool = True, tiled: bool = True):
         """schedule "ring" runs the ring's 2(N-1) steps; "fold" computes the same bits
         with hvdx_fold_allreduce (no per-step messages: a one-GPU bound, not the ring).
         With fuse_boundary (ring schedule, N >= 3) a fusion buffer's copy-in runs with
@@ -75,7 +76,10 @@ class FusedAllreduce:
         With the fused boundary, a bucket of at most small_bucket_bytes per rank (0:
         none) runs its whole cycle in one launch instead (compressed direct tensors
         excepted).  With pair_buckets (fused boundary) the fused buckets on the per-step
-        path run two at a time, every launch serving both.  All give the same bits."""
+        path run two at a time, every launch serving both.  With tiled (fused boundary,
+        N >= 3) the fused copies of those buckets are driven by tile tables cut once here
+        (hvdx_fuse_copy_tiles, hvdx_fuse_allreduce_tiled) instead of finding each stretch's
+        tensors in the kernel.  All give the same bits."""
         if schedule not in ("ring", "fold"):
             raise ValueError("schedule must be 'ring' or 'fold'")
         self.schedule = schedule
@@ -144,6 +148,18 @@ class FusedAllreduce:
             b.offset_dev = torch.tensor(b.offsets, dtype=torch.int64, device=dev)
             b.ptrs_dev = torch.tensor([self.tensors[r][t].data_ptr() for r in range(n) for t in b.tensors],
                                       dtype=torch.int64, device=dev)
+        self.tiled = tiled and self.fuse_boundary and n >= 3
+        if self.tiled:
+            for b in self.buckets:
+                if b.direct or b.small or b.count == 0:
+                    continue
+                tabs = []
+                for direction in (L.COPY_IN, L.COPY_OUT):
+                    numel = [self.numel[t] for t in b.tensors]
+                    arr, k = L.hvdx_fuse_copy_tiles(numel, b.offsets, b.count, self.dtype, self.buf_dtype, n, direction)
+                    host = torch.frombuffer(bytearray(bytes(arr)), dtype=torch.uint8)
+                    tabs += [host.to(dev), k]
+                b.tiles = tuple(tabs)
         self._buf_ptrs = [x.data_ptr() for x in self.bufs]
         self._buf2_ptrs = [x.data_ptr() for x in self.bufs2]
         _timeline.start_from_env()
@@ -187,12 +203,24 @@ class FusedAllreduce:
     def fused_cycle(self, b: Bucket, stream: int) -> None:
         """A fusion buffer's copy-in, ring and copy-out with the boundary steps fused
         (or, for a small bucket, all in one launch)."""
+        if self.tiled and not b.small:
+            L.hvdx_fuse_allreduce_tiled(self.tiled_desc(b, self._buf_ptrs), None, self.dtype, self.buf_dtype,
+                                        self.nranks, self.op, stream)
+            return
         fn = L.hvdx_fuse_allreduce_small if b.small else L.hvdx_fuse_allreduce
         fn(b.ptrs_dev.data_ptr(), b.numel_dev.data_ptr(), b.offset_dev.data_ptr(), len(b.tensors), self.dtype,
            self._buf_ptrs, b.count, self.buf_dtype, self.nranks, self.op, stream)
 
+    def tiled_desc(self, x: Bucket, bufs):
+        return (x.ptrs_dev.data_ptr(), x.numel_dev.data_ptr(), x.offset_dev.data_ptr(), len(x.tensors), bufs, x.count,
+                x.tiles[0].data_ptr(), x.tiles[1], x.tiles[2].data_ptr(), x.tiles[3])
+
     def fused_pair(self, a: Bucket, b: Bucket, stream: int) -> None:
         """Two fusion buffers' cycles with every launch serving both."""
+        if self.tiled:
+            L.hvdx_fuse_allreduce_tiled(self.tiled_desc(a, self._buf_ptrs), self.tiled_desc(b, self._buf2_ptrs),
+                                        self.dtype, self.buf_dtype, self.nranks, self.op, stream)
+            return
         desc = [(x.ptrs_dev.data_ptr(), x.numel_dev.data_ptr(), x.offset_dev.data_ptr(), len(x.tensors), bufs,
                  x.count) for x, bufs in ((a, self._buf_ptrs), (b, self._buf2_ptrs))]
         L.hvdx_fuse_allreduce_pair(desc[0], desc[1], self.dtype, self.buf_dtype, self.nranks, self.op, stream)

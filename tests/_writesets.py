@@ -526,3 +526,44 @@ def bcast_tensors_step(n, nbytes, root, step, k=K):
                 add(w[dst][t], np.arange(p - starts[t], stop - starts[t]))
                 add(rd[src][t], np.arange(p - starts[t], stop - starts[t]), "read")
     return w, rd
+
+
+# ---- the fused copies driven by tile tables (pack_tiles_kernel, unpack_tiles_kernel) ----
+def tile_lanes(length, V, aligned, U=1):
+    """Element indices (tile-relative) each lane of a 256-thread block takes, with repetition:
+    U V-element vectors per lane, 256 vectors apart (the lane holding the last, partial
+    vector finishes it element by element), or, when the copies are not vector-aligned,
+    elements strided by the block."""
+    out = []
+    for t in range(256):
+        if aligned:
+            for u in range(U):
+                i = (u * 256 + t) * V
+                out.extend(range(i, min(i + V, length)) if i < length else [])
+        else:
+            out.extend(range(t, length, 256))
+    return np.asarray(out, np.int64)
+
+
+def tiled_copy(kind, n, count, numel, tiles, V, aligned=True, U=1, k=K):
+    """pack_tiles_kernel ("pack": grid (tiles, n-1 slots), slot y = rank chunk+1+y) or
+    unpack_tiles_kernel ("unpack": grid (tiles, n ranks), the chunk's last-step receiver
+    reading its sender's buffer).  tiles: (pos, li, tensor, len, chunk) rows.
+    Returns (buf_writes (n, count), tensor_writes per rank and tensor, buf_reads (n, count))."""
+    bw = np.zeros((n, count), np.int64)
+    br = np.zeros((n, count), np.int64)
+    tw = [[np.zeros(m, np.int64) for m in numel] for _ in range(n)]
+    for pos, li, t, length, c in tiles:
+        assert length <= 256 * U * V, "a tile longer than a block takes"
+        e = tile_lanes(length, V, aligned, U) + k.lane_shift
+        if kind == "pack":
+            for y in range(n - 1):
+                r = (c + 1 + y) % n
+                add(bw[r], pos + e)
+        else:
+            rc = (c - 2) % n
+            for r in range(n):
+                frm = (r + k.receiver_from) % n if r == rc else r
+                add(tw[r][t], li + e)
+                add(br[frm], pos + e, "read")
+    return bw, tw, br

@@ -319,3 +319,84 @@ def test_broadcast_tensors_argument_checks():
     assert fs(FAKE, FAKE, FAKE, 3, 100, 4, 0, 6, None) == hv.ERR_INVALID  # steps 0..5 for 4 ranks
     assert fs(FAKE, FAKE, FAKE, 3, 100, 4, 0, -1, None) == hv.ERR_INVALID
     assert fs(FAKE, FAKE, FAKE, 3, 0, 4, 0, 5, None) == hv.OK
+
+
+def _tiles(numel, offset, count, te, be, n, direction):
+    arr, k = hv.hvdx_fuse_copy_tiles(numel, offset, count, te, be, n, direction)
+    return [(x.pos, x.li, x.tensor, x.len, x.chunk) for x in arr[:k]]
+
+
+def test_copy_tiles_cover_and_stay_inside_one_tensor_and_chunk():
+    """The tile tables of the fused copies: every buffer position (copy-in) or tensor
+    element (copy-out) in exactly one tile, each tile inside one tensor (or padding run)
+    and one ring chunk, at most 256 vectors long, on its grid (the buffer's for the
+    copy-in, the tensor's for the copy-out) except right after a chunk boundary off the
+    vector grid, where a short tile reaches the next vector boundary."""
+    g = np.random.default_rng(21)
+    for case in range(60):
+        te, be = [(0, 0), (0, 1), (1, 1)][case % 3]
+        vec = 4 if 0 in (te, be) else 8
+        tile = hv._lib.hvdx_fuse_tile_elems(te, be)
+        assert tile % (256 * vec) == 0 and 256 * vec <= tile <= 1024 * vec
+        n = int(g.integers(1, 20))
+        numel = [int(x) for x in g.integers(0, 3 * tile, size=g.integers(1, 9))]
+        align = [16, 2 if be == 1 else 4][case % 2] // (2 if be == 1 else 4)
+        offset, count = [], 0
+        for m in numel:
+            s = -(-count // align) * align + int(g.integers(0, 3)) * align  # gaps: padding runs
+            offset.append(s)
+            count = s + m
+        count += int(g.integers(0, 40))
+        starts, lengths = ring.chunk_bounds(count, n)
+        chunk_of = np.repeat(np.arange(n), lengths)
+        for direction in (hv.COPY_IN, hv.COPY_OUT):
+            tiles = _tiles(numel, offset, count, te, be, n, direction)
+            hits = np.zeros(count, np.int64)
+            for pos, li, t, length, c in tiles:
+                assert 1 <= length <= tile
+                hits[pos : pos + length] += 1
+                assert (chunk_of[pos : pos + length] == c).all()
+                if t >= 0:
+                    assert offset[t] <= pos and pos + length <= offset[t] + numel[t] and li == pos - offset[t]
+                    base = 0 if direction == hv.COPY_IN else offset[t]
+                else:
+                    assert direction == hv.COPY_IN and li == 0
+                    assert not any(o < pos + length and pos < o + m for o, m in zip(offset, numel) if m)
+                    base = 0
+                rel = pos - base
+                assert (rel + length - 1) // tile == rel // tile  # never across the tile grid
+                if rel % vec:  # starts off the vector grid: right after a chunk or tensor boundary
+                    assert pos in starts or pos in offset or direction == hv.COPY_IN
+                    assert (rel + length) % vec == 0 or pos + length == count or \
+                        pos + length in [s + ln for s, ln in zip(starts, lengths)] or \
+                        pos + length in [o + m for o, m in zip(offset, numel)] or pos + length in offset
+            inside = np.zeros(count, bool)
+            for o, m in zip(offset, numel):
+                inside[o : o + m] = True
+            if direction == hv.COPY_IN:
+                assert (hits == 1).all(), case
+            else:
+                assert (hits[inside] == 1).all() and (hits[~inside] == 0).all(), case
+
+
+def test_copy_tiles_argument_checks():
+    lib = ctypes.CDLL(hv.LIB_PATH)
+    f = lib.hvdx_fuse_copy_tiles
+    f.restype = ctypes.c_int64
+    f.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_int, ctypes.c_int,
+                  ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_int64]
+
+    def call(numel, offset, count, te=0, be=0, n=4, d=0, cap=0, tiles=None):
+        a = (ctypes.c_int64 * max(1, len(numel)))(*numel)
+        o = (ctypes.c_int64 * max(1, len(offset)))(*offset)
+        return f(a, o, len(numel), count, te, be, n, d, tiles, cap)
+
+    assert call([10, 20], [0, 12], 32) > 0
+    assert call([10, 20], [0, 8], 32) == hv.ERR_INVALID  # overlapping tensors
+    assert call([10, 20], [0, 12], 31) == hv.ERR_INVALID  # past the buffer
+    assert call([10], [0], 32, d=2) == hv.ERR_INVALID
+    assert call([10], [0], 32, te=1, be=0) == hv.ERR_UNSUPPORTED
+    assert call([10], [0], 32, n=0) == hv.ERR_INVALID
+    buf = (hv._lib.CopyTile * 1)()
+    assert call([3000], [0], 3000, cap=1, tiles=ctypes.cast(buf, ctypes.c_void_p)) == hv.ERR_WORKSPACE
+    assert call([], [], 0) == 0

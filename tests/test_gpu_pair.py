@@ -38,10 +38,10 @@ def test_pairs_match_oracle_and_single_cycles(case):
     host = [[(rng.standard_normal(k) * 0.01).astype(np.float32) for k in numel] for _ in range(n)]
     want1 = allreduce.allreduce(host, op, compress=compress, threshold=threshold)
     want2 = allreduce.allreduce(want1, op, compress=compress, threshold=threshold)
-    for pair in (True, False):
+    for pair, tiled in ((True, True), (False, True), (True, False), (False, False)):
         dev = [[torch.from_numpy(x).cuda() for x in row] for row in host]
         ar = hv.FusedAllreduce(dev, op=op, compress=compress, threshold_bytes=threshold, small_bucket_bytes=0,
-                               pair_buckets=pair)
+                               pair_buckets=pair, tiled=tiled)
         got_pairs = [(i, b.partner) for i, b in enumerate(ar.buckets) if b.pair == 1]
         assert got_pairs == (pairs if pair else [])
         for rep, want in enumerate((want1, want2)):  # the second call reduces the first's result again
@@ -49,7 +49,8 @@ def test_pairs_match_oracle_and_single_cycles(case):
             torch.cuda.synchronize()
             for r in range(n):
                 for t in range(len(numel)):
-                    assert_bits_equal(dev[r][t].cpu().numpy(), want[r][t], f"pair={pair} call {rep} rank {r} t {t}")
+                    assert_bits_equal(dev[r][t].cpu().numpy(), want[r][t],
+                                      f"pair={pair} tiled={tiled} call {rep} rank {r} t {t}")
 
 
 def test_pair_entry_point_directly():

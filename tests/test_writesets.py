@@ -301,3 +301,50 @@ def test_planted_copy_out_from_the_receiver_is_caught():
     q, rem = divmod(count, 4)
     s, length = W.chunk(2, q, rem)
     assert br[0, s : s + length].any()  # rank 0 receives chunk 2 and reads its own copy: caught
+
+
+# ---- tile-driven fused copies ----------------------------------------------------------
+def tiles_of(numel, offset, count, te, be, n, direction):
+    import paper_1802_05799_amd as hv
+
+    arr, k = hv.hvdx_fuse_copy_tiles(numel, offset, count, 0 if te == 4 else 1, 0 if be == 4 else 1, n, direction)
+    return [(x.pos, x.li, x.tensor, x.len, x.chunk) for x in arr[:k]]
+
+
+@pytest.mark.parametrize("esizes", [(4, 4), (4, 2), (2, 2)], ids=["f32", "f32-to-f16", "f16"])
+def test_tiled_copies_write_every_element_once(esizes):
+    import paper_1802_05799_amd as hv
+
+    te, be = esizes
+    V = W.vec_elems(te, be)
+    for numel in COPY_LAYOUTS + [[4096 * 3 + 1, 7, 2 * 4096 * 2]]:
+        for align in (16, be):
+            offset, count = plan(numel, be, align)
+            for n in (3, 5, 8):
+                q, rem = divmod(count, n)
+                tin = tiles_of(numel, offset, count, te, be, n, hv.COPY_IN)
+                tout = tiles_of(numel, offset, count, te, be, n, hv.COPY_OUT)
+                U = 2 if (te, be) == (4, 2) else 1  # vectors per lane of the built kernels
+                for aligned in (True, False):
+                    bw, _, _ = W.tiled_copy("pack", n, count, numel, tin, V, aligned, U)
+                    want = np.ones((n, count), np.int64)
+                    for c in range(n):  # the sender of chunk c stores nothing there
+                        s, length = W.chunk(c, q, rem)
+                        want[c, s : s + length] = 0
+                    assert np.array_equal(bw, want), ("pack", numel[:3], align, n, aligned)
+                    _, tw, br = W.tiled_copy("unpack", n, count, numel, tout, V, aligned, U)
+                    assert all((x == 1).all() for row in tw for x in row), ("unpack", numel[:3], align, n)
+                    for c in range(n):
+                        s, length = W.chunk(c, q, rem)
+                        assert not br[(c - 2) % n, s : s + length].any()
+
+
+def test_planted_tiled_lane_shift_is_caught():
+    import paper_1802_05799_amd as hv
+
+    numel = COPY_LAYOUTS[1]
+    offset, count = plan(numel, 4, 16)
+    tout = tiles_of(numel, offset, count, 4, 4, 3, hv.COPY_OUT)
+    with pytest.raises((AssertionError, IndexError)):
+        _, tw, _ = W.tiled_copy("unpack", 3, count, numel, tout, 4, True, k=W.Knobs(lane_shift=1))
+        assert all((x == 1).all() for row in tw for x in row)
