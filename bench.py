@@ -351,6 +351,10 @@ def short_kernel_name(full):
                 "rs_step_kernel", "ag_step_kernel"):
         if key in base:
             return key.replace("_pair", "").replace("_kernel", "") + ("_f16" if half else "_f32")
+    if "unpack_tiles_kernel" in base:  # tile-driven copies, always fused with a ring step
+        return "ag_unpack"
+    if "pack_tiles_kernel" in base:
+        return "pack_rs"
     if "unpack_pair_kernel" in base:  # two fusion buffers per launch, always fused with a ring step
         return "ag_unpack"
     if "pack_pair_kernel" in base:
@@ -370,6 +374,9 @@ def shape_of(full):
     import re
 
     two = " x2" if "pair_kernel" in full else ""
+    if "tiles_kernel" in full:  # the vectors per lane: the last template argument
+        m = re.search(r"tiles_kernel<[^>]*,\s*(\d+)>", full) or re.search(r"tiles_kernelI.*Li(\d+)EEEv", full)
+        return f"tiles<{m.group(1)}>" if m else "tiles"
     m = re.search(r"(Policy|CopyCfg)<[^>]*>", full)
     if m:
         return m.group(0).replace(" ", "") + two

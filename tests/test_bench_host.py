@@ -91,6 +91,11 @@ REAL_NAMES = {
     "true, true, false, 1, 256> >(hvdx::CopyPair, int, int, int)": ("ag_unpack", "CopyCfg<2,1,2,true,true,false,1,256> x2"),
     "_ZN4hvdx12_GLOBAL__N_116pack_pair_kernelIfDF16_NS0_7CopyCfgILi2ELi2ELi2ELb1ELb1ELb0ELi1ELi256EEEEEvNS_8CopyPairEiii":
         ("pack_rs", "CopyCfg<2,2,2,1,1,0,1,256> x2"),
+    "void hvdx::(anonymous namespace)::pack_tiles_kernel<float, float, 1>(hvdx::TiledCopy, int)": ("pack_rs", "tiles<1>"),
+    "void hvdx::(anonymous namespace)::unpack_tiles_kernel<float, float, 1>(hvdx::TiledCopy, int)":
+        ("ag_unpack", "tiles<1>"),
+    "_ZN4hvdx12_GLOBAL__N_117pack_tiles_kernelIfDF16_Li2EEEvNS_9TiledCopyEi": ("pack_rs", "tiles<2>"),
+    "_ZN4hvdx12_GLOBAL__N_119unpack_tiles_kernelIfDF16_Li2EEEvNS_9TiledCopyEi": ("ag_unpack", "tiles<2>"),
     "__amd_rocclr_copyBuffer": (None, ""),
 }
 
