@@ -28,6 +28,7 @@ import time
 ROOT = os.path.dirname(os.path.abspath(__file__))
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, 8 TB/s
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+REPLACE_IN_TENSORS = 1  # HVDX_REPLACE_IN_TENSORS: FusedAllreduce.replace when its replacing steps write the tensors
 
 
 def parse():
@@ -74,6 +75,11 @@ def kernel_bytes(ar, kind, bi, step):
     if kind in ("unpack", "ag_unpack"):  # the fused replacing step only changes which buffer is read
         return n * (es_b + es_t) * data
     compressed = b.direct and ar.compress
+    if not b.direct and ar.replace == REPLACE_IN_TENSORS and kind in ("rs_ag", "ag"):
+        # replacing steps into the tensors (HVDX_REPLACE_IN_TENSORS): the tensors' elements only
+        if kind == "rs_ag":  # owner's and sender's buffers in, owner's and the next rank's tensors out
+            return 2 * (es_b + es_t) * data
+        return 2 * es_t * data  # sender's tensors in, receiver's out
     if kind == "rs_ag":  # read owner and sender, write owner and the next rank
         if compressed:  # binary32 owner, binary16 sender (binary32 when N = 2: its first touch)
             return (16 if n == 2 else 14) * b.count
@@ -346,6 +352,10 @@ def short_kernel_name(full):
         return "cycle_small"
     if "chain_kernel" in base:
         return "ring_small"
+    # replacing steps that deliver into the tensors report as the ring step they are
+    for key in ("rs_ag_tiles_kernel", "ag_tiles_kernel"):
+        if key in base:
+            return key.replace("_tiles_kernel", "_step") + ("_f16" if half else "_f32")
     # a launch serving two fusion buffers' rings reports as the one-ring kernel of its step
     for key in ("rs_ag_step_pair_kernel", "rs_step_pair_kernel", "ag_step_pair_kernel", "rs_ag_step_kernel",
                 "rs_step_kernel", "ag_step_kernel"):

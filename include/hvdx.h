@@ -262,16 +262,30 @@ int64_t hvdx_fuse_tile_elems(int tensor_dtype, int buf_dtype);
 
 /*
  * hvdx_fuse_allreduce_tiled -- hvdx_fuse_allreduce (b1 NULL) or hvdx_fuse_allreduce_pair
- * (b0 and b1) with the fused copies driven by tile tables: the same result, bit for bit,
- * the same launches, the same scratch contents of the fusion buffers afterwards.
+ * (b0 and b1) with the fused copies driven by tile tables: the same result, bit for bit.
  *   b*->b              the bucket, as for hvdx_fuse_allreduce_pair
  *   b*->in_tiles       DEVICE array of n_in tiles from hvdx_fuse_copy_tiles(HVDX_COPY_IN)
  *   b*->out_tiles      DEVICE array of n_out tiles from hvdx_fuse_copy_tiles(HVDX_COPY_OUT)
  * for exactly this bucket (numel, offset, buf_count, both types and nranks): the tables
  * are device memory and are not checked; other tables make the kernels read or write
- * outside the buffers and tensors.  Errors as hvdx_fuse_allreduce_pair, and
- * HVDX_ERR_INVALID for a missing table or a negative tile count.
+ * outside the buffers and tensors.
+ *   replace            where the replacing steps (paper section 3) store the chunk each
+ *                      one delivers:
+ *     HVDX_REPLACE_IN_BUFFERS  in the receiver's fusion buffer, as in paper section 7
+ *                      (step 4, then the copy-out of step 5 fused with the last
+ *                      replacing step): the same launches as the untiled calls, and the
+ *                      fusion buffers end holding the result;
+ *     HVDX_REPLACE_IN_TENSORS  in the receiver's output tensors, from which the next step
+ *                      forwards it (the finished sum goes from adding step N-2 to the
+ *                      owner's and the next rank's tensors): every message of the ring
+ *                      in its order, no copy-out, one launch fewer; tensor_dtype must
+ *                      equal buf_dtype (else HVDX_ERR_UNSUPPORTED), and the fusion
+ *                      buffers are scratch afterwards.
+ * Errors as hvdx_fuse_allreduce_pair, and HVDX_ERR_INVALID for a missing table, a
+ * negative tile count or an unknown replace mode.
  */
+#define HVDX_REPLACE_IN_BUFFERS 0
+#define HVDX_REPLACE_IN_TENSORS 1
 typedef struct hvdx_tiled_bucket {
   hvdx_bucket b;
   const hvdx_copy_tile* in_tiles;
@@ -280,7 +294,7 @@ typedef struct hvdx_tiled_bucket {
   int64_t n_out;
 } hvdx_tiled_bucket;
 int hvdx_fuse_allreduce_tiled(const hvdx_tiled_bucket* b0, const hvdx_tiled_bucket* b1, int tensor_dtype,
-                              int buf_dtype, int nranks, int op, void* stream);
+                              int buf_dtype, int nranks, int op, int replace, void* stream);
 
 /*
  * hvdx_fuse_allreduce_small -- hvdx_fuse_allreduce for small fusion buffers: the same

@@ -7,6 +7,8 @@ to the HIP runtime torch already loaded (one runtime per process).
     ar = FusedAllreduce(per_rank_grads, op="average")   # plan + buffers, once
     ar()                                                  # reduce in place
 """
+import operator
+
 import torch  # noqa: F401  (must precede the library load)
 
 from ._lib import (  # noqa: F401
@@ -27,6 +29,8 @@ from ._lib import (  # noqa: F401
     OK,
     PHASE_ALLGATHER,
     PHASE_REDUCE_SCATTER,
+    REPLACE_IN_BUFFERS,
+    REPLACE_IN_TENSORS,
     SMALL_BUCKET_BYTES,
     SUM,
     HvdxError,
@@ -68,6 +72,9 @@ from .cycle import FusedAllreduce  # noqa: F401
 from .timeline import Timeline  # noqa: F401
 
 
+_NBYTES = operator.attrgetter("nbytes")
+
+
 class TensorBroadcast:
     """Rank `root`'s tensors copied into every other rank's (paper sections 4 and 5:
     consistent initial variables), every tensor of the list in one chain:
@@ -88,12 +95,16 @@ class TensorBroadcast:
         if any(len(ts) != nt for ts in per_rank):
             raise ValueError("every rank needs the same number of tensors")
         flat = [x for ts in per_rank for x in ts]
-        if not all(x.is_cuda and x.is_contiguous() for x in flat):
+        # four passes over the tensors, each one torch call per tensor (map: no bytecode per item)
+        if not all(map(torch.Tensor.is_contiguous, flat)):
             raise ValueError("broadcast needs contiguous GPU tensors")
-        if len({x.get_device() for x in flat}) > 1:
+        devices = set(map(torch.Tensor.get_device, flat))  # -1: not on a GPU
+        if -1 in devices:
+            raise ValueError("broadcast needs contiguous GPU tensors")
+        if len(devices) > 1:
             raise ValueError("broadcast needs every tensor on one GPU")
-        ptr = np.fromiter((x.data_ptr() for x in flat), dtype=np.int64, count=len(flat))
-        nbytes = np.fromiter((x.nbytes for x in flat), dtype=np.int64, count=len(flat)).reshape(n, nt)
+        ptr = np.fromiter(map(torch.Tensor.data_ptr, flat), dtype=np.int64, count=len(flat))
+        nbytes = np.fromiter(map(_NBYTES, flat), dtype=np.int64, count=len(flat)).reshape(n, nt)
         if (nbytes != nbytes[:1]).any():
             raise ValueError("tensor t must have the same byte count on every rank")
         live = nbytes.reshape(-1) > 0
@@ -107,9 +118,10 @@ class TensorBroadcast:
         # one upload: the rank-major pointer table, then the byte counts, then the starts
         host = torch.from_numpy(np.concatenate([ptr, nbytes[0], np.asarray(voff, dtype=np.int64), [0]]))
         self.tables = host.pin_memory().to(self.device, non_blocking=True)
+        upload = torch.cuda.current_stream(self.device)
         self._ready = torch.cuda.Event()  # a call on another stream waits for the upload
-        self._ready.record(torch.cuda.current_stream(self.device))
-        self._waited = set()
+        self._ready.record(upload)
+        self._waited = {upload.cuda_stream}  # calls on the upload stream follow it in order
         k = n * nt
         self._args = (self.tables.data_ptr(), self.tables.data_ptr() + 8 * k, self.tables.data_ptr() + 8 * (k + nt),
                       nt, self.total, n)

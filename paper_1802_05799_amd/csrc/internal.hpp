@@ -111,6 +111,11 @@ hipError_t launch_pack_tiles(const TiledCopy& k, int src_dtype, int buf_dtype, i
                              hipStream_t stream);
 hipError_t launch_unpack_tiles(const TiledCopy& k, int buf_dtype, int dst_dtype, int nranks, int64_t blocks,
                                hipStream_t stream);
+// Replacing steps that deliver into the tensors (tensor and buffer of one type), over
+// the copy-out's tiles: adding step N-2 with replacing step 0, and replacing step s.
+hipError_t launch_rs_ag_tiles(const TiledCopy& k, const RingArgs& a, int dtype, int divmode, int64_t blocks,
+                              hipStream_t stream);
+hipError_t launch_ag_tiles(const TiledCopy& k, int dtype, int nranks, int step, int64_t blocks, hipStream_t stream);
 // A small ring in one launch: each thread runs every step for its elements.
 hipError_t launch_chain(const RankPtrs& bufs, const RingArgs& a, int64_t count, int dtype, int divmode,
                         bool vector_ok, hipStream_t stream);

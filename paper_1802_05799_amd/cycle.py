@@ -67,7 +67,8 @@ class FusedAllreduce:
     def __init__(self, per_rank, op: str = "average", compress: bool = False,
                  threshold_bytes: int = L.DEFAULT_FUSION_THRESHOLD, align_bytes: int = L.DEFAULT_FUSION_ALIGN,
                  schedule: str = "ring", fuse_boundary: bool = True,
-                 small_bucket_bytes: int = L.SMALL_BUCKET_BYTES, pair_buckets: bool = True, tiled: bool = True):
+                 small_bucket_bytes: int = L.SMALL_BUCKET_BYTES, pair_buckets: bool = True, tiled: bool = True,
+                 replace_in_tensors: bool = True):
         """schedule "ring" runs the ring's 2(N-1) steps; "fold" computes the same bits
         with hvdx_fold_allreduce (no per-step messages: a one-GPU bound, not the ring).
         With fuse_boundary (ring schedule, N >= 3) a fusion buffer's copy-in runs with
@@ -79,7 +80,10 @@ class FusedAllreduce:
         path run two at a time, every launch serving both.  With tiled (fused boundary,
         N >= 3) the fused copies of those buckets are driven by tile tables cut once here
         (hvdx_fuse_copy_tiles, hvdx_fuse_allreduce_tiled) instead of finding each stretch's
-        tensors in the kernel.  All give the same bits."""
+        tensors in the kernel.  With replace_in_tensors (tiled, no compression) their
+        replacing steps deliver each chunk straight into the receiving rank's tensors and
+        forward it from there, so no copy-out follows (HVDX_REPLACE_IN_TENSORS); the
+        fusion buffers then end as scratch.  All give the same bits."""
         if schedule not in ("ring", "fold"):
             raise ValueError("schedule must be 'ring' or 'fold'")
         self.schedule = schedule
@@ -160,6 +164,8 @@ class FusedAllreduce:
                     host = torch.frombuffer(bytearray(bytes(arr)), dtype=torch.uint8)
                     tabs += [host.to(dev), k]
                 b.tiles = tuple(tabs)
+        in_tensors = replace_in_tensors and self.tiled and self.dtype == self.buf_dtype
+        self.replace = L.REPLACE_IN_TENSORS if in_tensors else L.REPLACE_IN_BUFFERS
         self._buf_ptrs = [x.data_ptr() for x in self.bufs]
         self._buf2_ptrs = [x.data_ptr() for x in self.bufs2]
         _timeline.start_from_env()
@@ -205,7 +211,7 @@ class FusedAllreduce:
         (or, for a small bucket, all in one launch)."""
         if self.tiled and not b.small:
             L.hvdx_fuse_allreduce_tiled(self.tiled_desc(b, self._buf_ptrs), None, self.dtype, self.buf_dtype,
-                                        self.nranks, self.op, stream)
+                                        self.nranks, self.op, self.replace, stream)
             return
         fn = L.hvdx_fuse_allreduce_small if b.small else L.hvdx_fuse_allreduce
         fn(b.ptrs_dev.data_ptr(), b.numel_dev.data_ptr(), b.offset_dev.data_ptr(), len(b.tensors), self.dtype,
@@ -219,7 +225,7 @@ class FusedAllreduce:
         """Two fusion buffers' cycles with every launch serving both."""
         if self.tiled:
             L.hvdx_fuse_allreduce_tiled(self.tiled_desc(a, self._buf_ptrs), self.tiled_desc(b, self._buf2_ptrs),
-                                        self.dtype, self.buf_dtype, self.nranks, self.op, stream)
+                                        self.dtype, self.buf_dtype, self.nranks, self.op, self.replace, stream)
             return
         desc = [(x.ptrs_dev.data_ptr(), x.numel_dev.data_ptr(), x.offset_dev.data_ptr(), len(x.tensors), bufs,
                  x.count) for x, bufs in ((a, self._buf_ptrs), (b, self._buf2_ptrs))]
@@ -229,7 +235,9 @@ class FusedAllreduce:
         """The kernels one call launches, in order: (kind, bucket index, step) with
         kind "pack", "pack_rs" (copy-in with adding step 0), "rs", "rs_ag" (adding
         step N-2 fused with replacing step 0), "ag", "ag_unpack" (replacing step N-2
-        with copy-out), "unpack", "fold", "ring" (the one-rank compressed round trip),
+        with copy-out; with the replacing steps in the tensors, "rs_ag" and "ag" 1..N-2
+        deliver into the tensors and no copy-out follows), "unpack", "fold", "ring"
+        (the one-rank compressed round trip),
         "cycle_small" or "ring_small" (a small bucket's whole cycle in one launch).
         A launch that serves a pair of buckets names both: (kind, (i, j), step)."""
         out = []
@@ -238,12 +246,7 @@ class FusedAllreduce:
             if b.count == 0 or b.pair == 2:
                 continue
             if b.pair == 1:
-                both = (bi, b.partner)
-                out.append(("pack_rs", both, 0))
-                out += [("rs", both, s) for s in range(1, n - 2)]
-                out.append(("rs_ag", both, n - 2))
-                out += [("ag", both, s) for s in range(1, n - 2)]
-                out.append(("ag_unpack", both, n - 2))
+                out += self._fused_sequence((bi, b.partner))
                 continue
             if b.small:
                 if not b.direct:
@@ -259,11 +262,7 @@ class FusedAllreduce:
                     out.append(("unpack", bi, -1))
                 continue
             if self.fuse_boundary and not b.direct and n >= 3:
-                out.append(("pack_rs", bi, 0))
-                out += [("rs", bi, s) for s in range(1, n - 2)]
-                out.append(("rs_ag", bi, n - 2))
-                out += [("ag", bi, s) for s in range(1, n - 2)]
-                out.append(("ag_unpack", bi, n - 2))
+                out += self._fused_sequence(bi)
                 continue
             if not b.direct:
                 out.append(("pack", bi, -1))
@@ -277,6 +276,13 @@ class FusedAllreduce:
             if not b.direct:
                 out.append(("unpack", bi, -1))
         return out
+
+    def _fused_sequence(self, bi):
+        n = self.nranks
+        out = [("pack_rs", bi, 0)] + [("rs", bi, s) for s in range(1, n - 2)] + [("rs_ag", bi, n - 2)]
+        if self.replace == L.REPLACE_IN_TENSORS:
+            return out + [("ag", bi, s) for s in range(1, n - 1)]
+        return out + [("ag", bi, s) for s in range(1, n - 2)] + [("ag_unpack", bi, n - 2)]
 
     def capture(self) -> "torch.cuda.CUDAGraph":
         """Record one call's launches (every bucket's copy-in, ring steps and copy-out)

@@ -24,6 +24,9 @@ class Knobs:
     chunk_tile_skip: int = 0  # tiles of a chunk skipped at its start (fused copies)
     skip_slot: int = 0  # the slot the fused copy-in leaves out (the sender: 0)
     receiver_from: int = -1  # the fused copy-out reads rank `receiver + this` (the sender: -1)
+    replace_sender: int = -1  # replacing step s into the tensors reads rank `chunk + s + this` (-1)
+    rs_ag_next: int = 0  # the fused step into the tensors also writes rank `chunk + this` (0)
+    tile_block_stride: int = 0  # block b of a replacing step takes tiles b*this + j (0: tiles per block)
 
 
 K = Knobs()
@@ -567,3 +570,40 @@ def tiled_copy(kind, n, count, numel, tiles, V, aligned=True, U=1, k=K):
                 add(tw[r][t], li + e)
                 add(br[frm], pos + e, "read")
     return bw, tw, br
+
+
+# ---- replacing steps into the tensors (rs_ag_tiles_kernel, ag_tiles_kernel) -----------
+def tiled_replace(kind, n, count, numel, tiles, V, step=0, aligned=True, U=1, k=K, tpb=2):
+    """rs_ag_tiles_kernel ("rs_ag": adding step N-2 and replacing step 0, from the owner's
+    and sender's buffers into the owner's and rank c's tensors; grid (tiles)) or
+    ag_tiles_kernel ("ag": replacing step `step`, rank c-1+step's tensors into rank
+    c+step's; grid (ceil(tiles / tpb)), block b taking tiles b*tpb .. b*tpb+tpb-1), over
+    the copy-out's tiles (padding tiles skipped).
+    Returns (tensor_writes, tensor_reads per rank and tensor, buf_reads (n, count))."""
+    tw = [[np.zeros(m, np.int64) for m in numel] for _ in range(n)]
+    tr = [[np.zeros(m, np.int64) for m in numel] for _ in range(n)]
+    br = np.zeros((n, count), np.int64)
+    if kind == "rs_ag":
+        order = range(len(tiles))
+    else:
+        stride = k.tile_block_stride or tpb
+        order = [g for b in range(-(-len(tiles) // tpb)) for g in (b * stride + j for j in range(tpb))
+                 if g < len(tiles)]
+    for g in order:
+        pos, li, t, length, c = tiles[g]
+        assert length <= 256 * U * V, "a tile longer than a block takes"
+        if t < 0:
+            continue
+        e = tile_lanes(length, V, aligned, U) + k.lane_shift
+        if kind == "rs_ag":
+            own = (c - 1) % n
+            snd = (own - 1) % n
+            add(br[own], pos + e, "read")
+            add(br[snd], pos + e, "read")
+            add(tw[own][t], li + e)
+            add(tw[(c + k.rs_ag_next) % n][t], li + e)
+        else:
+            snd = (c + step + k.replace_sender) % n
+            add(tr[snd][t], li + e, "read")
+            add(tw[(snd + 1) % n][t], li + e)
+    return tw, tr, br

@@ -242,6 +242,22 @@ def test_pair_argument_errors():
     assert lib.hvdx_fuse_allreduce_pair(None, None, hv.FLOAT32, hv.FLOAT32, 3, hv.SUM, None) == hv.ERR_INVALID
 
 
+def test_tiled_argument_errors():
+    """hvdx_fuse_allreduce_tiled refuses an unknown replace mode, and replacing in the
+    tensors when they are not of the buffer's type, before any launch."""
+    ft = hv.hvdx_fuse_allreduce_tiled
+    b3 = bufs(3, 64)
+    d0 = (FAKE, FAKE, FAKE, 3, b3, 64, FAKE, 4, FAKE, 4)
+    assert status_of(ft, d0, None, hv.FLOAT32, hv.FLOAT32, 3, hv.SUM, 2) == hv.ERR_INVALID
+    assert status_of(ft, d0, None, hv.FLOAT32, hv.FLOAT32, 3, hv.SUM, -1) == hv.ERR_INVALID
+    assert status_of(ft, d0, None, hv.FLOAT32, hv.FLOAT16, 3, hv.SUM, hv.REPLACE_IN_TENSORS) == hv.ERR_UNSUPPORTED
+    assert status_of(ft, d0, None, hv.FLOAT32, hv.FLOAT32, 2, hv.SUM, hv.REPLACE_IN_TENSORS) == hv.ERR_UNSUPPORTED
+    assert status_of(ft, (FAKE, FAKE, FAKE, 3, b3, 64, FAKE, 4, 0, 4), None, hv.FLOAT32, hv.FLOAT32, 3, hv.SUM,
+                     hv.REPLACE_IN_TENSORS) == hv.ERR_INVALID  # the copy-out tiles missing
+    assert status_of(ft, (FAKE, FAKE, FAKE, 3, b3, 0, FAKE, 0, FAKE, 0), None, hv.FLOAT32, hv.FLOAT32, 3, hv.SUM,
+                     hv.REPLACE_IN_TENSORS) == hv.OK  # an empty bucket: nothing launched
+
+
 def test_fused_allreduce_rejects_overlapping_tensors():
     """Paired launches read and write two buckets' tensors at once, so the cycle refuses
     tensors that share memory (checked on the host, before any device work)."""
@@ -319,6 +335,21 @@ def test_broadcast_tensors_argument_checks():
     assert fs(FAKE, FAKE, FAKE, 3, 100, 4, 0, 6, None) == hv.ERR_INVALID  # steps 0..5 for 4 ranks
     assert fs(FAKE, FAKE, FAKE, 3, 100, 4, 0, -1, None) == hv.ERR_INVALID
     assert fs(FAKE, FAKE, FAKE, 3, 0, 4, 0, 5, None) == hv.OK
+
+
+def test_tensor_broadcast_rejects_bad_lists_before_any_device_work():
+    """TensorBroadcast's checks on the tensor list, all on the host before its upload."""
+    import torch
+
+    base = torch.zeros(64)
+    with pytest.raises(ValueError, match="ranks"):
+        hv.TensorBroadcast([])
+    with pytest.raises(ValueError, match="same number"):
+        hv.TensorBroadcast([[base[:4]], [base[4:8], base[8:12]]])
+    with pytest.raises(ValueError, match="GPU"):  # host tensors
+        hv.TensorBroadcast([[base[:4]], [base[4:8]]])
+    with pytest.raises(ValueError, match="contiguous"):
+        hv.TensorBroadcast([[base[::2]], [base[1::2]]])
 
 
 def _tiles(numel, offset, count, te, be, n, direction):

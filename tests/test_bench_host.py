@@ -15,8 +15,9 @@ sys.path.insert(0, ROOT)
 import bench  # noqa: E402
 
 
-def fake_allreduce(nranks, numel, buckets, dtype=0, buf_dtype=0, compress=False):
+def fake_allreduce(nranks, numel, buckets, dtype=0, buf_dtype=0, compress=False, replace=0):
     return SimpleNamespace(nranks=nranks, numel=numel, dtype=dtype, buf_dtype=buf_dtype, compress=compress,
+                           replace=replace,
                            buckets=[SimpleNamespace(tensors=t, count=c, direct=d) for t, c, d in buckets])
 
 
@@ -52,6 +53,28 @@ def test_whole_cycle_bytes_match_the_step_count():
     total = sum(bench.kernel_bytes(ar, k, 0, s) for k, s in launches)
     separate = n * (4 * data + 4 * count) + (n - 1) * 5 * 4 * count + n * 8 * data
     assert total == separate - (3 + 1 + 1 + 2) * 4 * count
+
+
+def test_replacing_into_tensors_bytes():
+    """With the replacing steps writing the tensors, the fused step reads two buffers and
+    writes two ranks' tensors, a replacing step copies one rank's tensors to the next
+    (tensor elements only: padding is not moved), and no copy-out follows: against the
+    replacing steps in the buffers the cycle moves 2(N-1) fewer binary32 values per
+    buffer element (the copy-out's N reads and N writes, less one replacing step's read
+    and write, less the padding the fused step and the replacing steps no longer move)."""
+    n, data, count = 8, 1000, 1003
+    ar = fake_allreduce(n, [data, 50], [([0], count, False), ([1], 50, True)], replace=bench.REPLACE_IN_TENSORS)
+    assert bench.kernel_bytes(ar, "rs_ag", 0, n - 2) == 4 * 4 * data
+    assert bench.kernel_bytes(ar, "ag", 0, 3) == 2 * 4 * data
+    assert bench.kernel_bytes(ar, "ag", 1, 3) == 2 * 4 * 50 and bench.kernel_bytes(ar, "rs_ag", 1, n - 2) == 4 * 4 * 50
+    launches = [("pack_rs", 0)] + [("rs", s) for s in range(1, n - 2)] + [("rs_ag", n - 2)] \
+        + [("ag", s) for s in range(1, n - 1)]
+    into = sum(bench.kernel_bytes(ar, k, 0, s) for k, s in launches)
+    ab = fake_allreduce(n, [data], [([0], count, False)])
+    launches = [("pack_rs", 0)] + [("rs", s) for s in range(1, n - 2)] + [("rs_ag", n - 2)] \
+        + [("ag", s) for s in range(1, n - 2)] + [("ag_unpack", n - 2)]
+    buffers = sum(bench.kernel_bytes(ab, k, 0, s) for k, s in launches)
+    assert buffers - into == 2 * (n - 1) * 4 * count
 
 
 def test_a_launch_serving_two_buckets_counts_both():
@@ -96,6 +119,11 @@ REAL_NAMES = {
         ("ag_unpack", "tiles<1>"),
     "_ZN4hvdx12_GLOBAL__N_117pack_tiles_kernelIfDF16_Li2EEEvNS_9TiledCopyEi": ("pack_rs", "tiles<2>"),
     "_ZN4hvdx12_GLOBAL__N_119unpack_tiles_kernelIfDF16_Li2EEEvNS_9TiledCopyEi": ("ag_unpack", "tiles<2>"),
+    "void hvdx::(anonymous namespace)::rs_ag_tiles_kernel<float, 2, 1>(hvdx::TiledCopy, hvdx::RingArgs)":
+        ("rs_ag_step_f32", "tiles<1>"),
+    "void hvdx::(anonymous namespace)::ag_tiles_kernel<float, false, 1>(hvdx::TiledCopy, int, int)":
+        ("ag_step_f32", "tiles<1>"),
+    "_ZN4hvdx12_GLOBAL__N_115ag_tiles_kernelIDF16_Lb1ELi1EEEvNS_9TiledCopyEii": ("ag_step_f16", "tiles<1>"),
     "__amd_rocclr_copyBuffer": (None, ""),
 }
 

@@ -348,3 +348,57 @@ def test_planted_tiled_lane_shift_is_caught():
     with pytest.raises((AssertionError, IndexError)):
         _, tw, _ = W.tiled_copy("unpack", 3, count, numel, tout, 4, True, k=W.Knobs(lane_shift=1))
         assert all((x == 1).all() for row in tw for x in row)
+
+
+# ---- replacing steps delivered into the tensors -----------------------------------------
+def replace_phase(n, count, numel, offset, tiles, V, aligned, U, k=W.K):
+    """Runs the fused step and replacing steps 1..N-2 into the tensors on a model of which
+    tensor elements hold their final value; checks each launch on the way.  Returns the
+    final-value map."""
+    q, rem = divmod(count, n)
+    tw, _, br = W.tiled_replace("rs_ag", n, count, numel, tiles, V, aligned=aligned, U=U, k=k)
+    for c in range(n):  # chunk c is read from its owner c-1 and sender c-2 only
+        s, length = W.chunk(c, q, rem)
+        readers = {r for r in range(n) if br[r, s : s + length].any()}
+        assert readers <= {(c - 1) % n, (c - 2) % n}, (c, readers)
+    assert all((x <= 1).all() for row in tw for x in row), "an element written twice by the fused step"
+    final = [[x > 0 for x in row] for row in tw]
+    for step in range(1, n - 1):
+        tw, tr, _ = W.tiled_replace("ag", n, count, numel, tiles, V, step, aligned, U, k)
+        for r in range(n):
+            for t in range(len(numel)):
+                assert not (tr[r][t] > 0)[~final[r][t]].any(), f"step {step} forwards what rank {r} lacks"
+                assert not ((tw[r][t] > 0) & (tr[r][t] > 0)).any(), f"step {step} reads what it writes"
+                assert not ((tw[r][t] > 0) & final[r][t]).any(), f"step {step} writes rank {r} twice"
+                assert (tw[r][t] <= 1).all()
+                final[r][t] |= tw[r][t] > 0
+    return final
+
+
+@pytest.mark.parametrize("esize", [4, 2], ids=["f32", "f16"])
+def test_replacing_into_tensors_delivers_every_element_once(esize):
+    import paper_1802_05799_amd as hv
+
+    V = W.vec_elems(esize, esize)
+    for numel in COPY_LAYOUTS + [[4096 * 3 + 1, 7, 2 * 4096 * 2]]:
+        for align in (16, esize):
+            offset, count = plan(numel, esize, align)
+            for n in (3, 4, 7):
+                tout = tiles_of(numel, offset, count, esize, esize, n, hv.COPY_OUT)
+                for aligned in (True, False):
+                    final = replace_phase(n, count, numel, offset, tout, V, aligned, 1)
+                    assert all(x.all() for row in final for x in row), (numel[:3], align, n, aligned)
+
+
+@pytest.mark.parametrize("knobs", [W.Knobs(replace_sender=0), W.Knobs(rs_ag_next=1), W.Knobs(lane_shift=1),
+                                   W.Knobs(tile_block_stride=1)],
+                         ids=["sender", "next-rank", "lane", "tiles-per-block"])
+def test_planted_replacing_mistakes_are_caught(knobs):
+    import paper_1802_05799_amd as hv
+
+    numel = COPY_LAYOUTS[1]
+    offset, count = plan(numel, 4, 16)
+    tout = tiles_of(numel, offset, count, 4, 4, 5, hv.COPY_OUT)
+    with pytest.raises((AssertionError, IndexError)):
+        final = replace_phase(5, count, numel, offset, tout, 4, True, 1, knobs)
+        assert all(x.all() for row in final for x in row)
