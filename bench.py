@@ -28,7 +28,7 @@ import time
 ROOT = os.path.dirname(os.path.abspath(__file__))
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, 8 TB/s
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
-REPLACE_IN_TENSORS = 1  # HVDX_REPLACE_IN_TENSORS: FusedAllreduce.replace when its replacing steps write the tensors
+TILED_REPLACE_IN_TENSORS, TILED_ADD_FROM_TENSORS = 1, 2  # the HVDX_TILED_* bits of FusedAllreduce.tiled_flags
 
 
 def parse():
@@ -75,10 +75,16 @@ def kernel_bytes(ar, kind, bi, step):
     if kind in ("unpack", "ag_unpack"):  # the fused replacing step only changes which buffer is read
         return n * (es_b + es_t) * data
     compressed = b.direct and ar.compress
-    if not b.direct and ar.replace == REPLACE_IN_TENSORS and kind in ("rs_ag", "ag"):
-        # replacing steps into the tensors (HVDX_REPLACE_IN_TENSORS): the tensors' elements only
-        if kind == "rs_ag":  # owner's and sender's buffers in, owner's and the next rank's tensors out
-            return 2 * (es_b + es_t) * data
+    flags = 0 if b.direct else ar.tiled_flags
+    if flags & TILED_ADD_FROM_TENSORS and kind == "rs":  # the receiver's own elements from its tensors
+        if step == 0:  # the sender's too: two tensors in, the receiver's buffer out
+            return (2 * es_t + es_b) * data
+        return (es_t + 2 * es_b) * data  # the sender's buffer in; tensors' elements only, no padding
+    if flags & TILED_REPLACE_IN_TENSORS and kind in ("rs_ag", "ag"):
+        # replacing steps into the tensors: the tensors' elements only
+        if kind == "rs_ag":  # owner's values and sender's buffer in, owner's and the next rank's tensors out
+            own = es_t if flags & TILED_ADD_FROM_TENSORS else es_b
+            return (own + es_b + 2 * es_t) * data
         return 2 * es_t * data  # sender's tensors in, receiver's out
     if kind == "rs_ag":  # read owner and sender, write owner and the next rank
         if compressed:  # binary32 owner, binary16 sender (binary32 when N = 2: its first touch)

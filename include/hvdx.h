@@ -269,23 +269,28 @@ int64_t hvdx_fuse_tile_elems(int tensor_dtype, int buf_dtype);
  * for exactly this bucket (numel, offset, buf_count, both types and nranks): the tables
  * are device memory and are not checked; other tables make the kernels read or write
  * outside the buffers and tensors.
- *   replace            where the replacing steps (paper section 3) store the chunk each
- *                      one delivers:
- *     HVDX_REPLACE_IN_BUFFERS  in the receiver's fusion buffer, as in paper section 7
- *                      (step 4, then the copy-out of step 5 fused with the last
- *                      replacing step): the same launches as the untiled calls, and the
- *                      fusion buffers end holding the result;
- *     HVDX_REPLACE_IN_TENSORS  in the receiver's output tensors, from which the next step
- *                      forwards it (the finished sum goes from adding step N-2 to the
- *                      owner's and the next rank's tensors): every message of the ring
- *                      in its order, no copy-out, one launch fewer; tensor_dtype must
- *                      equal buf_dtype (else HVDX_ERR_UNSUPPORTED), and the fusion
- *                      buffers are scratch afterwards.
+ *   flags              0 (HVDX_TILED_BUFFERS): the fusion buffers as in paper section 7 --
+ *                      the copy-in fused with adding step 0, the ring in the buffers
+ *                      (step 4), the copy-out fused with the last replacing step (step 5);
+ *                      the same launches as the untiled calls, and the fusion buffers end
+ *                      holding the result.  Or a combination of:
+ *     HVDX_TILED_REPLACE_IN_TENSORS  the replacing steps (paper section 3) store the chunk
+ *                      each one delivers in the receiver's output tensors, from which the
+ *                      next step forwards it (the finished sum goes from adding step N-2 to
+ *                      the owner's and the next rank's tensors): no copy-out;
+ *     HVDX_TILED_ADD_FROM_TENSORS  (with REPLACE_IN_TENSORS) each adding step reads the
+ *                      receiver's own elements of its chunk from its tensors (and in step 0
+ *                      the sender's too), where the copy-in would have put them: no copy-in;
+ *                      the buffers then only ever hold received partial sums.
+ *                      Every message of the ring moves in its order with either flag;
+ *                      both need tensor_dtype == buf_dtype (else HVDX_ERR_UNSUPPORTED), and
+ *                      with either the fusion buffers are scratch afterwards.
  * Errors as hvdx_fuse_allreduce_pair, and HVDX_ERR_INVALID for a missing table, a
- * negative tile count or an unknown replace mode.
+ * negative tile count or an unknown flag.
  */
-#define HVDX_REPLACE_IN_BUFFERS 0
-#define HVDX_REPLACE_IN_TENSORS 1
+#define HVDX_TILED_BUFFERS 0
+#define HVDX_TILED_REPLACE_IN_TENSORS 1
+#define HVDX_TILED_ADD_FROM_TENSORS 2
 typedef struct hvdx_tiled_bucket {
   hvdx_bucket b;
   const hvdx_copy_tile* in_tiles;
@@ -294,7 +299,7 @@ typedef struct hvdx_tiled_bucket {
   int64_t n_out;
 } hvdx_tiled_bucket;
 int hvdx_fuse_allreduce_tiled(const hvdx_tiled_bucket* b0, const hvdx_tiled_bucket* b1, int tensor_dtype,
-                              int buf_dtype, int nranks, int op, int replace, void* stream);
+                              int buf_dtype, int nranks, int op, int flags, void* stream);
 
 /*
  * hvdx_fuse_allreduce_small -- hvdx_fuse_allreduce for small fusion buffers: the same

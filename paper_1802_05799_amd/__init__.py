@@ -29,8 +29,9 @@ from ._lib import (  # noqa: F401
     OK,
     PHASE_ALLGATHER,
     PHASE_REDUCE_SCATTER,
-    REPLACE_IN_BUFFERS,
-    REPLACE_IN_TENSORS,
+    TILED_ADD_FROM_TENSORS,
+    TILED_BUFFERS,
+    TILED_REPLACE_IN_TENSORS,
     SMALL_BUCKET_BYTES,
     SUM,
     HvdxError,

@@ -69,7 +69,7 @@ KERNEL_PACK, KERNEL_REDUCE_SCATTER, KERNEL_ALLGATHER, KERNEL_UNPACK, KERNEL_ROUN
 KERNEL_BROADCAST, KERNEL_RS_AG, KERNEL_FOLD = 5, 6, 7
 KERNEL_PACK_RS, KERNEL_AG_UNPACK = 8, 9
 KERNEL_RING_SMALL, KERNEL_CYCLE_SMALL = 10, 11
-REPLACE_IN_BUFFERS, REPLACE_IN_TENSORS = 0, 1
+TILED_BUFFERS, TILED_REPLACE_IN_TENSORS, TILED_ADD_FROM_TENSORS = 0, 1, 2
 
 
 class Bucket(ctypes.Structure):
@@ -271,11 +271,11 @@ def hvdx_fuse_tile_elems(tensor_dtype: int, buf_dtype: int) -> int:
     return lib.hvdx_fuse_tile_elems(tensor_dtype, buf_dtype)
 
 
-def hvdx_fuse_allreduce_tiled(t0, t1, tensor_dtype: int, buf_dtype: int, nranks: int, op: int, replace: int,
+def hvdx_fuse_allreduce_tiled(t0, t1, tensor_dtype: int, buf_dtype: int, nranks: int, op: int, flags: int,
                               stream: int = 0) -> None:
     """t0, t1 (t1 may be None): (tensors_dev, numel_dev, offset_dev, ntensors, bufs, buf_count,
-    in_tiles_dev, n_in, out_tiles_dev, n_out) each; replace: REPLACE_IN_BUFFERS or
-    REPLACE_IN_TENSORS."""
+    in_tiles_dev, n_in, out_tiles_dev, n_out) each; flags: TILED_BUFFERS, or
+    TILED_REPLACE_IN_TENSORS, optionally | TILED_ADD_FROM_TENSORS."""
     keep = []
 
     def desc(t):
@@ -288,7 +288,7 @@ def hvdx_fuse_allreduce_tiled(t0, t1, tensor_dtype: int, buf_dtype: int, nranks:
     d0 = desc(t0)
     d1 = desc(t1) if t1 is not None else None
     _check(lib.hvdx_fuse_allreduce_tiled(ctypes.addressof(d0), ctypes.addressof(d1) if d1 is not None else None,
-                                         tensor_dtype, buf_dtype, nranks, op, replace, stream))
+                                         tensor_dtype, buf_dtype, nranks, op, flags, stream))
 
 
 def hvdx_fuse_allreduce_small(tensors_dev: int, numel_dev: int, offset_dev: int, ntensors: int, tensor_dtype: int,

@@ -878,14 +878,16 @@ __global__ __launch_bounds__(kTileLanes) void unpack_tiles_kernel(TiledCopy k, i
 // Adding step N-2 and replacing step 0 of chunk c: the owner (rank c-1) completes its
 // sum from the sender's (c-2) buffer, and the finished value goes to the owner's and
 // rank c's tensors.  The owner's copy is not read again and streams; rank c's is the
-// sender's input in replacing step 1 and stays in the caches.
+// sender's input in replacing step 1 and stays in the caches.  OWN_T: the owner's own
+// value is read from its tensors (the adding steps never copied it into its buffer);
+// each lane reads an element there before it writes the result over it.
 #ifndef HVDX_RSAGT_NTL  // non-temporal buffer loads: the buffers are not read again
 #define HVDX_RSAGT_NTL true
 #endif
 #ifndef HVDX_RSAGT_NXT_NTS  // rank c's copy: replacing step 1 reads it
 #define HVDX_RSAGT_NXT_NTS false
 #endif
-template <typename T, int DIV, int U>
+template <typename T, int DIV, int U, bool OWN_T>
 __global__ __launch_bounds__(kTileLanes) void rs_ag_tiles_kernel(TiledCopy k, RingArgs a) {
   using VT = typename Vec<T>::type;
   constexpr int V = Vec<T>::n;
@@ -896,27 +898,43 @@ __global__ __launch_bounds__(kTileLanes) void rs_ag_tiles_kernel(TiledCopy k, Ri
   const int c = tl.chunk;
   const int own = c == 0 ? n - 1 : c - 1;
   const int snd = own == 0 ? n - 1 : own - 1;
-  const T* __restrict__ bo = static_cast<const T*>(k.m.bufs[b].p[own]) + tl.pos;
-  const T* __restrict__ bs = static_cast<const T*>(k.m.bufs[b].p[snd]) + tl.pos;
-  const bool bvec = aligned16(bo) && aligned16(bs);
-  VT mine[U], sent[U];
-#pragma unroll
-  for (int u = 0; u < U; ++u) {  // the buffer loads go out before the tensor pointers arrive
-    const int i = (u * kTileLanes + threadIdx.x) * V;
-    if (bvec && i + V <= tl.len) {
-      mine[u] = ld16<HVDX_RSAGT_NTL>(reinterpret_cast<const VT*>(bo + i));
-      sent[u] = ld16<HVDX_RSAGT_NTL>(reinterpret_cast<const VT*>(bs + i));
-    }
-  }
   const int64_t nt = k.m.ntensors[b];
-  T* __restrict__ d_own = static_cast<T*>(const_cast<void*>(k.m.t[b][(int64_t)own * nt + tl.tensor])) + tl.li;
-  T* __restrict__ d_nxt = static_cast<T*>(const_cast<void*>(k.m.t[b][(int64_t)c * nt + tl.tensor])) + tl.li;
+  const T* bs = static_cast<const T*>(k.m.bufs[b].p[snd]) + tl.pos;
+  const T* bo;  // no __restrict__: with OWN_T it is d_own
+  T* d_own;
+  T* d_nxt;
+  VT mine[U], sent[U];
+  auto load = [&](bool vec) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int i = (u * kTileLanes + threadIdx.x) * V;
+      if (vec && i + V <= tl.len) {
+        mine[u] = ld16<HVDX_RSAGT_NTL>(reinterpret_cast<const VT*>(bo + i));
+        sent[u] = ld16<HVDX_RSAGT_NTL>(reinterpret_cast<const VT*>(bs + i));
+      }
+    }
+  };
+  bool vec;
+  if constexpr (OWN_T) {
+    d_own = static_cast<T*>(const_cast<void*>(k.m.t[b][(int64_t)own * nt + tl.tensor])) + tl.li;
+    d_nxt = static_cast<T*>(const_cast<void*>(k.m.t[b][(int64_t)c * nt + tl.tensor])) + tl.li;
+    bo = d_own;
+    vec = aligned16(bo) && aligned16(bs) && aligned16(d_nxt);
+    load(vec);
+  } else {
+    bo = static_cast<const T*>(k.m.bufs[b].p[own]) + tl.pos;
+    const bool bvec = aligned16(bo) && aligned16(bs);
+    load(bvec);  // the buffer loads go out before the tensor pointers arrive
+    d_own = static_cast<T*>(const_cast<void*>(k.m.t[b][(int64_t)own * nt + tl.tensor])) + tl.li;
+    d_nxt = static_cast<T*>(const_cast<void*>(k.m.t[b][(int64_t)c * nt + tl.tensor])) + tl.li;
+    vec = bvec && aligned16(d_own) && aligned16(d_nxt);
+  }
   auto one = [&](int e) {
     const T v = combine1<DIV>(bo[e], bs[e], a);
     d_own[e] = v;
     d_nxt[e] = v;
   };
-  if (bvec && aligned16(d_own) && aligned16(d_nxt)) {
+  if (vec) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int i = (u * kTileLanes + threadIdx.x) * V;
@@ -930,6 +948,81 @@ __global__ __launch_bounds__(kTileLanes) void rs_ag_tiles_kernel(TiledCopy k, Ri
     }
   } else {
     for (int e = threadIdx.x; e < tl.len; e += kTileLanes) one(e);
+  }
+}
+
+// Adding step s <= N-3 with every rank's own values read from its tensors (the copy-in
+// fused with the step that first reads each chunk): rank c+s+1 adds its own elements of
+// chunk c to what rank c+s sent (its partial sum in its buffer, or at s = 0 its own
+// elements, also from its tensors) and keeps the sum in its buffer.  Over the copy-in's
+// tiles (on the buffer's tile grid); padding is skipped (nothing reads it).  Tensor
+// loads are non-temporal (each element is read once in the adding steps), the sender's
+// partial sum too (read once), the stores cached (the next step reads them).
+#ifndef HVDX_ADDT_TPB
+#define HVDX_ADDT_TPB 2
+#endif
+#ifndef HVDX_ADDT_NTL
+#define HVDX_ADDT_NTL true
+#endif
+#ifndef HVDX_ADDT_NTS
+#define HVDX_ADDT_NTS false
+#endif
+template <typename T, bool FIRST, int TPB, int U>
+__global__ __launch_bounds__(kTileLanes) void add_tiles_kernel(TiledCopy k, int step, int nranks, int64_t ntiles) {
+  using VT = typename Vec<T>::type;
+  constexpr int V = Vec<T>::n;
+  const T* mine[TPB];
+  const T* sent[TPB];
+  T* out[TPB];
+  int len[TPB];
+  bool vec[TPB];
+#pragma unroll
+  for (int j = 0; j < TPB; ++j) {
+    const int64_t g = (int64_t)blockIdx.x * TPB + j;
+    len[j] = 0;
+    mine[j] = nullptr;
+    sent[j] = nullptr;
+    out[j] = nullptr;
+    vec[j] = false;
+    if (g >= ntiles) continue;
+    const int b = g >= k.x0 ? 1 : 0;
+    const hvdx_copy_tile tl = k.tiles[b][b ? g - k.x0 : g];
+    if (tl.tensor < 0) continue;
+    int snd = tl.chunk + step;  // chunk < N and step <= N-3: below 2N
+    if (snd >= nranks) snd -= nranks;
+    const int rcv = snd + 1 == nranks ? 0 : snd + 1;
+    const int64_t nt = k.m.ntensors[b];
+    mine[j] = static_cast<const T*>(k.m.t[b][(int64_t)rcv * nt + tl.tensor]) + tl.li;
+    sent[j] = FIRST ? static_cast<const T*>(k.m.t[b][(int64_t)snd * nt + tl.tensor]) + tl.li
+                    : static_cast<const T*>(k.m.bufs[b].p[snd]) + tl.pos;
+    out[j] = static_cast<T*>(k.m.bufs[b].p[rcv]) + tl.pos;
+    len[j] = tl.len;
+    vec[j] = aligned16(mine[j]) && aligned16(sent[j]) && aligned16(out[j]);
+  }
+  VT x[TPB][U], y[TPB][U];
+#pragma unroll
+  for (int j = 0; j < TPB; ++j)
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int i = (u * kTileLanes + threadIdx.x) * V;
+      if (vec[j] && i + V <= len[j]) {
+        x[j][u] = ld16<HVDX_ADDT_NTL>(reinterpret_cast<const VT*>(mine[j] + i));
+        y[j][u] = ld16<HVDX_ADDT_NTL>(reinterpret_cast<const VT*>(sent[j] + i));
+      }
+    }
+#pragma unroll
+  for (int j = 0; j < TPB; ++j) {
+    if (vec[j]) {
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int i = (u * kTileLanes + threadIdx.x) * V;
+        if (i + V <= len[j]) st16<HVDX_ADDT_NTS>(reinterpret_cast<VT*>(out[j] + i), x[j][u] + y[j][u]);
+        else
+          for (int e = i; e < len[j] && e < i + V; ++e) out[j][e] = mine[j][e] + sent[j][e];
+      }
+    } else {
+      for (int e = threadIdx.x; e < len[j]; e += kTileLanes) out[j][e] = mine[j][e] + sent[j][e];
+    }
   }
 }
 
@@ -1251,20 +1344,41 @@ hipError_t launch_unpack_tiles(const TiledCopy& k, int buf_dtype, int dst_dtype,
   return hipGetLastError();
 }
 
-hipError_t launch_rs_ag_tiles(const TiledCopy& k, const RingArgs& a, int dtype, int divmode, int64_t blocks,
-                              hipStream_t stream) {
+hipError_t launch_rs_ag_tiles(const TiledCopy& k, const RingArgs& a, int dtype, int divmode, bool own_in_tensors,
+                              int64_t blocks, hipStream_t stream) {
   if (blocks < 1 || blocks > 0x7fffffff || a.n < 3) return hipErrorInvalidValue;
   const dim3 grid((unsigned)blocks);
   const dim3 block(kTileLanes);
-#define HVDX_RSAG_T(T, U)                                                                        \
-  do {                                                                                          \
-    if (divmode == DIV_NONE) HVDX_LAUNCH((rs_ag_tiles_kernel<T, DIV_NONE, U>), grid, block, 0, stream, k, a); \
-    else if (divmode == DIV_POW2) HVDX_LAUNCH((rs_ag_tiles_kernel<T, DIV_POW2, U>), grid, block, 0, stream, k, a); \
-    else HVDX_LAUNCH((rs_ag_tiles_kernel<T, DIV_TRUE, U>), grid, block, 0, stream, k, a);       \
+#define HVDX_RSAG_T(T, U, OWN)                                                                           \
+  do {                                                                                                  \
+    if (divmode == DIV_NONE) HVDX_LAUNCH((rs_ag_tiles_kernel<T, DIV_NONE, U, OWN>), grid, block, 0, stream, k, a); \
+    else if (divmode == DIV_POW2) HVDX_LAUNCH((rs_ag_tiles_kernel<T, DIV_POW2, U, OWN>), grid, block, 0, stream, k, a); \
+    else HVDX_LAUNCH((rs_ag_tiles_kernel<T, DIV_TRUE, U, OWN>), grid, block, 0, stream, k, a);           \
   } while (0)
-  if (dtype == HVDX_FLOAT32) HVDX_RSAG_T(float, HVDX_TILE_U32);
-  else HVDX_RSAG_T(_Float16, HVDX_TILE_UH);
+  if (dtype == HVDX_FLOAT32) {
+    if (own_in_tensors) HVDX_RSAG_T(float, HVDX_TILE_U32, true);
+    else HVDX_RSAG_T(float, HVDX_TILE_U32, false);
+  } else {
+    if (own_in_tensors) HVDX_RSAG_T(_Float16, HVDX_TILE_UH, true);
+    else HVDX_RSAG_T(_Float16, HVDX_TILE_UH, false);
+  }
 #undef HVDX_RSAG_T
+  return hipGetLastError();
+}
+
+hipError_t launch_add_tiles(const TiledCopy& k, int dtype, int nranks, int step, int64_t ntiles, hipStream_t stream) {
+  if (ntiles < 1 || ntiles > 0x7fffffff || nranks < 3 || step < 0 || step > nranks - 3) return hipErrorInvalidValue;
+  constexpr int TPB = HVDX_ADDT_TPB;
+  const dim3 grid((unsigned)((ntiles + TPB - 1) / TPB));
+  const dim3 block(kTileLanes);
+  const bool first = step == 0;
+  if (dtype == HVDX_FLOAT32) {
+    if (first) HVDX_LAUNCH((add_tiles_kernel<float, true, TPB, HVDX_TILE_U32>), grid, block, 0, stream, k, step, nranks, ntiles);
+    else HVDX_LAUNCH((add_tiles_kernel<float, false, TPB, HVDX_TILE_U32>), grid, block, 0, stream, k, step, nranks, ntiles);
+  } else {
+    if (first) HVDX_LAUNCH((add_tiles_kernel<_Float16, true, TPB, HVDX_TILE_UH>), grid, block, 0, stream, k, step, nranks, ntiles);
+    else HVDX_LAUNCH((add_tiles_kernel<_Float16, false, TPB, HVDX_TILE_UH>), grid, block, 0, stream, k, step, nranks, ntiles);
+  }
   return hipGetLastError();
 }
 

@@ -819,11 +819,13 @@ int64_t hvdx_fuse_copy_tiles(const int64_t* numel, const int64_t* offset, int nt
 }
 
 int hvdx_fuse_allreduce_tiled(const hvdx_tiled_bucket* t0, const hvdx_tiled_bucket* t1, int tensor_dtype,
-                              int buf_dtype, int nranks, int op, int replace, void* stream) {
+                              int buf_dtype, int nranks, int op, int flags, void* stream) {
   static const char* what = "hvdx_fuse_allreduce_tiled";
   if (!t0) return fail(HVDX_ERR_INVALID, "%s: the first bucket is NULL", what);
-  if (replace != HVDX_REPLACE_IN_BUFFERS && replace != HVDX_REPLACE_IN_TENSORS)
-    return fail(HVDX_ERR_INVALID, "%s: unknown replace mode %d", what, replace);
+  if (flags & ~(HVDX_TILED_REPLACE_IN_TENSORS | HVDX_TILED_ADD_FROM_TENSORS))
+    return fail(HVDX_ERR_INVALID, "%s: unknown flags 0x%x", what, flags);
+  const bool replace_t = flags & HVDX_TILED_REPLACE_IN_TENSORS;
+  const bool add_t = flags & HVDX_TILED_ADD_FROM_TENSORS;
   for (const hvdx_tiled_bucket* t : {t0, t1}) {
     if (!t) continue;
     const int rc = check_fusion(t->b.tensors, t->b.numel, t->b.offset, t->b.ntensors, tensor_dtype, t->b.bufs,
@@ -835,8 +837,10 @@ int hvdx_fuse_allreduce_tiled(const hvdx_tiled_bucket* t0, const hvdx_tiled_buck
   }
   if (op != HVDX_SUM && op != HVDX_AVERAGE) return fail(HVDX_ERR_INVALID, "%s: unknown op %d", what, op);
   if (nranks < 3) return fail(HVDX_ERR_UNSUPPORTED, "%s: needs 3 or more ranks", what);
-  if (replace == HVDX_REPLACE_IN_TENSORS && tensor_dtype != buf_dtype)
+  if (replace_t && tensor_dtype != buf_dtype)
     return fail(HVDX_ERR_UNSUPPORTED, "%s: replacing in the tensors needs tensors of the buffer's type", what);
+  if (add_t && !replace_t)
+    return fail(HVDX_ERR_UNSUPPORTED, "%s: adding from the tensors needs replacing in the tensors", what);
   const int es = elem_size(buf_dtype);
   if (t1 && t0->b.buf_count > 0 && t1->b.buf_count > 0) {  // both run at once: all 2N buffers disjoint
     std::vector<std::pair<uintptr_t, uintptr_t>> rg;
@@ -868,22 +872,34 @@ int hvdx_fuse_allreduce_tiled(const hvdx_tiled_bucket* t0, const hvdx_tiled_buck
     k.m.bufs[i] = rank_ptrs(run[i]->b.bufs, nranks);
     k.m.count[i] = run[i]->b.buf_count;
   }
-  {
-    TimedLaunch timed(HVDX_KERNEL_PACK_RS, 0, nranks, buf_dtype, HVDX_COMPRESS_NONE, both, st);
-    TimedLaunch timed_phase(HVDX_KERNEL_PACK_RS, 0, nranks, buf_dtype, HVDX_COMPRESS_NONE, both, st, -1, true);
-    k.tiles[0] = run[0]->in_tiles;
-    k.tiles[1] = nrun > 1 ? run[1]->in_tiles : nullptr;
-    k.x0 = run[0]->n_in;
-    const hipError_t e = hvdx::launch_pack_tiles(k, tensor_dtype, buf_dtype, nranks, n_in, st);
-    if (e != hipSuccess) return hip_fail(e, "tiled copy-in launch");
-  }
+  k.tiles[0] = run[0]->in_tiles;
+  k.tiles[1] = nrun > 1 ? run[1]->in_tiles : nullptr;
+  k.x0 = run[0]->n_in;
   int rc;
-  if (replace == HVDX_REPLACE_IN_TENSORS) {
-    if (nrun == 2) rc = run_pair_steps(&run[0]->b, &run[1]->b, buf_dtype, op, HVDX_KERNEL_REDUCE_SCATTER, 1, last,
-                                       nranks, st);
-    else rc = run_steps(run[0]->b.bufs, nranks, run[0]->b.buf_count, buf_dtype, op, HVDX_COMPRESS_NONE,
-                        HVDX_PHASE_REDUCE_SCATTER, 1, last, nullptr, st);
-    if (rc) return rc;
+  if (add_t) {  // adding steps 0 .. N-3 with every rank's own values read from its tensors
+    TimedLaunch timed_phase(HVDX_KERNEL_REDUCE_SCATTER, 0, nranks, buf_dtype, HVDX_COMPRESS_NONE, both, st, -1, true,
+                            last);
+    for (int s = 0; s < last; ++s) {
+      TimedLaunch timed(HVDX_KERNEL_REDUCE_SCATTER, s, nranks, buf_dtype, HVDX_COMPRESS_NONE, both, st);
+      const hipError_t e = hvdx::launch_add_tiles(k, buf_dtype, nranks, s, n_in, st);
+      if (e != hipSuccess) return hip_fail(e, "adding step from the tensors");
+    }
+  } else {
+    {
+      TimedLaunch timed(HVDX_KERNEL_PACK_RS, 0, nranks, buf_dtype, HVDX_COMPRESS_NONE, both, st);
+      TimedLaunch timed_phase(HVDX_KERNEL_PACK_RS, 0, nranks, buf_dtype, HVDX_COMPRESS_NONE, both, st, -1, true);
+      const hipError_t e = hvdx::launch_pack_tiles(k, tensor_dtype, buf_dtype, nranks, n_in, st);
+      if (e != hipSuccess) return hip_fail(e, "tiled copy-in launch");
+    }
+    if (replace_t) {
+      if (nrun == 2) rc = run_pair_steps(&run[0]->b, &run[1]->b, buf_dtype, op, HVDX_KERNEL_REDUCE_SCATTER, 1, last,
+                                         nranks, st);
+      else rc = run_steps(run[0]->b.bufs, nranks, run[0]->b.buf_count, buf_dtype, op, HVDX_COMPRESS_NONE,
+                          HVDX_PHASE_REDUCE_SCATTER, 1, last, nullptr, st);
+      if (rc) return rc;
+    }
+  }
+  if (replace_t) {
     if (n_out == 0) return HVDX_OK;  // every tensor empty: nothing to deliver
     k.tiles[0] = run[0]->out_tiles;
     k.tiles[1] = nrun > 1 ? run[1]->out_tiles : nullptr;
@@ -892,7 +908,7 @@ int hvdx_fuse_allreduce_tiled(const hvdx_tiled_bucket* t0, const hvdx_tiled_buck
       TimedLaunch timed(HVDX_KERNEL_RS_AG, last, nranks, buf_dtype, HVDX_COMPRESS_NONE, both, st);
       TimedLaunch timed_phase(HVDX_KERNEL_RS_AG, last, nranks, buf_dtype, HVDX_COMPRESS_NONE, both, st, -1, true);
       const hipError_t e = hvdx::launch_rs_ag_tiles(k, ring_args(nranks, run[0]->b.buf_count, last), buf_dtype,
-                                                    div_mode(op, nranks), n_out, st);
+                                                    div_mode(op, nranks), add_t, n_out, st);
       if (e != hipSuccess) return hip_fail(e, "replacing step 0 into the tensors");
     }
     TimedLaunch timed_phase(HVDX_KERNEL_ALLGATHER, 1, nranks, buf_dtype, HVDX_COMPRESS_NONE, both, st, -1, true,

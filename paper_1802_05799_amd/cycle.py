@@ -68,7 +68,7 @@ class FusedAllreduce:
                  threshold_bytes: int = L.DEFAULT_FUSION_THRESHOLD, align_bytes: int = L.DEFAULT_FUSION_ALIGN,
                  schedule: str = "ring", fuse_boundary: bool = True,
                  small_bucket_bytes: int = L.SMALL_BUCKET_BYTES, pair_buckets: bool = True, tiled: bool = True,
-                 replace_in_tensors: bool = True):
+                 replace_in_tensors: bool = True, add_from_tensors: bool = True):
         """schedule "ring" runs the ring's 2(N-1) steps; "fold" computes the same bits
         with hvdx_fold_allreduce (no per-step messages: a one-GPU bound, not the ring).
         With fuse_boundary (ring schedule, N >= 3) a fusion buffer's copy-in runs with
@@ -82,8 +82,10 @@ class FusedAllreduce:
         (hvdx_fuse_copy_tiles, hvdx_fuse_allreduce_tiled) instead of finding each stretch's
         tensors in the kernel.  With replace_in_tensors (tiled, no compression) their
         replacing steps deliver each chunk straight into the receiving rank's tensors and
-        forward it from there, so no copy-out follows (HVDX_REPLACE_IN_TENSORS); the
-        fusion buffers then end as scratch.  All give the same bits."""
+        forward it from there, so no copy-out follows (HVDX_TILED_REPLACE_IN_TENSORS);
+        with add_from_tensors as well, each adding step reads the receiver's own elements
+        from its tensors, so no copy-in either (HVDX_TILED_ADD_FROM_TENSORS) and the
+        fusion buffers hold only received partial sums.  All give the same bits."""
         if schedule not in ("ring", "fold"):
             raise ValueError("schedule must be 'ring' or 'fold'")
         self.schedule = schedule
@@ -165,7 +167,9 @@ class FusedAllreduce:
                     tabs += [host.to(dev), k]
                 b.tiles = tuple(tabs)
         in_tensors = replace_in_tensors and self.tiled and self.dtype == self.buf_dtype
-        self.replace = L.REPLACE_IN_TENSORS if in_tensors else L.REPLACE_IN_BUFFERS
+        self.tiled_flags = L.TILED_BUFFERS
+        if in_tensors:
+            self.tiled_flags = L.TILED_REPLACE_IN_TENSORS | (L.TILED_ADD_FROM_TENSORS if add_from_tensors else 0)
         self._buf_ptrs = [x.data_ptr() for x in self.bufs]
         self._buf2_ptrs = [x.data_ptr() for x in self.bufs2]
         _timeline.start_from_env()
@@ -211,7 +215,7 @@ class FusedAllreduce:
         (or, for a small bucket, all in one launch)."""
         if self.tiled and not b.small:
             L.hvdx_fuse_allreduce_tiled(self.tiled_desc(b, self._buf_ptrs), None, self.dtype, self.buf_dtype,
-                                        self.nranks, self.op, self.replace, stream)
+                                        self.nranks, self.op, self.tiled_flags, stream)
             return
         fn = L.hvdx_fuse_allreduce_small if b.small else L.hvdx_fuse_allreduce
         fn(b.ptrs_dev.data_ptr(), b.numel_dev.data_ptr(), b.offset_dev.data_ptr(), len(b.tensors), self.dtype,
@@ -225,7 +229,7 @@ class FusedAllreduce:
         """Two fusion buffers' cycles with every launch serving both."""
         if self.tiled:
             L.hvdx_fuse_allreduce_tiled(self.tiled_desc(a, self._buf_ptrs), self.tiled_desc(b, self._buf2_ptrs),
-                                        self.dtype, self.buf_dtype, self.nranks, self.op, self.replace, stream)
+                                        self.dtype, self.buf_dtype, self.nranks, self.op, self.tiled_flags, stream)
             return
         desc = [(x.ptrs_dev.data_ptr(), x.numel_dev.data_ptr(), x.offset_dev.data_ptr(), len(x.tensors), bufs,
                  x.count) for x, bufs in ((a, self._buf_ptrs), (b, self._buf2_ptrs))]
@@ -236,7 +240,8 @@ class FusedAllreduce:
         kind "pack", "pack_rs" (copy-in with adding step 0), "rs", "rs_ag" (adding
         step N-2 fused with replacing step 0), "ag", "ag_unpack" (replacing step N-2
         with copy-out; with the replacing steps in the tensors, "rs_ag" and "ag" 1..N-2
-        deliver into the tensors and no copy-out follows), "unpack", "fold", "ring"
+        deliver into the tensors and no copy-out follows; with the adding steps from the
+        tensors, "rs" 0..N-3 replace "pack_rs"), "unpack", "fold", "ring"
         (the one-rank compressed round trip),
         "cycle_small" or "ring_small" (a small bucket's whole cycle in one launch).
         A launch that serves a pair of buckets names both: (kind, (i, j), step)."""
@@ -279,8 +284,12 @@ class FusedAllreduce:
 
     def _fused_sequence(self, bi):
         n = self.nranks
-        out = [("pack_rs", bi, 0)] + [("rs", bi, s) for s in range(1, n - 2)] + [("rs_ag", bi, n - 2)]
-        if self.replace == L.REPLACE_IN_TENSORS:
+        if self.tiled_flags & L.TILED_ADD_FROM_TENSORS:
+            out = [("rs", bi, s) for s in range(n - 2)]
+        else:
+            out = [("pack_rs", bi, 0)] + [("rs", bi, s) for s in range(1, n - 2)]
+        out.append(("rs_ag", bi, n - 2))
+        if self.tiled_flags & L.TILED_REPLACE_IN_TENSORS:
             return out + [("ag", bi, s) for s in range(1, n - 1)]
         return out + [("ag", bi, s) for s in range(1, n - 2)] + [("ag_unpack", bi, n - 2)]
 

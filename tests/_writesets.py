@@ -27,6 +27,8 @@ class Knobs:
     replace_sender: int = -1  # replacing step s into the tensors reads rank `chunk + s + this` (-1)
     rs_ag_next: int = 0  # the fused step into the tensors also writes rank `chunk + this` (0)
     tile_block_stride: int = 0  # block b of a replacing step takes tiles b*this + j (0: tiles per block)
+    add_sender: int = 0  # adding step s from the tensors: the sender of chunk c is rank c+s+this (0)
+    fused_own_from_buffer: bool = False  # the fused step reads the owner's value from its buffer (False)
 
 
 K = Knobs()
@@ -607,3 +609,92 @@ def tiled_replace(kind, n, count, numel, tiles, V, step=0, aligned=True, U=1, k=
             add(tr[snd][t], li + e, "read")
             add(tw[(snd + 1) % n][t], li + e)
     return tw, tr, br
+
+
+# ---- the whole cycle with the adding steps from the tensors, as data -------------------
+def block_tiles(ntiles, tpb, stride=0):
+    """Tile indices in the order a grid of ceil(ntiles / tpb) blocks takes them, block b
+    taking tiles b*tpb + j (b*stride + j with a planted stride)."""
+    st = stride or tpb
+    return [g for b in range(-(-ntiles // tpb)) for g in (b * st + j for j in range(tpb)) if g < ntiles]
+
+
+class Launch:
+    """Reads and writes of one launch on named arrays, applied after the launch, with the
+    check that no element is both read and written by it (no order between its blocks)."""
+
+    def __init__(self):
+        self.reads, self.writes = [], []
+
+    def read(self, arr, idx):
+        self.reads.append((id(arr), arr, np.asarray(idx, np.int64)))
+        return arr[idx]
+
+    def write(self, arr, idx, val):
+        self.writes.append((id(arr), arr, np.asarray(idx, np.int64), np.asarray(val)))
+
+    def commit(self):
+        written = {}
+        for key, arr, idx, _ in self.writes:
+            m = written.setdefault(key, np.zeros(arr.size, np.int64))
+            np.add.at(m, idx, 1)
+        for m in written.values():
+            assert (m <= 1).all(), "an element written twice by one launch"
+        for key, arr, idx in self.reads:
+            if key in written:
+                assert not written[key][idx].any(), "an element read and written by one launch"
+        for _, arr, idx, val in self.writes:
+            arr[idx] = val
+
+
+def dataflow_cycle(n, count, numel, tin, tout, V, U=1, aligned=True, k=K, tpb=2):
+    """The fused cycle with HVDX_TILED_REPLACE_IN_TENSORS | HVDX_TILED_ADD_FROM_TENSORS on
+    values that record which ranks' inputs they hold (bit r for rank r): add_tiles_kernel
+    for adding steps 0..N-3 over the copy-in's tiles, rs_ag_tiles_kernel<..., OWN_T> and
+    ag_tiles_kernel over the copy-out's, each launch's reads and writes replayed from the
+    kernels' index arithmetic.  Checks that no value is counted twice, that each adding
+    step reads a rank's own elements while they still hold its input, that the fused
+    step completes every sum and that the replacing steps forward only complete sums.
+    Returns every rank's tensors."""
+    full = (1 << n) - 1
+    T = [[np.full(m, 1 << r, np.int64) for m in numel] for r in range(n)]
+    B = [np.zeros(count, np.int64) for _ in range(n)]
+    for step in range(n - 2):
+        L = Launch()
+        for g in block_tiles(len(tin), tpb, k.tile_block_stride):
+            pos, li, t, length, c = tin[g]
+            if t < 0:
+                continue
+            e = tile_lanes(length, V, aligned, U) + k.lane_shift
+            snd = (c + step + k.add_sender) % n
+            rcv = (snd + 1) % n
+            own = L.read(T[rcv][t], li + e)
+            assert (own == 1 << rcv).all(), f"step {step}: rank {rcv}'s own elements no longer its input"
+            sent = L.read(T[snd][t], li + e) if step == 0 else L.read(B[snd], pos + e)
+            assert not (own & sent).any(), f"step {step}: a rank's value counted twice"
+            L.write(B[rcv], pos + e, own | sent)
+        L.commit()
+    L = Launch()
+    for pos, li, t, length, c in tout:
+        e = tile_lanes(length, V, aligned, U) + k.lane_shift
+        own = (c - 1) % n
+        snd = (own - 1) % n
+        # the owner's elements: each read and then overwritten by the same lane, so not a
+        # read of the launch's own output (kept out of the race check)
+        mine = B[own][pos + e] if k.fused_own_from_buffer else T[own][t][li + e]
+        sent = L.read(B[snd], pos + e)
+        assert not (mine & sent).any() and ((mine | sent) == full).all(), "the fused step's sum is not complete"
+        L.write(T[own][t], li + e, mine | sent)
+        L.write(T[c][t], li + e, mine | sent)
+    L.commit()
+    for step in range(1, n - 1):
+        L = Launch()
+        for g in block_tiles(len(tout), tpb, k.tile_block_stride):
+            pos, li, t, length, c = tout[g]
+            e = tile_lanes(length, V, aligned, U) + k.lane_shift
+            snd = (c + step + k.replace_sender) % n
+            v = L.read(T[snd][t], li + e)
+            assert (v == full).all(), f"replacing step {step} forwards an incomplete sum"
+            L.write(T[(snd + 1) % n][t], li + e, v)
+        L.commit()
+    return T

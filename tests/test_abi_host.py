@@ -243,19 +243,23 @@ def test_pair_argument_errors():
 
 
 def test_tiled_argument_errors():
-    """hvdx_fuse_allreduce_tiled refuses an unknown replace mode, and replacing in the
-    tensors when they are not of the buffer's type, before any launch."""
+    """hvdx_fuse_allreduce_tiled refuses unknown flags, the tensor modes when the tensors
+    are not of the buffer's type, and adding from the tensors alone, before any launch."""
     ft = hv.hvdx_fuse_allreduce_tiled
     b3 = bufs(3, 64)
     d0 = (FAKE, FAKE, FAKE, 3, b3, 64, FAKE, 4, FAKE, 4)
-    assert status_of(ft, d0, None, hv.FLOAT32, hv.FLOAT32, 3, hv.SUM, 2) == hv.ERR_INVALID
+    both = hv.TILED_REPLACE_IN_TENSORS | hv.TILED_ADD_FROM_TENSORS
+    assert status_of(ft, d0, None, hv.FLOAT32, hv.FLOAT32, 3, hv.SUM, 4) == hv.ERR_INVALID
     assert status_of(ft, d0, None, hv.FLOAT32, hv.FLOAT32, 3, hv.SUM, -1) == hv.ERR_INVALID
-    assert status_of(ft, d0, None, hv.FLOAT32, hv.FLOAT16, 3, hv.SUM, hv.REPLACE_IN_TENSORS) == hv.ERR_UNSUPPORTED
-    assert status_of(ft, d0, None, hv.FLOAT32, hv.FLOAT32, 2, hv.SUM, hv.REPLACE_IN_TENSORS) == hv.ERR_UNSUPPORTED
-    assert status_of(ft, (FAKE, FAKE, FAKE, 3, b3, 64, FAKE, 4, 0, 4), None, hv.FLOAT32, hv.FLOAT32, 3, hv.SUM,
-                     hv.REPLACE_IN_TENSORS) == hv.ERR_INVALID  # the copy-out tiles missing
-    assert status_of(ft, (FAKE, FAKE, FAKE, 3, b3, 0, FAKE, 0, FAKE, 0), None, hv.FLOAT32, hv.FLOAT32, 3, hv.SUM,
-                     hv.REPLACE_IN_TENSORS) == hv.OK  # an empty bucket: nothing launched
+    for flags in (hv.TILED_REPLACE_IN_TENSORS, both):
+        assert status_of(ft, d0, None, hv.FLOAT32, hv.FLOAT16, 3, hv.SUM, flags) == hv.ERR_UNSUPPORTED
+        assert status_of(ft, d0, None, hv.FLOAT32, hv.FLOAT32, 2, hv.SUM, flags) == hv.ERR_UNSUPPORTED
+        assert status_of(ft, (FAKE, FAKE, FAKE, 3, b3, 64, FAKE, 4, 0, 4), None, hv.FLOAT32, hv.FLOAT32, 3, hv.SUM,
+                         flags) == hv.ERR_INVALID  # the copy-out tiles missing
+        assert status_of(ft, (FAKE, FAKE, FAKE, 3, b3, 0, FAKE, 0, FAKE, 0), None, hv.FLOAT32, hv.FLOAT32, 3, hv.SUM,
+                         flags) == hv.OK  # an empty bucket: nothing launched
+    assert status_of(ft, d0, None, hv.FLOAT32, hv.FLOAT32, 3, hv.SUM,
+                     hv.TILED_ADD_FROM_TENSORS) == hv.ERR_UNSUPPORTED  # needs the replacing steps in the tensors
 
 
 def test_fused_allreduce_rejects_overlapping_tensors():

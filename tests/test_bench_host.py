@@ -15,9 +15,9 @@ sys.path.insert(0, ROOT)
 import bench  # noqa: E402
 
 
-def fake_allreduce(nranks, numel, buckets, dtype=0, buf_dtype=0, compress=False, replace=0):
+def fake_allreduce(nranks, numel, buckets, dtype=0, buf_dtype=0, compress=False, flags=0):
     return SimpleNamespace(nranks=nranks, numel=numel, dtype=dtype, buf_dtype=buf_dtype, compress=compress,
-                           replace=replace,
+                           tiled_flags=flags,
                            buckets=[SimpleNamespace(tensors=t, count=c, direct=d) for t, c, d in buckets])
 
 
@@ -63,7 +63,7 @@ def test_replacing_into_tensors_bytes():
     buffer element (the copy-out's N reads and N writes, less one replacing step's read
     and write, less the padding the fused step and the replacing steps no longer move)."""
     n, data, count = 8, 1000, 1003
-    ar = fake_allreduce(n, [data, 50], [([0], count, False), ([1], 50, True)], replace=bench.REPLACE_IN_TENSORS)
+    ar = fake_allreduce(n, [data, 50], [([0], count, False), ([1], 50, True)], flags=bench.TILED_REPLACE_IN_TENSORS)
     assert bench.kernel_bytes(ar, "rs_ag", 0, n - 2) == 4 * 4 * data
     assert bench.kernel_bytes(ar, "ag", 0, 3) == 2 * 4 * data
     assert bench.kernel_bytes(ar, "ag", 1, 3) == 2 * 4 * 50 and bench.kernel_bytes(ar, "rs_ag", 1, n - 2) == 4 * 4 * 50
@@ -75,6 +75,19 @@ def test_replacing_into_tensors_bytes():
         + [("ag", s) for s in range(1, n - 2)] + [("ag_unpack", n - 2)]
     buffers = sum(bench.kernel_bytes(ab, k, 0, s) for k, s in launches)
     assert buffers - into == 2 * (n - 1) * 4 * count
+
+
+def test_adding_from_tensors_bytes():
+    """With the adding steps reading each receiver's own elements from its tensors as well,
+    a cycle moves only the ring's messages: 3 elements per adding step, 4 in the fused step,
+    2 per replacing step, each over the tensors' elements (5N-6 per element in all)."""
+    n, data, count = 8, 1000, 1003
+    flags = bench.TILED_REPLACE_IN_TENSORS | bench.TILED_ADD_FROM_TENSORS
+    ar = fake_allreduce(n, [data, 50], [([0], count, False), ([1], 50, True)], flags=flags)
+    assert bench.kernel_bytes(ar, "rs", 0, 0) == bench.kernel_bytes(ar, "rs", 0, 3) == 3 * 4 * data
+    assert bench.kernel_bytes(ar, "rs", 1, 3) == 3 * 4 * 50  # a direct tensor's ring is not affected
+    launches = [("rs", s) for s in range(n - 2)] + [("rs_ag", n - 2)] + [("ag", s) for s in range(1, n - 1)]
+    assert sum(bench.kernel_bytes(ar, k, 0, s) for k, s in launches) == (5 * n - 6) * 4 * data
 
 
 def test_a_launch_serving_two_buckets_counts_both():

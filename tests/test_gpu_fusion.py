@@ -118,25 +118,29 @@ CYCLE_CASES = [
 ]
 
 
-@pytest.mark.parametrize("mode", ["ring", "ring-misaligned", "ring-buffers", "ring-lookup", "ring-one-launch",
-                                  "ring-separate", "fold"])
+@pytest.mark.parametrize("mode", ["ring", "ring-misaligned", "ring-copy-in", "ring-buffers", "ring-lookup",
+                                  "ring-one-launch", "ring-separate", "fold"])
 @pytest.mark.parametrize("case", range(len(CYCLE_CASES)))
 def test_fused_allreduce_matches_oracle(case, mode):
-    """"ring": the fused boundary with tile-driven copies, the replacing steps delivering
-    into the tensors when nothing is compressed; "ring-misaligned": the same with tensors
-    at odd element offsets (the element paths); "ring-buffers": the replacing steps in the
-    fusion buffers, then the copy-out; "ring-lookup": the copies that find their tensors
-    in the kernel (hvdx_fuse_allreduce, hvdx_fuse_allreduce_pair)."""
+    """"ring": the fused boundary, tile-driven, with (when nothing is compressed) the adding
+    steps reading the ranks' own values from their tensors and the replacing steps
+    delivering into them; "ring-misaligned": the same with tensors at odd element offsets
+    (the element paths); "ring-copy-in": the copy-in fused with adding step 0, the rest
+    of the adding steps in the buffers, the replacing steps into the tensors;
+    "ring-buffers": the ring in the fusion buffers between the fused copies;
+    "ring-lookup": the copies that find their tensors in the kernel (hvdx_fuse_allreduce,
+    hvdx_fuse_allreduce_pair)."""
     numel, n, threshold, compress, op = CYCLE_CASES[case]
     rng = np.random.default_rng(300 + case)
     host, dev, keep = make_tensors(rng, n, numel, np.float32, misalign=mode == "ring-misaligned")
     say(f"cycle case={case} n={n} threshold={threshold} compress={compress} mode={mode}")
     ar = hv.FusedAllreduce(dev, op=op, compress=compress, threshold_bytes=threshold,
                            schedule="fold" if mode == "fold" else "ring",
-                           fuse_boundary=mode in ("ring", "ring-misaligned", "ring-buffers", "ring-lookup",
-                                                  "ring-one-launch"),
+                           fuse_boundary=mode in ("ring", "ring-misaligned", "ring-copy-in", "ring-buffers",
+                                                  "ring-lookup", "ring-one-launch"),
                            small_bucket_bytes=hv.SMALL_BUCKET_BYTES if mode == "ring-one-launch" else 0,
-                           tiled=mode != "ring-lookup", replace_in_tensors=mode != "ring-buffers")
+                           tiled=mode != "ring-lookup", replace_in_tensors=mode != "ring-buffers",
+                           add_from_tensors=mode not in ("ring-copy-in", "ring-buffers"))
     ar()
     torch.cuda.synchronize()
     want = allreduce.allreduce(host, op, compress=compress, threshold=threshold)

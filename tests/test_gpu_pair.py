@@ -38,12 +38,14 @@ def test_pairs_match_oracle_and_single_cycles(case):
     host = [[(rng.standard_normal(k) * 0.01).astype(np.float32) for k in numel] for _ in range(n)]
     want1 = allreduce.allreduce(host, op, compress=compress, threshold=threshold)
     want2 = allreduce.allreduce(want1, op, compress=compress, threshold=threshold)
-    for pair, tiled, into in ((True, True, True), (False, True, True), (True, True, False), (False, True, False),
-                              (True, False, False), (False, False, False)):
+    for pair, tiled, into, add in ((True, True, True, True), (False, True, True, True), (True, True, True, False),
+                                   (False, True, True, False), (True, True, False, False), (False, True, False, False),
+                                   (True, False, False, False), (False, False, False, False)):
         dev = [[torch.from_numpy(x).cuda() for x in row] for row in host]
         ar = hv.FusedAllreduce(dev, op=op, compress=compress, threshold_bytes=threshold, small_bucket_bytes=0,
-                               pair_buckets=pair, tiled=tiled, replace_in_tensors=into)
-        assert ar.replace == (hv.REPLACE_IN_TENSORS if into and not compress else hv.REPLACE_IN_BUFFERS)
+                               pair_buckets=pair, tiled=tiled, replace_in_tensors=into, add_from_tensors=add)
+        want_flags = 0 if compress or not into else hv.TILED_REPLACE_IN_TENSORS | (hv.TILED_ADD_FROM_TENSORS * add)
+        assert ar.tiled_flags == want_flags
         got_pairs = [(i, b.partner) for i, b in enumerate(ar.buckets) if b.pair == 1]
         assert got_pairs == (pairs if pair else [])
         for rep, want in enumerate((want1, want2)):  # the second call reduces the first's result again
@@ -52,7 +54,7 @@ def test_pairs_match_oracle_and_single_cycles(case):
             for r in range(n):
                 for t in range(len(numel)):
                     assert_bits_equal(dev[r][t].cpu().numpy(), want[r][t],
-                                      f"pair={pair} tiled={tiled} into={into} call {rep} rank {r} t {t}")
+                                      f"pair={pair} tiled={tiled} flags={want_flags} call {rep} rank {r} t {t}")
 
 
 def test_pair_entry_point_directly():

@@ -20,13 +20,17 @@ def tensors(n, numel, seed=0):
     return [[torch.from_numpy((g.standard_normal(k) * 0.01).astype(np.float32)).cuda() for k in numel] for _ in range(n)]
 
 
-@pytest.mark.parametrize("fuse_boundary,into", [(True, True), (True, False), (False, True)],
-                         ids=["fused-boundary", "fused-boundary-replace-in-buffers", "separate"])
-def test_records_follow_launches(fuse_boundary, into):
-    say(f"timeline records fuse_boundary={fuse_boundary} replace_in_tensors={into}")
+MODES = {"fused-boundary": (True, True, True), "fused-boundary-copy-in": (True, True, False),
+         "fused-boundary-buffers": (True, False, False), "separate": (False, True, True)}
+
+
+@pytest.mark.parametrize("mode", list(MODES))
+def test_records_follow_launches(mode):
+    fuse_boundary, into, add = MODES[mode]
+    say(f"timeline records {mode}")
     per_rank = tensors(5, [7, 4000, 100, 30000, 5])
     ar = hv.FusedAllreduce(per_rank, op="average", threshold_bytes=40000, fuse_boundary=fuse_boundary,
-                           small_bucket_bytes=0, replace_in_tensors=into)
+                           small_bucket_bytes=0, replace_in_tensors=into, add_from_tensors=add)
     sid = torch.cuda.current_stream().cuda_stream
     launches = ar.kernel_sequence()
     with hv.Timeline(capacity=1000) as tl:
@@ -83,23 +87,26 @@ def test_environment_variable_writes_trace(tmp_path):
     subprocess.run([sys.executable, "-c", code], env=env, check=True, timeout=120)
     trace = json.loads(path.read_text())
     names = [e["name"] for e in trace["traceEvents"] if e["ph"] == "X" and e["tid"] == 0]
-    # the replacing steps deliver into the tensors: no copy-out after replacing step 2
-    assert names == ["copy in + reduce-scatter 0", "reduce-scatter 1", "reduce-scatter + allgather 2",
-                     "allgather 1", "allgather 2"] * 2
+    # the adding steps read the tensors (no copy-in), the replacing steps write them (no copy-out)
+    assert names == ["reduce-scatter 0", "reduce-scatter 1", "reduce-scatter + allgather 2", "allgather 1",
+                     "allgather 2"] * 2
 
 
-@pytest.mark.parametrize("fuse_boundary,into", [(True, True), (True, False), (False, True)],
-                         ids=["fused-boundary", "fused-boundary-replace-in-buffers", "separate"])
-def test_per_phase_records(fuse_boundary, into):
+@pytest.mark.parametrize("mode", list(MODES))
+def test_per_phase_records(mode):
+    fuse_boundary, into, add = MODES[mode]
     per_rank = tensors(6, [7, 4000, 100, 30000, 5])
     ar = hv.FusedAllreduce(per_rank, op="average", threshold_bytes=40000, fuse_boundary=fuse_boundary,
-                           small_bucket_bytes=0, replace_in_tensors=into)
+                           small_bucket_bytes=0, replace_in_tensors=into, add_from_tensors=add)
     with hv.Timeline(capacity=100, per_phase=True) as tl:
         ar()
     got = [(r["kind"], r["step"], r["launches"]) for r in tl.records]
     want = []
     for bi, b in enumerate(ar.buckets):
         if b.pair == 2:  # ran together with an earlier bucket: that pair's records cover it
+            continue
+        if fuse_boundary and not b.direct and add:  # steps 0-3 from the tensors, 4 + 0, steps 1-4 into them
+            want += [(1, 0, 4), (6, 4, 1), (2, 1, 4)]
             continue
         if fuse_boundary and not b.direct and into:  # copy-in + step 0, steps 1-3, 4 + 0, steps 1-4
             want += [(8, 0, 1), (1, 1, 3), (6, 4, 1), (2, 1, 4)]

@@ -75,28 +75,34 @@ def check2_on_device(w, storage, starts):
 
 
 @pytest.mark.parametrize(
-    "name,threshold,fuse_boundary,into",
-    [("tiny", 64 << 20, True, True), ("resnet50", 64 << 20, True, True), ("inceptionv3", 64 << 20, True, True),
-     ("vgg16", 64 << 20, True, True), ("vgg16fp16", 64 << 20, True, True), ("resnet50", 0, True, True),
-     ("inceptionv3", 1 << 20, True, True), ("resnet50", 64 << 20, True, False), ("vgg16", 64 << 20, True, False),
-     ("resnet50", 64 << 20, False, True), ("vgg16", 64 << 20, False, True), ("vgg16fp16", 64 << 20, False, True)],
+    "name,threshold,fuse_boundary,mode",
+    [("tiny", 64 << 20, True, "tensors"), ("resnet50", 64 << 20, True, "tensors"),
+     ("inceptionv3", 64 << 20, True, "tensors"), ("vgg16", 64 << 20, True, "tensors"),
+     ("vgg16fp16", 64 << 20, True, "tensors"), ("resnet50", 0, True, "tensors"),
+     ("inceptionv3", 1 << 20, True, "tensors"), ("resnet50", 64 << 20, True, "copy-in"),
+     ("resnet50", 64 << 20, True, "buffers"), ("vgg16", 64 << 20, True, "buffers"),
+     ("resnet50", 64 << 20, False, "tensors"), ("vgg16", 64 << 20, False, "tensors"),
+     ("vgg16fp16", 64 << 20, False, "tensors")],
     ids=["tiny", "resnet50", "inceptionv3", "vgg16", "vgg16fp16", "resnet50-unfused", "inceptionv3-1MiB",
-         "resnet50-replace-in-buffers", "vgg16-replace-in-buffers", "resnet50-separate-boundary",
+         "resnet50-copy-in", "resnet50-buffers", "vgg16-buffers", "resnet50-separate-boundary",
          "vgg16-separate-boundary", "vgg16fp16-separate-boundary"],
 )
-def test_full_workload(name, threshold, fuse_boundary, into):
+def test_full_workload(name, threshold, fuse_boundary, mode):
     """Threshold 0 is the unfused ablation: every tensor reduced by its own ring.  With
-    fuse_boundary=False copy-in, ring and copy-out run as separate calls; into=False keeps
-    the replacing steps in the fusion buffers (then the copy-out)."""
+    fuse_boundary=False copy-in, ring and copy-out run as separate calls.  Mode "tensors"
+    (the default) runs the fused buckets' adding steps from the tensors and their
+    replacing steps into them; "copy-in" only the latter; "buffers" the ring in the
+    fusion buffers between the copies."""
     w = configs.get(name)
-    say(f"workload {name} threshold {threshold} fuse_boundary {fuse_boundary} into {into}: generate")
+    say(f"workload {name} threshold {threshold} fuse_boundary {fuse_boundary} mode {mode}: generate")
     per_rank, storage, starts = wgpu.make_rank_tensors(w)
     torch.cuda.synchronize()
     say(f"workload {name}: C oracle on {native.max_threads()} host threads")
     host = oracle_storages(w, storage, starts, threshold)
     say(f"workload {name}: allreduce")
     ar = hv.FusedAllreduce(per_rank, op=w.op, compress=w.compress, threshold_bytes=threshold,
-                           fuse_boundary=fuse_boundary, replace_in_tensors=into)
+                           fuse_boundary=fuse_boundary, replace_in_tensors=mode != "buffers",
+                           add_from_tensors=mode == "tensors")
     plan = fusion.fuse_plan(w.numel(), 2 if w.compress else 4, threshold)
     assert [(b.count, b.direct) for b in plan] == [(b.count, b.direct) for b in ar.buckets]
     ar()

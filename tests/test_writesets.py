@@ -402,3 +402,36 @@ def test_planted_replacing_mistakes_are_caught(knobs):
     with pytest.raises((AssertionError, IndexError)):
         final = replace_phase(5, count, numel, offset, tout, 4, True, 1, knobs)
         assert all(x.all() for row in final for x in row)
+
+
+# ---- the cycle with the adding steps from the tensors, as data --------------------------
+@pytest.mark.parametrize("esize", [4, 2], ids=["f32", "f16"])
+def test_cycle_from_and_into_tensors_sums_every_input_once(esize):
+    import paper_1802_05799_amd as hv
+
+    V = W.vec_elems(esize, esize)
+    for numel in COPY_LAYOUTS + [[4096 * 3 + 1, 7, 2 * 4096 * 2]]:
+        for align in (16, esize):
+            offset, count = plan(numel, esize, align)
+            for n in (3, 4, 7):
+                tin = tiles_of(numel, offset, count, esize, esize, n, hv.COPY_IN)
+                tout = tiles_of(numel, offset, count, esize, esize, n, hv.COPY_OUT)
+                for aligned in (True, False):
+                    T = W.dataflow_cycle(n, count, numel, tin, tout, V, 1, aligned)
+                    full = (1 << n) - 1
+                    assert all((x == full).all() for row in T for x in row), (numel[:3], align, n, aligned)
+
+
+@pytest.mark.parametrize("knobs", [W.Knobs(add_sender=1), W.Knobs(fused_own_from_buffer=True),
+                                   W.Knobs(replace_sender=0), W.Knobs(tile_block_stride=1), W.Knobs(lane_shift=1)],
+                         ids=["adding-sender", "own-from-buffer", "replacing-sender", "tiles-per-block", "lane"])
+def test_planted_cycle_mistakes_are_caught(knobs):
+    import paper_1802_05799_amd as hv
+
+    numel = COPY_LAYOUTS[1]
+    offset, count = plan(numel, 4, 16)
+    tin = tiles_of(numel, offset, count, 4, 4, 5, hv.COPY_IN)
+    tout = tiles_of(numel, offset, count, 4, 4, 5, hv.COPY_OUT)
+    with pytest.raises((AssertionError, IndexError)):
+        T = W.dataflow_cycle(5, count, numel, tin, tout, 4, 1, True, knobs)
+        assert all((x == 31).all() for row in T for x in row)
