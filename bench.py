@@ -112,7 +112,10 @@ def kernel_name(ar, kind, bi):
     if kind in ("cycle_small", "ring_small"):
         return kind
     if kind in ("rs", "ag", "rs_ag"):
-        if b.direct and ar.compress:
+        flags = 0 if b.direct else ar.tiled_flags
+        # a compressed bucket's steps that read or write binary32 tensors are the compressed ring's
+        tensor_side = flags & TILED_ADD_FROM_TENSORS if kind == "rs" else flags & TILED_REPLACE_IN_TENSORS
+        if ar.compress and (b.direct or tensor_side):
             return f"{kind}_step_c16"
         return f"{kind}_step_{'f16' if (ar.buf_dtype == 1 and not b.direct) else 'f32'}"
     return kind
@@ -358,10 +361,13 @@ def short_kernel_name(full):
         return "cycle_small"
     if "chain_kernel" in base:
         return "ring_small"
-    # replacing steps that deliver into the tensors report as the ring step they are
-    for key in ("rs_ag_tiles_kernel", "ag_tiles_kernel"):
+    # the tile-driven ring steps report as the ring step they are; binary32 tensors with
+    # binary16 buffers are the compressed ring's (its replacing steps copy binary32)
+    mixed = re.search(r"tiles_kernel<float, _Float16", base) or re.search(r"tiles_kernelIfDF16_", base)
+    for key, step in (("rs_ag_tiles_kernel", "rs_ag_step"), ("add_tiles_kernel", "rs_step"),
+                      ("ag_tiles_kernel", "ag_step")):
         if key in base:
-            return key.replace("_tiles_kernel", "_step") + ("_f16" if half else "_f32")
+            return step + ("_c16" if mixed else "_f16" if half else "_f32")
     # a launch serving two fusion buffers' rings reports as the one-ring kernel of its step
     for key in ("rs_ag_step_pair_kernel", "rs_step_pair_kernel", "ag_step_pair_kernel", "rs_ag_step_kernel",
                 "rs_step_kernel", "ag_step_kernel"):

@@ -123,15 +123,16 @@ __device__ __forceinline__ void st16(V* p, V v) {
 template <>
 struct Mover<float, float> {
   using buf_vec = f32x4;
-  // 4 tensor elements -> one buffer vector (tensor side may be unaligned)
-  template <bool NT>
+  // 4 tensor elements -> one buffer vector (tensor side may be unaligned, unless the
+  // caller has checked it: ALIGNED)
+  template <bool NT, bool ALIGNED = false>
   __device__ static f32x4 load(const float* src) {
-    if (aligned16(src)) return ld16<NT>(reinterpret_cast<const f32x4*>(src));
+    if (ALIGNED || aligned16(src)) return ld16<NT>(reinterpret_cast<const f32x4*>(src));
     return f32x4{src[0], src[1], src[2], src[3]};
   }
-  template <bool NT>
+  template <bool NT, bool ALIGNED = false>
   __device__ static void store(float* dst, f32x4 v) {
-    if (aligned16(dst)) {
+    if (ALIGNED || aligned16(dst)) {
       st16<NT>(reinterpret_cast<f32x4*>(dst), v);
       return;
     }
@@ -145,17 +146,17 @@ struct Mover<float, float> {
 template <>
 struct Mover<_Float16, _Float16> {
   using buf_vec = f16x8;
-  template <bool NT>
+  template <bool NT, bool ALIGNED = false>
   __device__ static f16x8 load(const _Float16* src) {
-    if (aligned16(src)) return ld16<NT>(reinterpret_cast<const f16x8*>(src));
+    if (ALIGNED || aligned16(src)) return ld16<NT>(reinterpret_cast<const f16x8*>(src));
     f16x8 h;
 #pragma unroll
     for (int k = 0; k < 8; ++k) h[k] = src[k];
     return h;
   }
-  template <bool NT>
+  template <bool NT, bool ALIGNED = false>
   __device__ static void store(_Float16* dst, f16x8 v) {
-    if (aligned16(dst)) {
+    if (ALIGNED || aligned16(dst)) {
       st16<NT>(reinterpret_cast<f16x8*>(dst), v);
       return;
     }
@@ -169,21 +170,21 @@ struct Mover<_Float16, _Float16> {
 template <>
 struct Mover<float, _Float16> {  // tensor binary32 (16-byte vectors), buffer binary16 (8-byte vectors)
   using buf_vec = f16x4;
-  template <bool NT>
+  template <bool NT, bool ALIGNED = false>
   __device__ static f16x4 load(const float* src) {
-    const f32x4 x = aligned16(src) ? ld16<NT>(reinterpret_cast<const f32x4*>(src))
+    const f32x4 x = ALIGNED || aligned16(src) ? ld16<NT>(reinterpret_cast<const f32x4*>(src))
                                    : f32x4{src[0], src[1], src[2], src[3]};
     f16x4 h;
 #pragma unroll
     for (int k = 0; k < 4; ++k) h[k] = (_Float16)x[k];
     return h;
   }
-  template <bool NT>
+  template <bool NT, bool ALIGNED = false>
   __device__ static void store(float* dst, f16x4 h) {
     f32x4 x;
 #pragma unroll
     for (int k = 0; k < 4; ++k) x[k] = (float)h[k];
-    if (aligned16(dst)) {
+    if (ALIGNED || aligned16(dst)) {
       st16<NT>(reinterpret_cast<f32x4*>(dst), x);
       return;
     }
@@ -887,10 +888,12 @@ __global__ __launch_bounds__(kTileLanes) void unpack_tiles_kernel(TiledCopy k, i
 #ifndef HVDX_RSAGT_NXT_NTS  // rank c's copy: replacing step 1 reads it
 #define HVDX_RSAGT_NXT_NTS false
 #endif
-template <typename T, int DIV, int U, bool OWN_T>
+template <typename TT, typename TB, int DIV, bool OWN_T, int U>
 __global__ __launch_bounds__(kTileLanes) void rs_ag_tiles_kernel(TiledCopy k, RingArgs a) {
-  using VT = typename Vec<T>::type;
-  constexpr int V = Vec<T>::n;
+  using M = Mover<TT, TB>;
+  using VB = typename M::buf_vec;
+  constexpr int V = BufVec<TT, TB>::n;
+  constexpr size_t VBB = sizeof(VB);
   const int b = (int64_t)blockIdx.x >= k.x0 ? 1 : 0;
   const hvdx_copy_tile tl = k.tiles[b][b ? (int64_t)blockIdx.x - k.x0 : (int64_t)blockIdx.x];
   if (tl.tensor < 0) return;
@@ -899,38 +902,42 @@ __global__ __launch_bounds__(kTileLanes) void rs_ag_tiles_kernel(TiledCopy k, Ri
   const int own = c == 0 ? n - 1 : c - 1;
   const int snd = own == 0 ? n - 1 : own - 1;
   const int64_t nt = k.m.ntensors[b];
-  const T* bs = static_cast<const T*>(k.m.bufs[b].p[snd]) + tl.pos;
-  const T* bo;  // no __restrict__: with OWN_T it is d_own
-  T* d_own;
-  T* d_nxt;
-  VT mine[U], sent[U];
-  auto load = [&](bool vec) {
+  const TB* bs = static_cast<const TB*>(k.m.bufs[b].p[snd]) + tl.pos;
+  const TB* bo = static_cast<const TB*>(k.m.bufs[b].p[own]) + tl.pos;  // not read with OWN_T
+  TT* d_own;
+  TT* d_nxt;
+  VB mine[U], sent[U];
+  bool vec;
+  auto aligned_b = [](const void* p) { return reinterpret_cast<uintptr_t>(p) % VBB == 0; };
+  if constexpr (OWN_T) {  // the owner's own value from its tensors: the pointers first
+    d_own = static_cast<TT*>(const_cast<void*>(k.m.t[b][(int64_t)own * nt + tl.tensor])) + tl.li;
+    d_nxt = static_cast<TT*>(const_cast<void*>(k.m.t[b][(int64_t)c * nt + tl.tensor])) + tl.li;
+    vec = aligned16(d_own) && aligned_b(bs) && aligned16(d_nxt);
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int i = (u * kTileLanes + threadIdx.x) * V;
       if (vec && i + V <= tl.len) {
-        mine[u] = ld16<HVDX_RSAGT_NTL>(reinterpret_cast<const VT*>(bo + i));
-        sent[u] = ld16<HVDX_RSAGT_NTL>(reinterpret_cast<const VT*>(bs + i));
+        mine[u] = M::template load<HVDX_RSAGT_NTL, true>(d_own + i);
+        sent[u] = ld16<HVDX_RSAGT_NTL>(reinterpret_cast<const VB*>(bs + i));
       }
     }
-  };
-  bool vec;
-  if constexpr (OWN_T) {
-    d_own = static_cast<T*>(const_cast<void*>(k.m.t[b][(int64_t)own * nt + tl.tensor])) + tl.li;
-    d_nxt = static_cast<T*>(const_cast<void*>(k.m.t[b][(int64_t)c * nt + tl.tensor])) + tl.li;
-    bo = d_own;
-    vec = aligned16(bo) && aligned16(bs) && aligned16(d_nxt);
-    load(vec);
   } else {
-    bo = static_cast<const T*>(k.m.bufs[b].p[own]) + tl.pos;
-    const bool bvec = aligned16(bo) && aligned16(bs);
-    load(bvec);  // the buffer loads go out before the tensor pointers arrive
-    d_own = static_cast<T*>(const_cast<void*>(k.m.t[b][(int64_t)own * nt + tl.tensor])) + tl.li;
-    d_nxt = static_cast<T*>(const_cast<void*>(k.m.t[b][(int64_t)c * nt + tl.tensor])) + tl.li;
+    const bool bvec = aligned_b(bo) && aligned_b(bs);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {  // the buffer loads go out before the tensor pointers arrive
+      const int i = (u * kTileLanes + threadIdx.x) * V;
+      if (bvec && i + V <= tl.len) {
+        mine[u] = ld16<HVDX_RSAGT_NTL>(reinterpret_cast<const VB*>(bo + i));
+        sent[u] = ld16<HVDX_RSAGT_NTL>(reinterpret_cast<const VB*>(bs + i));
+      }
+    }
+    d_own = static_cast<TT*>(const_cast<void*>(k.m.t[b][(int64_t)own * nt + tl.tensor])) + tl.li;
+    d_nxt = static_cast<TT*>(const_cast<void*>(k.m.t[b][(int64_t)c * nt + tl.tensor])) + tl.li;
     vec = bvec && aligned16(d_own) && aligned16(d_nxt);
   }
-  auto one = [&](int e) {
-    const T v = combine1<DIV>(bo[e], bs[e], a);
+  auto one = [&](int e) {  // with OWN_T each lane reads its element before it writes over it
+    const TB m = OWN_T ? M::cvt_in(d_own[e]) : bo[e];
+    const TT v = M::cvt_out(combine1<DIV>(m, bs[e], a));
     d_own[e] = v;
     d_nxt[e] = v;
   };
@@ -939,9 +946,9 @@ __global__ __launch_bounds__(kTileLanes) void rs_ag_tiles_kernel(TiledCopy k, Ri
     for (int u = 0; u < U; ++u) {
       const int i = (u * kTileLanes + threadIdx.x) * V;
       if (i + V <= tl.len) {
-        const VT v = combine<DIV>(mine[u], sent[u], a);
-        st16<true>(reinterpret_cast<VT*>(d_own + i), v);
-        st16<HVDX_RSAGT_NXT_NTS>(reinterpret_cast<VT*>(d_nxt + i), v);
+        const VB v = combine<DIV>(mine[u], sent[u], a);
+        M::template store<true, true>(d_own + i, v);
+        M::template store<HVDX_RSAGT_NXT_NTS, true>(d_nxt + i, v);
       } else {
         for (int e = i; e < tl.len && e < i + V; ++e) one(e);  // the tile's last, partial vector
       }
@@ -967,21 +974,26 @@ __global__ __launch_bounds__(kTileLanes) void rs_ag_tiles_kernel(TiledCopy k, Ri
 #ifndef HVDX_ADDT_NTS
 #define HVDX_ADDT_NTS false
 #endif
-template <typename T, bool FIRST, int TPB, int U>
+template <typename TT, typename TB, bool FIRST, int TPB, int U>
 __global__ __launch_bounds__(kTileLanes) void add_tiles_kernel(TiledCopy k, int step, int nranks, int64_t ntiles) {
-  using VT = typename Vec<T>::type;
-  constexpr int V = Vec<T>::n;
-  const T* mine[TPB];
-  const T* sent[TPB];
-  T* out[TPB];
+  using M = Mover<TT, TB>;
+  using VB = typename M::buf_vec;
+  constexpr int V = BufVec<TT, TB>::n;
+  constexpr size_t VBB = sizeof(VB);
+  const TT* mine[TPB];
+  const TT* sent_t[TPB];  // the sender's tensor (step 0)
+  const TB* sent_b[TPB];  // the sender's buffer (later steps)
+  TB* out[TPB];
   int len[TPB];
   bool vec[TPB];
+  auto aligned_b = [](const void* p) { return reinterpret_cast<uintptr_t>(p) % VBB == 0; };
 #pragma unroll
   for (int j = 0; j < TPB; ++j) {
     const int64_t g = (int64_t)blockIdx.x * TPB + j;
     len[j] = 0;
     mine[j] = nullptr;
-    sent[j] = nullptr;
+    sent_t[j] = nullptr;
+    sent_b[j] = nullptr;
     out[j] = nullptr;
     vec[j] = false;
     if (g >= ntiles) continue;
@@ -992,36 +1004,40 @@ __global__ __launch_bounds__(kTileLanes) void add_tiles_kernel(TiledCopy k, int 
     if (snd >= nranks) snd -= nranks;
     const int rcv = snd + 1 == nranks ? 0 : snd + 1;
     const int64_t nt = k.m.ntensors[b];
-    mine[j] = static_cast<const T*>(k.m.t[b][(int64_t)rcv * nt + tl.tensor]) + tl.li;
-    sent[j] = FIRST ? static_cast<const T*>(k.m.t[b][(int64_t)snd * nt + tl.tensor]) + tl.li
-                    : static_cast<const T*>(k.m.bufs[b].p[snd]) + tl.pos;
-    out[j] = static_cast<T*>(k.m.bufs[b].p[rcv]) + tl.pos;
+    mine[j] = static_cast<const TT*>(k.m.t[b][(int64_t)rcv * nt + tl.tensor]) + tl.li;
+    if (FIRST) sent_t[j] = static_cast<const TT*>(k.m.t[b][(int64_t)snd * nt + tl.tensor]) + tl.li;
+    else sent_b[j] = static_cast<const TB*>(k.m.bufs[b].p[snd]) + tl.pos;
+    out[j] = static_cast<TB*>(k.m.bufs[b].p[rcv]) + tl.pos;
     len[j] = tl.len;
-    vec[j] = aligned16(mine[j]) && aligned16(sent[j]) && aligned16(out[j]);
+    vec[j] = aligned16(mine[j]) && (FIRST ? aligned16(sent_t[j]) : aligned_b(sent_b[j])) && aligned_b(out[j]);
   }
-  VT x[TPB][U], y[TPB][U];
+  VB x[TPB][U], y[TPB][U];
 #pragma unroll
   for (int j = 0; j < TPB; ++j)
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int i = (u * kTileLanes + threadIdx.x) * V;
       if (vec[j] && i + V <= len[j]) {
-        x[j][u] = ld16<HVDX_ADDT_NTL>(reinterpret_cast<const VT*>(mine[j] + i));
-        y[j][u] = ld16<HVDX_ADDT_NTL>(reinterpret_cast<const VT*>(sent[j] + i));
+        x[j][u] = M::template load<HVDX_ADDT_NTL, true>(mine[j] + i);
+        y[j][u] = FIRST ? M::template load<HVDX_ADDT_NTL, true>(sent_t[j] + i)
+                        : ld16<HVDX_ADDT_NTL>(reinterpret_cast<const VB*>(sent_b[j] + i));
       }
     }
+  auto one = [&](int j, int e) {
+    out[j][e] = M::cvt_in(mine[j][e]) + (FIRST ? M::cvt_in(sent_t[j][e]) : sent_b[j][e]);
+  };
 #pragma unroll
   for (int j = 0; j < TPB; ++j) {
     if (vec[j]) {
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int i = (u * kTileLanes + threadIdx.x) * V;
-        if (i + V <= len[j]) st16<HVDX_ADDT_NTS>(reinterpret_cast<VT*>(out[j] + i), x[j][u] + y[j][u]);
+        if (i + V <= len[j]) st16<HVDX_ADDT_NTS>(reinterpret_cast<VB*>(out[j] + i), x[j][u] + y[j][u]);
         else
-          for (int e = i; e < len[j] && e < i + V; ++e) out[j][e] = mine[j][e] + sent[j][e];
+          for (int e = i; e < len[j] && e < i + V; ++e) one(j, e);
       }
     } else {
-      for (int e = threadIdx.x; e < len[j]; e += kTileLanes) out[j][e] = mine[j][e] + sent[j][e];
+      for (int e = threadIdx.x; e < len[j]; e += kTileLanes) one(j, e);
     }
   }
 }
@@ -1344,57 +1360,69 @@ hipError_t launch_unpack_tiles(const TiledCopy& k, int buf_dtype, int dst_dtype,
   return hipGetLastError();
 }
 
-hipError_t launch_rs_ag_tiles(const TiledCopy& k, const RingArgs& a, int dtype, int divmode, bool own_in_tensors,
-                              int64_t blocks, hipStream_t stream) {
+hipError_t launch_rs_ag_tiles(const TiledCopy& k, const RingArgs& a, int tensor_dtype, int buf_dtype, int divmode,
+                              bool own_in_tensors, int64_t blocks, hipStream_t stream) {
   if (blocks < 1 || blocks > 0x7fffffff || a.n < 3) return hipErrorInvalidValue;
   const dim3 grid((unsigned)blocks);
   const dim3 block(kTileLanes);
-#define HVDX_RSAG_T(T, U, OWN)                                                                           \
-  do {                                                                                                  \
-    if (divmode == DIV_NONE) HVDX_LAUNCH((rs_ag_tiles_kernel<T, DIV_NONE, U, OWN>), grid, block, 0, stream, k, a); \
-    else if (divmode == DIV_POW2) HVDX_LAUNCH((rs_ag_tiles_kernel<T, DIV_POW2, U, OWN>), grid, block, 0, stream, k, a); \
-    else HVDX_LAUNCH((rs_ag_tiles_kernel<T, DIV_TRUE, U, OWN>), grid, block, 0, stream, k, a);           \
+#define HVDX_RSAG_T(TT, TB, U, OWN)                                                                       \
+  do {                                                                                                   \
+    if (divmode == DIV_NONE)                                                                             \
+      HVDX_LAUNCH((rs_ag_tiles_kernel<TT, TB, DIV_NONE, OWN, U>), grid, block, 0, stream, k, a);         \
+    else if (divmode == DIV_POW2)                                                                        \
+      HVDX_LAUNCH((rs_ag_tiles_kernel<TT, TB, DIV_POW2, OWN, U>), grid, block, 0, stream, k, a);         \
+    else HVDX_LAUNCH((rs_ag_tiles_kernel<TT, TB, DIV_TRUE, OWN, U>), grid, block, 0, stream, k, a);      \
   } while (0)
-  if (dtype == HVDX_FLOAT32) {
-    if (own_in_tensors) HVDX_RSAG_T(float, HVDX_TILE_U32, true);
-    else HVDX_RSAG_T(float, HVDX_TILE_U32, false);
+  if (tensor_dtype == HVDX_FLOAT32 && buf_dtype == HVDX_FLOAT32) {
+    if (own_in_tensors) HVDX_RSAG_T(float, float, HVDX_TILE_U32, true);
+    else HVDX_RSAG_T(float, float, HVDX_TILE_U32, false);
+  } else if (tensor_dtype == HVDX_FLOAT32) {
+    if (own_in_tensors) HVDX_RSAG_T(float, _Float16, HVDX_TILE_U16, true);
+    else HVDX_RSAG_T(float, _Float16, HVDX_TILE_U16, false);
   } else {
-    if (own_in_tensors) HVDX_RSAG_T(_Float16, HVDX_TILE_UH, true);
-    else HVDX_RSAG_T(_Float16, HVDX_TILE_UH, false);
+    if (own_in_tensors) HVDX_RSAG_T(_Float16, _Float16, HVDX_TILE_UH, true);
+    else HVDX_RSAG_T(_Float16, _Float16, HVDX_TILE_UH, false);
   }
 #undef HVDX_RSAG_T
   return hipGetLastError();
 }
 
-hipError_t launch_add_tiles(const TiledCopy& k, int dtype, int nranks, int step, int64_t ntiles, hipStream_t stream) {
+hipError_t launch_add_tiles(const TiledCopy& k, int tensor_dtype, int buf_dtype, int nranks, int step, int64_t ntiles,
+                            hipStream_t stream) {
   if (ntiles < 1 || ntiles > 0x7fffffff || nranks < 3 || step < 0 || step > nranks - 3) return hipErrorInvalidValue;
   constexpr int TPB = HVDX_ADDT_TPB;
   const dim3 grid((unsigned)((ntiles + TPB - 1) / TPB));
   const dim3 block(kTileLanes);
-  const bool first = step == 0;
-  if (dtype == HVDX_FLOAT32) {
-    if (first) HVDX_LAUNCH((add_tiles_kernel<float, true, TPB, HVDX_TILE_U32>), grid, block, 0, stream, k, step, nranks, ntiles);
-    else HVDX_LAUNCH((add_tiles_kernel<float, false, TPB, HVDX_TILE_U32>), grid, block, 0, stream, k, step, nranks, ntiles);
-  } else {
-    if (first) HVDX_LAUNCH((add_tiles_kernel<_Float16, true, TPB, HVDX_TILE_UH>), grid, block, 0, stream, k, step, nranks, ntiles);
-    else HVDX_LAUNCH((add_tiles_kernel<_Float16, false, TPB, HVDX_TILE_UH>), grid, block, 0, stream, k, step, nranks, ntiles);
-  }
+#define HVDX_ADD_T(TT, TB, U)                                                                              \
+  do {                                                                                                    \
+    if (step == 0)                                                                                        \
+      HVDX_LAUNCH((add_tiles_kernel<TT, TB, true, TPB, U>), grid, block, 0, stream, k, step, nranks, ntiles);  \
+    else HVDX_LAUNCH((add_tiles_kernel<TT, TB, false, TPB, U>), grid, block, 0, stream, k, step, nranks, ntiles); \
+  } while (0)
+  if (tensor_dtype == HVDX_FLOAT32 && buf_dtype == HVDX_FLOAT32) HVDX_ADD_T(float, float, HVDX_TILE_U32);
+  else if (tensor_dtype == HVDX_FLOAT32) HVDX_ADD_T(float, _Float16, HVDX_TILE_U16);
+  else HVDX_ADD_T(_Float16, _Float16, HVDX_TILE_UH);
+#undef HVDX_ADD_T
   return hipGetLastError();
 }
 
-hipError_t launch_ag_tiles(const TiledCopy& k, int dtype, int nranks, int step, int64_t ntiles, hipStream_t stream) {
+hipError_t launch_ag_tiles(const TiledCopy& k, int tensor_dtype, int buf_dtype, int nranks, int step, int64_t ntiles,
+                           hipStream_t stream) {
   if (ntiles < 1 || ntiles > 0x7fffffff || nranks < 3 || step < 1 || step > nranks - 2) return hipErrorInvalidValue;
   constexpr int TPB = HVDX_AGT_TPB;
   const dim3 grid((unsigned)((ntiles + TPB - 1) / TPB));
   const dim3 block(kTileLanes);
   const bool last = step == nranks - 2;
-  if (dtype == HVDX_FLOAT32) {
-    if (last) HVDX_LAUNCH((ag_tiles_kernel<float, true, TPB, HVDX_TILE_U32>), grid, block, 0, stream, k, step, nranks, ntiles);
-    else HVDX_LAUNCH((ag_tiles_kernel<float, false, TPB, HVDX_TILE_U32>), grid, block, 0, stream, k, step, nranks, ntiles);
-  } else {
-    if (last) HVDX_LAUNCH((ag_tiles_kernel<_Float16, true, TPB, HVDX_TILE_UH>), grid, block, 0, stream, k, step, nranks, ntiles);
-    else HVDX_LAUNCH((ag_tiles_kernel<_Float16, false, TPB, HVDX_TILE_UH>), grid, block, 0, stream, k, step, nranks, ntiles);
-  }
+  // the tensors' own type; the tiles hold what tile_vectors(tensor, buffer) vectors per lane cover
+#define HVDX_AG_T(T, U)                                                                                         \
+  do {                                                                                                         \
+    if (last) HVDX_LAUNCH((ag_tiles_kernel<T, true, TPB, U>), grid, block, 0, stream, k, step, nranks, ntiles);  \
+    else HVDX_LAUNCH((ag_tiles_kernel<T, false, TPB, U>), grid, block, 0, stream, k, step, nranks, ntiles);      \
+  } while (0)
+  if (tensor_dtype == HVDX_FLOAT32 && buf_dtype == HVDX_FLOAT32) HVDX_AG_T(float, HVDX_TILE_U32);
+  else if (tensor_dtype == HVDX_FLOAT32) HVDX_AG_T(float, HVDX_TILE_U16);
+  else HVDX_AG_T(_Float16, HVDX_TILE_UH);
+#undef HVDX_AG_T
   return hipGetLastError();
 }
 

@@ -837,8 +837,8 @@ int hvdx_fuse_allreduce_tiled(const hvdx_tiled_bucket* t0, const hvdx_tiled_buck
   }
   if (op != HVDX_SUM && op != HVDX_AVERAGE) return fail(HVDX_ERR_INVALID, "%s: unknown op %d", what, op);
   if (nranks < 3) return fail(HVDX_ERR_UNSUPPORTED, "%s: needs 3 or more ranks", what);
-  if (replace_t && tensor_dtype != buf_dtype)
-    return fail(HVDX_ERR_UNSUPPORTED, "%s: replacing in the tensors needs tensors of the buffer's type", what);
+  if (replace_t && tensor_dtype == HVDX_FLOAT16 && buf_dtype == HVDX_FLOAT32)
+    return fail(HVDX_ERR_UNSUPPORTED, "%s: binary16 tensors with binary32 buffers", what);
   if (add_t && !replace_t)
     return fail(HVDX_ERR_UNSUPPORTED, "%s: adding from the tensors needs replacing in the tensors", what);
   const int es = elem_size(buf_dtype);
@@ -881,7 +881,7 @@ int hvdx_fuse_allreduce_tiled(const hvdx_tiled_bucket* t0, const hvdx_tiled_buck
                             last);
     for (int s = 0; s < last; ++s) {
       TimedLaunch timed(HVDX_KERNEL_REDUCE_SCATTER, s, nranks, buf_dtype, HVDX_COMPRESS_NONE, both, st);
-      const hipError_t e = hvdx::launch_add_tiles(k, buf_dtype, nranks, s, n_in, st);
+      const hipError_t e = hvdx::launch_add_tiles(k, tensor_dtype, buf_dtype, nranks, s, n_in, st);
       if (e != hipSuccess) return hip_fail(e, "adding step from the tensors");
     }
   } else {
@@ -907,15 +907,15 @@ int hvdx_fuse_allreduce_tiled(const hvdx_tiled_bucket* t0, const hvdx_tiled_buck
     {
       TimedLaunch timed(HVDX_KERNEL_RS_AG, last, nranks, buf_dtype, HVDX_COMPRESS_NONE, both, st);
       TimedLaunch timed_phase(HVDX_KERNEL_RS_AG, last, nranks, buf_dtype, HVDX_COMPRESS_NONE, both, st, -1, true);
-      const hipError_t e = hvdx::launch_rs_ag_tiles(k, ring_args(nranks, run[0]->b.buf_count, last), buf_dtype,
-                                                    div_mode(op, nranks), add_t, n_out, st);
+      const hipError_t e = hvdx::launch_rs_ag_tiles(k, ring_args(nranks, run[0]->b.buf_count, last), tensor_dtype,
+                                                    buf_dtype, div_mode(op, nranks), add_t, n_out, st);
       if (e != hipSuccess) return hip_fail(e, "replacing step 0 into the tensors");
     }
     TimedLaunch timed_phase(HVDX_KERNEL_ALLGATHER, 1, nranks, buf_dtype, HVDX_COMPRESS_NONE, both, st, -1, true,
                             last);
     for (int s = 1; s <= last; ++s) {
       TimedLaunch timed(HVDX_KERNEL_ALLGATHER, s, nranks, buf_dtype, HVDX_COMPRESS_NONE, both, st);
-      const hipError_t e = hvdx::launch_ag_tiles(k, buf_dtype, nranks, s, n_out, st);
+      const hipError_t e = hvdx::launch_ag_tiles(k, tensor_dtype, buf_dtype, nranks, s, n_out, st);
       if (e != hipSuccess) return hip_fail(e, "replacing step into the tensors");
     }
     return HVDX_OK;

@@ -80,12 +80,14 @@ class FusedAllreduce:
         path run two at a time, every launch serving both.  With tiled (fused boundary,
         N >= 3) the fused copies of those buckets are driven by tile tables cut once here
         (hvdx_fuse_copy_tiles, hvdx_fuse_allreduce_tiled) instead of finding each stretch's
-        tensors in the kernel.  With replace_in_tensors (tiled, no compression) their
-        replacing steps deliver each chunk straight into the receiving rank's tensors and
-        forward it from there, so no copy-out follows (HVDX_TILED_REPLACE_IN_TENSORS);
-        with add_from_tensors as well, each adding step reads the receiver's own elements
-        from its tensors, so no copy-in either (HVDX_TILED_ADD_FROM_TENSORS) and the
-        fusion buffers hold only received partial sums.  All give the same bits."""
+        tensors in the kernel.  With replace_in_tensors (tiled) their replacing steps
+        deliver each chunk straight into the receiving rank's tensors and forward it from
+        there, so no copy-out follows (HVDX_TILED_REPLACE_IN_TENSORS); with
+        add_from_tensors as well, each adding step reads the receiver's own elements from
+        its tensors, so no copy-in either (HVDX_TILED_ADD_FROM_TENSORS) and the fusion
+        buffers hold only received partial sums.  Compressed buckets then work as the
+        compressed ring of a direct tensor does: binary16 partial sums, binary32 values
+        (binary16 results held exactly) in the replacing steps.  All give the same bits."""
         if schedule not in ("ring", "fold"):
             raise ValueError("schedule must be 'ring' or 'fold'")
         self.schedule = schedule
@@ -166,7 +168,7 @@ class FusedAllreduce:
                     host = torch.frombuffer(bytearray(bytes(arr)), dtype=torch.uint8)
                     tabs += [host.to(dev), k]
                 b.tiles = tuple(tabs)
-        in_tensors = replace_in_tensors and self.tiled and self.dtype == self.buf_dtype
+        in_tensors = replace_in_tensors and self.tiled
         self.tiled_flags = L.TILED_BUFFERS
         if in_tensors:
             self.tiled_flags = L.TILED_REPLACE_IN_TENSORS | (L.TILED_ADD_FROM_TENSORS if add_from_tensors else 0)

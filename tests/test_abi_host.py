@@ -243,8 +243,8 @@ def test_pair_argument_errors():
 
 
 def test_tiled_argument_errors():
-    """hvdx_fuse_allreduce_tiled refuses unknown flags, the tensor modes when the tensors
-    are not of the buffer's type, and adding from the tensors alone, before any launch."""
+    """hvdx_fuse_allreduce_tiled refuses unknown flags, binary16 tensors with binary32
+    buffers, and adding from the tensors alone, before any launch."""
     ft = hv.hvdx_fuse_allreduce_tiled
     b3 = bufs(3, 64)
     d0 = (FAKE, FAKE, FAKE, 3, b3, 64, FAKE, 4, FAKE, 4)
@@ -252,7 +252,7 @@ def test_tiled_argument_errors():
     assert status_of(ft, d0, None, hv.FLOAT32, hv.FLOAT32, 3, hv.SUM, 4) == hv.ERR_INVALID
     assert status_of(ft, d0, None, hv.FLOAT32, hv.FLOAT32, 3, hv.SUM, -1) == hv.ERR_INVALID
     for flags in (hv.TILED_REPLACE_IN_TENSORS, both):
-        assert status_of(ft, d0, None, hv.FLOAT32, hv.FLOAT16, 3, hv.SUM, flags) == hv.ERR_UNSUPPORTED
+        assert status_of(ft, d0, None, hv.FLOAT16, hv.FLOAT32, 3, hv.SUM, flags) == hv.ERR_UNSUPPORTED
         assert status_of(ft, d0, None, hv.FLOAT32, hv.FLOAT32, 2, hv.SUM, flags) == hv.ERR_UNSUPPORTED
         assert status_of(ft, (FAKE, FAKE, FAKE, 3, b3, 64, FAKE, 4, 0, 4), None, hv.FLOAT32, hv.FLOAT32, 3, hv.SUM,
                          flags) == hv.ERR_INVALID  # the copy-out tiles missing

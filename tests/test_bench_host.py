@@ -132,11 +132,16 @@ REAL_NAMES = {
         ("ag_unpack", "tiles<1>"),
     "_ZN4hvdx12_GLOBAL__N_117pack_tiles_kernelIfDF16_Li2EEEvNS_9TiledCopyEi": ("pack_rs", "tiles<2>"),
     "_ZN4hvdx12_GLOBAL__N_119unpack_tiles_kernelIfDF16_Li2EEEvNS_9TiledCopyEi": ("ag_unpack", "tiles<2>"),
-    "void hvdx::(anonymous namespace)::rs_ag_tiles_kernel<float, 2, 1>(hvdx::TiledCopy, hvdx::RingArgs)":
-        ("rs_ag_step_f32", "tiles<1>"),
-    "void hvdx::(anonymous namespace)::ag_tiles_kernel<float, false, 1>(hvdx::TiledCopy, int, int)":
+    "void hvdx::(anonymous namespace)::rs_ag_tiles_kernel<float, float, 2, true, 1>(hvdx::TiledCopy, "
+    "hvdx::RingArgs)": ("rs_ag_step_f32", "tiles<1>"),
+    "void hvdx::(anonymous namespace)::ag_tiles_kernel<float, false, 2, 1>(hvdx::TiledCopy, int, int, long)":
         ("ag_step_f32", "tiles<1>"),
-    "_ZN4hvdx12_GLOBAL__N_115ag_tiles_kernelIDF16_Lb1ELi1EEEvNS_9TiledCopyEii": ("ag_step_f16", "tiles<1>"),
+    "_ZN4hvdx12_GLOBAL__N_115ag_tiles_kernelIDF16_Lb1ELi2ELi1EEEvNS_9TiledCopyEiil": ("ag_step_f16", "tiles<1>"),
+    "void hvdx::(anonymous namespace)::add_tiles_kernel<float, float, true, 2, 1>(hvdx::TiledCopy, int, int, long)":
+        ("rs_step_f32", "tiles<1>"),
+    "_ZN4hvdx12_GLOBAL__N_116add_tiles_kernelIfDF16_Lb0ELi2ELi2EEEvNS_9TiledCopyEiil": ("rs_step_c16", "tiles<2>"),
+    "_ZN4hvdx12_GLOBAL__N_118rs_ag_tiles_kernelIfDF16_Li2ELb1ELi2EEEvNS_9TiledCopyENS_8RingArgsE":
+        ("rs_ag_step_c16", "tiles<2>"),
     "__amd_rocclr_copyBuffer": (None, ""),
 }
 

@@ -44,7 +44,7 @@ def test_pairs_match_oracle_and_single_cycles(case):
         dev = [[torch.from_numpy(x).cuda() for x in row] for row in host]
         ar = hv.FusedAllreduce(dev, op=op, compress=compress, threshold_bytes=threshold, small_bucket_bytes=0,
                                pair_buckets=pair, tiled=tiled, replace_in_tensors=into, add_from_tensors=add)
-        want_flags = 0 if compress or not into else hv.TILED_REPLACE_IN_TENSORS | (hv.TILED_ADD_FROM_TENSORS * add)
+        want_flags = hv.TILED_REPLACE_IN_TENSORS | (hv.TILED_ADD_FROM_TENSORS * add) if into else 0
         assert ar.tiled_flags == want_flags
         got_pairs = [(i, b.partner) for i, b in enumerate(ar.buckets) if b.pair == 1]
         assert got_pairs == (pairs if pair else [])

@@ -405,19 +405,21 @@ def test_planted_replacing_mistakes_are_caught(knobs):
 
 
 # ---- the cycle with the adding steps from the tensors, as data --------------------------
-@pytest.mark.parametrize("esize", [4, 2], ids=["f32", "f16"])
-def test_cycle_from_and_into_tensors_sums_every_input_once(esize):
+@pytest.mark.parametrize("esizes", [(4, 4), (4, 2), (2, 2)], ids=["f32", "f32-to-f16", "f16"])
+def test_cycle_from_and_into_tensors_sums_every_input_once(esizes):
     import paper_1802_05799_amd as hv
 
-    V = W.vec_elems(esize, esize)
+    te, be = esizes
+    V = W.vec_elems(te, be)
+    U = 2 if (te, be) == (4, 2) else 1  # vectors per lane of the built kernels
     for numel in COPY_LAYOUTS + [[4096 * 3 + 1, 7, 2 * 4096 * 2]]:
-        for align in (16, esize):
-            offset, count = plan(numel, esize, align)
+        for align in (16, be):
+            offset, count = plan(numel, be, align)
             for n in (3, 4, 7):
-                tin = tiles_of(numel, offset, count, esize, esize, n, hv.COPY_IN)
-                tout = tiles_of(numel, offset, count, esize, esize, n, hv.COPY_OUT)
+                tin = tiles_of(numel, offset, count, te, be, n, hv.COPY_IN)
+                tout = tiles_of(numel, offset, count, te, be, n, hv.COPY_OUT)
                 for aligned in (True, False):
-                    T = W.dataflow_cycle(n, count, numel, tin, tout, V, 1, aligned)
+                    T = W.dataflow_cycle(n, count, numel, tin, tout, V, U, aligned)
                     full = (1 << n) - 1
                     assert all((x == full).all() for row in T for x in row), (numel[:3], align, n, aligned)
 
