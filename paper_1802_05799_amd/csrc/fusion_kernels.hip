@@ -1,4 +1,5 @@
-// Tensor Fusion copy-in and copy-out kernels (paper section 7, steps 3 and 5).
+// Tensor Fusion copy-in and copy-out kernels (paper section 7, steps 3 and 5), and the
+// ring steps of a fusion buffer run on the ranks' tensors (further below).
 //
 // The iteration space is the fusion buffer, not the tensor list: block x owns one
 // tile of buffer positions and serves it for every rank.  Each lane handles one
@@ -864,17 +865,22 @@ __global__ __launch_bounds__(kTileLanes) void unpack_tiles_kernel(TiledCopy k, i
   }
 }
 
-// ---- replacing steps that deliver into the tensors ------------------------------------
+// ---- the ring on the tensors ------------------------------------------------------------
 //
 // With every rank in one memory, a replacing step can write the chunk it delivers
 // straight into the receiver's output tensors instead of its fusion buffer, and the
 // next step forwards it from there: each rank's tensors then end holding the result
-// with no copy-out (it saves reading and writing every rank's whole buffer once).
-// The messages and their order are the ring's; only where a received chunk is stored
-// changes.  The tiles are the copy-out's (each inside one tensor and one ring chunk,
-// starting on the tensor's own tile grid), and buffer and tensors share one element
-// type, so a replacing step moves as many bytes as in the buffers.  Padding tiles
-// have no tensor and are skipped.
+// with no copy-out.  Likewise an adding step can read the receiver's own elements of
+// its chunk from its tensors, where the copy-in would have taken them (in adding step s
+// rank c+s+1 touches chunk c for the first time): no copy-in, and the fusion buffers
+// hold only the partial sums received.  The messages and their order are the ring's;
+// only where a rank's own input is read and where a received chunk is stored change.
+// The kernels run over the plan's tile tables (each tile inside one tensor and one ring
+// chunk): the adding steps over the copy-in's (on the buffer's tile grid), the others
+// over the copy-out's (on the tensor's).  With binary32 tensors and binary16 buffers
+// this is the compressed ring: elements rounded where first read, binary16 partial
+// sums, binary32 values (binary16 results held exactly) in the replacing steps.
+// Padding tiles have no tensor and are skipped.
 
 // Adding step N-2 and replacing step 0 of chunk c: the owner (rank c-1) completes its
 // sum from the sender's (c-2) buffer, and the finished value goes to the owner's and
