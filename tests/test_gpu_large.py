@@ -1,7 +1,8 @@
 """Buffers longer than 2^31 elements: the ring and the fused cycle keep 64-bit positions.
 
 Three ranks of 2^31 + 4099 binary32 elements (8.6 GB each) through hvdx_ring_allreduce,
-and one tensor of that length per rank through hvdx_fuse_allreduce (tensors plus fusion
+and one tensor of that length per rank through hvdx_fuse_allreduce and through
+FusedAllreduce's ring on the tensors (tile tables of 2.1M tiles; tensors plus fusion
 buffers, 52 GB in all).  Values come from the seeded generator shared with the
 workloads.  The C oracle runs the same allreduce over host copies of the inputs; every
 element of every rank must match it bit for bit."""
@@ -67,5 +68,21 @@ def test_fused_cycle_beyond_2_to_31_elements():
     torch.cuda.synchronize()
     del bufs
     check(rows, [h[0] for h in host], "fused cycle")
+    del rows, host
+    torch.cuda.empty_cache()
+
+
+def test_ring_on_tensors_beyond_2_to_31_elements():
+    say(f"large ring on the tensors: {N} ranks x one tensor of {COUNT} elements")
+    rows = filled()
+    host = [[x.cpu().numpy()] for x in rows]
+    native.allreduce(host, "average", threshold=4 * COUNT, threads=native.max_threads(), out=host)
+    ar = hv.FusedAllreduce([[x] for x in rows], op="average", threshold_bytes=4 * COUNT)
+    assert not ar.buckets[0].direct and not ar.buckets[0].small
+    assert ar.tiled_flags == hv.TILED_REPLACE_IN_TENSORS | hv.TILED_ADD_FROM_TENSORS
+    ar()
+    torch.cuda.synchronize()
+    del ar
+    check(rows, [h[0] for h in host], "ring on the tensors")
     del rows, host
     torch.cuda.empty_cache()
