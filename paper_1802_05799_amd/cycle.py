@@ -77,7 +77,8 @@ class FusedAllreduce:
         With the fused boundary, a bucket of at most small_bucket_bytes per rank (0:
         none) runs its whole cycle in one launch instead (compressed direct tensors
         excepted).  With pair_buckets (fused boundary) the fused buckets on the per-step
-        path run two at a time, every launch serving both.  With tiled (fused boundary,
+        path run two at a time, every launch serving both; if one of them is left alone,
+        the first small fused bucket joins it there instead of taking its one launch.  With tiled (fused boundary,
         N >= 3) the fused copies of those buckets are driven by tile tables cut once here
         (hvdx_fuse_copy_tiles, hvdx_fuse_allreduce_tiled) instead of finding each stretch's
         tensors in the kernel.  With replace_in_tensors (tiled) their replacing steps
@@ -134,6 +135,13 @@ class FusedAllreduce:
             # member's place, so a direct tensor or small bucket between the two runs after both
             # (the buckets share no data: the bits do not depend on the order)
             ok = [i for i, x in enumerate(self.buckets) if not x.direct and not x.small and x.count > 0]
+            small = [i for i, x in enumerate(self.buckets) if not x.direct and x.small and x.count > 0]
+            if len(ok) % 2 and small:
+                # a per-step bucket left alone takes the first small fused bucket along: its few
+                # elements then ride in the other's 2N-2 launches instead of a launch of their own
+                # whose threads walk all 2N-2 steps one after another
+                self.buckets[small[0]].small = False
+                ok = sorted(ok + small[:1])
             for i, j in zip(ok[0::2], ok[1::2]):
                 self.buckets[i].pair, self.buckets[i].partner = 1, j
                 self.buckets[j].pair, self.buckets[j].partner = 2, i

@@ -107,3 +107,25 @@ def test_pair_entry_point_directly():
         for t in (0, 1):
             assert_bits_equal(dev[r][t].cpu().numpy(), got[r][t], f"empty partner: rank {r} t {t}")
         assert_bits_equal(dev[r][2].cpu().numpy(), before[r][2], f"empty partner untouched: rank {r}")
+
+
+def test_small_bucket_rides_along_with_a_lone_one():
+    """Buckets 0 (tensors 0, 1) and 1 (tensor 2) paired, 2 (tensor 3: 400 bytes per rank)
+    small, 3 (tensor 4) direct, 4 (tensor 5) alone: bucket 4 takes bucket 2 along instead
+    of bucket 2 running its own launch."""
+    numel = [9000, 7000, 16384, 100, 20000, 15000]
+    n = 6
+    rng = np.random.default_rng(4300)
+    host = [[(rng.standard_normal(k) * 0.01).astype(np.float32) for k in numel] for _ in range(n)]
+    for op in ("average", "sum"):
+        say(f"small bucket riding along: {op}")
+        want = allreduce.allreduce(host, op, threshold=65536)
+        dev = [[torch.from_numpy(x).cuda() for x in row] for row in host]
+        ar = hv.FusedAllreduce(dev, op=op, threshold_bytes=65536, small_bucket_bytes=4096)
+        assert [(i, b.partner) for i, b in enumerate(ar.buckets) if b.pair == 1] == [(0, 1), (2, 4)]
+        assert not any(k == "cycle_small" for k, _, _ in ar.kernel_sequence())
+        ar()
+        torch.cuda.synchronize()
+        for r in range(n):
+            for t in range(len(numel)):
+                assert_bits_equal(dev[r][t].cpu().numpy(), want[r][t], f"{op} rank {r} t {t}")
