@@ -282,9 +282,12 @@ int64_t hvdx_fuse_tile_elems(int tensor_dtype, int buf_dtype);
  *                      receiver's own elements of its chunk from its tensors (and in step 0
  *                      the sender's too), where the copy-in would have put them: no copy-in;
  *                      the buffers then only ever hold received partial sums.
- *                      Every message of the ring moves in its order with either flag;
- *                      both need tensor_dtype == buf_dtype (else HVDX_ERR_UNSUPPORTED), and
- *                      with either the fusion buffers are scratch afterwards.
+ *                      Every message of the ring moves in its order with either flag, and
+ *                      with either the fusion buffers are scratch afterwards.  With binary32
+ *                      tensors and binary16 buffers (compression) these are the compressed
+ *                      ring's steps: elements rounded to binary16 where first read, binary16
+ *                      partial sums, and replacing steps that copy the binary32 values
+ *                      holding the binary16 results exactly (twice the binary16 width).
  * Errors as hvdx_fuse_allreduce_pair, and HVDX_ERR_INVALID for a missing table, a
  * negative tile count or an unknown flag.
  */
