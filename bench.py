@@ -143,7 +143,7 @@ MALL_FLUSH_BYTES = 1 << 30  # written between allreduces: 4x the 256 MB Infinity
 
 
 def measure(name, steps, warmup, threshold=64 << 20, per_kernel_pass=True, schedule="ring", graph_pass=True,
-            flush_bytes=0):
+            flush_bytes=0, **modes):
     """Time `steps` allreduces of workload `name`.  With flush_bytes, a buffer that
     large is overwritten before every allreduce (outside its timing), so each one
     starts with none of its data in the Infinity Cache; each allreduce then has its
@@ -156,7 +156,8 @@ def measure(name, steps, warmup, threshold=64 << 20, per_kernel_pass=True, sched
 
     w = configs.get(name)
     per_rank, storage, starts = wgpu.make_rank_tensors(w)
-    ar = hv.FusedAllreduce(per_rank, op=w.op, compress=w.compress, threshold_bytes=threshold, schedule=schedule)
+    ar = hv.FusedAllreduce(per_rank, op=w.op, compress=w.compress, threshold_bytes=threshold, schedule=schedule,
+                           **modes)
     stream = torch.cuda.current_stream()
     sid = stream.cuda_stream
     scratch = torch.empty(flush_bytes // 4, dtype=torch.float32, device="cuda") if flush_bytes else None
@@ -686,6 +687,19 @@ def main():
                                 "share": round(v["share"], 4)} for k, v in r["kernels"].items()},
             }
 
+    # the fusion buffers' ring on the tensors (the default) against the paper's copies: the
+    # copy-in kept (fused with adding step 0), and the whole ring in the buffers between
+    # the copy-in and the copy-out (fused with the first and last steps); same bits
+    buffer_modes = {}
+    if not args.no_per_config:
+        for name in ("resnet50", "inceptionv3", "vgg16", "vgg16fp16"):
+            row = {"ring_on_tensors_ms": per_config[name]["ms_per_step"]}
+            for key, kw in (("copy_in_ms", {"add_from_tensors": False}), ("paper_copies_ms", {"replace_in_tensors": False})):
+                r = measure(name, max(3, args.steps // 2), 2, per_kernel_pass=False, graph_pass=False, **kw)
+                row[key] = round(r["ms_per_step"], 4)
+            buffer_modes[name] = row
+            print(f"# {name} fusion buffer modes: {row}", file=sys.stderr, flush=True)
+
     # fusion ablation (paper section 7): ResNet-50 and Inception-V3 with other buffer
     # sizes; threshold 0 reduces every tensor with its own ring (no fusion)
     ablation = {}
@@ -767,12 +781,16 @@ def main():
             "simulated_ranks": head["nranks"],
             "op": "average",
             "fusion_threshold_bytes": 64 << 20,
+            # adding steps read each rank's own elements from its tensors, partial sums in the
+            # fusion buffers, replacing steps write the tensors (fusion_buffer_modes: the others)
+            "fusion_buffer_mode": "ring_on_tensors",
             "buckets": head["buckets"],
         },
         "busbw_GBps": round(head["busbw_GBps"], 2),
         "roofline": roofline,
         "ring_roofline": ring_roofline,
         "per_config": per_config,
+        "fusion_buffer_modes": buffer_modes,
         "fusion_ablation": {"by_workload_and_threshold_bytes": ablation},
         "broadcast": bcast,
         "fold_schedule": fold,

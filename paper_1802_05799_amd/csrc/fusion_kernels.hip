@@ -865,6 +865,24 @@ __global__ __launch_bounds__(kTileLanes) void unpack_tiles_kernel(TiledCopy k, i
   }
 }
 
+// The block index a tile kernel works on.  The blocks the hardware hands to one of the 8
+// XCDs (block b goes to XCD b mod 8) take one contiguous run of tiles, so two neighbouring
+// tiles that share a cache line (a tile's reads on the side it does not write start off
+// the lines) mostly share that XCD's L2; a bijection on [0, gridDim.x) for any grid size.
+// Measured on MI355X against block b taking tile run b: ResNet-50 and Inception-V3 -2%
+// per step (their ring steps +1 to +3 points of peak), VGG-16 -0.3%, VGG-16 fp16 unchanged.
+#ifndef HVDX_XCD_BLOCKS
+#define HVDX_XCD_BLOCKS 1
+#endif
+__device__ __forceinline__ int64_t tile_block() {
+  const int64_t b = blockIdx.x;
+  if constexpr (HVDX_XCD_BLOCKS) {
+    const int64_t g = gridDim.x, q = g / 8, r = g % 8, x = b % 8;
+    return x * q + (x < r ? x : r) + b / 8;
+  }
+  return b;
+}
+
 // ---- the ring on the tensors ------------------------------------------------------------
 //
 // With every rank in one memory, a replacing step can write the chunk it delivers
@@ -900,8 +918,9 @@ __global__ __launch_bounds__(kTileLanes) void rs_ag_tiles_kernel(TiledCopy k, Ri
   using VB = typename M::buf_vec;
   constexpr int V = BufVec<TT, TB>::n;
   constexpr size_t VBB = sizeof(VB);
-  const int b = (int64_t)blockIdx.x >= k.x0 ? 1 : 0;
-  const hvdx_copy_tile tl = k.tiles[b][b ? (int64_t)blockIdx.x - k.x0 : (int64_t)blockIdx.x];
+  const int64_t blk = tile_block();
+  const int b = blk >= k.x0 ? 1 : 0;
+  const hvdx_copy_tile tl = k.tiles[b][b ? blk - k.x0 : blk];
   if (tl.tensor < 0) return;
   const int n = a.n;
   const int c = tl.chunk;
@@ -995,7 +1014,7 @@ __global__ __launch_bounds__(kTileLanes) void add_tiles_kernel(TiledCopy k, int 
   auto aligned_b = [](const void* p) { return reinterpret_cast<uintptr_t>(p) % VBB == 0; };
 #pragma unroll
   for (int j = 0; j < TPB; ++j) {
-    const int64_t g = (int64_t)blockIdx.x * TPB + j;
+    const int64_t g = tile_block() * TPB + j;
     len[j] = 0;
     mine[j] = nullptr;
     sent_t[j] = nullptr;
@@ -1074,7 +1093,7 @@ __global__ __launch_bounds__(kTileLanes) void ag_tiles_kernel(TiledCopy k, int s
   bool vec[TPB];
 #pragma unroll
   for (int j = 0; j < TPB; ++j) {
-    const int64_t g = (int64_t)blockIdx.x * TPB + j;
+    const int64_t g = tile_block() * TPB + j;
     len[j] = 0;
     src[j] = nullptr;
     dst[j] = nullptr;

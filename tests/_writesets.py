@@ -29,6 +29,7 @@ class Knobs:
     tile_block_stride: int = 0  # block b of a replacing step takes tiles b*this + j (0: tiles per block)
     add_sender: int = 0  # adding step s from the tensors: the sender of chunk c is rank c+s+this (0)
     fused_own_from_buffer: bool = False  # the fused step reads the owner's value from its buffer (False)
+    xcd_shift: int = 0  # added to a block's XCD in tile_block() (0)
 
 
 K = Knobs()
@@ -585,12 +586,7 @@ def tiled_replace(kind, n, count, numel, tiles, V, step=0, aligned=True, U=1, k=
     tw = [[np.zeros(m, np.int64) for m in numel] for _ in range(n)]
     tr = [[np.zeros(m, np.int64) for m in numel] for _ in range(n)]
     br = np.zeros((n, count), np.int64)
-    if kind == "rs_ag":
-        order = range(len(tiles))
-    else:
-        stride = k.tile_block_stride or tpb
-        order = [g for b in range(-(-len(tiles) // tpb)) for g in (b * stride + j for j in range(tpb))
-                 if g < len(tiles)]
+    order = block_tiles(len(tiles), 1 if kind == "rs_ag" else tpb, 0 if kind == "rs_ag" else k.tile_block_stride, k)
     for g in order:
         pos, li, t, length, c = tiles[g]
         assert length <= 256 * U * V, "a tile longer than a block takes"
@@ -612,11 +608,19 @@ def tiled_replace(kind, n, count, numel, tiles, V, step=0, aligned=True, U=1, k=
 
 
 # ---- the whole cycle with the adding steps from the tensors, as data -------------------
-def block_tiles(ntiles, tpb, stride=0):
+def tile_block(b, grid, k=K):
+    """tile_block(): the blocks of one XCD (b mod 8) take one contiguous run."""
+    q, r = divmod(grid, 8)
+    x = (b + k.xcd_shift) % 8
+    return x * q + min(x, r) + b // 8
+
+
+def block_tiles(ntiles, tpb, stride=0, k=K):
     """Tile indices in the order a grid of ceil(ntiles / tpb) blocks takes them, block b
-    taking tiles b*tpb + j (b*stride + j with a planted stride)."""
+    taking tiles tile_block(b)*tpb + j (with a planted stride, *stride + j)."""
     st = stride or tpb
-    return [g for b in range(-(-ntiles // tpb)) for g in (b * st + j for j in range(tpb)) if g < ntiles]
+    grid = -(-ntiles // tpb)
+    return [g for b in range(grid) for g in (tile_block(b, grid, k) * st + j for j in range(tpb)) if g < ntiles]
 
 
 class Launch:
@@ -661,7 +665,7 @@ def dataflow_cycle(n, count, numel, tin, tout, V, U=1, aligned=True, k=K, tpb=2)
     B = [np.zeros(count, np.int64) for _ in range(n)]
     for step in range(n - 2):
         L = Launch()
-        for g in block_tiles(len(tin), tpb, k.tile_block_stride):
+        for g in block_tiles(len(tin), tpb, k.tile_block_stride, k):
             pos, li, t, length, c = tin[g]
             if t < 0:
                 continue
@@ -675,7 +679,8 @@ def dataflow_cycle(n, count, numel, tin, tout, V, U=1, aligned=True, k=K, tpb=2)
             L.write(B[rcv], pos + e, own | sent)
         L.commit()
     L = Launch()
-    for pos, li, t, length, c in tout:
+    for g in block_tiles(len(tout), 1, 0, k):
+        pos, li, t, length, c = tout[g]
         e = tile_lanes(length, V, aligned, U) + k.lane_shift
         own = (c - 1) % n
         snd = (own - 1) % n
@@ -689,7 +694,7 @@ def dataflow_cycle(n, count, numel, tin, tout, V, U=1, aligned=True, k=K, tpb=2)
     L.commit()
     for step in range(1, n - 1):
         L = Launch()
-        for g in block_tiles(len(tout), tpb, k.tile_block_stride):
+        for g in block_tiles(len(tout), tpb, k.tile_block_stride, k):
             pos, li, t, length, c = tout[g]
             e = tile_lanes(length, V, aligned, U) + k.lane_shift
             snd = (c + step + k.replace_sender) % n

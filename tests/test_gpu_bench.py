@@ -28,6 +28,7 @@ def test_bench_prints_one_complete_json_line(monkeypatch, capsys):
     assert out["steps"] == 3 and out["warmup"] == 1 and out["higher_is_better"] is True
     assert out["scaling"] == "weak" and out["vs_baseline"] is None and out["data"] == "synthetic"
     assert out["dtype"] == "f32" and out["config"]["workload"] == "resnet50"
+    assert out["config"]["fusion_buffer_mode"] == "ring_on_tensors" and out["fusion_buffer_modes"] == {}
     # value is one rank's binary32 gradient bytes over the step time
     rank_bytes = 4 * 25_557_032
     assert out["value"] == pytest.approx(rank_bytes / (out["ms_per_step"] * 1e-3) / 1e9, rel=2e-3)

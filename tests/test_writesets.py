@@ -425,8 +425,10 @@ def test_cycle_from_and_into_tensors_sums_every_input_once(esizes):
 
 
 @pytest.mark.parametrize("knobs", [W.Knobs(add_sender=1), W.Knobs(fused_own_from_buffer=True),
-                                   W.Knobs(replace_sender=0), W.Knobs(tile_block_stride=1), W.Knobs(lane_shift=1)],
-                         ids=["adding-sender", "own-from-buffer", "replacing-sender", "tiles-per-block", "lane"])
+                                   W.Knobs(replace_sender=0), W.Knobs(tile_block_stride=1), W.Knobs(lane_shift=1),
+                                   W.Knobs(xcd_shift=1)],
+                         ids=["adding-sender", "own-from-buffer", "replacing-sender", "tiles-per-block", "lane",
+                              "xcd-runs"])
 def test_planted_cycle_mistakes_are_caught(knobs):
     import paper_1802_05799_amd as hv
 
@@ -437,3 +439,8 @@ def test_planted_cycle_mistakes_are_caught(knobs):
     with pytest.raises((AssertionError, IndexError)):
         T = W.dataflow_cycle(5, count, numel, tin, tout, 4, 1, True, knobs)
         assert all((x == 31).all() for row in T for x in row)
+
+
+def test_xcd_block_order_is_a_bijection():
+    for grid in list(range(1, 70)) + [4099, (1 << 20) + 3]:
+        assert sorted(W.tile_block(b, grid) for b in range(grid)) == list(range(grid))
