@@ -261,14 +261,19 @@ int64_t hvdx_fuse_copy_tiles(const int64_t* numel, const int64_t* offset, int nt
 int64_t hvdx_fuse_tile_elems(int tensor_dtype, int buf_dtype);
 
 /*
- * hvdx_fuse_allreduce_tiled -- hvdx_fuse_allreduce (b1 NULL) or hvdx_fuse_allreduce_pair
- * (b0 and b1) with the fused copies driven by tile tables: the same result, bit for bit.
- *   b*->b              the bucket, as for hvdx_fuse_allreduce_pair
- *   b*->in_tiles       DEVICE array of n_in tiles from hvdx_fuse_copy_tiles(HVDX_COPY_IN)
- *   b*->out_tiles      DEVICE array of n_out tiles from hvdx_fuse_copy_tiles(HVDX_COPY_OUT)
- * for exactly this bucket (numel, offset, buf_count, both types and nranks): the tables
- * are device memory and are not checked; other tables make the kernels read or write
- * outside the buffers and tensors.
+ * hvdx_fuse_allreduce_tiled -- the Tensor Fusion cycle of 1 to HVDX_TILED_MAX_BUCKETS
+ * fusion buffers, every launch serving all of them, with the fused copies driven by tile
+ * tables: the same result, bit for bit, as hvdx_fuse_allreduce on each bucket.
+ *   buckets[nbuckets]  host array of bucket descriptors, each as for
+ *                      hvdx_fuse_allreduce_pair, plus
+ *     in_tiles         DEVICE array of n_in tiles from hvdx_fuse_copy_tiles(HVDX_COPY_IN)
+ *     out_tiles        DEVICE array of n_out tiles from hvdx_fuse_copy_tiles(HVDX_COPY_OUT)
+ *                      for exactly this bucket (numel, offset, buf_count, both types and
+ *                      nranks): the tables are device memory and are not checked; other
+ *                      tables make the kernels read or write outside the buffers and
+ *                      tensors.  All buckets' fusion buffers must be pairwise disjoint.
+ *                      More than two buckets (with something to reduce) need both tensor
+ *                      flags; with HVDX_TILED_REPLACE_IN_TENSORS, buckets x nranks <= 256.
  *   flags              0 (HVDX_TILED_BUFFERS): the fusion buffers as in paper section 7 --
  *                      the copy-in fused with adding step 0, the ring in the buffers
  *                      (step 4), the copy-out fused with the last replacing step (step 5);
@@ -288,9 +293,11 @@ int64_t hvdx_fuse_tile_elems(int tensor_dtype, int buf_dtype);
  *                      ring's steps: elements rounded to binary16 where first read, binary16
  *                      partial sums, and replacing steps that copy the binary32 values
  *                      holding the binary16 results exactly (twice the binary16 width).
- * Errors as hvdx_fuse_allreduce_pair, and HVDX_ERR_INVALID for a missing table, a
- * negative tile count or an unknown flag.
+ * Errors as hvdx_fuse_allreduce_pair, HVDX_ERR_INVALID for a missing table, a negative
+ * tile count, an unknown flag or a bucket count out of range, HVDX_ERR_UNSUPPORTED for
+ * more buckets than the flags allow.
  */
+#define HVDX_TILED_MAX_BUCKETS 4
 #define HVDX_TILED_BUFFERS 0
 #define HVDX_TILED_REPLACE_IN_TENSORS 1
 #define HVDX_TILED_ADD_FROM_TENSORS 2
@@ -301,8 +308,8 @@ typedef struct hvdx_tiled_bucket {
   const hvdx_copy_tile* out_tiles;
   int64_t n_out;
 } hvdx_tiled_bucket;
-int hvdx_fuse_allreduce_tiled(const hvdx_tiled_bucket* b0, const hvdx_tiled_bucket* b1, int tensor_dtype,
-                              int buf_dtype, int nranks, int op, int flags, void* stream);
+int hvdx_fuse_allreduce_tiled(const hvdx_tiled_bucket* buckets, int nbuckets, int tensor_dtype, int buf_dtype,
+                              int nranks, int op, int flags, void* stream);
 
 /*
  * hvdx_fuse_allreduce_small -- hvdx_fuse_allreduce for small fusion buffers: the same

@@ -31,6 +31,8 @@ from ._lib import (  # noqa: F401
     PHASE_REDUCE_SCATTER,
     TILED_ADD_FROM_TENSORS,
     TILED_BUFFERS,
+    TILED_MAX_BUCKETS,
+    TILED_MAX_BUFFERS,
     TILED_REPLACE_IN_TENSORS,
     SMALL_BUCKET_BYTES,
     SUM,

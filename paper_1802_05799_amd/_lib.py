@@ -41,7 +41,7 @@ _SIGNATURES = {
     "hvdx_fuse_allreduce_small": (_i, [_p, _p, _p, _i, _i, _pp, _i64, _i, _i, _i, _p]),
     "hvdx_fuse_allreduce_pair": (_i, [_p, _p, _i, _i, _i, _i, _p]),
     "hvdx_fuse_copy_tiles": (_i64, [_pi64, _p, _i, _i64, _i, _i, _i, _i, _p, _i64]),
-    "hvdx_fuse_allreduce_tiled": (_i, [_p, _p, _i, _i, _i, _i, _i, _p]),
+    "hvdx_fuse_allreduce_tiled": (_i, [_p, _i, _i, _i, _i, _i, _i, _p]),
     "hvdx_fuse_tile_elems": (_i64, [_i, _i]),
     "hvdx_ring_allreduce": (_i, [_pp, _i, _i64, _i, _i, _i, _p, _sz, _p]),
     "hvdx_ring_allreduce_small": (_i, [_pp, _i, _i64, _i, _i, _p]),
@@ -70,6 +70,7 @@ KERNEL_BROADCAST, KERNEL_RS_AG, KERNEL_FOLD = 5, 6, 7
 KERNEL_PACK_RS, KERNEL_AG_UNPACK = 8, 9
 KERNEL_RING_SMALL, KERNEL_CYCLE_SMALL = 10, 11
 TILED_BUFFERS, TILED_REPLACE_IN_TENSORS, TILED_ADD_FROM_TENSORS = 0, 1, 2
+TILED_MAX_BUCKETS, TILED_MAX_BUFFERS = 4, 256  # buckets per call; buckets x ranks in the tensor modes
 
 
 class Bucket(ctypes.Structure):
@@ -271,24 +272,21 @@ def hvdx_fuse_tile_elems(tensor_dtype: int, buf_dtype: int) -> int:
     return lib.hvdx_fuse_tile_elems(tensor_dtype, buf_dtype)
 
 
-def hvdx_fuse_allreduce_tiled(t0, t1, tensor_dtype: int, buf_dtype: int, nranks: int, op: int, flags: int,
+def hvdx_fuse_allreduce_tiled(descs, tensor_dtype: int, buf_dtype: int, nranks: int, op: int, flags: int,
                               stream: int = 0) -> None:
-    """t0, t1 (t1 may be None): (tensors_dev, numel_dev, offset_dev, ntensors, bufs, buf_count,
-    in_tiles_dev, n_in, out_tiles_dev, n_out) each; flags: TILED_BUFFERS, or
-    TILED_REPLACE_IN_TENSORS, optionally | TILED_ADD_FROM_TENSORS."""
+    """descs: one to TILED_MAX_BUCKETS buckets, each (tensors_dev, numel_dev, offset_dev,
+    ntensors, bufs, buf_count, in_tiles_dev, n_in, out_tiles_dev, n_out); flags:
+    TILED_BUFFERS, or TILED_REPLACE_IN_TENSORS, optionally | TILED_ADD_FROM_TENSORS."""
     keep = []
-
-    def desc(t):
+    arr = (TiledBucket * max(1, len(descs)))()
+    for i, t in enumerate(descs):
         tensors_dev, numel_dev, offset_dev, ntensors, bufs, buf_count, in_dev, n_in, out_dev, n_out = t
-        pb, arr = _ptr_array(bufs)
-        keep.append(arr)
-        return TiledBucket(Bucket(tensors_dev, numel_dev, offset_dev, ntensors, pb, buf_count), in_dev, n_in, out_dev,
-                           n_out)
-
-    d0 = desc(t0)
-    d1 = desc(t1) if t1 is not None else None
-    _check(lib.hvdx_fuse_allreduce_tiled(ctypes.addressof(d0), ctypes.addressof(d1) if d1 is not None else None,
-                                         tensor_dtype, buf_dtype, nranks, op, flags, stream))
+        pb, a = _ptr_array(bufs)
+        keep.append(a)
+        arr[i] = TiledBucket(Bucket(tensors_dev, numel_dev, offset_dev, ntensors, pb, buf_count), in_dev, n_in,
+                             out_dev, n_out)
+    _check(lib.hvdx_fuse_allreduce_tiled(ctypes.addressof(arr), len(descs), tensor_dtype, buf_dtype, nranks, op,
+                                         flags, stream))
 
 
 def hvdx_fuse_allreduce_small(tensors_dev: int, numel_dev: int, offset_dev: int, ntensors: int, tensor_dtype: int,

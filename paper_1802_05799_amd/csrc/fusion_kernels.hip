@@ -883,6 +883,16 @@ __device__ __forceinline__ int64_t tile_block() {
   return b;
 }
 
+// The bucket that tile g of a TiledRing launch belongs to, and g's index in its table.
+__device__ __forceinline__ int ring_bucket(const TiledRing& k, int64_t g, int64_t* local) {
+  int b = 0;
+#pragma unroll
+  for (int i = 1; i < kRingBuckets; ++i)
+    if (i < k.nbuckets && g >= k.end[i - 1]) b = i;
+  *local = b ? g - k.end[b - 1] : g;
+  return b;
+}
+
 // ---- the ring on the tensors ------------------------------------------------------------
 //
 // With every rank in one memory, a replacing step can write the chunk it delivers
@@ -913,30 +923,30 @@ __device__ __forceinline__ int64_t tile_block() {
 #define HVDX_RSAGT_NXT_NTS false
 #endif
 template <typename TT, typename TB, int DIV, bool OWN_T, int U>
-__global__ __launch_bounds__(kTileLanes) void rs_ag_tiles_kernel(TiledCopy k, RingArgs a) {
+__global__ __launch_bounds__(kTileLanes) void rs_ag_tiles_kernel(TiledRing k, RingArgs a) {
   using M = Mover<TT, TB>;
   using VB = typename M::buf_vec;
   constexpr int V = BufVec<TT, TB>::n;
   constexpr size_t VBB = sizeof(VB);
-  const int64_t blk = tile_block();
-  const int b = blk >= k.x0 ? 1 : 0;
-  const hvdx_copy_tile tl = k.tiles[b][b ? blk - k.x0 : blk];
+  int64_t li;
+  const int b = ring_bucket(k, tile_block(), &li);
+  const hvdx_copy_tile tl = k.tiles[b][li];
   if (tl.tensor < 0) return;
   const int n = a.n;
   const int c = tl.chunk;
   const int own = c == 0 ? n - 1 : c - 1;
   const int snd = own == 0 ? n - 1 : own - 1;
-  const int64_t nt = k.m.ntensors[b];
-  const TB* bs = static_cast<const TB*>(k.m.bufs[b].p[snd]) + tl.pos;
-  const TB* bo = static_cast<const TB*>(k.m.bufs[b].p[own]) + tl.pos;  // not read with OWN_T
+  const int64_t nt = k.ntensors[b];
+  const TB* bs = static_cast<const TB*>(k.bufs[b * n + snd]) + tl.pos;
+  const TB* bo = static_cast<const TB*>(k.bufs[b * n + own]) + tl.pos;  // not read with OWN_T
   TT* d_own;
   TT* d_nxt;
   VB mine[U], sent[U];
   bool vec;
   auto aligned_b = [](const void* p) { return reinterpret_cast<uintptr_t>(p) % VBB == 0; };
   if constexpr (OWN_T) {  // the owner's own value from its tensors: the pointers first
-    d_own = static_cast<TT*>(const_cast<void*>(k.m.t[b][(int64_t)own * nt + tl.tensor])) + tl.li;
-    d_nxt = static_cast<TT*>(const_cast<void*>(k.m.t[b][(int64_t)c * nt + tl.tensor])) + tl.li;
+    d_own = static_cast<TT*>(const_cast<void*>(k.t[b][(int64_t)own * nt + tl.tensor])) + tl.li;
+    d_nxt = static_cast<TT*>(const_cast<void*>(k.t[b][(int64_t)c * nt + tl.tensor])) + tl.li;
     vec = aligned16(d_own) && aligned_b(bs) && aligned16(d_nxt);
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -956,8 +966,8 @@ __global__ __launch_bounds__(kTileLanes) void rs_ag_tiles_kernel(TiledCopy k, Ri
         sent[u] = ld16<HVDX_RSAGT_NTL>(reinterpret_cast<const VB*>(bs + i));
       }
     }
-    d_own = static_cast<TT*>(const_cast<void*>(k.m.t[b][(int64_t)own * nt + tl.tensor])) + tl.li;
-    d_nxt = static_cast<TT*>(const_cast<void*>(k.m.t[b][(int64_t)c * nt + tl.tensor])) + tl.li;
+    d_own = static_cast<TT*>(const_cast<void*>(k.t[b][(int64_t)own * nt + tl.tensor])) + tl.li;
+    d_nxt = static_cast<TT*>(const_cast<void*>(k.t[b][(int64_t)c * nt + tl.tensor])) + tl.li;
     vec = bvec && aligned16(d_own) && aligned16(d_nxt);
   }
   auto one = [&](int e) {  // with OWN_T each lane reads its element before it writes over it
@@ -1000,7 +1010,7 @@ __global__ __launch_bounds__(kTileLanes) void rs_ag_tiles_kernel(TiledCopy k, Ri
 #define HVDX_ADDT_NTS false
 #endif
 template <typename TT, typename TB, bool FIRST, int TPB, int U>
-__global__ __launch_bounds__(kTileLanes) void add_tiles_kernel(TiledCopy k, int step, int nranks, int64_t ntiles) {
+__global__ __launch_bounds__(kTileLanes) void add_tiles_kernel(TiledRing k, int step, int64_t ntiles) {
   using M = Mover<TT, TB>;
   using VB = typename M::buf_vec;
   constexpr int V = BufVec<TT, TB>::n;
@@ -1022,17 +1032,19 @@ __global__ __launch_bounds__(kTileLanes) void add_tiles_kernel(TiledCopy k, int 
     out[j] = nullptr;
     vec[j] = false;
     if (g >= ntiles) continue;
-    const int b = g >= k.x0 ? 1 : 0;
-    const hvdx_copy_tile tl = k.tiles[b][b ? g - k.x0 : g];
+    int64_t loc;
+    const int b = ring_bucket(k, g, &loc);
+    const hvdx_copy_tile tl = k.tiles[b][loc];
     if (tl.tensor < 0) continue;
+    const int n = k.nranks;
     int snd = tl.chunk + step;  // chunk < N and step <= N-3: below 2N
-    if (snd >= nranks) snd -= nranks;
-    const int rcv = snd + 1 == nranks ? 0 : snd + 1;
-    const int64_t nt = k.m.ntensors[b];
-    mine[j] = static_cast<const TT*>(k.m.t[b][(int64_t)rcv * nt + tl.tensor]) + tl.li;
-    if (FIRST) sent_t[j] = static_cast<const TT*>(k.m.t[b][(int64_t)snd * nt + tl.tensor]) + tl.li;
-    else sent_b[j] = static_cast<const TB*>(k.m.bufs[b].p[snd]) + tl.pos;
-    out[j] = static_cast<TB*>(k.m.bufs[b].p[rcv]) + tl.pos;
+    if (snd >= n) snd -= n;
+    const int rcv = snd + 1 == n ? 0 : snd + 1;
+    const int64_t nt = k.ntensors[b];
+    mine[j] = static_cast<const TT*>(k.t[b][(int64_t)rcv * nt + tl.tensor]) + tl.li;
+    if (FIRST) sent_t[j] = static_cast<const TT*>(k.t[b][(int64_t)snd * nt + tl.tensor]) + tl.li;
+    else sent_b[j] = static_cast<const TB*>(k.bufs[b * n + snd]) + tl.pos;
+    out[j] = static_cast<TB*>(k.bufs[b * n + rcv]) + tl.pos;
     len[j] = tl.len;
     vec[j] = aligned16(mine[j]) && (FIRST ? aligned16(sent_t[j]) : aligned_b(sent_b[j])) && aligned_b(out[j]);
   }
@@ -1084,7 +1096,7 @@ __global__ __launch_bounds__(kTileLanes) void add_tiles_kernel(TiledCopy k, int 
 #define HVDX_AGT_NTS false
 #endif
 template <typename T, bool LAST, int TPB, int U>
-__global__ __launch_bounds__(kTileLanes) void ag_tiles_kernel(TiledCopy k, int step, int nranks, int64_t ntiles) {
+__global__ __launch_bounds__(kTileLanes) void ag_tiles_kernel(TiledRing k, int step, int64_t ntiles) {
   using VT = typename Vec<T>::type;
   constexpr int V = Vec<T>::n;
   const T* src[TPB];
@@ -1099,15 +1111,17 @@ __global__ __launch_bounds__(kTileLanes) void ag_tiles_kernel(TiledCopy k, int s
     dst[j] = nullptr;
     vec[j] = false;
     if (g >= ntiles) continue;
-    const int b = g >= k.x0 ? 1 : 0;
-    const hvdx_copy_tile tl = k.tiles[b][b ? g - k.x0 : g];
+    int64_t loc;
+    const int b = ring_bucket(k, g, &loc);
+    const hvdx_copy_tile tl = k.tiles[b][loc];
     if (tl.tensor < 0) continue;
+    const int n = k.nranks;
     int snd = tl.chunk + step - 1;  // chunk < N and step <= N-2: below 2N
-    if (snd >= nranks) snd -= nranks;
-    const int rcv = snd + 1 == nranks ? 0 : snd + 1;
-    const int64_t nt = k.m.ntensors[b];
-    src[j] = static_cast<const T*>(k.m.t[b][(int64_t)snd * nt + tl.tensor]) + tl.li;
-    dst[j] = static_cast<T*>(const_cast<void*>(k.m.t[b][(int64_t)rcv * nt + tl.tensor])) + tl.li;
+    if (snd >= n) snd -= n;
+    const int rcv = snd + 1 == n ? 0 : snd + 1;
+    const int64_t nt = k.ntensors[b];
+    src[j] = static_cast<const T*>(k.t[b][(int64_t)snd * nt + tl.tensor]) + tl.li;
+    dst[j] = static_cast<T*>(const_cast<void*>(k.t[b][(int64_t)rcv * nt + tl.tensor])) + tl.li;
     len[j] = tl.len;
     vec[j] = aligned16(src[j]) && aligned16(dst[j]);
   }
@@ -1385,10 +1399,18 @@ hipError_t launch_unpack_tiles(const TiledCopy& k, int buf_dtype, int dst_dtype,
   return hipGetLastError();
 }
 
-hipError_t launch_rs_ag_tiles(const TiledCopy& k, const RingArgs& a, int tensor_dtype, int buf_dtype, int divmode,
-                              bool own_in_tensors, int64_t blocks, hipStream_t stream) {
-  if (blocks < 1 || blocks > 0x7fffffff || a.n < 3) return hipErrorInvalidValue;
-  const dim3 grid((unsigned)blocks);
+static int64_t ring_tiles(const TiledRing& k) { return k.nbuckets > 0 ? k.end[k.nbuckets - 1] : 0; }
+
+static bool ring_ok(const TiledRing& k) {
+  const int64_t n = ring_tiles(k);
+  return k.nbuckets >= 1 && k.nbuckets <= kRingBuckets && k.nranks >= 3 &&
+         (int64_t)k.nbuckets * k.nranks <= kRingBufPtrs && n >= 1 && n <= 0x7fffffff;
+}
+
+hipError_t launch_rs_ag_tiles(const TiledRing& k, const RingArgs& a, int tensor_dtype, int buf_dtype, int divmode,
+                              bool own_in_tensors, hipStream_t stream) {
+  if (!ring_ok(k) || a.n != k.nranks) return hipErrorInvalidValue;
+  const dim3 grid((unsigned)ring_tiles(k));
   const dim3 block(kTileLanes);
 #define HVDX_RSAG_T(TT, TB, U, OWN)                                                                       \
   do {                                                                                                   \
@@ -1412,17 +1434,16 @@ hipError_t launch_rs_ag_tiles(const TiledCopy& k, const RingArgs& a, int tensor_
   return hipGetLastError();
 }
 
-hipError_t launch_add_tiles(const TiledCopy& k, int tensor_dtype, int buf_dtype, int nranks, int step, int64_t ntiles,
-                            hipStream_t stream) {
-  if (ntiles < 1 || ntiles > 0x7fffffff || nranks < 3 || step < 0 || step > nranks - 3) return hipErrorInvalidValue;
+hipError_t launch_add_tiles(const TiledRing& k, int tensor_dtype, int buf_dtype, int step, hipStream_t stream) {
+  if (!ring_ok(k) || step < 0 || step > k.nranks - 3) return hipErrorInvalidValue;
   constexpr int TPB = HVDX_ADDT_TPB;
+  const int64_t ntiles = ring_tiles(k);
   const dim3 grid((unsigned)((ntiles + TPB - 1) / TPB));
   const dim3 block(kTileLanes);
 #define HVDX_ADD_T(TT, TB, U)                                                                              \
   do {                                                                                                    \
-    if (step == 0)                                                                                        \
-      HVDX_LAUNCH((add_tiles_kernel<TT, TB, true, TPB, U>), grid, block, 0, stream, k, step, nranks, ntiles);  \
-    else HVDX_LAUNCH((add_tiles_kernel<TT, TB, false, TPB, U>), grid, block, 0, stream, k, step, nranks, ntiles); \
+    if (step == 0) HVDX_LAUNCH((add_tiles_kernel<TT, TB, true, TPB, U>), grid, block, 0, stream, k, step, ntiles); \
+    else HVDX_LAUNCH((add_tiles_kernel<TT, TB, false, TPB, U>), grid, block, 0, stream, k, step, ntiles);        \
   } while (0)
   if (tensor_dtype == HVDX_FLOAT32 && buf_dtype == HVDX_FLOAT32) HVDX_ADD_T(float, float, HVDX_TILE_U32);
   else if (tensor_dtype == HVDX_FLOAT32) HVDX_ADD_T(float, _Float16, HVDX_TILE_U16);
@@ -1431,18 +1452,18 @@ hipError_t launch_add_tiles(const TiledCopy& k, int tensor_dtype, int buf_dtype,
   return hipGetLastError();
 }
 
-hipError_t launch_ag_tiles(const TiledCopy& k, int tensor_dtype, int buf_dtype, int nranks, int step, int64_t ntiles,
-                           hipStream_t stream) {
-  if (ntiles < 1 || ntiles > 0x7fffffff || nranks < 3 || step < 1 || step > nranks - 2) return hipErrorInvalidValue;
+hipError_t launch_ag_tiles(const TiledRing& k, int tensor_dtype, int buf_dtype, int step, hipStream_t stream) {
+  if (!ring_ok(k) || step < 1 || step > k.nranks - 2) return hipErrorInvalidValue;
   constexpr int TPB = HVDX_AGT_TPB;
+  const int64_t ntiles = ring_tiles(k);
   const dim3 grid((unsigned)((ntiles + TPB - 1) / TPB));
   const dim3 block(kTileLanes);
-  const bool last = step == nranks - 2;
+  const bool last = step == k.nranks - 2;
   // the tensors' own type; the tiles hold what tile_vectors(tensor, buffer) vectors per lane cover
-#define HVDX_AG_T(T, U)                                                                                         \
-  do {                                                                                                         \
-    if (last) HVDX_LAUNCH((ag_tiles_kernel<T, true, TPB, U>), grid, block, 0, stream, k, step, nranks, ntiles);  \
-    else HVDX_LAUNCH((ag_tiles_kernel<T, false, TPB, U>), grid, block, 0, stream, k, step, nranks, ntiles);      \
+#define HVDX_AG_T(T, U)                                                                                  \
+  do {                                                                                                  \
+    if (last) HVDX_LAUNCH((ag_tiles_kernel<T, true, TPB, U>), grid, block, 0, stream, k, step, ntiles);  \
+    else HVDX_LAUNCH((ag_tiles_kernel<T, false, TPB, U>), grid, block, 0, stream, k, step, ntiles);      \
   } while (0)
   if (tensor_dtype == HVDX_FLOAT32 && buf_dtype == HVDX_FLOAT32) HVDX_AG_T(float, HVDX_TILE_U32);
   else if (tensor_dtype == HVDX_FLOAT32) HVDX_AG_T(float, HVDX_TILE_U16);

@@ -818,16 +818,19 @@ int64_t hvdx_fuse_copy_tiles(const int64_t* numel, const int64_t* offset, int nt
   return n;
 }
 
-int hvdx_fuse_allreduce_tiled(const hvdx_tiled_bucket* t0, const hvdx_tiled_bucket* t1, int tensor_dtype,
-                              int buf_dtype, int nranks, int op, int flags, void* stream) {
+static_assert(hvdx::kRingBuckets == HVDX_TILED_MAX_BUCKETS, "one launch descriptor slot per bucket");
+
+int hvdx_fuse_allreduce_tiled(const hvdx_tiled_bucket* buckets, int nbuckets, int tensor_dtype, int buf_dtype,
+                              int nranks, int op, int flags, void* stream) {
   static const char* what = "hvdx_fuse_allreduce_tiled";
-  if (!t0) return fail(HVDX_ERR_INVALID, "%s: the first bucket is NULL", what);
+  if (!buckets || nbuckets < 1 || nbuckets > HVDX_TILED_MAX_BUCKETS)
+    return fail(HVDX_ERR_INVALID, "%s: need 1 to %d buckets", what, HVDX_TILED_MAX_BUCKETS);
   if (flags & ~(HVDX_TILED_REPLACE_IN_TENSORS | HVDX_TILED_ADD_FROM_TENSORS))
     return fail(HVDX_ERR_INVALID, "%s: unknown flags 0x%x", what, flags);
   const bool replace_t = flags & HVDX_TILED_REPLACE_IN_TENSORS;
   const bool add_t = flags & HVDX_TILED_ADD_FROM_TENSORS;
-  for (const hvdx_tiled_bucket* t : {t0, t1}) {
-    if (!t) continue;
+  for (int i = 0; i < nbuckets; ++i) {
+    const hvdx_tiled_bucket* t = &buckets[i];
     const int rc = check_fusion(t->b.tensors, t->b.numel, t->b.offset, t->b.ntensors, tensor_dtype, t->b.bufs,
                                 t->b.buf_count, buf_dtype, nranks, what);
     if (rc) return rc;
@@ -841,30 +844,56 @@ int hvdx_fuse_allreduce_tiled(const hvdx_tiled_bucket* t0, const hvdx_tiled_buck
     return fail(HVDX_ERR_UNSUPPORTED, "%s: binary16 tensors with binary32 buffers", what);
   if (add_t && !replace_t)
     return fail(HVDX_ERR_UNSUPPORTED, "%s: adding from the tensors needs replacing in the tensors", what);
-  const int es = elem_size(buf_dtype);
-  if (t1 && t0->b.buf_count > 0 && t1->b.buf_count > 0) {  // both run at once: all 2N buffers disjoint
-    std::vector<std::pair<uintptr_t, uintptr_t>> rg;
-    for (const hvdx_tiled_bucket* t : {t0, t1})
-      for (int r = 0; r < nranks; ++r) {
-        const uintptr_t x = reinterpret_cast<uintptr_t>(t->b.bufs[r]);
-        rg.emplace_back(x, x + (uintptr_t)t->b.buf_count * es);
-      }
-    if (overlapping(rg)) return fail(HVDX_ERR_ALIAS, "%s: fusion buffers of the two buckets overlap", what);
-  }
-  // the buckets with something to reduce, one or two
-  const hvdx_tiled_bucket* run[2] = {nullptr, nullptr};
+  // the buckets with something to reduce
+  const hvdx_tiled_bucket* run[HVDX_TILED_MAX_BUCKETS];
   int nrun = 0;
-  for (const hvdx_tiled_bucket* t : {t0, t1})
-    if (t && t->b.buf_count > 0) run[nrun++] = t;
+  for (int i = 0; i < nbuckets; ++i)
+    if (buckets[i].b.buf_count > 0) run[nrun++] = &buckets[i];
+  if (nrun > 2 && !add_t)
+    return fail(HVDX_ERR_UNSUPPORTED, "%s: more than two buckets need both tensor flags", what);
+  if (replace_t && (int64_t)nrun * nranks > hvdx::kRingBufPtrs)
+    return fail(HVDX_ERR_UNSUPPORTED, "%s: %d buckets of %d ranks: at most %d buffers per launch", what, nrun, nranks,
+                hvdx::kRingBufPtrs);
+  const int es = elem_size(buf_dtype);
+  if (nrun > 1) {  // they run at once: all their buffers disjoint
+    std::vector<std::pair<uintptr_t, uintptr_t>> rg;
+    for (int i = 0; i < nrun; ++i)
+      for (int r = 0; r < nranks; ++r) {
+        const uintptr_t x = reinterpret_cast<uintptr_t>(run[i]->b.bufs[r]);
+        rg.emplace_back(x, x + (uintptr_t)run[i]->b.buf_count * es);
+      }
+    if (overlapping(rg)) return fail(HVDX_ERR_ALIAS, "%s: fusion buffers of two buckets overlap", what);
+  }
   if (nrun == 0) return HVDX_OK;
-  const int64_t n_in = run[0]->n_in + (nrun > 1 ? run[1]->n_in : 0);
-  const int64_t n_out = run[0]->n_out + (nrun > 1 ? run[1]->n_out : 0);
+  int64_t n_in = 0, n_out = 0, all = 0;
+  for (int i = 0; i < nrun; ++i) {
+    n_in += run[i]->n_in;
+    n_out += run[i]->n_out;
+    all += run[i]->b.buf_count;
+  }
   if (n_in > 0x7fffffff || n_out > 0x7fffffff) return fail(HVDX_ERR_UNSUPPORTED, "%s: too many tiles", what);
   hipStream_t st = static_cast<hipStream_t>(stream);
   const int last = nranks - 2;
-  const int64_t both = run[0]->b.buf_count + (nrun > 1 ? run[1]->b.buf_count : 0);
-  hvdx::TiledCopy k{};
+  // the ring on the tensors: one descriptor for all buckets, its tile tables set per step kind
+  hvdx::TiledRing ring{};
+  ring.nbuckets = nrun;
+  ring.nranks = nranks;
   for (int i = 0; i < nrun; ++i) {
+    ring.t[i] = run[i]->b.tensors;
+    ring.ntensors[i] = run[i]->b.ntensors;
+    for (int r = 0; r < nranks && replace_t; ++r) ring.bufs[i * nranks + r] = run[i]->b.bufs[r];
+  }
+  auto use_tiles = [&](bool out) {
+    int64_t at = 0;
+    for (int i = 0; i < nrun; ++i) {
+      ring.tiles[i] = out ? run[i]->out_tiles : run[i]->in_tiles;
+      at += out ? run[i]->n_out : run[i]->n_in;
+      ring.end[i] = at;
+    }
+  };
+  // the copies of one or two buckets (the paper's buffers)
+  hvdx::TiledCopy k{};
+  for (int i = 0; i < nrun && i < 2; ++i) {
     k.m.t[i] = run[i]->b.tensors;
     k.m.numel[i] = run[i]->b.numel;
     k.m.offset[i] = run[i]->b.offset;
@@ -877,17 +906,18 @@ int hvdx_fuse_allreduce_tiled(const hvdx_tiled_bucket* t0, const hvdx_tiled_buck
   k.x0 = run[0]->n_in;
   int rc;
   if (add_t) {  // adding steps 0 .. N-3 with every rank's own values read from its tensors
-    TimedLaunch timed_phase(HVDX_KERNEL_REDUCE_SCATTER, 0, nranks, buf_dtype, HVDX_COMPRESS_NONE, both, st, -1, true,
+    use_tiles(false);
+    TimedLaunch timed_phase(HVDX_KERNEL_REDUCE_SCATTER, 0, nranks, buf_dtype, HVDX_COMPRESS_NONE, all, st, -1, true,
                             last);
     for (int s = 0; s < last; ++s) {
-      TimedLaunch timed(HVDX_KERNEL_REDUCE_SCATTER, s, nranks, buf_dtype, HVDX_COMPRESS_NONE, both, st);
-      const hipError_t e = hvdx::launch_add_tiles(k, tensor_dtype, buf_dtype, nranks, s, n_in, st);
+      TimedLaunch timed(HVDX_KERNEL_REDUCE_SCATTER, s, nranks, buf_dtype, HVDX_COMPRESS_NONE, all, st);
+      const hipError_t e = hvdx::launch_add_tiles(ring, tensor_dtype, buf_dtype, s, st);
       if (e != hipSuccess) return hip_fail(e, "adding step from the tensors");
     }
   } else {
     {
-      TimedLaunch timed(HVDX_KERNEL_PACK_RS, 0, nranks, buf_dtype, HVDX_COMPRESS_NONE, both, st);
-      TimedLaunch timed_phase(HVDX_KERNEL_PACK_RS, 0, nranks, buf_dtype, HVDX_COMPRESS_NONE, both, st, -1, true);
+      TimedLaunch timed(HVDX_KERNEL_PACK_RS, 0, nranks, buf_dtype, HVDX_COMPRESS_NONE, all, st);
+      TimedLaunch timed_phase(HVDX_KERNEL_PACK_RS, 0, nranks, buf_dtype, HVDX_COMPRESS_NONE, all, st, -1, true);
       const hipError_t e = hvdx::launch_pack_tiles(k, tensor_dtype, buf_dtype, nranks, n_in, st);
       if (e != hipSuccess) return hip_fail(e, "tiled copy-in launch");
     }
@@ -901,21 +931,19 @@ int hvdx_fuse_allreduce_tiled(const hvdx_tiled_bucket* t0, const hvdx_tiled_buck
   }
   if (replace_t) {
     if (n_out == 0) return HVDX_OK;  // every tensor empty: nothing to deliver
-    k.tiles[0] = run[0]->out_tiles;
-    k.tiles[1] = nrun > 1 ? run[1]->out_tiles : nullptr;
-    k.x0 = run[0]->n_out;
+    use_tiles(true);
     {
-      TimedLaunch timed(HVDX_KERNEL_RS_AG, last, nranks, buf_dtype, HVDX_COMPRESS_NONE, both, st);
-      TimedLaunch timed_phase(HVDX_KERNEL_RS_AG, last, nranks, buf_dtype, HVDX_COMPRESS_NONE, both, st, -1, true);
-      const hipError_t e = hvdx::launch_rs_ag_tiles(k, ring_args(nranks, run[0]->b.buf_count, last), tensor_dtype,
-                                                    buf_dtype, div_mode(op, nranks), add_t, n_out, st);
+      TimedLaunch timed(HVDX_KERNEL_RS_AG, last, nranks, buf_dtype, HVDX_COMPRESS_NONE, all, st);
+      TimedLaunch timed_phase(HVDX_KERNEL_RS_AG, last, nranks, buf_dtype, HVDX_COMPRESS_NONE, all, st, -1, true);
+      const hipError_t e = hvdx::launch_rs_ag_tiles(ring, ring_args(nranks, run[0]->b.buf_count, last), tensor_dtype,
+                                                    buf_dtype, div_mode(op, nranks), add_t, st);
       if (e != hipSuccess) return hip_fail(e, "replacing step 0 into the tensors");
     }
-    TimedLaunch timed_phase(HVDX_KERNEL_ALLGATHER, 1, nranks, buf_dtype, HVDX_COMPRESS_NONE, both, st, -1, true,
+    TimedLaunch timed_phase(HVDX_KERNEL_ALLGATHER, 1, nranks, buf_dtype, HVDX_COMPRESS_NONE, all, st, -1, true,
                             last);
     for (int s = 1; s <= last; ++s) {
-      TimedLaunch timed(HVDX_KERNEL_ALLGATHER, s, nranks, buf_dtype, HVDX_COMPRESS_NONE, both, st);
-      const hipError_t e = hvdx::launch_ag_tiles(k, tensor_dtype, buf_dtype, nranks, s, n_out, st);
+      TimedLaunch timed(HVDX_KERNEL_ALLGATHER, s, nranks, buf_dtype, HVDX_COMPRESS_NONE, all, st);
+      const hipError_t e = hvdx::launch_ag_tiles(ring, tensor_dtype, buf_dtype, s, st);
       if (e != hipSuccess) return hip_fail(e, "replacing step into the tensors");
     }
     return HVDX_OK;
@@ -924,7 +952,7 @@ int hvdx_fuse_allreduce_tiled(const hvdx_tiled_bucket* t0, const hvdx_tiled_buck
     rc = run_pair_steps(&run[0]->b, &run[1]->b, buf_dtype, op, HVDX_KERNEL_REDUCE_SCATTER, 1, last, nranks, st);
     if (rc) return rc;
     {
-      TimedLaunch timed_phase(HVDX_KERNEL_RS_AG, last, nranks, buf_dtype, HVDX_COMPRESS_NONE, both, st, -1, true);
+      TimedLaunch timed_phase(HVDX_KERNEL_RS_AG, last, nranks, buf_dtype, HVDX_COMPRESS_NONE, all, st, -1, true);
       rc = run_pair_step(&run[0]->b, &run[1]->b, buf_dtype, op, HVDX_KERNEL_RS_AG, last, nranks, st);
       if (rc) return rc;
     }
@@ -945,8 +973,8 @@ int hvdx_fuse_allreduce_tiled(const hvdx_tiled_bucket* t0, const hvdx_tiled_buck
   }
   if (rc) return rc;
   if (n_out == 0) return HVDX_OK;  // every tensor empty: nothing to copy out
-  TimedLaunch timed(HVDX_KERNEL_AG_UNPACK, last, nranks, buf_dtype, HVDX_COMPRESS_NONE, both, st);
-  TimedLaunch timed_phase(HVDX_KERNEL_AG_UNPACK, last, nranks, buf_dtype, HVDX_COMPRESS_NONE, both, st, -1, true);
+  TimedLaunch timed(HVDX_KERNEL_AG_UNPACK, last, nranks, buf_dtype, HVDX_COMPRESS_NONE, all, st);
+  TimedLaunch timed_phase(HVDX_KERNEL_AG_UNPACK, last, nranks, buf_dtype, HVDX_COMPRESS_NONE, all, st, -1, true);
   k.tiles[0] = run[0]->out_tiles;
   k.tiles[1] = nrun > 1 ? run[1]->out_tiles : nullptr;
   k.x0 = run[0]->n_out;

@@ -111,17 +111,31 @@ hipError_t launch_pack_tiles(const TiledCopy& k, int src_dtype, int buf_dtype, i
                              hipStream_t stream);
 hipError_t launch_unpack_tiles(const TiledCopy& k, int buf_dtype, int dst_dtype, int nranks, int64_t blocks,
                                hipStream_t stream);
+// The ring on the tensors of one to kRingBuckets fusion buffers, every launch serving
+// all of them: the launch's tiles [end[i-1], end[i]) are bucket i's (from tiles[i]),
+// bucket i's tensor pointer table is the DEVICE table t[i] (rank-major, ntensors[i] per
+// rank), and its rank r fusion buffer is bufs[i * nranks + r].
+constexpr int kRingBuckets = 4;
+constexpr int kRingBufPtrs = 256;  // nbuckets * nranks at most
+struct TiledRing {
+  const hvdx_copy_tile* tiles[kRingBuckets];
+  int64_t end[kRingBuckets];
+  void* const* t[kRingBuckets];
+  int64_t ntensors[kRingBuckets];
+  int nbuckets;
+  int nranks;
+  void* bufs[kRingBufPtrs];
+};
+
 // Replacing steps that deliver into the tensors, over the copy-out's tiles: adding step
 // N-2 with replacing step 0 (own_in_tensors: the owner's value from its tensors), and
 // replacing step s between the tensors.
-hipError_t launch_rs_ag_tiles(const TiledCopy& k, const RingArgs& a, int tensor_dtype, int buf_dtype, int divmode,
-                              bool own_in_tensors, int64_t blocks, hipStream_t stream);
-hipError_t launch_ag_tiles(const TiledCopy& k, int tensor_dtype, int buf_dtype, int nranks, int step, int64_t ntiles,
-                           hipStream_t stream);
+hipError_t launch_rs_ag_tiles(const TiledRing& k, const RingArgs& a, int tensor_dtype, int buf_dtype, int divmode,
+                              bool own_in_tensors, hipStream_t stream);
+hipError_t launch_ag_tiles(const TiledRing& k, int tensor_dtype, int buf_dtype, int step, hipStream_t stream);
 // Adding step s (0 .. N-3) reading every receiver's own values from its tensors (and at
 // s = 0 the sender's too), over the copy-in's tiles.
-hipError_t launch_add_tiles(const TiledCopy& k, int tensor_dtype, int buf_dtype, int nranks, int step, int64_t ntiles,
-                            hipStream_t stream);
+hipError_t launch_add_tiles(const TiledRing& k, int tensor_dtype, int buf_dtype, int step, hipStream_t stream);
 // A small ring in one launch: each thread runs every step for its elements.
 hipError_t launch_chain(const RankPtrs& bufs, const RingArgs& a, int64_t count, int dtype, int divmode,
                         bool vector_ok, hipStream_t stream);

@@ -2,22 +2,26 @@
 
 `FusedAllreduce` is built once for a fixed set of gradient tensors (one list per
 simulated rank, all in GPU memory) and then reduces them in place each time it is
-called: for every fusion buffer of the plan, copy in (pack), ring-allreduce, copy
-out (unpack); a tensor larger than the buffer runs the ring in place on the rank
-tensors themselves.  Torch provides the device memory and the stream; every step
-is a libhvdx kernel.
+called: every fusion buffer of the plan goes through the ring-allreduce of paper
+section 3; a tensor larger than the buffer runs the ring in place on the rank tensors
+themselves.  By default a fusion buffer's ring runs on the ranks' tensors: its adding
+steps read each rank's own elements from the tensors (where a copy-in would take them
+from), the buffers hold the partial sums received, and its replacing steps write the
+tensors (where a copy-out would put them); the paper's copies are options.  Torch
+provides the device memory and the stream; every step is a libhvdx kernel.
 
 The fusion buffers are allocated once, at the size of the largest fused bucket
 (at most the threshold, 64 MiB by default), and reused for every bucket, as the
 paper's step 2 describes.  The descriptor arrays the kernels read (tensor pointers,
-sizes, offsets) are uploaded once at construction, so the tensors must stay
-allocated and in place for the object's lifetime.
+sizes, offsets, tile tables) are uploaded once at construction, so the tensors must
+stay allocated and in place for the object's lifetime.
 
 Buckets of at most `small_bucket_bytes` per rank (4 MiB by default) run their whole
 cycle in one launch (hvdx_fuse_allreduce_small, hvdx_ring_allreduce_small): there a
 ring step's launch costs more than its messages.  Fused buckets on the per-step path
-run two at a time, paired in plan order (hvdx_fuse_allreduce_pair: each launch serves
-both), the second of a pair with fusion buffers of its own.  Same bits either way.
+run in groups, in plan order, every launch serving the whole group (up to four
+buffers with the ring on the tensors, else two), each member after the first with
+fusion buffers of its own.  Same bits either way.
 """
 from __future__ import annotations
 
@@ -44,14 +48,14 @@ class Bucket:
     ptrs_dev: torch.Tensor | None = None
     small: bool = False  # the whole cycle in one launch
     tiles: tuple | None = None  # (device copy-in table, tiles, device copy-out table, tiles)
-    pair: int = 0  # 1: runs together with the later bucket `partner`; 2: with an earlier one
-    partner: int = -1  # (the second of a pair has fusion buffers of its own)
+    group: tuple = ()  # the buckets (this one included) whose cycles share every launch, or ()
+    slot: int = 0  # position in the group: slot k uses fusion buffer set k; slot 0 runs the group
 
 
 def _check_disjoint(tensors) -> None:
     """Raise ValueError when two of the tensors (any ranks) share memory.  The kernels
-    read and write every rank's tensors in one launch (both buckets' in a paired
-    launch), so a tensor listed twice, or two views of one storage, would make the
+    read and write every rank's tensors in one launch (all of a group's buckets' in a
+    grouped launch), so a tensor listed twice, or two views of one storage, would make the
     result depend on the order of blocks; the device pointers cannot be checked on the
     C side."""
     spans = sorted((x.data_ptr(), x.data_ptr() + x.numel() * x.element_size(), r, t)
@@ -77,9 +81,11 @@ class FusedAllreduce:
         With the fused boundary, a bucket of at most small_bucket_bytes per rank (0:
         none) runs its whole cycle in one launch instead (compressed direct tensors
         excepted).  With pair_buckets (fused boundary) the fused buckets on the per-step
-        path run two at a time, every launch serving both; if one of them is left alone,
-        the first small fused bucket joins it there instead of taking its one launch.  With tiled (fused boundary,
-        N >= 3) the fused copies of those buckets are driven by tile tables cut once here
+        path run in groups, every launch serving the group: up to TILED_MAX_BUCKETS (and
+        TILED_MAX_BUFFERS // N) with both tensor flags, else two; if the last group is
+        short, the first small fused bucket joins it instead of taking its one launch.
+        With tiled (fused boundary, N >= 3) the fused copies of those buckets are driven by
+        tile tables cut once here
         (hvdx_fuse_copy_tiles, hvdx_fuse_allreduce_tiled) instead of finding each stretch's
         tensors in the kernel.  With replace_in_tensors (tiled) their replacing steps
         deliver each chunk straight into the receiving rank's tensors and forward it from
@@ -130,29 +136,44 @@ class FusedAllreduce:
             b.small = (self.fuse_boundary and b.count * es <= small_bucket_bytes
                        and not (b.direct and self.compress))
 
+        self.tiled = tiled and self.fuse_boundary and n >= 3
+        self.tiled_flags = L.TILED_BUFFERS
+        if replace_in_tensors and self.tiled:
+            self.tiled_flags = L.TILED_REPLACE_IN_TENSORS | (L.TILED_ADD_FROM_TENSORS if add_from_tensors else 0)
+        self.groups = []
         if pair_buckets and self.fuse_boundary and n >= 3:
-            # fused buckets on the per-step path, paired in plan order; a pair runs at its first
-            # member's place, so a direct tensor or small bucket between the two runs after both
-            # (the buckets share no data: the bits do not depend on the order)
+            # fused buckets on the per-step path, grouped in plan order: with the ring on the
+            # tensors as many as one launch takes, else two (the two-buffer kernels); a group
+            # runs at its first member's place, so a direct tensor or small bucket between its
+            # members runs after them (the buckets share no data: the bits do not depend on
+            # the order)
+            size = 2
+            if self.tiled_flags & L.TILED_ADD_FROM_TENSORS:
+                size = max(2, min(L.TILED_MAX_BUCKETS, L.TILED_MAX_BUFFERS // n))
             ok = [i for i, x in enumerate(self.buckets) if not x.direct and not x.small and x.count > 0]
             small = [i for i, x in enumerate(self.buckets) if not x.direct and x.small and x.count > 0]
-            if len(ok) % 2 and small:
-                # a per-step bucket left alone takes the first small fused bucket along: its few
-                # elements then ride in the other's 2N-2 launches instead of a launch of their own
-                # whose threads walk all 2N-2 steps one after another
+            if len(ok) % size and small:
+                # a group left short takes the first small fused bucket along: its few elements
+                # then ride in the others' 2N-2 launches instead of a launch of their own whose
+                # threads walk all 2N-2 steps one after another
                 self.buckets[small[0]].small = False
                 ok = sorted(ok + small[:1])
-            for i, j in zip(ok[0::2], ok[1::2]):
-                self.buckets[i].pair, self.buckets[i].partner = 1, j
-                self.buckets[j].pair, self.buckets[j].partner = 2, i
+            for g in range(0, len(ok), size):
+                members = tuple(ok[g : g + size])
+                if len(members) < 2:
+                    continue
+                self.groups.append(members)
+                for slot, i in enumerate(members):
+                    self.buckets[i].group, self.buckets[i].slot = members, slot
 
         dev = self.device
-        cap = max([b.count for b in self.buckets if not b.direct and b.pair != 2], default=0)
-        cap2 = max([b.count for b in self.buckets if b.pair == 2], default=0)
-        # one fusion buffer per rank, allocated once and reused for every bucket; the
-        # second bucket of a pair runs at the same time as the first and has its own
-        self.bufs = [torch.empty(max(cap, 1), dtype=_TORCH_DTYPE[self.buf_dtype], device=dev) for _ in range(n)]
-        self.bufs2 = [torch.empty(cap2, dtype=_TORCH_DTYPE[self.buf_dtype], device=dev) for _ in range(n if cap2 else 0)]
+        # one fusion buffer per rank, allocated once and reused for every bucket; the other
+        # members of a group run at the same time as the first and have buffers of their own
+        nslots = max([len(g) for g in self.groups], default=1)
+        caps = [max([b.count for b in self.buckets if not b.direct and b.slot == k], default=0) for k in range(nslots)]
+        self.buf_sets = [[torch.empty(max(c, 1) if k == 0 else c, dtype=_TORCH_DTYPE[self.buf_dtype], device=dev)
+                          for _ in range(n)] for k, c in enumerate(caps)]
+        self.bufs = self.buf_sets[0]
         ws = max([L.hvdx_ring_workspace_bytes(n, b.count, self.dtype, self.compress)
                   for b in self.buckets if b.direct], default=0)
         self.workspace = torch.empty(max(ws, 1), dtype=torch.uint8, device=dev)
@@ -164,7 +185,6 @@ class FusedAllreduce:
             b.offset_dev = torch.tensor(b.offsets, dtype=torch.int64, device=dev)
             b.ptrs_dev = torch.tensor([self.tensors[r][t].data_ptr() for r in range(n) for t in b.tensors],
                                       dtype=torch.int64, device=dev)
-        self.tiled = tiled and self.fuse_boundary and n >= 3
         if self.tiled:
             for b in self.buckets:
                 if b.direct or b.small or b.count == 0:
@@ -176,21 +196,16 @@ class FusedAllreduce:
                     host = torch.frombuffer(bytearray(bytes(arr)), dtype=torch.uint8)
                     tabs += [host.to(dev), k]
                 b.tiles = tuple(tabs)
-        in_tensors = replace_in_tensors and self.tiled
-        self.tiled_flags = L.TILED_BUFFERS
-        if in_tensors:
-            self.tiled_flags = L.TILED_REPLACE_IN_TENSORS | (L.TILED_ADD_FROM_TENSORS if add_from_tensors else 0)
-        self._buf_ptrs = [x.data_ptr() for x in self.bufs]
-        self._buf2_ptrs = [x.data_ptr() for x in self.bufs2]
+        self._buf_ptrs = [[x.data_ptr() for x in bs] for bs in self.buf_sets]
         _timeline.start_from_env()
 
     # ---- the steps, exposed separately for tracing ------------------------------------
     def pack(self, b: Bucket, stream: int) -> None:
         L.hvdx_fuse_pack(b.ptrs_dev.data_ptr(), b.numel_dev.data_ptr(), b.offset_dev.data_ptr(), len(b.tensors),
-                         self.dtype, self._buf_ptrs, b.count, self.buf_dtype, self.nranks, stream)
+                         self.dtype, self._buf_ptrs[0], b.count, self.buf_dtype, self.nranks, stream)
 
     def unpack(self, b: Bucket, stream: int) -> None:
-        L.hvdx_fuse_unpack(self._buf_ptrs, b.count, self.buf_dtype, b.ptrs_dev.data_ptr(), b.numel_dev.data_ptr(),
+        L.hvdx_fuse_unpack(self._buf_ptrs[0], b.count, self.buf_dtype, b.ptrs_dev.data_ptr(), b.numel_dev.data_ptr(),
                            b.offset_dev.data_ptr(), len(b.tensors), self.dtype, self.nranks, stream)
 
     def ring_args(self, b: Bucket):
@@ -199,7 +214,7 @@ class FusedAllreduce:
             t = b.tensors[0]
             ptrs = [self.tensors[r][t].data_ptr() for r in range(self.nranks)]
             return ptrs, b.count, self.dtype, self.compress, self.workspace.data_ptr(), self.workspace_bytes
-        return self._buf_ptrs, b.count, self.buf_dtype, L.COMPRESS_NONE, 0, 0
+        return self._buf_ptrs[0], b.count, self.buf_dtype, L.COMPRESS_NONE, 0, 0
 
     def ring(self, b: Bucket, stream: int) -> None:
         ptrs, count, dtype, compress, ws, wsb = self.ring_args(b)
@@ -224,25 +239,26 @@ class FusedAllreduce:
         """A fusion buffer's copy-in, ring and copy-out with the boundary steps fused
         (or, for a small bucket, all in one launch)."""
         if self.tiled and not b.small:
-            L.hvdx_fuse_allreduce_tiled(self.tiled_desc(b, self._buf_ptrs), None, self.dtype, self.buf_dtype,
-                                        self.nranks, self.op, self.tiled_flags, stream)
+            L.hvdx_fuse_allreduce_tiled([self.tiled_desc(b)], self.dtype, self.buf_dtype, self.nranks, self.op,
+                                        self.tiled_flags, stream)
             return
         fn = L.hvdx_fuse_allreduce_small if b.small else L.hvdx_fuse_allreduce
         fn(b.ptrs_dev.data_ptr(), b.numel_dev.data_ptr(), b.offset_dev.data_ptr(), len(b.tensors), self.dtype,
-           self._buf_ptrs, b.count, self.buf_dtype, self.nranks, self.op, stream)
+           self._buf_ptrs[0], b.count, self.buf_dtype, self.nranks, self.op, stream)
 
-    def tiled_desc(self, x: Bucket, bufs):
-        return (x.ptrs_dev.data_ptr(), x.numel_dev.data_ptr(), x.offset_dev.data_ptr(), len(x.tensors), bufs, x.count,
-                x.tiles[0].data_ptr(), x.tiles[1], x.tiles[2].data_ptr(), x.tiles[3])
+    def tiled_desc(self, x: Bucket):
+        return (x.ptrs_dev.data_ptr(), x.numel_dev.data_ptr(), x.offset_dev.data_ptr(), len(x.tensors),
+                self._buf_ptrs[x.slot], x.count, x.tiles[0].data_ptr(), x.tiles[1], x.tiles[2].data_ptr(), x.tiles[3])
 
-    def fused_pair(self, a: Bucket, b: Bucket, stream: int) -> None:
-        """Two fusion buffers' cycles with every launch serving both."""
+    def fused_group(self, members, stream: int) -> None:
+        """The cycles of a group of fusion buffers with every launch serving all of them."""
+        bs = [self.buckets[i] for i in members]
         if self.tiled:
-            L.hvdx_fuse_allreduce_tiled(self.tiled_desc(a, self._buf_ptrs), self.tiled_desc(b, self._buf2_ptrs),
-                                        self.dtype, self.buf_dtype, self.nranks, self.op, self.tiled_flags, stream)
+            L.hvdx_fuse_allreduce_tiled([self.tiled_desc(x) for x in bs], self.dtype, self.buf_dtype, self.nranks,
+                                        self.op, self.tiled_flags, stream)
             return
-        desc = [(x.ptrs_dev.data_ptr(), x.numel_dev.data_ptr(), x.offset_dev.data_ptr(), len(x.tensors), bufs,
-                 x.count) for x, bufs in ((a, self._buf_ptrs), (b, self._buf2_ptrs))]
+        desc = [(x.ptrs_dev.data_ptr(), x.numel_dev.data_ptr(), x.offset_dev.data_ptr(), len(x.tensors),
+                 self._buf_ptrs[x.slot], x.count) for x in bs]
         L.hvdx_fuse_allreduce_pair(desc[0], desc[1], self.dtype, self.buf_dtype, self.nranks, self.op, stream)
 
     def kernel_sequence(self):
@@ -254,14 +270,14 @@ class FusedAllreduce:
         tensors, "rs" 0..N-3 replace "pack_rs"), "unpack", "fold", "ring"
         (the one-rank compressed round trip),
         "cycle_small" or "ring_small" (a small bucket's whole cycle in one launch).
-        A launch that serves a pair of buckets names both: (kind, (i, j), step)."""
+        A launch that serves a group of buckets names them all: (kind, (i, j, ...), step)."""
         out = []
         n = self.nranks
         for bi, b in enumerate(self.buckets):
-            if b.count == 0 or b.pair == 2:
+            if b.count == 0 or b.slot > 0:
                 continue
-            if b.pair == 1:
-                out += self._fused_sequence((bi, b.partner))
+            if b.group:
+                out += self._fused_sequence(b.group)
                 continue
             if b.small:
                 if not b.direct:
@@ -324,9 +340,9 @@ class FusedAllreduce:
         if stream is None:
             stream = torch.cuda.current_stream(self.device).cuda_stream
         for i, b in enumerate(self.buckets):
-            if b.pair == 1:
-                self.fused_pair(b, self.buckets[b.partner], stream)
-            elif b.pair == 2:
+            if b.group and b.slot == 0:
+                self.fused_group(b.group, stream)
+            elif b.group:
                 continue
             elif b.direct:
                 self.ring(b, stream)

@@ -30,6 +30,7 @@ class Knobs:
     add_sender: int = 0  # adding step s from the tensors: the sender of chunk c is rank c+s+this (0)
     fused_own_from_buffer: bool = False  # the fused step reads the owner's value from its buffer (False)
     xcd_shift: int = 0  # added to a block's XCD in tile_block() (0)
+    bucket_end_shift: int = 0  # added to each bucket's first launch tile in ring_bucket() (0)
 
 
 K = Knobs()
@@ -651,55 +652,78 @@ class Launch:
             arr[idx] = val
 
 
+def ring_bucket(ends, g, k=K):
+    """ring_bucket(): the bucket whose tiles [ends[b-1], ends[b]) hold the launch's tile g."""
+    b = 0
+    for i in range(1, len(ends)):
+        if g >= ends[i - 1] + k.bucket_end_shift:
+            b = i
+    return b, g - (ends[b - 1] if b else 0)
+
+
 def dataflow_cycle(n, count, numel, tin, tout, V, U=1, aligned=True, k=K, tpb=2):
-    """The fused cycle with HVDX_TILED_REPLACE_IN_TENSORS | HVDX_TILED_ADD_FROM_TENSORS on
+    """dataflow_group for one bucket; returns its ranks' tensors."""
+    return dataflow_group(n, [(count, numel, tin, tout)], V, U, aligned, k, tpb)[0]
+
+
+def dataflow_group(n, buckets, V, U=1, aligned=True, k=K, tpb=2):
+    """The cycle with HVDX_TILED_REPLACE_IN_TENSORS | HVDX_TILED_ADD_FROM_TENSORS of one to
+    four buckets (count, numel, copy-in tiles, copy-out tiles) sharing every launch, on
     values that record which ranks' inputs they hold (bit r for rank r): add_tiles_kernel
-    for adding steps 0..N-3 over the copy-in's tiles, rs_ag_tiles_kernel<..., OWN_T> and
-    ag_tiles_kernel over the copy-out's, each launch's reads and writes replayed from the
-    kernels' index arithmetic.  Checks that no value is counted twice, that each adding
-    step reads a rank's own elements while they still hold its input, that the fused
-    step completes every sum and that the replacing steps forward only complete sums.
-    Returns every rank's tensors."""
+    for adding steps 0..N-3 over the copy-in tiles, rs_ag_tiles_kernel<..., OWN_T> and
+    ag_tiles_kernel over the copy-out tiles, each launch's reads and writes replayed from
+    the kernels' index arithmetic (the launch's tiles are the buckets' tables one after
+    another).  Checks that no launch reads what it writes, that each adding step reads a
+    rank's own elements while they still hold its input, that no value is counted twice,
+    that the fused step completes every sum and that the replacing steps forward only
+    complete sums.  Returns every bucket's ranks' tensors."""
     full = (1 << n) - 1
-    T = [[np.full(m, 1 << r, np.int64) for m in numel] for r in range(n)]
-    B = [np.zeros(count, np.int64) for _ in range(n)]
+    T = [[[np.full(m, 1 << r, np.int64) for m in numel] for r in range(n)] for _, numel, _, _ in buckets]
+    B = [[np.zeros(count, np.int64) for _ in range(n)] for count, _, _, _ in buckets]
+
+    def launch_tiles(which, per_block):
+        tabs = [bk[2] if which == "in" else bk[3] for bk in buckets]
+        ends = list(np.cumsum([len(t) for t in tabs]))
+        for g in block_tiles(int(ends[-1]), per_block, k.tile_block_stride if per_block > 1 else 0, k):
+            b, loc = ring_bucket(ends, g, k)
+            if loc >= len(tabs[b]):
+                raise IndexError(f"tile {loc} of bucket {b} past its table")
+            yield b, tabs[b][loc]
+
     for step in range(n - 2):
         L = Launch()
-        for g in block_tiles(len(tin), tpb, k.tile_block_stride, k):
-            pos, li, t, length, c = tin[g]
+        for b, (pos, li, t, length, c) in launch_tiles("in", tpb):
             if t < 0:
                 continue
             e = tile_lanes(length, V, aligned, U) + k.lane_shift
             snd = (c + step + k.add_sender) % n
             rcv = (snd + 1) % n
-            own = L.read(T[rcv][t], li + e)
+            own = L.read(T[b][rcv][t], li + e)
             assert (own == 1 << rcv).all(), f"step {step}: rank {rcv}'s own elements no longer its input"
-            sent = L.read(T[snd][t], li + e) if step == 0 else L.read(B[snd], pos + e)
+            sent = L.read(T[b][snd][t], li + e) if step == 0 else L.read(B[b][snd], pos + e)
             assert not (own & sent).any(), f"step {step}: a rank's value counted twice"
-            L.write(B[rcv], pos + e, own | sent)
+            L.write(B[b][rcv], pos + e, own | sent)
         L.commit()
     L = Launch()
-    for g in block_tiles(len(tout), 1, 0, k):
-        pos, li, t, length, c = tout[g]
+    for b, (pos, li, t, length, c) in launch_tiles("out", 1):
         e = tile_lanes(length, V, aligned, U) + k.lane_shift
         own = (c - 1) % n
         snd = (own - 1) % n
         # the owner's elements: each read and then overwritten by the same lane, so not a
         # read of the launch's own output (kept out of the race check)
-        mine = B[own][pos + e] if k.fused_own_from_buffer else T[own][t][li + e]
-        sent = L.read(B[snd], pos + e)
+        mine = B[b][own][pos + e] if k.fused_own_from_buffer else T[b][own][t][li + e]
+        sent = L.read(B[b][snd], pos + e)
         assert not (mine & sent).any() and ((mine | sent) == full).all(), "the fused step's sum is not complete"
-        L.write(T[own][t], li + e, mine | sent)
-        L.write(T[c][t], li + e, mine | sent)
+        L.write(T[b][own][t], li + e, mine | sent)
+        L.write(T[b][c][t], li + e, mine | sent)
     L.commit()
     for step in range(1, n - 1):
         L = Launch()
-        for g in block_tiles(len(tout), tpb, k.tile_block_stride, k):
-            pos, li, t, length, c = tout[g]
+        for b, (pos, li, t, length, c) in launch_tiles("out", tpb):
             e = tile_lanes(length, V, aligned, U) + k.lane_shift
             snd = (c + step + k.replace_sender) % n
-            v = L.read(T[snd][t], li + e)
+            v = L.read(T[b][snd][t], li + e)
             assert (v == full).all(), f"replacing step {step} forwards an incomplete sum"
-            L.write(T[(snd + 1) % n][t], li + e, v)
+            L.write(T[b][(snd + 1) % n][t], li + e, v)
         L.commit()
     return T

@@ -249,17 +249,30 @@ def test_tiled_argument_errors():
     b3 = bufs(3, 64)
     d0 = (FAKE, FAKE, FAKE, 3, b3, 64, FAKE, 4, FAKE, 4)
     both = hv.TILED_REPLACE_IN_TENSORS | hv.TILED_ADD_FROM_TENSORS
-    assert status_of(ft, d0, None, hv.FLOAT32, hv.FLOAT32, 3, hv.SUM, 4) == hv.ERR_INVALID
-    assert status_of(ft, d0, None, hv.FLOAT32, hv.FLOAT32, 3, hv.SUM, -1) == hv.ERR_INVALID
+    assert status_of(ft, [d0], hv.FLOAT32, hv.FLOAT32, 3, hv.SUM, 4) == hv.ERR_INVALID
+    assert status_of(ft, [d0], hv.FLOAT32, hv.FLOAT32, 3, hv.SUM, -1) == hv.ERR_INVALID
     for flags in (hv.TILED_REPLACE_IN_TENSORS, both):
-        assert status_of(ft, d0, None, hv.FLOAT16, hv.FLOAT32, 3, hv.SUM, flags) == hv.ERR_UNSUPPORTED
-        assert status_of(ft, d0, None, hv.FLOAT32, hv.FLOAT32, 2, hv.SUM, flags) == hv.ERR_UNSUPPORTED
-        assert status_of(ft, (FAKE, FAKE, FAKE, 3, b3, 64, FAKE, 4, 0, 4), None, hv.FLOAT32, hv.FLOAT32, 3, hv.SUM,
+        assert status_of(ft, [d0], hv.FLOAT16, hv.FLOAT32, 3, hv.SUM, flags) == hv.ERR_UNSUPPORTED
+        assert status_of(ft, [d0], hv.FLOAT32, hv.FLOAT32, 2, hv.SUM, flags) == hv.ERR_UNSUPPORTED
+        assert status_of(ft, [(FAKE, FAKE, FAKE, 3, b3, 64, FAKE, 4, 0, 4)], hv.FLOAT32, hv.FLOAT32, 3, hv.SUM,
                          flags) == hv.ERR_INVALID  # the copy-out tiles missing
-        assert status_of(ft, (FAKE, FAKE, FAKE, 3, b3, 0, FAKE, 0, FAKE, 0), None, hv.FLOAT32, hv.FLOAT32, 3, hv.SUM,
+        assert status_of(ft, [(FAKE, FAKE, FAKE, 3, b3, 0, FAKE, 0, FAKE, 0)], hv.FLOAT32, hv.FLOAT32, 3, hv.SUM,
                          flags) == hv.OK  # an empty bucket: nothing launched
-    assert status_of(ft, d0, None, hv.FLOAT32, hv.FLOAT32, 3, hv.SUM,
+    assert status_of(ft, [d0], hv.FLOAT32, hv.FLOAT32, 3, hv.SUM,
                      hv.TILED_ADD_FROM_TENSORS) == hv.ERR_UNSUPPORTED  # needs the replacing steps in the tensors
+    # bucket counts: 1 to 4; three or more only with both tensor flags; buckets x ranks <= 256
+    stride = 1 << 24
+    many = [(FAKE, FAKE, FAKE, 3, [x + i * stride for x in b3], 64, FAKE, 4, FAKE, 4) for i in range(5)]
+    assert status_of(ft, [], hv.FLOAT32, hv.FLOAT32, 3, hv.SUM, both) == hv.ERR_INVALID
+    assert status_of(ft, many, hv.FLOAT32, hv.FLOAT32, 3, hv.SUM, both) == hv.ERR_INVALID
+    assert status_of(ft, many[:3], hv.FLOAT32, hv.FLOAT32, 3, hv.SUM,
+                     hv.TILED_REPLACE_IN_TENSORS) == hv.ERR_UNSUPPORTED
+    assert status_of(ft, many[:3], hv.FLOAT32, hv.FLOAT32, 3, hv.SUM, hv.TILED_BUFFERS) == hv.ERR_UNSUPPORTED
+    b100 = bufs(100, 64)
+    big = [(FAKE, FAKE, FAKE, 3, [x + i * (1 << 34) for x in b100], 64, FAKE, 4, FAKE, 4) for i in range(3)]
+    assert status_of(ft, big, hv.FLOAT32, hv.FLOAT32, 100, hv.SUM, both) == hv.ERR_UNSUPPORTED  # 300 buffers
+    overlap = [many[0], (FAKE, FAKE, FAKE, 3, [b3[0] + 64, many[1][4][1], many[1][4][2]], 64, FAKE, 4, FAKE, 4)]
+    assert status_of(ft, overlap, hv.FLOAT32, hv.FLOAT32, 3, hv.SUM, both) == hv.ERR_ALIAS
 
 
 def test_fused_allreduce_rejects_overlapping_tensors():

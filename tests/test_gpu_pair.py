@@ -8,7 +8,7 @@ import torch
 
 import paper_1802_05799_amd as hv
 from _gpu import assert_bits_equal, say
-from oracle import allreduce
+from oracle import allreduce, fusion
 
 pytestmark = pytest.mark.gpu
 
@@ -46,8 +46,15 @@ def test_pairs_match_oracle_and_single_cycles(case):
                                pair_buckets=pair, tiled=tiled, replace_in_tensors=into, add_from_tensors=add)
         want_flags = hv.TILED_REPLACE_IN_TENSORS | (hv.TILED_ADD_FROM_TENSORS * add) if into else 0
         assert ar.tiled_flags == want_flags
-        got_pairs = [(i, b.partner) for i, b in enumerate(ar.buckets) if b.pair == 1]
-        assert got_pairs == (pairs if pair else [])
+        # groups of up to four with the ring on the tensors (two at 128 ranks), else pairs
+        size = min(hv.TILED_MAX_BUCKETS, hv.TILED_MAX_BUFFERS // n) if want_flags & hv.TILED_ADD_FROM_TENSORS else 2
+        per_step = sorted({i for p in pairs for i in p} | {i for i, b in enumerate(fusion.fuse_plan(
+            numel, 2 if compress else 4, threshold)) if not b.direct and b.count > 0})
+        want_groups = [tuple(per_step[g : g + size]) for g in range(0, len(per_step), size)] if pair else []
+        want_groups = [g for g in want_groups if len(g) > 1]
+        assert ar.groups == want_groups
+        if size == 2 and pair:
+            assert want_groups == pairs
         for rep, want in enumerate((want1, want2)):  # the second call reduces the first's result again
             ar()
             torch.cuda.synchronize()
@@ -110,9 +117,9 @@ def test_pair_entry_point_directly():
 
 
 def test_small_bucket_rides_along_with_a_lone_one():
-    """Buckets 0 (tensors 0, 1) and 1 (tensor 2) paired, 2 (tensor 3: 400 bytes per rank)
-    small, 3 (tensor 4) direct, 4 (tensor 5) alone: bucket 4 takes bucket 2 along instead
-    of bucket 2 running its own launch."""
+    """Buckets 0 (tensors 0, 1), 1 (tensor 2) and 4 (tensor 5) on the per-step path, 2
+    (tensor 3: 400 bytes per rank) small, 3 (tensor 4) direct: the group of three takes
+    bucket 2 along instead of bucket 2 running its own launch."""
     numel = [9000, 7000, 16384, 100, 20000, 15000]
     n = 6
     rng = np.random.default_rng(4300)
@@ -122,7 +129,7 @@ def test_small_bucket_rides_along_with_a_lone_one():
         want = allreduce.allreduce(host, op, threshold=65536)
         dev = [[torch.from_numpy(x).cuda() for x in row] for row in host]
         ar = hv.FusedAllreduce(dev, op=op, threshold_bytes=65536, small_bucket_bytes=4096)
-        assert [(i, b.partner) for i, b in enumerate(ar.buckets) if b.pair == 1] == [(0, 1), (2, 4)]
+        assert ar.groups == [(0, 1, 2, 4)]
         assert not any(k == "cycle_small" for k, _, _ in ar.kernel_sequence())
         ar()
         torch.cuda.synchronize()

@@ -103,7 +103,7 @@ def test_per_phase_records(mode):
     got = [(r["kind"], r["step"], r["launches"]) for r in tl.records]
     want = []
     for bi, b in enumerate(ar.buckets):
-        if b.pair == 2:  # ran together with an earlier bucket: that pair's records cover it
+        if b.slot > 0:  # ran together with an earlier bucket: that group's records cover it
             continue
         if fuse_boundary and not b.direct and add:  # steps 0-3 from the tensors, 4 + 0, steps 1-4 into them
             want += [(1, 0, 4), (6, 4, 1), (2, 1, 4)]

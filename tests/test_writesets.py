@@ -444,3 +444,36 @@ def test_planted_cycle_mistakes_are_caught(knobs):
 def test_xcd_block_order_is_a_bijection():
     for grid in list(range(1, 70)) + [4099, (1 << 20) + 3]:
         assert sorted(W.tile_block(b, grid) for b in range(grid)) == list(range(grid))
+
+
+def test_buckets_sharing_every_launch_each_sum_their_own_inputs():
+    """Up to four buckets (as FusedAllreduce groups them) in every launch of the ring on
+    the tensors: each tile finds its bucket from the running tile counts."""
+    import paper_1802_05799_amd as hv
+
+    layouts = [COPY_LAYOUTS[1], [4096 * 3 + 1, 7, 2 * 4096 * 2], [5, 1, 3000], COPY_LAYOUTS[0]]
+    for te, be in ((4, 4), (4, 2)):
+        V, U = W.vec_elems(te, be), (2 if be == 2 else 1)
+        for nb in (2, 3, 4):
+            for n in (3, 5):
+                bk = []
+                for numel in layouts[:nb]:
+                    offset, count = plan(numel, be, 16)
+                    bk.append((count, numel, tiles_of(numel, offset, count, te, be, n, hv.COPY_IN),
+                               tiles_of(numel, offset, count, te, be, n, hv.COPY_OUT)))
+                Ts = W.dataflow_group(n, bk, V, U)
+                full = (1 << n) - 1
+                assert all((x == full).all() for T in Ts for row in T for x in row), (te, be, nb, n)
+
+
+def test_planted_bucket_boundary_is_caught():
+    import paper_1802_05799_amd as hv
+
+    bk = []
+    for numel in (COPY_LAYOUTS[1], [5, 1, 3000]):
+        offset, count = plan(numel, 4, 16)
+        bk.append((count, numel, tiles_of(numel, offset, count, 4, 4, 4, hv.COPY_IN),
+                   tiles_of(numel, offset, count, 4, 4, 4, hv.COPY_OUT)))
+    with pytest.raises((AssertionError, IndexError)):
+        Ts = W.dataflow_group(4, bk, 4, 1, True, W.Knobs(bucket_end_shift=1))
+        assert all((x == 15).all() for T in Ts for row in T for x in row)
