@@ -122,9 +122,9 @@ CYCLE_CASES = [
                                   "ring-one-launch", "ring-separate", "fold"])
 @pytest.mark.parametrize("case", range(len(CYCLE_CASES)))
 def test_fused_allreduce_matches_oracle(case, mode):
-    """"ring": the fused boundary, tile-driven, with (when nothing is compressed) the adding
-    steps reading the ranks' own values from their tensors and the replacing steps
-    delivering into them; "ring-misaligned": the same with tensors at odd element offsets
+    """"ring": the fused boundary, tile-driven, with the adding steps reading the ranks' own
+    values from their tensors and the replacing steps delivering into them (compressed:
+    the compressed ring's form of it); "ring-misaligned": the same with tensors at odd element offsets
     (the element paths); "ring-copy-in": the copy-in fused with adding step 0, the rest
     of the adding steps in the buffers, the replacing steps into the tensors;
     "ring-buffers": the ring in the fusion buffers between the fused copies;
@@ -205,3 +205,35 @@ def test_copy_kernels_fused_with_ring_steps(case, misalign):
             assert_bits_equal(dev[r][t].cpu().numpy(), want[t], f"rank {r} tensor {t}")
         assert_bits_equal(bufs[r][: b.count].cpu().numpy(), before[r], f"buffer of rank {r}")
 
+
+
+BINARY16_CASES = [
+    # (numel, nranks, threshold bytes, op): binary16 tensors and buffers, no compression
+    ([7, 64, 100, 1000, 4608, 4096, 513, 10000], 4, 64 << 20, "average"),
+    ([3000, 1, 2, 50000, 64, 64, 64, 128 * 1024, 9], 6, 40000, "average"),  # buckets and direct tensors
+    ([5000, 300, 70001, 9, 2048 * 3 + 5], 13, 16384, "sum"),
+    ([5000, 300, 70000, 9], 128, 20000, "average"),
+]
+
+
+@pytest.mark.parametrize("mode", ["tensors", "tensors-misaligned", "copy-in", "buffers", "lookup"])
+@pytest.mark.parametrize("case", range(len(BINARY16_CASES)))
+def test_binary16_tensors_every_mode(case, mode):
+    """binary16 gradients (binary16 buffers, no compression) through each way of running
+    the fused buckets: the ring on the tensors (aligned, and at odd element offsets: the
+    element paths), the copy-in kept, the ring in the buffers, the searching copies."""
+    numel, n, threshold, op = BINARY16_CASES[case]
+    rng = np.random.default_rng(700 + case)
+    host, dev, keep = make_tensors(rng, n, numel, np.float16, misalign=mode == "tensors-misaligned")
+    say(f"binary16 tensors case={case} n={n} mode={mode}")
+    ar = hv.FusedAllreduce(dev, op=op, threshold_bytes=threshold, small_bucket_bytes=0, tiled=mode != "lookup",
+                           replace_in_tensors=mode not in ("buffers", "lookup"),
+                           add_from_tensors=mode in ("tensors", "tensors-misaligned"))
+    want = allreduce.allreduce(host, op, threshold=threshold)
+    for rep in range(2):  # the second call reduces the first's result again
+        ar()
+        torch.cuda.synchronize()
+        for r in range(n):
+            for t in range(len(numel)):
+                assert_bits_equal(dev[r][t].cpu().numpy(), want[r][t], f"call {rep} rank {r} tensor {t}")
+        want = allreduce.allreduce(want, op, threshold=threshold)
