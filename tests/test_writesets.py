@@ -304,6 +304,13 @@ def test_planted_copy_out_from_the_receiver_is_caught():
 
 
 # ---- tile-driven fused copies ----------------------------------------------------------
+def lane_vectors(te, be):
+    """Vectors per lane of the built tile kernels: a tile is what 256 lanes move."""
+    import paper_1802_05799_amd as hv
+
+    return hv.hvdx_fuse_tile_elems(0 if te == 4 else 1, 0 if be == 4 else 1) // (256 * W.vec_elems(te, be))
+
+
 def tiles_of(numel, offset, count, te, be, n, direction):
     import paper_1802_05799_amd as hv
 
@@ -324,7 +331,7 @@ def test_tiled_copies_write_every_element_once(esizes):
                 q, rem = divmod(count, n)
                 tin = tiles_of(numel, offset, count, te, be, n, hv.COPY_IN)
                 tout = tiles_of(numel, offset, count, te, be, n, hv.COPY_OUT)
-                U = 2 if (te, be) == (4, 2) else 1  # vectors per lane of the built kernels
+                U = lane_vectors(te, be)
                 for aligned in (True, False):
                     bw, _, _ = W.tiled_copy("pack", n, count, numel, tin, V, aligned, U)
                     want = np.ones((n, count), np.int64)
@@ -411,7 +418,7 @@ def test_cycle_from_and_into_tensors_sums_every_input_once(esizes):
 
     te, be = esizes
     V = W.vec_elems(te, be)
-    U = 2 if (te, be) == (4, 2) else 1  # vectors per lane of the built kernels
+    U = lane_vectors(te, be)
     for numel in COPY_LAYOUTS + [[4096 * 3 + 1, 7, 2 * 4096 * 2]]:
         for align in (16, be):
             offset, count = plan(numel, be, align)
@@ -453,7 +460,7 @@ def test_buckets_sharing_every_launch_each_sum_their_own_inputs():
 
     layouts = [COPY_LAYOUTS[1], [4096 * 3 + 1, 7, 2 * 4096 * 2], [5, 1, 3000], COPY_LAYOUTS[0]]
     for te, be in ((4, 4), (4, 2)):
-        V, U = W.vec_elems(te, be), (2 if be == 2 else 1)
+        V, U = W.vec_elems(te, be), lane_vectors(te, be)
         for nb in (2, 3, 4):
             for n in (3, 5):
                 bk = []
