@@ -271,7 +271,10 @@ int64_t hvdx_fuse_tile_elems(int tensor_dtype, int buf_dtype);
  *                      for exactly this bucket (numel, offset, buf_count, both types and
  *                      nranks): the tables are device memory and are not checked; other
  *                      tables make the kernels read or write outside the buffers and
- *                      tensors.  All buckets' fusion buffers must be pairwise disjoint.
+ *                      tensors.  All buckets' fusion buffers must be pairwise disjoint
+ *                      (checked), and every rank's tensors of all buckets disjoint from one
+ *                      another and from the buffers (not checked: the tables are device
+ *                      memory; overlapping tensors give results that depend on block order).
  *                      More than two buckets (with something to reduce) need both tensor
  *                      flags; with HVDX_TILED_REPLACE_IN_TENSORS, buckets x nranks <= 256.
  *   flags              0 (HVDX_TILED_BUFFERS): the fusion buffers as in paper section 7 --
