@@ -115,6 +115,9 @@ CYCLE_CASES = [
     ([1], 1, 64, True, "average"),
     ([5000, 300, 70000, 9], 128, 40000, False, "average"),  # the most ranks a call takes
     ([5000, 300, 70000, 9], 128, 40000, True, "average"),
+    ([0, 5, 0, 0, 7, 1, 0], 8, 64 << 20, False, "average"),  # empty tensors; fewer elements than ranks
+    ([0, 5, 0, 0, 7, 1, 0], 8, 64 << 20, True, "sum"),
+    ([1, 0, 1], 3, 64, False, "sum"),  # one element per bucket
 ]
 
 
