@@ -29,6 +29,9 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, 8 TB/s
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 TILED_REPLACE_IN_TENSORS, TILED_ADD_FROM_TENSORS = 1, 2  # the HVDX_TILED_* bits of FusedAllreduce.tiled_flags
+# FusedAllreduce arguments of each way of running the fusion buffers
+BUFFER_MODES = {"ring_on_tensors": {}, "copy_in": {"add_from_tensors": False},
+                "paper_copies": {"replace_in_tensors": False}}
 
 
 def parse():
@@ -40,6 +43,9 @@ def parse():
     p.add_argument("--broadcast-workload", default="resnet50",
                    help="workload whose parameters the broadcast measurement sends (161 tensors for ResNet-50)")
     p.add_argument("--no-per-config", action="store_true", help="time only the headline workload")
+    p.add_argument("--fusion-buffer-mode", default="ring_on_tensors", choices=sorted(BUFFER_MODES),
+                   help="how the headline workload's fusion buffers run: the ring on the tensors (default), the "
+                        "copy-in kept, or the paper's copies around a ring in the buffers (same bits)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-ablation", action="store_true", help="skip the fusion-threshold sweep")
     p.add_argument("--no-broadcast", action="store_true", help="skip the broadcast measurement")
@@ -646,7 +652,7 @@ def main():
         del src, dst
         torch.cuda.empty_cache()
 
-    head = measure(args.workload, args.steps, args.warmup)
+    head = measure(args.workload, args.steps, args.warmup, **BUFFER_MODES[args.fusion_buffer_mode])
     print(f"# {args.workload}: {head['ms_per_step']:.3f} ms/step, {head['algbw_GBps']:.1f} GB/s, "
           f"graph {head['graph_ms_per_step']:.3f} ms/step", file=sys.stderr,
           flush=True)
@@ -655,7 +661,7 @@ def main():
         from workloads import configs
 
         for name in configs.WORKLOADS:
-            if name == args.workload:
+            if name == args.workload and args.fusion_buffer_mode == "ring_on_tensors":
                 r = head
             else:
                 r = measure(name, max(3, args.steps // 2), 2)
@@ -694,7 +700,7 @@ def main():
     if not args.no_per_config:
         for name in ("resnet50", "inceptionv3", "vgg16", "vgg16fp16"):
             row = {"ring_on_tensors_ms": per_config[name]["ms_per_step"]}
-            for key, kw in (("copy_in_ms", {"add_from_tensors": False}), ("paper_copies_ms", {"replace_in_tensors": False})):
+            for key, kw in (("copy_in_ms", BUFFER_MODES["copy_in"]), ("paper_copies_ms", BUFFER_MODES["paper_copies"])):
                 r = measure(name, max(3, args.steps // 2), 2, per_kernel_pass=False, graph_pass=False, **kw)
                 row[key] = round(r["ms_per_step"], 4)
             buffer_modes[name] = row
@@ -783,7 +789,7 @@ def main():
             "fusion_threshold_bytes": 64 << 20,
             # adding steps read each rank's own elements from its tensors, partial sums in the
             # fusion buffers, replacing steps write the tensors (fusion_buffer_modes: the others)
-            "fusion_buffer_mode": "ring_on_tensors",
+            "fusion_buffer_mode": args.fusion_buffer_mode,
             "buckets": head["buckets"],
         },
         "busbw_GBps": round(head["busbw_GBps"], 2),

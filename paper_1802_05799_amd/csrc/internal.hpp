@@ -58,8 +58,8 @@ constexpr int kTileLanes = 256;
 #ifndef HVDX_TILE_U32
 #define HVDX_TILE_U32 1  // binary32 tensors and buffers
 #endif
-#ifndef HVDX_TILE_U16  // binary32 tensors, binary16 buffers: one vector per lane.  Two had made the copies
-#define HVDX_TILE_U16 1  // 3 points faster; the ring on the tensors is 0.9% faster per step with one
+#ifndef HVDX_TILE_U16  // binary32 tensors, binary16 buffers: one vector per lane.  Two make the copies of
+#define HVDX_TILE_U16 1  // the paper's mode 3 points faster; the ring on the tensors is 1% faster with one
 #endif
 #ifndef HVDX_TILE_UH
 #define HVDX_TILE_UH 1  // binary16 tensors and buffers

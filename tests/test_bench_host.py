@@ -193,3 +193,14 @@ def test_bench_refuses_more_than_one_gpu():
                        text=True, timeout=120)
     assert p.returncode == 2
     assert "one GPU" in p.stderr
+
+
+def test_fusion_buffer_modes_are_fused_allreduce_arguments():
+    import inspect
+
+    from paper_1802_05799_amd import cycle
+
+    params = inspect.signature(cycle.FusedAllreduce.__init__).parameters
+    assert bench.BUFFER_MODES["ring_on_tensors"] == {}
+    for mode in bench.BUFFER_MODES.values():
+        assert all(k in params and params[k].default is True for k in mode) and all(v is False for v in mode.values())
